@@ -1,0 +1,62 @@
+"""Seeded synthetic inputs shared by the tests, the smoke check and the bench.
+
+This module holds none of the W4A8 method's arithmetic: it only draws random
+numbers with the shapes and distributions of the paper's MoE workloads (a
+Qwen3-family layer: 256 routed experts, top-8 routing, one shared expert;
+Sec. 2.2) and turns router logits into top-k ids and weights.  Quantization,
+dot products and the expert MLP live in the HIP library and, separately, in
+the oracle.
+
+Draw order for a layer, one ``numpy.random.default_rng(seed)`` (PCG64):
+expert weights, then hidden states, then the per-expert router bias, then the
+router logits.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+def rng(seed: int = 0) -> np.random.Generator:
+    return np.random.default_rng(seed)
+
+
+def normal_f32(g: np.random.Generator, shape, std: float = 1.0) -> np.ndarray:
+    """fp32 N(0, std^2) values."""
+    x = g.standard_normal(shape, dtype=np.float32)
+    if std != 1.0:
+        x *= np.float32(std)
+    return x
+
+
+def routing(g: np.random.Generator, T: int, E: int, k: int, bias_std: float = 0.0,
+            renormalize: bool = True):
+    """Router stand-in: logits ~ N(0,1) plus an optional per-expert bias
+    ~ N(0, bias_std^2) (skews the expert load for prefill); softmax over E in
+    fp32; top-k with ties broken by the lower expert index; the k weights
+    renormalized to sum to 1.  Returns ids int32 [T,k], weights fp32 [T,k]."""
+    bias = normal_f32(g, (E,), bias_std) if bias_std > 0 else np.zeros(E, np.float32)
+    logits = normal_f32(g, (T, E)) + bias[None, :]
+    z = logits - logits.max(axis=1, keepdims=True)
+    p = np.exp(z, dtype=np.float32)
+    p /= p.sum(axis=1, keepdims=True, dtype=np.float32)
+    order = np.argsort(-p, axis=1, kind="stable")[:, :k]
+    ids = order.astype(np.int32)
+    w = np.take_along_axis(p, order, axis=1).astype(np.float32)
+    if renormalize:
+        w = (w / w.sum(axis=1, keepdims=True, dtype=np.float32)).astype(np.float32)
+    return ids, w
+
+
+def q4_0_random_blocks(g: np.random.Generator, rows: int, K: int,
+                       weight_std: float = 0.02) -> np.ndarray:
+    """Random bytes in the 18-byte Q4_0 block layout: uniform 4-bit codes and a
+    random-sign fp16 scale whose magnitude matches that of N(0, weight_std^2)
+    weights (largest |w| of 32 draws, divided by 8).  Used where fp32 weights
+    for every expert would be too large to draw and keep on the host."""
+    nb = K // 32
+    blocks = g.integers(0, 256, size=(rows * nb, 18), dtype=np.uint8)
+    amax = np.abs(g.standard_normal((rows * nb, 32), dtype=np.float32)).max(axis=1)
+    sign = np.where(g.integers(0, 2, size=rows * nb) == 0, -1.0, 1.0).astype(np.float32)
+    d = (sign * amax * np.float32(weight_std / 8.0)).astype(np.float16)
+    blocks[:, 0:2] = d.view(np.uint8).reshape(-1, 2)
+    return blocks.reshape(rows, nb * 18)
