@@ -1,0 +1,170 @@
+/*
+ * w4a8.h -- C ABI of libw4a8.so: Q4_0-weight x Q8_0-activation (W4A8) matrix
+ * products over routed Mixture-of-Experts experts, for AMD Instinct MI355X
+ * (gfx950).
+ *
+ * The method: 4-bit group-wise weights paired with 8-bit per-group
+ * activations so that the inner product runs as integer multiply-adds, then
+ * one scaling per group (paper Sec. 2.3 "Weight quantization", Sec. 3.3 "CPU
+ * decode: W4A8"), applied to a sparse MoE feed-forward layer with top-k routed
+ * experts and one always-on shared expert (Sec. 2.2 "The model"), where all
+ * routed token-expert pairs of a layer are processed by one grouped launch
+ * rather than one launch per expert (Sec. 3.2 "GPU prefill").
+ *
+ * Formats (fixed by this ABI):
+ *   Q4_0 block, 18 bytes, 32 weights: fp16 scale d (little endian), then 16
+ *     bytes; byte j holds code q_j in its low nibble and q_{j+16} in its high
+ *     nibble; weight value = (q - 8) * d, q in 0..15.  Quantizer: d =
+ *     fp16(m / -8) where m is the signed weight of largest magnitude (first
+ *     index on ties), q = clamp(floor(w * (1/d) + 8.5), 0, 15) with 1/d taken
+ *     as 0 when d == 0.
+ *   Q8_0 block, 34 bytes, 32 activations: fp16 scale d, then 32 int8 codes;
+ *     d = fp16(amax / 127), q = clamp(round_half_away(x * (1/d)), -127, 127),
+ *     q = 0 when d == 0.  Every step is one IEEE binary32 operation, fp16
+ *     rounding is to nearest even with subnormals kept.
+ *   A matrix of N rows by K columns is N rows of K/32 consecutive blocks.
+ *
+ * Conventions for every entry point:
+ *   - All data pointers are DEVICE pointers owned by the caller; the library
+ *     never allocates, frees or keeps them after the call returns.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *     Work is enqueued asynchronously; a return of W4A8_OK means the
+ *     arguments were valid and the kernels were launched.
+ *   - Every base pointer must be 16-byte aligned (W4A8_EALIGN otherwise).
+ *   - Shapes are validated on the host before anything is launched; on an
+ *     error nothing is enqueued and no output is touched.
+ *   - Calls are thread-safe and re-entrant: the library keeps no state other
+ *     than a per-device "is gfx950" check.  Concurrent calls must not share
+ *     output or workspace buffers.
+ */
+#ifndef W4A8_H
+#define W4A8_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define W4A8_OK          0
+#define W4A8_ENULL      -1  /* a required pointer is NULL                        */
+#define W4A8_ESHAPE     -2  /* bad shape (see each entry point)                  */
+#define W4A8_ERANGE     -3  /* k, E or a size outside the supported range        */
+#define W4A8_EWORKSPACE -4  /* workspace smaller than moe_w4a8_workspace_size()  */
+#define W4A8_EALIGN     -5  /* a base pointer is not 16-byte aligned             */
+#define W4A8_EHIP       -6  /* a HIP runtime call or kernel launch failed        */
+#define W4A8_EDEVICE    -7  /* the current device is not gfx950                  */
+
+#define W4A8_Q4_0_BLOCK_BYTES 18
+#define W4A8_Q8_0_BLOCK_BYTES 34
+#define W4A8_BLOCK 32
+
+/* Static, NUL-terminated description of a status code (never NULL). */
+const char *w4a8_strerror(int code);
+
+/*
+ * Q8_0 quantization of activations (Sec. 3.3: "quantized per group to 8-bit").
+ *   x   [rows][K] fp32, row-major.
+ *   xq  [rows][K/32] Q8_0 blocks (rows * K/32 * 34 bytes).
+ * K % 32 != 0, rows < 0 or K <= 0 -> W4A8_ESHAPE.  rows == 0 is a no-op.
+ * Result is bit-identical to the format definition above.
+ */
+int q8_0_quantize(const float *x, void *xq, int64_t rows, int64_t K, void *stream);
+
+/*
+ * Q4_0 quantization of weights (Sec. 2.3: group-wise symmetric 4-bit, two
+ * values per byte, one scale per group).  Used to prepare expert tensors.
+ *   w   [rows][K] fp32.   wq  [rows][K/32] Q4_0 blocks.
+ * K % 32 != 0, rows < 0 or K <= 0 -> W4A8_ESHAPE.  Bit-identical to the
+ * format definition above.
+ */
+int q4_0_quantize(const float *w, void *wq, int64_t rows, int64_t K, void *stream);
+
+/*
+ * W4A8 matrix-vector product, the decode kernel (Sec. 3.3, integer
+ * multiply-add of 4-bit weights with 8-bit activations):
+ *   y[n] = sum_b d_w[n,b] * d_x[b] * s[n,b],  s[n,b] = sum_i (q_w - 8) * q_x
+ * with s exact in int32 and the scaled sum in fp32.
+ *   w   [N][K/32] Q4_0 blocks;  xq [K/32] Q8_0 blocks;  y [N] fp32 (written).
+ * K % 256 != 0 (every row then starts 16-byte aligned), N <= 0 or K <= 0
+ * -> W4A8_ESHAPE.
+ */
+int q4q8_gemv(const void *w, const void *xq, float *y, int64_t N, int64_t K, void *stream);
+
+/*
+ * Bytes of device workspace moe_w4a8_forward needs for these sizes, or 0 if
+ * the sizes are invalid.  The workspace must be zero-filled once before its
+ * first use (moe_w4a8_workspace_init does that); the library leaves its
+ * synchronisation words zero again when each call completes, so it can be
+ * reused by later calls with sizes up to the ones it was sized for.
+ */
+size_t moe_w4a8_workspace_size(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k);
+
+/* Zero-fill a workspace on `stream` with a kernel (no hipMemset node, so it
+ * may be captured into a graph). */
+int moe_w4a8_workspace_init(void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * Byte offsets of the documented workspace regions for these sizes, written
+ * to offsets[0..W4A8_WS_NFIELDS-1] (see W4A8_WS_*).  Returns W4A8_OK or
+ * W4A8_ESHAPE/W4A8_ERANGE.  The regions are valid after a forward call
+ * completes and until the next call using the same workspace:
+ *   W4A8_WS_XQ    Q8_0(hidden), [T][H/32] blocks.
+ *   W4A8_WS_H     fp32 h = SiLU(gate) * up, [P][I], P = T*k + T pairs.
+ *   W4A8_WS_HQ    Q8_0(h), [P][I/32] blocks.
+ *   W4A8_WS_PERM  int32 [T*k + T]: pairs sorted by expert (stable in pair
+ *                 index), routed pairs first, then the T shared pairs.
+ *   W4A8_WS_COUNT int32 [E]: routed pairs per expert.
+ * Pair numbering: routed slot j of token t is pair t*k + j; the shared expert
+ * of token t is pair T*k + t.  Rows of skipped slots are not written.
+ */
+#define W4A8_WS_XQ     0
+#define W4A8_WS_H      1
+#define W4A8_WS_HQ     2
+#define W4A8_WS_PERM   3
+#define W4A8_WS_COUNT  4
+#define W4A8_WS_NFIELDS 5
+int moe_w4a8_workspace_layout(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
+                              size_t *offsets);
+
+/*
+ * One routed + shared MoE feed-forward layer in W4A8 (Sec. 2.2: top-k routed
+ * experts plus an always-on shared expert; Sec. 3.2: one grouped pass over
+ * all routed token-expert pairs; Sec. 3.3: W4A8 integer products):
+ *
+ *   xq_t        = Q8_0(hidden[t])
+ *   for each slot j with e = topk_ids[t][j] in [0, E), and the shared expert:
+ *     gu        = W4A8(w_gate_up[e], xq_t)              2I values, fp32
+ *     h         = SiLU(gu[0:I]) * gu[I:2I]              fp32
+ *     y         = W4A8(w_down[e], Q8_0(h))              H values, fp32
+ *   out[t]      = sum_j topk_w[t][j] * y_j + y_shared
+ *
+ *   hidden     [T][H] fp32.
+ *   topk_ids   [T][k] int32.  An id outside [0, E) (e.g. -1) skips the slot;
+ *              a repeated id contributes once per slot.
+ *   topk_w     [T][k] fp32 routing weights (used as given).
+ *   w_gate_up  [E][2I][H/32] Q4_0 blocks: rows 0..I-1 gate, I..2I-1 up.
+ *   w_down     [E][H][I/32] Q4_0 blocks.
+ *   ws_gate_up, ws_down: the shared expert, shapes [2I][H/32] and [H][I/32];
+ *              both NULL = no shared expert (one NULL alone -> W4A8_ENULL).
+ *   out        [T][H] fp32, overwritten.
+ *   workspace  ws_bytes >= moe_w4a8_workspace_size(T,H,I,E,k), zero-filled
+ *              before its first use.
+ * Shapes: H % 256, I % 256 != 0, T < 0 -> W4A8_ESHAPE; k < 1, k > 32, E < 1,
+ * E > 4096 or T*(k+1) >= 2^31 -> W4A8_ERANGE.  T == 0 is a no-op.
+ * Results: Q8_0 stages bit-exact with the format definition for the fp32
+ * values they receive; float outputs within fp32 rounding of the exact sums.
+ */
+int moe_w4a8_forward(const float *hidden, const int32_t *topk_ids, const float *topk_w,
+                     const void *w_gate_up, const void *w_down,
+                     const void *ws_gate_up, const void *ws_down,
+                     float *out, int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
+                     void *workspace, size_t ws_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* W4A8_H */

@@ -1,1 +1,158 @@
-"""W4A8 MoE hot path for MI355X (binding filled in below)."""
+"""W4A8 (Q4_0 weight x Q8_0 activation) MoE hot path for AMD MI355X (gfx950).
+
+A thin ctypes binding over ``libw4a8.so``: every function marshals torch
+tensors (device memory and the current HIP stream) into the C ABI declared in
+``include/w4a8.h`` and raises on a non-zero status.  All arithmetic runs in the
+HIP kernels; there is no CPU or PyTorch fallback -- if the library is missing
+or the device is not gfx950 the calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libw4a8.so")
+
+OK, ENULL, ESHAPE, ERANGE, EWORKSPACE, EALIGN, EHIP, EDEVICE = 0, -1, -2, -3, -4, -5, -6, -7
+Q4_0_BLOCK_BYTES = 18
+Q8_0_BLOCK_BYTES = 34
+WS_XQ, WS_H, WS_HQ, WS_PERM, WS_COUNT, WS_NFIELDS = 0, 1, 2, 3, 4, 5
+
+EXPORTS = ("w4a8_strerror", "q8_0_quantize", "q4_0_quantize", "q4q8_gemv",
+           "moe_w4a8_workspace_size", "moe_w4a8_workspace_init",
+           "moe_w4a8_workspace_layout", "moe_w4a8_forward")
+
+_lib = None
+
+
+class W4A8Error(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        super().__init__(f"{where}: {strerror(code)} ({code})")
+
+
+def lib() -> ctypes.CDLL:
+    """Load libw4a8.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                           "`python -m paper_2606_24031_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    P, I64, SZ = ctypes.c_void_p, ctypes.c_int64, ctypes.c_size_t
+    L.w4a8_strerror.argtypes = [ctypes.c_int]
+    L.w4a8_strerror.restype = ctypes.c_char_p
+    for name in ("q8_0_quantize", "q4_0_quantize"):
+        getattr(L, name).argtypes = [P, P, I64, I64, P]
+        getattr(L, name).restype = ctypes.c_int
+    L.q4q8_gemv.argtypes = [P, P, P, I64, I64, P]
+    L.q4q8_gemv.restype = ctypes.c_int
+    L.moe_w4a8_workspace_size.argtypes = [I64, I64, I64, I64, I64]
+    L.moe_w4a8_workspace_size.restype = SZ
+    L.moe_w4a8_workspace_init.argtypes = [P, SZ, P]
+    L.moe_w4a8_workspace_init.restype = ctypes.c_int
+    L.moe_w4a8_workspace_layout.argtypes = [I64, I64, I64, I64, I64, P]
+    L.moe_w4a8_workspace_layout.restype = ctypes.c_int
+    L.moe_w4a8_forward.argtypes = [P, P, P, P, P, P, P, P, I64, I64, I64, I64, I64, P, SZ, P]
+    L.moe_w4a8_forward.restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def strerror(code: int) -> str:
+    return lib().w4a8_strerror(code).decode()
+
+
+def _check(rc: int, where: str):
+    if rc != OK:
+        raise W4A8Error(rc, where)
+
+
+def _stream(stream):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _p(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _u8(t):
+    import torch
+    assert t.dtype == torch.uint8 and t.is_contiguous()
+    return t
+
+
+# ------------------------------------------------------------------ entry points
+def q8_0_quantize(x, out=None, stream=None):
+    """Q8_0 of fp32 rows x [rows, K] -> uint8 [rows, K/32*34] on x's device."""
+    import torch
+    assert x.dtype == torch.float32 and x.is_contiguous()
+    rows, K = (1, x.numel()) if x.dim() == 1 else (x.numel() // x.shape[-1], x.shape[-1])
+    if out is None:
+        out = torch.empty((rows, K // 32 * Q8_0_BLOCK_BYTES), dtype=torch.uint8, device=x.device)
+    _check(lib().q8_0_quantize(_p(x), _p(_u8(out)), rows, K, _stream(stream)), "q8_0_quantize")
+    return out
+
+
+def q4_0_quantize(w, out=None, stream=None):
+    """Q4_0 of fp32 rows w [rows, K] -> uint8 [rows, K/32*18] on w's device."""
+    import torch
+    assert w.dtype == torch.float32 and w.is_contiguous()
+    rows, K = (1, w.numel()) if w.dim() == 1 else (w.numel() // w.shape[-1], w.shape[-1])
+    if out is None:
+        out = torch.empty((rows, K // 32 * Q4_0_BLOCK_BYTES), dtype=torch.uint8, device=w.device)
+    _check(lib().q4_0_quantize(_p(w), _p(_u8(out)), rows, K, _stream(stream)), "q4_0_quantize")
+    return out
+
+
+def q4q8_gemv(w, xq, N, K, y=None, stream=None):
+    """y[N] = W4A8(w [N, K/32 Q4_0 blocks], xq [K/32 Q8_0 blocks]) in fp32."""
+    import torch
+    if y is None:
+        y = torch.empty(N, dtype=torch.float32, device=w.device)
+    _check(lib().q4q8_gemv(_p(_u8(w)), _p(_u8(xq)), _p(y), N, K, _stream(stream)), "q4q8_gemv")
+    return y
+
+
+def moe_workspace_size(T, H, I, E, k) -> int:
+    return int(lib().moe_w4a8_workspace_size(T, H, I, E, k))
+
+
+def moe_workspace(T, H, I, E, k, device="cuda", stream=None):
+    """Allocate and zero-fill a workspace for these sizes."""
+    import torch
+    n = moe_workspace_size(T, H, I, E, k)
+    if n == 0:
+        raise W4A8Error(ESHAPE, "moe_workspace_size")
+    ws = torch.empty(n, dtype=torch.uint8, device=device)
+    _check(lib().moe_w4a8_workspace_init(_p(ws), n, _stream(stream)), "moe_w4a8_workspace_init")
+    return ws
+
+
+def moe_workspace_layout(T, H, I, E, k) -> dict:
+    offs = (ctypes.c_size_t * WS_NFIELDS)()
+    _check(lib().moe_w4a8_workspace_layout(T, H, I, E, k, offs), "moe_w4a8_workspace_layout")
+    return {"xq": offs[WS_XQ], "h": offs[WS_H], "hq": offs[WS_HQ], "perm": offs[WS_PERM],
+            "count": offs[WS_COUNT]}
+
+
+def moe_forward(hidden, topk_ids, topk_w, w_gate_up, w_down, ws_gate_up, ws_down,
+                H, I, E, k, workspace, out=None, stream=None):
+    """One routed + shared W4A8 MoE layer; returns out [T, H] fp32."""
+    import torch
+    T = hidden.shape[0]
+    assert hidden.dtype == torch.float32 and hidden.is_contiguous()
+    assert topk_ids.dtype == torch.int32 and topk_ids.is_contiguous()
+    assert topk_w.dtype == torch.float32 and topk_w.is_contiguous()
+    if out is None:
+        out = torch.empty((T, H), dtype=torch.float32, device=hidden.device)
+    rc = lib().moe_w4a8_forward(_p(hidden), _p(topk_ids), _p(topk_w), _p(_u8(w_gate_up)),
+                                _p(_u8(w_down)), _p(ws_gate_up), _p(ws_down), _p(out),
+                                T, H, I, E, k, _p(workspace), workspace.numel(),
+                                _stream(stream))
+    _check(rc, "moe_w4a8_forward")
+    return out

@@ -1,0 +1,172 @@
+// Internal device helpers shared by the gfx950 kernels of libw4a8.
+//
+// Register-level decoding of the two block formats.  A lane that owns eight
+// consecutive blocks of a row holds 144 bytes of Q4_0 (36 dwords, 16-byte
+// aligned when the row length is a multiple of 256) or 272 bytes of Q8_0 (68
+// dwords).  Blocks at even positions start on a dword boundary and their
+// payload is two bytes off; odd blocks are the other way round, so each
+// payload dword is one v_alignbyte away from the raw loads.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/w4a8.h"
+
+namespace w4a8 {
+
+constexpr int QK = 32;
+constexpr int Q4B = W4A8_Q4_0_BLOCK_BYTES;  // 18
+constexpr int Q8B = W4A8_Q8_0_BLOCK_BYTES;  // 34
+
+__device__ __forceinline__ float f16_bits_to_f32(uint32_t bits) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)(bits & 0xFFFFu));
+}
+
+__device__ __forceinline__ uint32_t f32_to_f16_bits(float f) {
+  // v_cvt_f16_f32: round to nearest even (default mode), fp16 denormals kept.
+  // The empty asm pins f as an fp32 register value: otherwise the compiler
+  // may fuse the producing multiply into v_fma_mix with a +0 addend, which
+  // turns a -0 scale into +0.
+  asm volatile("" : "+v"(f));
+  return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)f);
+}
+
+__device__ __forceinline__ uint32_t align2(uint32_t hi, uint32_t lo) {
+  // bytes 2,3 of lo followed by bytes 0,1 of hi
+  return __builtin_amdgcn_alignbyte(hi, lo, 2);
+}
+
+__device__ __forceinline__ int sdot4(int a, int b, int c) {
+  return __builtin_amdgcn_sdot4(a, b, c, false);
+}
+
+// Eight Q8_0 blocks in registers: codes q[k][c] hold elements 4c..4c+3 of
+// block k; corr[k] = -8 * sum of the 32 codes (folds the Q4_0 offset of 8
+// into the integer dot); d[k] the block scale.
+struct Act8 {
+  int q[8][8];
+  int corr[8];
+  float d[8];
+};
+
+// p: 272 bytes (8 blocks), 16-byte aligned.
+__device__ __forceinline__ void load_act8(const uint8_t *__restrict__ p, Act8 &a) {
+  uint32_t D[68];
+  const uint4 *v = reinterpret_cast<const uint4 *>(p);
+#pragma unroll
+  for (int i = 0; i < 17; i++) {
+    uint4 t = v[i];
+    D[4 * i + 0] = t.x; D[4 * i + 1] = t.y; D[4 * i + 2] = t.z; D[4 * i + 3] = t.w;
+  }
+#pragma unroll
+  for (int k = 0; k < 8; k++) {
+    const int i = k >> 1;
+    if ((k & 1) == 0) {
+      const int base = 17 * i;
+      a.d[k] = f16_bits_to_f32(D[base]);
+#pragma unroll
+      for (int c = 0; c < 8; c++) a.q[k][c] = (int)align2(D[base + c + 1], D[base + c]);
+    } else {
+      const int base = 17 * i + 8;
+      a.d[k] = f16_bits_to_f32(D[base] >> 16);
+#pragma unroll
+      for (int c = 0; c < 8; c++) a.q[k][c] = (int)D[base + 1 + c];
+    }
+    int s = 0;
+#pragma unroll
+    for (int c = 0; c < 8; c++) s = sdot4(a.q[k][c], 0x01010101, s);
+    a.corr[k] = -8 * s;
+  }
+}
+
+// Eight Q4_0 blocks of one row (144 bytes) in 36 raw dwords.
+struct W8 {
+  uint32_t D[36];
+};
+
+__device__ __forceinline__ void load_w8(const uint8_t *__restrict__ p, W8 &w) {
+  const uint4 *v = reinterpret_cast<const uint4 *>(p);
+#pragma unroll
+  for (int i = 0; i < 9; i++) {
+    uint4 t = v[i];
+    w.D[4 * i + 0] = t.x; w.D[4 * i + 1] = t.y; w.D[4 * i + 2] = t.z; w.D[4 * i + 3] = t.w;
+  }
+}
+
+// Scale and the four payload dwords (nibble bytes 4c..4c+3) of block k.
+__device__ __forceinline__ float w8_scale(const W8 &w, int k) {
+  const int i = k >> 1;
+  return (k & 1) == 0 ? f16_bits_to_f32(w.D[9 * i]) : f16_bits_to_f32(w.D[9 * i + 4] >> 16);
+}
+__device__ __forceinline__ uint32_t w8_nib(const W8 &w, int k, int c) {
+  const int i = k >> 1;
+  return (k & 1) == 0 ? align2(w.D[9 * i + c + 1], w.D[9 * i + c]) : w.D[9 * i + 5 + c];
+}
+
+// Exact int32 block dot s = sum (q_w - 8) * q_a of block k.
+__device__ __forceinline__ int blockdot(const W8 &w, const Act8 &a, int k) {
+  int s = a.corr[k];
+#pragma unroll
+  for (int c = 0; c < 4; c++) {
+    const uint32_t n = w8_nib(w, k, c);
+    s = sdot4((int)(n & 0x0F0F0F0Fu), a.q[k][c], s);
+    s = sdot4((int)((n >> 4) & 0x0F0F0F0Fu), a.q[k][4 + c], s);
+  }
+  return s;
+}
+
+// acc + sum over the eight blocks of d_w * d_a * s, in fp32.
+__device__ __forceinline__ float dot8(const W8 &w, const Act8 &a, float acc) {
+#pragma unroll
+  for (int k = 0; k < 8; k++) {
+    const int s = blockdot(w, a, k);
+    acc = fmaf((float)s, w8_scale(w, k) * a.d[k], acc);
+  }
+  return acc;
+}
+
+// Sum over groups of `width` consecutive lanes (width a power of two <= 64).
+template <int WIDTH>
+__device__ __forceinline__ float lane_group_sum(float v) {
+#pragma unroll
+  for (int o = WIDTH / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, WIDTH);
+  return v;
+}
+
+// Q8_0 of one 32-value block held by 8 consecutive lanes, 4 values each
+// (lane j of the 8 holds elements 4j..4j+3).  Returns the four codes packed
+// in a dword and, through d16, the block's fp16 scale bits.  Same fp32 steps
+// as the format definition: amax, one division by 127, fp16 RNE, one
+// reciprocal of the stored scale, one multiply per element, round half away.
+__device__ __forceinline__ uint32_t q8_0_block8(const float v[4], uint32_t &d16) {
+  float amax = fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3])));
+#pragma unroll
+  for (int o = 4; o > 0; o >>= 1) amax = fmaxf(amax, __shfl_xor(amax, o, 8));
+  const float d32 = amax / 127.0f;
+  d16 = f32_to_f16_bits(d32);
+  const float df = f16_bits_to_f32(d16);
+  uint32_t packed = 0;
+  if (df != 0.0f) {
+    const float id = 1.0f / df;
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+      int q = (int)roundf(v[i] * id);
+      q = q > 127 ? 127 : (q < -127 ? -127 : q);
+      packed |= ((uint32_t)q & 0xFFu) << (8 * i);
+    }
+  }
+  return packed;
+}
+
+// Store a Q8_0 block produced by 8 lanes: lane j writes codes 4j..4j+3 at
+// byte 2 + 4j (two 16-bit stores, the block is only 2-byte aligned) and lane
+// 0 the scale.
+__device__ __forceinline__ void store_q8_0_block8(uint8_t *blk, int j, uint32_t packed, uint32_t d16) {
+  uint16_t *p = reinterpret_cast<uint16_t *>(blk + 2 + 4 * j);
+  p[0] = (uint16_t)(packed & 0xFFFFu);
+  p[1] = (uint16_t)(packed >> 16);
+  if (j == 0) *reinterpret_cast<uint16_t *>(blk) = (uint16_t)d16;
+}
+
+}  // namespace w4a8

@@ -1,0 +1,22 @@
+// Host-side helpers shared by the libw4a8 entry points.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/w4a8.h"
+
+namespace w4a8 {
+
+// W4A8_OK if the current device is gfx950, else W4A8_EDEVICE / W4A8_EHIP.
+// Cached per device after the first query.
+int check_device();
+
+// W4A8_EHIP if a launch on this thread failed since the last check.
+int check_launch();
+
+inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+inline hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s); }
+
+}  // namespace w4a8

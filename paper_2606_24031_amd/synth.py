@@ -47,16 +47,25 @@ def routing(g: np.random.Generator, T: int, E: int, k: int, bias_std: float = 0.
     return ids, w
 
 
+def random_bytes(g: np.random.Generator, n: int) -> np.ndarray:
+    """n uniform random bytes (raw 64-bit PCG64 outputs viewed as bytes)."""
+    raw = g.bit_generator.random_raw((n + 7) // 8)
+    return raw.view(np.uint8)[:n]
+
+
 def q4_0_random_blocks(g: np.random.Generator, rows: int, K: int,
                        weight_std: float = 0.02) -> np.ndarray:
     """Random bytes in the 18-byte Q4_0 block layout: uniform 4-bit codes and a
-    random-sign fp16 scale whose magnitude matches that of N(0, weight_std^2)
-    weights (largest |w| of 32 draws, divided by 8).  Used where fp32 weights
-    for every expert would be too large to draw and keep on the host."""
+    random-sign fp16 scale near that of N(0, weight_std^2) weights (the
+    largest |w| of 32 such draws is about 2.0-2.8 std, divided by 8).  Used
+    where fp32 weights for every expert would be too large to draw on the
+    host.  The scale's magnitude and sign are taken from the block's own
+    random bytes 0 and 2 before the scale overwrites bytes 0-1."""
     nb = K // 32
-    blocks = g.integers(0, 256, size=(rows * nb, 18), dtype=np.uint8)
-    amax = np.abs(g.standard_normal((rows * nb, 32), dtype=np.float32)).max(axis=1)
-    sign = np.where(g.integers(0, 2, size=rows * nb) == 0, -1.0, 1.0).astype(np.float32)
-    d = (sign * amax * np.float32(weight_std / 8.0)).astype(np.float16)
-    blocks[:, 0:2] = d.view(np.uint8).reshape(-1, 2)
+    n = rows * nb
+    blocks = random_bytes(g, n * 18).reshape(n, 18)
+    u = np.arange(256, dtype=np.float32) * np.float32(1.0 / 255.0)
+    table = (np.float32(weight_std / 8.0) * (np.float32(2.0) + np.float32(0.8) * u)).astype(np.float16)
+    bits = table.view(np.uint16)[blocks[:, 0]] | ((blocks[:, 2].astype(np.uint16) & 1) << 15)
+    blocks[:, 0:2] = bits.view(np.uint8).reshape(-1, 2)
     return blocks.reshape(rows, nb * 18)

@@ -1,0 +1,99 @@
+"""The C ABI library loads, exports every entry point include/w4a8.h declares,
+and rejects bad arguments on the host (these paths return before any device
+call, so they run without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2606_24031_amd as w4
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "w4a8.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b([a-z_0-9]+)\s*\(", src)) - {"defined"})
+
+
+def test_header_declares_the_binding_exports():
+    assert _declared() == sorted(w4.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = w4.lib()
+    for name in _declared():
+        assert hasattr(lib, name), name
+
+
+def test_strerror_covers_every_code():
+    for code in (w4.OK, w4.ENULL, w4.ESHAPE, w4.ERANGE, w4.EWORKSPACE, w4.EALIGN, w4.EHIP, w4.EDEVICE):
+        msg = w4.strerror(code)
+        assert msg and msg != "unknown status code"
+    assert w4.strerror(12345) == "unknown status code"
+
+
+def _fake(addr):
+    return ctypes.c_void_p(addr)
+
+
+A = 0x10000   # an aligned fake device address (never dereferenced: validation fails first)
+
+
+def test_quantize_argument_errors():
+    L = w4.lib()
+    for fn in (L.q8_0_quantize, L.q4_0_quantize):
+        assert fn(None, _fake(A), 4, 64, None) == w4.ENULL
+        assert fn(_fake(A), None, 4, 64, None) == w4.ENULL
+        assert fn(_fake(A), _fake(A), 4, 48, None) == w4.ESHAPE
+        assert fn(_fake(A), _fake(A), -1, 64, None) == w4.ESHAPE
+        assert fn(_fake(A), _fake(A), 4, 0, None) == w4.ESHAPE
+        assert fn(_fake(A + 4), _fake(A), 4, 64, None) == w4.EALIGN
+        assert fn(_fake(A), _fake(A), 0, 64, None) == w4.OK       # empty: no-op
+        assert fn(_fake(A), _fake(A), 1 << 40, 64, None) == w4.ERANGE
+
+
+def test_gemv_argument_errors():
+    L = w4.lib()
+    y = _fake(A)
+    assert L.q4q8_gemv(None, _fake(A), y, 8, 256, None) == w4.ENULL
+    assert L.q4q8_gemv(_fake(A), _fake(A), y, 8, 128, None) == w4.ESHAPE   # K % 256
+    assert L.q4q8_gemv(_fake(A), _fake(A), y, 0, 256, None) == w4.ESHAPE
+    assert L.q4q8_gemv(_fake(A), _fake(A + 2), y, 8, 256, None) == w4.EALIGN
+
+
+def test_moe_workspace_size_and_layout():
+    assert w4.moe_workspace_size(1, 2048, 512, 256, 8) > 0
+    assert w4.moe_workspace_size(1, 2000, 512, 256, 8) == 0          # H % 256
+    assert w4.moe_workspace_size(1, 2048, 512, 256, 0) == 0          # k < 1
+    assert w4.moe_workspace_size(1, 2048, 512, 5000, 8) == 0         # E > 4096
+    small = w4.moe_workspace_size(1, 2048, 512, 256, 8)
+    big = w4.moe_workspace_size(947, 2048, 512, 256, 8)
+    assert big > small
+    lay = w4.moe_workspace_layout(947, 2048, 512, 256, 8)
+    assert all(v % 256 == 0 for v in lay.values())
+    assert lay["hq"] - lay["h"] >= (947 * 9) * 512 * 4
+    with pytest.raises(w4.W4A8Error):
+        w4.moe_workspace_layout(3, 100, 512, 256, 8)
+
+
+def test_moe_argument_errors():
+    L = w4.lib()
+    f = L.moe_w4a8_forward
+    T, H, I, E, k = 2, 256, 256, 4, 2
+    ws = w4.moe_workspace_size(T, H, I, E, k)
+    p = _fake(A)
+    args = lambda **kw: [kw.get(n, p) for n in ("x", "ids", "w", "wgu", "wd", "sgu", "sd", "out")]
+    assert f(*args(x=None), T, H, I, E, k, p, ws, None) == w4.ENULL
+    assert f(*args(sgu=None), T, H, I, E, k, p, ws, None) == w4.ENULL      # one shared ptr alone
+    assert f(*args(), T, 255, I, E, k, p, ws, None) == w4.ESHAPE
+    assert f(*args(), T, H, 128, E, k, p, ws, None) == w4.ESHAPE
+    assert f(*args(), -1, H, I, E, k, p, ws, None) == w4.ESHAPE
+    assert f(*args(), T, H, I, E, 0, p, ws, None) == w4.ERANGE
+    assert f(*args(), T, H, I, E, 33, p, ws, None) == w4.ERANGE
+    assert f(*args(), T, H, I, 0, k, p, ws, None) == w4.ERANGE
+    assert f(*args(x=_fake(A + 8)), T, H, I, E, k, p, ws, None) == w4.EALIGN
+    assert f(*args(), T, H, I, E, k, p, ws - 1, None) == w4.EWORKSPACE
+    assert f(*args(), 0, H, I, E, k, p, ws, None) == w4.OK                 # empty: no-op

@@ -1,0 +1,247 @@
+"""GPU parity: every entry point of libw4a8, called through the C ABI, against
+the CPU oracle on the same seeded inputs.
+
+Bit-exact: Q8_0 and Q4_0 bytes, int32 block dots (through unit scales), the
+routing permutation and counts, and run-to-run determinism.  Floats: within
+1e-5 of sum |d_w d_a s| elementwise.  MoE layers: see tests/moe_check.py."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_24031_amd import synth
+import paper_2606_24031_amd as w4
+from tests import moe_check
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+DEV = "cuda"
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+# ------------------------------------------------------------------ quantizers
+def _activation_rows(g, rows, K):
+    x = synth.normal_f32(g, (rows, K))
+    x *= (2.0 ** g.integers(-8, 8, size=(rows, 1))).astype(np.float32)
+    x[g.random((rows, K)) < 0.01] = 0.0
+    return x
+
+
+def _special_rows(K):
+    rows = []
+    z = np.zeros(K, np.float32); rows.append(z)                              # zero blocks
+    t = np.zeros(K, np.float32); t[::32] = 127.0; t[1::32] = 0.5; t[2::32] = -2.5; t[3::32] = 63.5
+    rows.append(t)                                                          # exact .5 ties at d = 1
+    s = np.full(K, 1.0e-6, np.float32); s[::7] = -3.0e-6; rows.append(s)    # fp16-subnormal scale
+    u = np.full(K, 1e-40, np.float32); rows.append(u)                       # fp32 subnormal input
+    b = np.full(K, 8.0e6, np.float32); b[::3] = -1.0; rows.append(b)        # large scale
+    return np.stack(rows)
+
+
+@pytest.mark.parametrize("rows,K", [(1, 32), (3, 96), (7, 2048), (129, 512), (1000, 1024)])
+def test_q8_0_bit_exact(rows, K):
+    g = synth.rng(100 + rows)
+    x = np.concatenate([_activation_rows(g, rows, K), _special_rows(K)])
+    gpu = host(w4.q8_0_quantize(dev(x)))
+    assert np.array_equal(gpu, oracle.q8_0_quantize(x))
+
+
+@pytest.mark.parametrize("rows,K", [(1, 32), (5, 160), (64, 2048), (1023, 512)])
+def test_q4_0_bit_exact(rows, K):
+    g = synth.rng(200 + rows)
+    w = synth.normal_f32(g, (rows, K), 0.02)
+    specials = _special_rows(K)
+    specials[2] *= np.float32(0.05)   # |m|/8 below the fp16 normal range: low clamp
+    w = np.concatenate([w, specials, -specials])
+    gpu = host(w4.q4_0_quantize(dev(w)))
+    assert np.array_equal(gpu, oracle.q4_0_quantize(w))
+
+
+# ------------------------------------------------------------------ gemv
+@pytest.mark.parametrize("N,K", [(1024, 1024), (1, 256), (7, 768), (333, 2048),
+                                 (64, 16384), (5, 32768), (4097, 512)])
+def test_gemv_matches_oracle(N, K):
+    g = synth.rng(300 + N)
+    W = synth.normal_f32(g, (N, K), 0.02)
+    x = synth.normal_f32(g, (K,))
+    wq = w4.q4_0_quantize(dev(W))
+    xq = w4.q8_0_quantize(dev(x))
+    wq_ref, xq_ref = oracle.q4_0_quantize(W), oracle.q8_0_quantize(x)
+    assert np.array_equal(host(wq), wq_ref) and np.array_equal(host(xq), xq_ref)
+    y = host(w4.q4q8_gemv(wq, xq, N, K))
+    y_ref, R = oracle.gemv(wq_ref, xq_ref, N, K)
+    assert np.all(np.abs(y - y_ref) <= 1e-5 * R)
+
+
+@pytest.mark.parametrize("N,K", [(256, 2048), (33, 1024)])
+def test_gemv_unit_scales_give_exact_integer_dots(N, K):
+    """With every scale 1.0 each partial sum is an integer below 2^24, so the
+    fp32 result equals the int32 block-dot sum exactly, in any order."""
+    g = synth.rng(400 + N)
+    w = synth.q4_0_random_blocks(g, N, K).reshape(N, K // 32, 18)
+    w[:, :, 0:2] = np.array([0x3C00], np.uint16).view(np.uint8)
+    xq = oracle.q8_0_quantize(synth.normal_f32(g, (K,))).reshape(K // 32, 34)
+    xq[:, 0:2] = np.array([0x3C00], np.uint16).view(np.uint8)
+    y = host(w4.q4q8_gemv(dev(w), dev(xq), N, K))
+    y_ref, _ = oracle.gemv(w, xq, N, K)
+    assert np.array_equal(y.astype(np.float64), y_ref)
+
+
+def test_gemv_zero_codes_give_zero():
+    N, K = 100, 512
+    w = np.zeros((N, K // 32, 18), np.uint8)
+    w[:, :, 0:2] = np.array([0x2E66], np.uint16).view(np.uint8)
+    w[:, :, 2:] = 0x88
+    g = synth.rng(5)
+    xq = w4.q8_0_quantize(dev(synth.normal_f32(g, (K,))))
+    assert not host(w4.q4q8_gemv(dev(w), xq, N, K)).any()
+
+
+# ------------------------------------------------------------------ MoE layer
+class Layer:
+    def __init__(self, seed, H, I, E, shared=True):
+        g = synth.rng(seed)
+        self.H, self.I, self.E = H, I, E
+        self.w_gu = synth.q4_0_random_blocks(g, E * 2 * I, H)
+        self.w_d = synth.q4_0_random_blocks(g, E * H, I)
+        self.ws_gu = synth.q4_0_random_blocks(g, 2 * I, H) if shared else None
+        self.ws_d = synth.q4_0_random_blocks(g, H, I) if shared else None
+        self.d_gu, self.d_d = dev(self.w_gu), dev(self.w_d)
+        self.d_sgu = dev(self.ws_gu) if shared else None
+        self.d_sd = dev(self.ws_d) if shared else None
+        self.g = g
+
+    def run(self, x, ids, wts, k, ws=None):
+        T = x.shape[0]
+        if ws is None:
+            ws = w4.moe_workspace(T, self.H, self.I, self.E, k)
+        out = w4.moe_forward(dev(x), dev(ids), dev(wts), self.d_gu, self.d_d, self.d_sgu,
+                             self.d_sd, self.H, self.I, self.E, k, ws)
+        lay = w4.moe_workspace_layout(T, self.H, self.I, self.E, k)
+        P = T * k + T
+        wsn = host(ws)
+        h = wsn[lay["h"]:lay["h"] + P * self.I * 4].view(np.float32).reshape(P, self.I)
+        hq = wsn[lay["hq"]:lay["hq"] + P * (self.I // 32) * 34].reshape(P, -1)
+        perm = wsn[lay["perm"]:lay["perm"] + P * 4].view(np.int32)
+        count = wsn[lay["count"]:lay["count"] + self.E * 4].view(np.int32)
+        return host(out), h, hq, perm, count, ws
+
+    def check(self, x, ids, wts, k, out, h, hq):
+        return moe_check.check_layer(out, h, hq, x, ids, wts, self.w_gu, self.w_d, self.ws_gu,
+                                     self.ws_d, self.H, self.I, self.E, k)
+
+
+def _check_route(ids, E, shared, perm, count):
+    T, k = ids.shape
+    flat = ids.ravel()
+    valid = (flat >= 0) & (flat < E)
+    assert np.array_equal(count, np.bincount(flat[valid], minlength=E)[:E])
+    order = np.argsort(np.where(valid, flat, E), kind="stable")[: valid.sum()]
+    nr = valid.sum()
+    assert np.array_equal(perm[:nr], order)
+    if shared:
+        assert np.array_equal(perm[nr:nr + T], T * k + np.arange(T))
+
+
+@pytest.fixture(scope="module")
+def small_layer():
+    return Layer(7, 256, 256, 4)
+
+
+def test_moe_small_with_special_routing(small_layer):
+    L = small_layer
+    g = synth.rng(8)
+    T, k = 6, 3
+    x = synth.normal_f32(g, (T, L.H))
+    ids, wts = synth.routing(g, T, L.E, k)
+    ids[1, 2] = -1                 # skipped slot
+    ids[2, 1] = ids[2, 0]          # duplicate expert in one token
+    ids[3, :] = 2                  # all slots on one expert
+    ids[4, 0] = 99                 # id >= E: skipped
+    wts[5, :] = 0.0                # shared expert only
+    out, h, hq, perm, count, _ = L.run(x, ids, wts, k)
+    _check_route(ids, L.E, True, perm, count)
+    ids_o = ids.copy(); ids_o[ids_o >= L.E] = -1
+    L.check(x, ids_o, wts, k, out, h, hq)
+
+
+def test_moe_no_shared_expert():
+    L = Layer(9, 512, 256, 3, shared=False)
+    g = synth.rng(10)
+    T, k = 9, 2
+    x = synth.normal_f32(g, (T, L.H))
+    ids, wts = synth.routing(g, T, L.E, k)
+    out, h, hq, perm, count, _ = L.run(x, ids, wts, k)
+    _check_route(ids, L.E, False, perm, count)
+    L.check(x, ids, wts, k, out, h, hq)
+
+
+def test_moe_ragged_group_count_and_odd_K():
+    """H = I = 768 (three 8-block groups per row, not a power of two)."""
+    L = Layer(11, 768, 768, 5)
+    g = synth.rng(12)
+    T, k = 7, 2
+    x = synth.normal_f32(g, (T, L.H))
+    ids, wts = synth.routing(g, T, L.E, k)
+    out, h, hq, perm, count, _ = L.run(x, ids, wts, k)
+    L.check(x, ids, wts, k, out, h, hq)
+
+
+@pytest.fixture(scope="module")
+def qwen_layer():
+    """H=2048, I=512, 256 routed experts + 1 shared (the paper's layer shape)."""
+    return Layer(0, 2048, 512, 256)
+
+
+def test_moe_decode_m1(qwen_layer):
+    L = qwen_layer
+    g = synth.rng(20)
+    x = synth.normal_f32(g, (1, L.H))
+    ids, wts = synth.routing(g, 1, L.E, 8)
+    out, h, hq, perm, count, ws = L.run(x, ids, wts, 8)
+    _check_route(ids, L.E, True, perm, count)
+    st = L.check(x, ids, wts, 8, out, h, hq)
+    assert st["pairs"] == 9
+    # same workspace again: identical bytes
+    out2, *_ = L.run(x, ids, wts, 8, ws=ws)
+    assert np.array_equal(out, out2)
+
+
+def test_moe_decode_m32(qwen_layer):
+    L = qwen_layer
+    g = synth.rng(21)
+    x = synth.normal_f32(g, (32, L.H))
+    ids, wts = synth.routing(g, 32, L.E, 8)
+    out, h, hq, perm, count, _ = L.run(x, ids, wts, 8)
+    _check_route(ids, L.E, True, perm, count)
+    L.check(x, ids, wts, 8, out, h, hq)
+
+
+def test_moe_prefill_947_sampled_tokens(qwen_layer):
+    L = qwen_layer
+    g = synth.rng(22)
+    T, k = 947, 8
+    x = synth.normal_f32(g, (T, L.H))
+    ids, wts = synth.routing(g, T, L.E, k, bias_std=1.0)
+    out, h, hq, perm, count, ws = L.run(x, ids, wts, k)
+    _check_route(ids, L.E, True, perm, count)
+    # tokens through the heaviest expert, the first and last token, and a few more
+    heavy = int(np.argmax(count))
+    through_heavy = np.nonzero((ids == heavy).any(axis=1))[0]
+    tokens = sorted(set([0, T - 1] + through_heavy[:4].tolist() + through_heavy[-2:].tolist()
+                        + g.choice(T, 8, replace=False).tolist()))
+    o, hh, qq, Ts = moe_check.gather_tokens(tokens, T, k, out, h, hq)
+    L.check(x[tokens], ids[tokens], wts[tokens], k, o, hh, qq)
+    out2, *_ = L.run(x, ids, wts, k, ws=ws)
+    assert np.array_equal(out, out2)
