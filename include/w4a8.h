@@ -116,7 +116,8 @@ int moe_w4a8_workspace_init(void *workspace, size_t ws_bytes, void *stream);
  *   W4A8_WS_HQ    Q8_0(h), [P][I/32] blocks.
  *   W4A8_WS_PERM  int32 [T*k + T]: pairs sorted by expert (stable in pair
  *                 index), routed pairs first, then the T shared pairs.
- *   W4A8_WS_COUNT int32 [E]: routed pairs per expert.
+ *   W4A8_WS_COUNT int32 [E]: routed pairs per expert (not written when T == 1).
+ *   W4A8_WS_SYNC  synchronisation words: zero before and after every call.
  * Pair numbering: routed slot j of token t is pair t*k + j; the shared expert
  * of token t is pair T*k + t.  Rows of skipped slots are not written.
  */
@@ -125,7 +126,8 @@ int moe_w4a8_workspace_init(void *workspace, size_t ws_bytes, void *stream);
 #define W4A8_WS_HQ     2
 #define W4A8_WS_PERM   3
 #define W4A8_WS_COUNT  4
-#define W4A8_WS_NFIELDS 5
+#define W4A8_WS_SYNC   5
+#define W4A8_WS_NFIELDS 6
 int moe_w4a8_workspace_layout(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
                               size_t *offsets);
 

@@ -135,6 +135,9 @@ class Layer:
         hq = wsn[lay["hq"]:lay["hq"] + P * (self.I // 32) * 34].reshape(P, -1)
         perm = wsn[lay["perm"]:lay["perm"] + P * 4].view(np.int32)
         count = wsn[lay["count"]:lay["count"] + self.E * 4].view(np.int32)
+        assert not wsn[lay["sync"]:lay["sync_end"]].any(), "sync words not back to zero"
+        xq = wsn[lay["xq"]:lay["xq"] + T * (self.H // 32) * 34].reshape(T, -1)
+        assert np.array_equal(xq, oracle.q8_0_quantize(x)), "workspace Q8_0(x)"
         return host(out), h, hq, perm, count, ws
 
     def check(self, x, ids, wts, k, out, h, hq):
@@ -210,12 +213,65 @@ def test_moe_decode_m1(qwen_layer):
     x = synth.normal_f32(g, (1, L.H))
     ids, wts = synth.routing(g, 1, L.E, 8)
     out, h, hq, perm, count, ws = L.run(x, ids, wts, 8)
-    _check_route(ids, L.E, True, perm, count)
     st = L.check(x, ids, wts, 8, out, h, hq)
     assert st["pairs"] == 9
     # same workspace again: identical bytes
     out2, *_ = L.run(x, ids, wts, 8, ws=ws)
     assert np.array_equal(out, out2)
+
+
+def test_moe_decode_m1_many_steps_one_workspace(qwen_layer):
+    """Back-to-back single-token calls on one workspace with fresh routing,
+    including skipped slots and a repeated expert: the in-kernel counters must
+    return to zero after every call."""
+    L = qwen_layer
+    g = synth.rng(23)
+    ws = w4.moe_workspace(1, L.H, L.I, L.E, 8)
+    for step in range(6):
+        x = synth.normal_f32(g, (1, L.H))
+        ids, wts = synth.routing(g, 1, L.E, 8)
+        if step == 2:
+            ids[0, 3] = -1
+        if step == 3:
+            ids[0, 5] = ids[0, 1]
+        if step == 4:
+            ids[0, :] = -1
+        out, h, hq, _, _, _ = L.run(x, ids, wts, 8, ws=ws)
+        L.check(x, ids, wts, 8, out, h, hq)
+
+
+def test_moe_decode_m1_wait_fallback(qwen_layer, monkeypatch):
+    """Force the bounded wait of the single-launch decode kernel to expire at
+    once (spin limit 0 set from the host): every down-projection workgroup
+    then computes its pair's h itself.  Same bytes as the normal path, and the
+    counters still return to zero."""
+    L = qwen_layer
+    g = synth.rng(24)
+    x = synth.normal_f32(g, (1, L.H))
+    ids, wts = synth.routing(g, 1, L.E, 8)
+    ws = w4.moe_workspace(1, L.H, L.I, L.E, 8)
+    out, h, hq, *_ = L.run(x, ids, wts, 8, ws=ws)
+    monkeypatch.setenv("W4A8_DECODE_SPIN_TICKS", "0")
+    out_fb, h_fb, hq_fb, *_ = L.run(x, ids, wts, 8, ws=ws)
+    monkeypatch.delenv("W4A8_DECODE_SPIN_TICKS")
+    assert np.array_equal(out, out_fb) and np.array_equal(hq, hq_fb)
+    L.check(x, ids, wts, 8, out_fb, h_fb, hq_fb)
+    x2 = synth.normal_f32(g, (1, L.H))
+    ids2, wts2 = synth.routing(g, 1, L.E, 8)
+    out2, h2, hq2, *_ = L.run(x2, ids2, wts2, 8, ws=ws)
+    L.check(x2, ids2, wts2, 8, out2, h2, hq2)
+
+
+def test_moe_decode_m1_no_shared_small_shapes():
+    """Single-token path at other shapes: H = 768 (three 8-block groups per
+    row), I = 256, no shared expert, k = 3."""
+    L = Layer(25, 768, 256, 6, shared=False)
+    g = synth.rng(26)
+    for _ in range(3):
+        x = synth.normal_f32(g, (1, L.H))
+        ids, wts = synth.routing(g, 1, L.E, 3)
+        out, h, hq, *_ = L.run(x, ids, wts, 3)
+        L.check(x, ids, wts, 3, out, h, hq)
 
 
 def test_moe_decode_m32(qwen_layer):
