@@ -1,0 +1,303 @@
+#!/usr/bin/env python3
+"""Throughput of the W4A8 MoE layer on one MI355X.
+
+Headline workload (one "step" = one whole MoE layer at decode M = 1: Q8_0 of
+the token, routing, gate/up W4A8 GEMV, SiLU * up, Q8_0(h), down W4A8 GEMV,
+weighted combine with the shared expert): hidden 2048, expert intermediate
+512, 256 routed experts + 1 shared, top-8 from softmax of N(0,1) router
+logits, Q4_0 expert weights quantized from N(0, 0.02^2), fp32 hidden ~ N(0,1).
+
+Timing: eight distinct layers (3.6 GB of Q4_0) are cycled with fresh routing
+and a fresh token every step, so the experts a step touches are not resident
+in the 256 MB last-level cache; all inputs are in HBM before the timed region;
+the K steps are captured in one HIP graph and replayed once between HIP events
+recorded on the stream the kernels run on.  `value` is algorithmic bytes
+(Q4_0 bytes of the distinct experts each step touches, plus the fp32 token in
+and out, ids and weights) / time, in GB/s.
+
+The line also carries the 947-token prefill of the same layer (router bias
+~ N(0,1)) in tokens/s per layer, the roofline of the dominant kernel, and the
+CPU oracle timed on this host on a bounded sample of the decode workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+H, I, E, K_TOP = 2048, 512, 256, 8
+EXPERT_BYTES = (2 * I * (H // 32) + H * (I // 32)) * 18   # 1,769,472
+HBM_PEAK_GBPS = 8000.0
+METRIC = "MoE-layer W4A8 GEMV GB/s (% HBM peak) at M=1; prefill tokens/s per layer"
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2000)
+    ap.add_argument("--warmup", type=int, default=100)
+    ap.add_argument("--layers", type=int, default=8, help="distinct weight sets cycled")
+    ap.add_argument("--prefill-steps", type=int, default=8)
+    ap.add_argument("--no-prefill", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true", help="launch steps eagerly")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--seed", type=int, default=0)
+    return ap.parse_args()
+
+
+def make_layer(torch, w4, gen, dev):
+    """One layer's Q4_0 weights from N(0, 0.02^2) fp32, quantized on the GPU
+    by the library's Q4_0 kernel, 16 experts at a time."""
+    w_gu = torch.empty((E, 2 * I, H // 32 * 18), dtype=torch.uint8, device=dev)
+    w_d = torch.empty((E, H, I // 32 * 18), dtype=torch.uint8, device=dev)
+    chunk = 16
+    for e0 in range(0, E, chunk):
+        f = torch.randn((chunk * 2 * I, H), generator=gen, device=dev) * 0.02
+        w4.q4_0_quantize(f, out=w_gu[e0:e0 + chunk].view(chunk * 2 * I, -1))
+        f = torch.randn((chunk * H, I), generator=gen, device=dev) * 0.02
+        w4.q4_0_quantize(f, out=w_d[e0:e0 + chunk].view(chunk * H, -1))
+    s_gu = w4.q4_0_quantize(torch.randn((2 * I, H), generator=gen, device=dev) * 0.02)
+    s_d = w4.q4_0_quantize(torch.randn((H, I), generator=gen, device=dev) * 0.02)
+    return w_gu, w_d, s_gu, s_d
+
+
+def step_bytes(ids_row) -> int:
+    distinct = len({int(e) for e in ids_row if 0 <= e < E})
+    return (distinct + 1) * EXPERT_BYTES + 2 * H * 4 * (len(ids_row) // K_TOP) + ids_row.size * 8
+
+
+def source_sha(files) -> str:
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+DECODE_SOURCES = ["paper_2606_24031_amd/csrc/decode.hip", "paper_2606_24031_amd/csrc/w4a8_dev.h"]
+
+
+def measured_traffic():
+    """HBM bytes per launch of the decode kernel from the committed rocprofv3
+    PMC summary, if it was taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", "decode_m1_hbm_traffic.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m_sha = re.search(r"source_sha:\s*([0-9a-f]+)", text)
+    m_val = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not m_sha or not m_val or m_sha.group(1) != source_sha(DECODE_SOURCES):
+        return None
+    return float(m_val.group(1))
+
+
+def bench_decode(torch, w4, synth, layers, args, dev):
+    rng = synth.rng(args.seed + 1)
+    nsteps = args.steps
+    total = nsteps + args.warmup
+    ids_all, wts_all = synth.routing(rng, total, E, K_TOP)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(args.seed + 2)
+    x_all = torch.randn((total, 1, H), generator=gen, device=dev)
+    ids_d = torch.from_numpy(ids_all).to(dev).view(total, 1, K_TOP)
+    wts_d = torch.from_numpy(wts_all).to(dev).view(total, 1, K_TOP)
+    ws = w4.moe_workspace(1, H, I, E, K_TOP, device=dev)
+    out = torch.empty((1, H), dtype=torch.float32, device=dev)
+
+    def step(i):
+        L = layers[i % len(layers)]
+        w4.moe_forward(x_all[i], ids_d[i], wts_d[i], L[0], L[1], L[2], L[3], H, I, E, K_TOP,
+                       ws, out=out)
+
+    log(f"decode: warmup {args.warmup} steps")
+    for i in range(args.warmup):
+        step(nsteps + i)
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    if args.no_graph:
+        torch.cuda.synchronize()
+        ev0.record()
+        for i in range(nsteps):
+            step(i)
+        ev1.record()
+        torch.cuda.synchronize()
+    else:
+        log(f"decode: capturing {nsteps} steps in a HIP graph")
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for i in range(nsteps):
+                step(i)
+        graph.replay()   # untimed first replay
+        torch.cuda.synchronize()
+        log("decode: timed replay")
+        ev0.record()
+        graph.replay()
+        ev1.record()
+        torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1)
+    nbytes = sum(step_bytes(ids_all[i]) for i in range(nsteps))
+    return ms, nbytes
+
+
+def bench_prefill(torch, w4, synth, layers, args, dev):
+    T = 947
+    rng = synth.rng(args.seed + 3)
+    n = args.prefill_steps
+    ids_l, wts_l, byts = [], [], []
+    for _ in range(n + 2):
+        ids, wts = synth.routing(rng, T, E, K_TOP, bias_std=1.0)
+        ids_l.append(torch.from_numpy(ids).to(dev))
+        wts_l.append(torch.from_numpy(wts).to(dev))
+        touched = len(set(ids.ravel().tolist()))
+        byts.append((touched + 1) * EXPERT_BYTES + 2 * T * H * 4 + ids.size * 8)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(args.seed + 4)
+    xs = [torch.randn((T, H), generator=gen, device=dev) for _ in range(n + 2)]
+    ws = w4.moe_workspace(T, H, I, E, K_TOP, device=dev)
+    out = torch.empty((T, H), dtype=torch.float32, device=dev)
+
+    def step(i):
+        L = layers[i % len(layers)]
+        w4.moe_forward(xs[i], ids_l[i], wts_l[i], L[0], L[1], L[2], L[3], H, I, E, K_TOP, ws,
+                       out=out)
+
+    log(f"prefill 947 tokens: warmup 2, timed {n}")
+    step(n)
+    step(n + 1)
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for i in range(n):
+        step(i)
+    ev1.record()
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / n
+    return {"tokens": T, "ms_per_layer": round(ms, 4),
+            "tokens_per_s_per_layer": round(T / (ms / 1e3), 1),
+            "GBps": round(sum(byts[:n]) / n / (ms / 1e3) / 1e9, 1),
+            "hbm_peak_frac": round(sum(byts[:n]) / n / (ms / 1e3) / 1e9 / HBM_PEAK_GBPS, 4)}
+
+
+def physical_threads_note():
+    try:
+        out = os.popen("lscpu").read()
+        soc = int(re.search(r"Socket\(s\):\s+(\d+)", out).group(1))
+        cps = int(re.search(r"Core\(s\) per socket:\s+(\d+)", out).group(1))
+        return soc * cps
+    except Exception:
+        return None
+
+
+def cpu_baseline(synth, seconds):
+    """The oracle on this host: independent single-token decode steps of the
+    same layer shape, OpenMP across tokens, until `seconds` have elapsed."""
+    import numpy as np
+    import oracle
+    g = synth.rng(7)
+    # eight random experts' bytes tiled over the 256 (timing does not depend
+    # on the values; keeps host generation short)
+    gu8 = synth.q4_0_random_blocks(g, 8 * 2 * I, H).reshape(8, 2 * I, -1)
+    d8 = synth.q4_0_random_blocks(g, 8 * H, I).reshape(8, H, -1)
+    w_gu = np.ascontiguousarray(np.tile(gu8, (E // 8, 1, 1)))
+    w_d = np.ascontiguousarray(np.tile(d8, (E // 8, 1, 1)))
+    s_gu, s_d = gu8[0].copy(), d8[0].copy()
+    threads = oracle.threads()
+    batch = max(1, threads)
+    done_tokens, done_bytes, t_used = 0, 0, 0.0
+    while t_used < seconds:
+        x = synth.normal_f32(g, (batch, H))
+        ids, wts = synth.routing(g, batch, E, K_TOP)
+        t0 = time.perf_counter()
+        oracle.moe(x, ids, wts, w_gu, w_d, s_gu, s_d, H, I, E, K_TOP, want_intermediates=False)
+        t_used += time.perf_counter() - t0
+        done_tokens += batch
+        done_bytes += sum(step_bytes(ids[t]) for t in range(batch))
+    return {"value": round(done_bytes / t_used / 1e9, 3), "unit": "GB/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"{done_tokens} independent M=1 decode steps of the same layer shape "
+                      f"(256+1 experts, top-8), {t_used:.1f} s, OpenMP across tokens, "
+                      f"{physical_threads_note()} physical cores on this host"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the layer runs "
+              "on a single MI355X and no multi-GPU path is part of this build.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2606_24031_amd as w4
+    from paper_2606_24031_amd import synth
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    log(f"generating {args.layers} layers of Q4_0 weights on the GPU")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(args.seed)
+    layers = [make_layer(torch, w4, gen, dev) for _ in range(args.layers)]
+    torch.cuda.synchronize()
+
+    ms, nbytes = bench_decode(torch, w4, synth, layers, args, dev)
+    ms_step = ms / args.steps
+    gbps = nbytes / (ms / 1e3) / 1e9
+    bytes_per_launch = nbytes / args.steps
+    log(f"decode: {ms_step * 1e3:.2f} us/step, {gbps:.0f} GB/s")
+
+    prefill = None
+    if not args.no_prefill:
+        prefill = bench_prefill(torch, w4, synth, layers, args, dev)
+        log(f"prefill: {prefill}")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log(f"cpu baseline: oracle for ~{args.cpu_seconds:.0f} s")
+        cpu = cpu_baseline(synth, args.cpu_seconds)
+        log(f"cpu baseline: {cpu}")
+
+    traffic = measured_traffic()
+    rec = {
+        "metric": METRIC,
+        "value": round(gbps, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int8",
+        "data": "synthetic",
+        "config": {"workload": "moe_layer_decode_m1", "T": 1, "hidden": H, "expert_intermediate": I,
+                   "routed_experts": E, "top_k": K_TOP, "shared_experts": 1,
+                   "weight_sets_cycled": args.layers,
+                   "launch": "eager" if args.no_graph else "hipGraph",
+                   "bytes_per_step": round(bytes_per_launch)},
+        "roofline": {"bound": "hbm", "kernel": "decode_kernel (whole layer, one launch per step)",
+                     "achieved": round(bytes_per_launch / (ms_step / 1e3) / 1e9, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(bytes_per_launch / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBPS, 4),
+                     "traffic": traffic},
+        "cpu_baseline": cpu,
+        "prefill_947": prefill,
+    }
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -64,6 +64,7 @@ def _load():
     lib.orc_moe.restype = ctypes.c_int
     lib.orc_q8_0_candidates.argtypes = [P, P, I64, P, P, P, P]
     lib.orc_q8_0_candidates.restype = ctypes.c_int
+    lib.orc_threads.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -74,6 +75,11 @@ def _ptr(a):
 
 def _c(a, dtype):
     return np.ascontiguousarray(a, dtype=dtype)
+
+
+def threads() -> int:
+    """OpenMP threads the oracle's parallel loops use (OMP_NUM_THREADS)."""
+    return int(_load().orc_threads())
 
 
 # ---------------------------------------------------------------- fp16

@@ -41,6 +41,7 @@
  * "parity unpinned": they are covered by the float tolerance only.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -413,4 +414,16 @@ int orc_q8_0_candidates(const float *h, const float *dh, int64_t K,
         }
     }
     return rc;
+}
+
+/* Number of OpenMP threads the parallel loops above use. */
+int orc_threads(void)
+{
+    int n = 1;
+    #pragma omp parallel
+    {
+        #pragma omp single
+        n = omp_get_num_threads();
+    }
+    return n;
 }

@@ -18,7 +18,12 @@
 // The wait is bounded: after `spin_limit` ticks of the 100 MHz real-time
 // counter a B item computes the pair's h itself (the same code, so the same
 // bytes), so progress never depends on the order in which the hardware starts
-// workgroups.  Counters return to zero when the call completes: every
+// workgroups.  Hand-off data (h, the per-pair y) crosses XCDs through
+// agent-coherent (sc1) stores and loads: a writer waits until its stores are
+// acknowledged (vmcnt 0) before the workgroup barrier and the counter add, a
+// reader polls the counter and then reads with sc1 loads, so no whole-L2
+// writeback or invalidate is needed.  Counters return to zero when the call
+// completes: every
 // arrival adds to a per-pair word (A items +1, B items +0x10000) and the
 // arrival that completes the total clears it; the per-slab combine counter is
 // cleared by its last arrival.
@@ -62,12 +67,29 @@ __device__ __forceinline__ bool pair_valid(const DecodeArgs &a, int q, int &expe
 
 __device__ __forceinline__ float silu_f32(float g) { return g / (1.0f + expf(-g)); }
 
-__device__ __forceinline__ uint32_t atomic_add_acq_rel(uint32_t *p, uint32_t v) {
-  return __hip_atomic_fetch_add(p, v, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+__device__ __forceinline__ uint32_t counter_add(uint32_t *p, uint32_t v) {
+  return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+__device__ __forceinline__ uint32_t counter_load(const uint32_t *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void counter_clear(uint32_t *p) {
+  __hip_atomic_store(p, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// agent-coherent (sc1) store and load of hand-off data
+__device__ __forceinline__ void st_agent(float *p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_agent(const float *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// wait until this wave's stores are acknowledged (s_waitcnt vmcnt(0))
+__device__ __forceinline__ void wait_stores() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 // Q8_0 of n contiguous fp32 values (n % 32 == 0) from global memory into LDS,
-// 8 lanes per block.
+// 8 lanes per block.  COHERENT: read with agent-coherent loads (data another
+// workgroup wrote during this launch).
+template <bool COHERENT>
 __device__ void quantize_to_lds(const float *__restrict__ src, uint8_t *lds, int n) {
   const int tasks = n / 4;  // 8 lanes x 4 values per block
   for (int t0 = 0; t0 < tasks; t0 += NT) {
@@ -75,8 +97,13 @@ __device__ void quantize_to_lds(const float *__restrict__ src, uint8_t *lds, int
     const bool live = t < tasks;   // tasks % 8 == 0: whole 8-lane groups agree
     float v[4] = {0.f, 0.f, 0.f, 0.f};
     if (live) {
-      const float4 f = reinterpret_cast<const float4 *>(src)[t];
-      v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
+      if (COHERENT) {
+#pragma unroll
+        for (int i = 0; i < 4; i++) v[i] = ld_agent(src + 4 * t + i);
+      } else {
+        const float4 f = reinterpret_cast<const float4 *>(src)[t];
+        v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
+      }
     }
     uint32_t d16;
     const uint32_t packed = q8_0_block8(v, d16);
@@ -130,7 +157,7 @@ __device__ __forceinline__ void store_h(const DecodeArgs &a, int q, int c0, cons
   constexpr int HC = 128 / LPR;
   if (threadIdx.x < HC) {
     const float hv = silu_f32(shrow[threadIdx.x]) * shrow[HC + threadIdx.x];
-    a.h[(int64_t)q * a.I + c0 + threadIdx.x] = hv;
+    st_agent(a.h + (int64_t)q * a.I + c0 + threadIdx.x, hv);
   }
 }
 
@@ -151,7 +178,7 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
     int e;
     if (!pair_valid(a, q, e)) {
       if (item == 0) {                              // workspace copy of Q8_0(x)
-        quantize_to_lds(a.x, lds, a.H);
+        quantize_to_lds<false>(a.x, lds, a.H);
         __syncthreads();
         for (int i = threadIdx.x; i < (a.H / 32) * Q8B / 2; i += NT)
           reinterpret_cast<uint16_t *>(a.xq)[i] = reinterpret_cast<const uint16_t *>(lds)[i];
@@ -163,7 +190,7 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
     W8 wpre;
     load_gateup_pre<LPRA>(a, W, c0, wpre);          // weight loads in flight first
     uint8_t *xq_lds = lds;
-    quantize_to_lds(a.x, xq_lds, a.H);
+    quantize_to_lds<false>(a.x, xq_lds, a.H);
     __syncthreads();
     if (item == 0)                                  // workspace copy of Q8_0(x)
       for (int i = threadIdx.x; i < (a.H / 32) * Q8B / 2; i += NT)
@@ -171,12 +198,12 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
     gateup_rows<LPRA>(a, W, c0, xq_lds, wpre, shrow);
     __syncthreads();
     store_h<LPRA>(a, q, c0, shrow);
-    __threadfence();
+    wait_stores();
     __syncthreads();
     if (threadIdx.x == 0) {
       const uint32_t total = (uint32_t)a.n_a + ((uint32_t)a.n_b << 16);
-      const uint32_t old = atomic_add_acq_rel(&a.pair_cnt[q], 1u);
-      if (old + 1u == total) __hip_atomic_store(&a.pair_cnt[q], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const uint32_t old = counter_add(&a.pair_cnt[q], 1u);
+      if (old + 1u == total) counter_clear(&a.pair_cnt[q]);
     }
     return;
   }
@@ -208,7 +235,7 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
     const uint64_t t0 = wall_clock64();
     int ok = 0;
     for (;;) {
-      const uint32_t v = __hip_atomic_load(&a.pair_cnt[q], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+      const uint32_t v = counter_load(&a.pair_cnt[q]);
       if ((v & 0xFFFFu) >= (uint32_t)a.n_a) { ok = 1; break; }
       if ((int64_t)(wall_clock64() - t0) > a.spin_limit) break;
       __builtin_amdgcn_s_sleep(2);
@@ -220,7 +247,7 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
     // fallback: compute every h slab of this pair here (same code, same bytes)
     const uint8_t *W = (e < a.E) ? a.w_gu + (int64_t)e * (2 * a.I) * (a.H / 256) * (8 * Q4B) : a.ws_gu;
     uint8_t *xq_lds = lds;
-    quantize_to_lds(a.x, xq_lds, a.H);
+    quantize_to_lds<false>(a.x, xq_lds, a.H);
     __syncthreads();
     for (int s = 0; s < a.n_a; s++) {
       W8 w;
@@ -230,14 +257,13 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
       store_h<LPRA>(a, q, s * HC, shrow);
       __syncthreads();
     }
-    __threadfence();
+    wait_stores();
     __syncthreads();
   }
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 
   // Q8_0(h) of the pair into LDS; the first slab also stores it to the workspace
   uint8_t *hq_lds = lds;
-  quantize_to_lds(a.h + (int64_t)q * a.I, hq_lds, a.I);
+  quantize_to_lds<true>(a.h + (int64_t)q * a.I, hq_lds, a.I);
   __syncthreads();
   if (slab == 0)
     for (int i = threadIdx.x; i < (a.I / 32) * Q8B / 2; i += NT)
@@ -259,26 +285,25 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
   }
   acc = lane_group_sum<LPRB>(acc);
   const float wq = (q < a.k) ? a.topk_w[q] : 1.0f;
-  if (li == 0) a.y[(int64_t)q * a.H + n] = wq * acc;
-  __threadfence();
+  if (li == 0) st_agent(a.y + (int64_t)q * a.H + n, wq * acc);
+  wait_stores();
   __syncthreads();
   if (threadIdx.x == 0) {
     const uint32_t total = (uint32_t)a.n_a + ((uint32_t)a.n_b << 16);
-    const uint32_t old = atomic_add_acq_rel(&a.pair_cnt[q], 0x10000u);
-    if (old + 0x10000u == total) __hip_atomic_store(&a.pair_cnt[q], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const uint32_t prev = atomic_add_acq_rel(&a.slab_cnt[slab], 1u);
+    const uint32_t old = counter_add(&a.pair_cnt[q], 0x10000u);
+    if (old + 0x10000u == total) counter_clear(&a.pair_cnt[q]);
+    const uint32_t prev = counter_add(&a.slab_cnt[slab], 1u);
     flag = (prev + 1u == (uint32_t)nvalid) ? 1 : 0;
-    if (flag) __hip_atomic_store(&a.slab_cnt[slab], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (flag) counter_clear(&a.slab_cnt[slab]);
   }
   __syncthreads();
   if (!flag) return;
   // last pair to finish this slab: out = sum over slots in order, then shared
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   for (int i = threadIdx.x; i < RB; i += NT) {
     float s = 0.0f;
     for (int j = 0; j < npairs; j++) {
       int ej;
-      if (pair_valid(a, j, ej)) s += a.y[(int64_t)j * a.H + (int64_t)slab * RB + i];
+      if (pair_valid(a, j, ej)) s += ld_agent(a.y + (int64_t)j * a.H + (int64_t)slab * RB + i);
     }
     a.out[(int64_t)slab * RB + i] = s;
   }
