@@ -117,7 +117,8 @@ int moe_w4a8_workspace_init(void *workspace, size_t ws_bytes, void *stream);
  *   W4A8_WS_PERM  int32 [T*k + T]: pairs sorted by expert (stable in pair
  *                 index), routed pairs first, then the T shared pairs.
  *   W4A8_WS_COUNT int32 [E]: routed pairs per expert (not written when T == 1).
- *   W4A8_WS_SYNC  synchronisation words: zero before and after every call.
+ *   W4A8_WS_SYNC  start of the synchronisation words, which end at
+ *                 W4A8_WS_SYNC_END: zero before and after every call.
  * Pair numbering: routed slot j of token t is pair t*k + j; the shared expert
  * of token t is pair T*k + t.  Rows of skipped slots are not written.
  */
@@ -127,7 +128,8 @@ int moe_w4a8_workspace_init(void *workspace, size_t ws_bytes, void *stream);
 #define W4A8_WS_PERM   3
 #define W4A8_WS_COUNT  4
 #define W4A8_WS_SYNC   5
-#define W4A8_WS_NFIELDS 6
+#define W4A8_WS_SYNC_END 6
+#define W4A8_WS_NFIELDS 7
 int moe_w4a8_workspace_layout(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
                               size_t *offsets);
 

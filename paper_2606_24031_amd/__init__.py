@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(HERE, "libw4a8.so")
 OK, ENULL, ESHAPE, ERANGE, EWORKSPACE, EALIGN, EHIP, EDEVICE = 0, -1, -2, -3, -4, -5, -6, -7
 Q4_0_BLOCK_BYTES = 18
 Q8_0_BLOCK_BYTES = 34
-WS_XQ, WS_H, WS_HQ, WS_PERM, WS_COUNT, WS_SYNC, WS_NFIELDS = 0, 1, 2, 3, 4, 5, 6
+WS_XQ, WS_H, WS_HQ, WS_PERM, WS_COUNT, WS_SYNC, WS_SYNC_END, WS_NFIELDS = 0, 1, 2, 3, 4, 5, 6, 7
 
 EXPORTS = ("w4a8_strerror", "q8_0_quantize", "q4_0_quantize", "q4q8_gemv",
            "moe_w4a8_workspace_size", "moe_w4a8_workspace_init",
@@ -137,7 +137,7 @@ def moe_workspace_layout(T, H, I, E, k) -> dict:
     offs = (ctypes.c_size_t * WS_NFIELDS)()
     _check(lib().moe_w4a8_workspace_layout(T, H, I, E, k, offs), "moe_w4a8_workspace_layout")
     return {"xq": offs[WS_XQ], "h": offs[WS_H], "hq": offs[WS_HQ], "perm": offs[WS_PERM],
-            "count": offs[WS_COUNT], "sync": offs[WS_SYNC], "sync_end": offs[WS_PERM]}
+            "count": offs[WS_COUNT], "sync": offs[WS_SYNC], "sync_end": offs[WS_SYNC_END]}
 
 
 def moe_forward(hidden, topk_ids, topk_w, w_gate_up, w_down, ws_gate_up, ws_down,

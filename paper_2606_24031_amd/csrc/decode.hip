@@ -1,32 +1,35 @@
 // Single-token MoE layer in one kernel launch (decode, T = 1).
 //
 // At M = 1 the layer streams (k + 1) experts' weights (8 routed + 1 shared,
-// 15.9 MB for the Qwen3-family shape) and does almost no arithmetic, so the
-// cost is the latency of a few passes over HBM; an extra kernel boundary
-// costs about as much as a quarter of the whole layer.  Everything therefore
-// runs in one grid of two kinds of workgroups (the routed top-k experts and
-// the always-on shared expert of Sec. 2.2; the W4A8 product of Sec. 3.3):
+// 15.9 MB for the Qwen3-family shape) and does almost no arithmetic, so its
+// cost is HBM latency plus the chain of hand-offs between the gate/up and the
+// down projection; an extra kernel boundary alone costs about a third of the
+// layer.  Everything therefore runs in one grid of two kinds of workgroups
+// (the routed top-k experts and the always-on shared expert of Sec. 2.2; the
+// W4A8 product of Sec. 3.3):
 //
-//   A items (pair q, 128/LPR h columns): issue the gate and up weight loads,
-//     quantize x to Q8_0 into LDS, take the W4A8 dots, h = SiLU(g) * u,
-//     store h, then count the slab done in a per-pair counter.
-//   B items (pair q, 256/LPR down rows): issue the down weight loads first,
-//     then wait for the pair's counter, quantize h to Q8_0 into LDS, take the
-//     dots, store w_q * y; the last of the pairs to finish a row slab adds
-//     the slab up in slot order (then the shared pair) and writes out.
+//   A items (pair q, 32-column block b of h): issue the 64 gate/up row loads
+//     (one 144-byte eight-block group per lane for H = 2048),
+//     quantize x to Q8_0 into LDS, take the W4A8 dots, h = SiLU(g) * u, and
+//     publish Q8_0 of the 32 h values (exactly one block); count it in the
+//     pair's counter.
+//   B items (slab of RB down rows, all pairs): issue the down weight loads of
+//     every pair first, wait until every pair's h blocks are published, read
+//     them, take the dots and write out[n] = sum_q w_q y_q[n] (slots in
+//     order, then the shared expert) -- the combine never leaves the
+//     workgroup.
 //
 // The wait is bounded: after `spin_limit` ticks of the 100 MHz real-time
-// counter a B item computes the pair's h itself (the same code, so the same
-// bytes), so progress never depends on the order in which the hardware starts
-// workgroups.  Hand-off data (h, the per-pair y) crosses XCDs through
-// agent-coherent (sc1) stores and loads: a writer waits until its stores are
-// acknowledged (vmcnt 0) before the workgroup barrier and the counter add, a
+// counter a B item computes the missing Q8_0(h) blocks itself (the same code,
+// so the same bytes), so progress never depends on the order in which the
+// hardware starts workgroups.  Hand-off data crosses XCDs through agent-
+// coherent (sc1) stores and loads: a writer waits until its stores are
+// acknowledged (vmcnt 0) before the workgroup barrier and the counter add; a
 // reader polls the counter and then reads with sc1 loads, so no whole-L2
-// writeback or invalidate is needed.  Counters return to zero when the call
-// completes: every
-// arrival adds to a per-pair word (A items +1, B items +0x10000) and the
-// arrival that completes the total clears it; the per-slab combine counter is
-// cleared by its last arrival.
+// writeback or invalidate is needed.  Every workgroup finally arrives at a
+// two-level counter (one word per XCD slot, then one top word); the last
+// arrival of the launch clears every counter, so the sync words are zero
+// again when the call completes.
 #include <cstdlib>
 
 #include "w4a8_dev.h"
@@ -36,7 +39,18 @@ namespace w4a8 {
 
 namespace {
 
-constexpr int NT = 256;  // threads per workgroup
+constexpr int NT = 512;    // threads per workgroup
+constexpr int NSUB = 8;    // first-level arrival counters
+
+// Sync words (uint32, zero between calls), each alone in its own 256-byte
+// line: same-line atomics and polls serialize in the memory system, which
+// costs microseconds at this scale.  Slots: pair counters [64], arrival
+// counters [NSUB], top arrival counter [1].
+constexpr int SYNC_STRIDE = 64;   // words between sync slots (256 bytes)
+constexpr int SYNC_PAIR = 0, SYNC_SUB = 64, SYNC_TOP = 64 + NSUB, SYNC_SLOTS = 64 + NSUB + 1;
+__device__ __forceinline__ uint32_t *sync_word(uint32_t *sync, int slot) {
+  return sync + slot * SYNC_STRIDE;
+}
 
 struct DecodeArgs {
   const float *x;          // [H]
@@ -44,15 +58,14 @@ struct DecodeArgs {
   const float *topk_w;     // [k]
   const uint8_t *w_gu, *w_d, *ws_gu, *ws_d;
   float *out;              // [H]
-  uint32_t *pair_cnt;      // [k + 1]
-  uint32_t *slab_cnt;      // [H / RB]
-  uint8_t *xq;             // workspace copy of Q8_0(x)  [H/32 blocks]
-  float *h;                // [(k + 1)][I]
-  uint8_t *hq;             // [(k + 1)][I/32 blocks]
-  float *y;                // [(k + 1)][H]
+  uint32_t *sync;
+  uint32_t *xfer;          // Q8_0(h) hand-off: [(k+1)][I/32][9 words]: scale, 8 code words
+  uint8_t *xq;             // documented copy of Q8_0(x)   [H/32 blocks]
+  float *h;                // documented copy of h          [(k+1)][I]
+  uint8_t *hq;             // documented copy of Q8_0(h)    [(k+1)][I/32 blocks]
   int H, I, E, k;
-  int n_a;                 // A items per pair
-  int n_b;                 // B items per pair
+  int rb;                  // down rows per B item
+  int n_b;                 // B items
   int64_t spin_limit;      // real-time ticks before a B item computes h itself
 };
 
@@ -73,290 +86,343 @@ __device__ __forceinline__ uint32_t counter_add(uint32_t *p, uint32_t v) {
 __device__ __forceinline__ uint32_t counter_load(const uint32_t *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ void counter_clear(uint32_t *p) {
-  __hip_atomic_store(p, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-// agent-coherent (sc1) store and load of hand-off data
-__device__ __forceinline__ void st_agent(float *p, float v) {
+// agent-coherent (sc1) store and load of hand-off words
+__device__ __forceinline__ void st_agent(uint32_t *p, uint32_t v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ float ld_agent(const float *p) {
+__device__ __forceinline__ uint32_t ld_agent(const uint32_t *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 // wait until this wave's stores are acknowledged (s_waitcnt vmcnt(0))
 __device__ __forceinline__ void wait_stores() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
-// Q8_0 of n contiguous fp32 values (n % 32 == 0) from global memory into LDS,
-// 8 lanes per block.  COHERENT: read with agent-coherent loads (data another
-// workgroup wrote during this launch).
-template <bool COHERENT>
-__device__ void quantize_to_lds(const float *__restrict__ src, uint8_t *lds, int n) {
-  const int tasks = n / 4;  // 8 lanes x 4 values per block
+__device__ __forceinline__ const uint8_t *expert_gu(const DecodeArgs &a, int e) {
+  return e < a.E ? a.w_gu + (int64_t)e * (2 * a.I) * (a.H / 256) * (8 * Q4B) : a.ws_gu;
+}
+__device__ __forceinline__ const uint8_t *expert_d(const DecodeArgs &a, int e) {
+  return e < a.E ? a.w_d + (int64_t)e * a.H * (a.I / 256) * (8 * Q4B) : a.ws_d;
+}
+
+// LDS staging of activation blocks (see dot8_lds): codes [n][8] dwords,
+// scale [n] fp32, correction [n] int32, carved from one dynamic LDS buffer.
+struct ActBuf {
+  uint4 *codes;
+  float *d;
+  int *corr;
+};
+
+__device__ __forceinline__ ActBuf act_buf(uint8_t *base, int nblocks) {
+  ActBuf b;
+  b.codes = reinterpret_cast<uint4 *>(base);
+  b.d = reinterpret_cast<float *>(base + (size_t)nblocks * 32);
+  b.corr = reinterpret_cast<int *>(base + (size_t)nblocks * 36);
+  return b;
+}
+__host__ __device__ constexpr size_t act_buf_bytes(int nblocks) {
+  return ((size_t)nblocks * 40 + 15) / 16 * 16;
+}
+
+// Q8_0 of x (fp32 [H], global) into the LDS staging; with `xq_out` also the
+// 34-byte blocks to global memory.  8 lanes per block, 4 values per lane.
+// `first` is the lane's first float4 of x, loaded by the caller ahead of the
+// weight loads (a wave's loads return in order, so x is then not stuck
+// behind the weights).
+__device__ void quantize_x_to_lds(const DecodeArgs &a, ActBuf xb, uint8_t *xq_out,
+                                  float4 first) {
+  const int tasks = a.H / 4;
   for (int t0 = 0; t0 < tasks; t0 += NT) {
     const int t = t0 + threadIdx.x;
-    const bool live = t < tasks;   // tasks % 8 == 0: whole 8-lane groups agree
+    const bool live = t < tasks;  // tasks % 8 == 0: whole 8-lane groups agree
     float v[4] = {0.f, 0.f, 0.f, 0.f};
     if (live) {
-      if (COHERENT) {
-#pragma unroll
-        for (int i = 0; i < 4; i++) v[i] = ld_agent(src + 4 * t + i);
-      } else {
-        const float4 f = reinterpret_cast<const float4 *>(src)[t];
-        v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
-      }
+      const float4 f = t0 == 0 ? first : reinterpret_cast<const float4 *>(a.x)[t];
+      v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
     }
     uint32_t d16;
     const uint32_t packed = q8_0_block8(v, d16);
-    if (live) store_q8_0_block8(lds + (t >> 3) * Q8B, t & 7, packed, d16);
+    int sum = sdot4((int)packed, 0x01010101, 0);
+#pragma unroll
+    for (int o = 4; o > 0; o >>= 1) sum += __shfl_xor(sum, o, 8);
+    if (live) {
+      const int blk = t >> 3, j = t & 7;
+      reinterpret_cast<uint32_t *>(xb.codes)[blk * 8 + j] = packed;
+      if (j == 0) {
+        xb.d[blk] = f16_bits_to_f32(d16);
+        xb.corr[blk] = -8 * sum;
+      }
+      if (xq_out) store_q8_0_block8(xq_out + blk * Q8B, j, packed, d16);
+    }
   }
 }
 
-// Gate/up W4A8 dots for h columns [c0, c0 + HC) of one expert, HC = 128/LPR:
-// lane (row rr = tid / LPR, K-groups li, li + LPR, ...), rows 0..HC-1 gate,
-// HC..2HC-1 up.  `wpre` holds the lane's first weight group, already loaded.
-// Returns through shrow[2*HC] (LDS).
-template <int LPR>
-__device__ void gateup_rows(const DecodeArgs &a, const uint8_t *W, int c0, const uint8_t *xq_lds,
-                            const W8 &wpre, float *shrow) {
-  constexpr int HC = 128 / LPR;
-  const int rr = threadIdx.x / LPR, li = threadIdx.x % LPR;
+// Gate/up for h block b of pair q with expert e: 64 rows (32 gate + 32 up) of
+// G = H/256 eight-block groups each, unit u = row * G + g over the NT lanes.
+// Publishes Q8_0 of the 32 h values to the hand-off buffer (sc1) and, for
+// inspection, h and the 34-byte block to the documented workspace regions.
+// xb must hold Q8_0(x); `w0` is the lane's first unit, already loaded.
+// Uses part[64 * G] and hv[32] in LDS.
+__device__ void gateup_block(const DecodeArgs &a, int q, int e, int b, ActBuf xb, const W8 &w0,
+                             float *part, float *hv) {
   const int G = a.H / 256;
+  const int units = 64 * G;
+  const uint8_t *W = expert_gu(a, e);
   const int64_t rowbytes = (int64_t)G * 8 * Q4B;
-  const int64_t row = rr < HC ? c0 + rr : a.I + c0 + (rr - HC);
-  float acc = 0.0f;
-  if (li < G) {
-    Act8 x;
-    load_act8(xq_lds + li * (8 * Q8B), x);
-    acc = dot8(wpre, x, acc);
+  for (int u = threadIdx.x, j = 0; u < units; u += NT, j++) {
+    const int row = u / G, g = u % G;
+    const uint4 *codes = xb.codes + g * 16;
+    const float *dd = xb.d + g * 8;
+    const int *cc = xb.corr + g * 8;
+    float acc;
+    if (j == 0) {
+      acc = dot8_lds(w0, codes, dd, cc, 0.0f);
+    } else {
+      const int64_t r = row < 32 ? b * 32 + row : a.I + b * 32 + (row - 32);
+      W8 w;
+      load_w8(W + r * rowbytes + (int64_t)g * (8 * Q4B), w);
+      acc = dot8_lds(w, codes, dd, cc, 0.0f);
+    }
+    part[u] = acc;
   }
-  for (int g = li + LPR; g < G; g += LPR) {
-    W8 w;
-    load_w8(W + row * rowbytes + (int64_t)g * (8 * Q4B), w);
-    Act8 x;
-    load_act8(xq_lds + g * (8 * Q8B), x);
-    acc = dot8(w, x, acc);
+  __syncthreads();
+  if (threadIdx.x < 64) {               // row sums in fixed group order
+    float s = 0.0f;
+    for (int g = 0; g < G; g++) s += part[threadIdx.x * G + g];
+    part[threadIdx.x * G] = s;
   }
-  acc = lane_group_sum<LPR>(acc);
-  if (li == 0) shrow[rr] = acc;
+  __syncthreads();
+  if (threadIdx.x < 32) {
+    const float gsum = part[threadIdx.x * G], usum = part[(32 + threadIdx.x) * G];
+    const float h = silu_f32(gsum) * usum;
+    hv[threadIdx.x] = h;
+    a.h[(int64_t)q * a.I + b * 32 + threadIdx.x] = h;
+  }
+  __syncthreads();
+  if (threadIdx.x < 8) {                // Q8_0 of the 32-value block, 8 lanes
+    const int j = threadIdx.x;
+    const float v[4] = {hv[4 * j], hv[4 * j + 1], hv[4 * j + 2], hv[4 * j + 3]};
+    uint32_t d16;
+    const uint32_t packed = q8_0_block8(v, d16);
+    uint32_t *xf = a.xfer + ((int64_t)q * (a.I / 32) + b) * 9;
+    st_agent(xf + 1 + j, packed);
+    if (j == 0) st_agent(xf, d16);
+    store_q8_0_block8(a.hq + ((int64_t)q * (a.I / 32) + b) * Q8B, j, packed, d16);
+  }
 }
 
-template <int LPR>
-__device__ __forceinline__ void load_gateup_pre(const DecodeArgs &a, const uint8_t *W, int c0,
-                                                W8 &w) {
-  constexpr int HC = 128 / LPR;
-  const int rr = threadIdx.x / LPR, li = threadIdx.x % LPR;
+__device__ __forceinline__ void load_gateup_unit(const DecodeArgs &a, int e, int b, W8 &w0) {
   const int G = a.H / 256;
-  const int64_t rowbytes = (int64_t)G * 8 * Q4B;
-  const int64_t row = rr < HC ? c0 + rr : a.I + c0 + (rr - HC);
-  if (li < G) load_w8(W + row * rowbytes + (int64_t)li * (8 * Q4B), w);
-}
-
-// h = SiLU(gate) * up for the HC columns in shrow, stored to the workspace.
-template <int LPR>
-__device__ __forceinline__ void store_h(const DecodeArgs &a, int q, int c0, const float *shrow) {
-  constexpr int HC = 128 / LPR;
-  if (threadIdx.x < HC) {
-    const float hv = silu_f32(shrow[threadIdx.x]) * shrow[HC + threadIdx.x];
-    st_agent(a.h + (int64_t)q * a.I + c0 + threadIdx.x, hv);
+  const int u = threadIdx.x;
+  if (u < 64 * G) {
+    const int64_t rowbytes = (int64_t)G * 8 * Q4B;
+    const int row = u / G, g = u % G;
+    const int64_t r = row < 32 ? b * 32 + row : a.I + b * 32 + (row - 32);
+    load_w8(expert_gu(a, e) + r * rowbytes + (int64_t)g * (8 * Q4B), w0);
   }
 }
 
-template <int LPRA, int LPRB>
+__device__ __forceinline__ float4 load_x_first(const DecodeArgs &a) {
+  return threadIdx.x < a.H / 4 ? reinterpret_cast<const float4 *>(a.x)[threadIdx.x]
+                               : make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
+// Last arrival of the launch clears every sync word.
+__device__ void arrive(const DecodeArgs &a) {
+  if (threadIdx.x != 0) return;
+  const int nblocks = (int)gridDim.x;
+  const int s = blockIdx.x % NSUB;
+  const uint32_t sub_total = (uint32_t)((nblocks - s + NSUB - 1) / NSUB);
+  const uint32_t old = counter_add(sync_word(a.sync, SYNC_SUB + s), 1u);
+  if (old + 1u != sub_total) return;
+  const uint32_t nsubs = (uint32_t)(nblocks < NSUB ? nblocks : NSUB);
+  const uint32_t top = counter_add(sync_word(a.sync, SYNC_TOP), 1u);
+  if (top + 1u != nsubs) return;
+  for (int i = 0; i < SYNC_SLOTS; i++)
+    __hip_atomic_store(sync_word(a.sync, i), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
   extern __shared__ __align__(16) uint8_t lds[];
-  constexpr int HC = 128 / LPRA;   // h columns per A item
-  constexpr int RB = 256 / LPRB;   // down rows per B item
-  __shared__ float shrow[2 * HC];
+  __shared__ float hv[32];
   __shared__ int flag;
   const int npairs = a.k + 1;
+  const int nb_h = a.I / 32;                  // A items per pair
+  const int na_total = npairs * nb_h;
   const int item = blockIdx.x;
-  const int na_total = npairs * a.n_a;
+  const int nbx = a.H / 32;                   // blocks of Q8_0(x)
 
   if (item < na_total) {
     // ------------------------------------------------------------ A item
-    const int q = item / a.n_a, slab = item % a.n_a;
+    const int q = item / nb_h, b = item % nb_h;
     int e;
-    if (!pair_valid(a, q, e)) {
-      if (item == 0) {                              // workspace copy of Q8_0(x)
-        quantize_to_lds<false>(a.x, lds, a.H);
-        __syncthreads();
-        for (int i = threadIdx.x; i < (a.H / 32) * Q8B / 2; i += NT)
-          reinterpret_cast<uint16_t *>(a.xq)[i] = reinterpret_cast<const uint16_t *>(lds)[i];
-      }
-      return;
+    const bool valid = pair_valid(a, q, e);
+    const float4 x0 = load_x_first(a);                 // x first, then the weights
+    W8 w0;
+    if (valid) load_gateup_unit(a, e, b, w0);
+    const ActBuf xb = act_buf(lds, nbx);
+    float *part = reinterpret_cast<float *>(lds + act_buf_bytes(nbx));
+    if (valid || item == 0) {
+      quantize_x_to_lds(a, xb, item == 0 ? a.xq : nullptr, x0);
+      __syncthreads();
     }
-    const uint8_t *W = (e < a.E) ? a.w_gu + (int64_t)e * (2 * a.I) * (a.H / 256) * (8 * Q4B) : a.ws_gu;
-    const int c0 = slab * HC;
-    W8 wpre;
-    load_gateup_pre<LPRA>(a, W, c0, wpre);          // weight loads in flight first
-    uint8_t *xq_lds = lds;
-    quantize_to_lds<false>(a.x, xq_lds, a.H);
-    __syncthreads();
-    if (item == 0)                                  // workspace copy of Q8_0(x)
-      for (int i = threadIdx.x; i < (a.H / 32) * Q8B / 2; i += NT)
-        reinterpret_cast<uint16_t *>(a.xq)[i] = reinterpret_cast<const uint16_t *>(xq_lds)[i];
-    gateup_rows<LPRA>(a, W, c0, xq_lds, wpre, shrow);
-    __syncthreads();
-    store_h<LPRA>(a, q, c0, shrow);
-    wait_stores();
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      const uint32_t total = (uint32_t)a.n_a + ((uint32_t)a.n_b << 16);
-      const uint32_t old = counter_add(&a.pair_cnt[q], 1u);
-      if (old + 1u == total) counter_clear(&a.pair_cnt[q]);
+    if (valid) {
+      gateup_block(a, q, e, b, xb, w0, part, hv);
+      wait_stores();
+      __syncthreads();
+      if (threadIdx.x == 0) counter_add(sync_word(a.sync, SYNC_PAIR + q), 1u);
     }
+    arrive(a);
     return;
   }
 
   // -------------------------------------------------------------- B item
-  const int bi = item - na_total;
-  const int q = bi / a.n_b, slab = bi % a.n_b;
-  int nvalid = 0;
-  for (int j = 0; j < npairs; j++) {
-    int ej;
-    nvalid += pair_valid(a, j, ej) ? 1 : 0;
-  }
-  int e;
-  if (!pair_valid(a, q, e)) {
-    if (nvalid == 0 && q == 0)                      // nothing routed: out = 0
-      for (int n = threadIdx.x; n < RB; n += NT) a.out[slab * RB + n] = 0.0f;
-    return;
-  }
+  const int slab = item - na_total;
+  const int rb = a.rb;
   const int GI = a.I / 256;
   const int64_t rowbytes = (int64_t)GI * 8 * Q4B;
-  const uint8_t *Wd = (e < a.E) ? a.w_d + (int64_t)e * a.H * rowbytes : a.ws_d;
-  const int r = threadIdx.x / LPRB, li = threadIdx.x % LPRB;
-  const int64_t n = (int64_t)slab * RB + r;
+  const int units = npairs * rb * GI;
+  // unit u = (q * rb + r) * GI + g; one unit per lane (units <= NT)
+  const int uq = threadIdx.x / (rb * GI), ur = (threadIdx.x / GI) % rb, ug = threadIdx.x % GI;
+  const int64_t un = (int64_t)slab * rb + ur;
+  int ue = 0;
+  const bool ulive = threadIdx.x < units && pair_valid(a, uq, ue) && un < a.H;
   W8 wpre;
-  if (li < GI) load_w8(Wd + n * rowbytes + (int64_t)li * (8 * Q4B), wpre);   // in flight first
+  if (ulive) load_w8(expert_d(a, ue) + un * rowbytes + (int64_t)ug * (8 * Q4B), wpre);
 
-  // wait for the pair's h (bounded)
-  if (threadIdx.x == 0) {
+  // wait until every valid pair has all nb_h blocks of Q8_0(h) (bounded):
+  // lane q polls pair q, all pairs at once (a coherent poll costs ~0.3 us
+  // under load, so polling them one after another would add up)
+  {
     const uint64_t t0 = wall_clock64();
-    int ok = 0;
+    int ev;
+    const bool mine = threadIdx.x < npairs && pair_valid(a, threadIdx.x, ev);
     for (;;) {
-      const uint32_t v = counter_load(&a.pair_cnt[q]);
-      if ((v & 0xFFFFu) >= (uint32_t)a.n_a) { ok = 1; break; }
-      if ((int64_t)(wall_clock64() - t0) > a.spin_limit) break;
+      const int ready = !mine || counter_load(sync_word(a.sync, SYNC_PAIR + threadIdx.x)) >=
+                                     (uint32_t)nb_h;
+      if (__syncthreads_and(ready)) { if (threadIdx.x == 0) flag = 1; break; }
+      if (threadIdx.x == 0) flag = (int64_t)(wall_clock64() - t0) > a.spin_limit ? 0 : 2;
+      __syncthreads();
+      if (flag == 0) break;
       __builtin_amdgcn_s_sleep(2);
+      __syncthreads();   // everyone has read flag before thread 0 rewrites it
     }
-    flag = ok;
   }
   __syncthreads();
   if (!flag) {
-    // fallback: compute every h slab of this pair here (same code, same bytes)
-    const uint8_t *W = (e < a.E) ? a.w_gu + (int64_t)e * (2 * a.I) * (a.H / 256) * (8 * Q4B) : a.ws_gu;
-    uint8_t *xq_lds = lds;
-    quantize_to_lds<false>(a.x, xq_lds, a.H);
+    // fallback: produce every pair's Q8_0(h) here (same code, same bytes)
+    const ActBuf xb = act_buf(lds, nbx);
+    float *gpart = reinterpret_cast<float *>(lds + act_buf_bytes(nbx));
+    quantize_x_to_lds(a, xb, nullptr, load_x_first(a));
     __syncthreads();
-    for (int s = 0; s < a.n_a; s++) {
-      W8 w;
-      load_gateup_pre<LPRA>(a, W, s * HC, w);
-      gateup_rows<LPRA>(a, W, s * HC, xq_lds, w, shrow);
-      __syncthreads();
-      store_h<LPRA>(a, q, s * HC, shrow);
-      __syncthreads();
+    for (int q = 0; q < npairs; q++) {
+      int e;
+      if (!pair_valid(a, q, e)) continue;
+      for (int b = 0; b < nb_h; b++) {
+        W8 w0;
+        load_gateup_unit(a, e, b, w0);
+        gateup_block(a, q, e, b, xb, w0, gpart, hv);
+        __syncthreads();
+      }
     }
     wait_stores();
     __syncthreads();
   }
-
-  // Q8_0(h) of the pair into LDS; the first slab also stores it to the workspace
-  uint8_t *hq_lds = lds;
-  quantize_to_lds<true>(a.h + (int64_t)q * a.I, hq_lds, a.I);
-  __syncthreads();
-  if (slab == 0)
-    for (int i = threadIdx.x; i < (a.I / 32) * Q8B / 2; i += NT)
-      reinterpret_cast<uint16_t *>(a.hq + (int64_t)q * (a.I / 32) * Q8B)[i] =
-          reinterpret_cast<const uint16_t *>(hq_lds)[i];
-
-  float acc = 0.0f;
-  if (li < GI) {
-    Act8 x;
-    load_act8(hq_lds + li * (8 * Q8B), x);
-    acc = dot8(wpre, x, acc);
-  }
-  for (int g = li + LPRB; g < GI; g += LPRB) {
-    W8 w;
-    load_w8(Wd + n * rowbytes + (int64_t)g * (8 * Q4B), w);
-    Act8 x;
-    load_act8(hq_lds + g * (8 * Q8B), x);
-    acc = dot8(w, x, acc);
-  }
-  acc = lane_group_sum<LPRB>(acc);
-  const float wq = (q < a.k) ? a.topk_w[q] : 1.0f;
-  if (li == 0) st_agent(a.y + (int64_t)q * a.H + n, wq * acc);
-  wait_stores();
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const uint32_t total = (uint32_t)a.n_a + ((uint32_t)a.n_b << 16);
-    const uint32_t old = counter_add(&a.pair_cnt[q], 0x10000u);
-    if (old + 0x10000u == total) counter_clear(&a.pair_cnt[q]);
-    const uint32_t prev = counter_add(&a.slab_cnt[slab], 1u);
-    flag = (prev + 1u == (uint32_t)nvalid) ? 1 : 0;
-    if (flag) counter_clear(&a.slab_cnt[slab]);
+  // Q8_0(h) of every valid pair: hand-off words -> LDS staging
+  const int nbh_all = npairs * nb_h;
+  const ActBuf hb = act_buf(lds, nbh_all);
+  float *part = reinterpret_cast<float *>(lds + act_buf_bytes(nbh_all));
+  for (int i = threadIdx.x; i < nbh_all * 9; i += NT) {
+    const int blk = i / 9, w = i % 9;
+    int e;
+    if (!pair_valid(a, blk / nb_h, e)) continue;
+    const uint32_t v = ld_agent(a.xfer + i);
+    if (w == 0)
+      hb.d[blk] = f16_bits_to_f32(v);
+    else
+      reinterpret_cast<uint32_t *>(hb.codes)[blk * 8 + (w - 1)] = v;
   }
   __syncthreads();
-  if (!flag) return;
-  // last pair to finish this slab: out = sum over slots in order, then shared
-  for (int i = threadIdx.x; i < RB; i += NT) {
-    float s = 0.0f;
-    for (int j = 0; j < npairs; j++) {
-      int ej;
-      if (pair_valid(a, j, ej)) s += ld_agent(a.y + (int64_t)j * a.H + (int64_t)slab * RB + i);
+  for (int blk = threadIdx.x; blk < nbh_all; blk += NT) {
+    int e;
+    if (!pair_valid(a, blk / nb_h, e)) continue;
+    const uint32_t *c = reinterpret_cast<const uint32_t *>(hb.codes) + blk * 8;
+    int s = 0;
+#pragma unroll
+    for (int i = 0; i < 8; i++) s = sdot4((int)c[i], 0x01010101, s);
+    hb.corr[blk] = -8 * s;
+  }
+  __syncthreads();
+  if (threadIdx.x < units) {
+    float acc = 0.0f;
+    if (ulive) {
+      const int blk0 = uq * nb_h + ug * 8;
+      if (flag) {
+        acc = dot8_lds(wpre, hb.codes + blk0 * 2, hb.d + blk0, hb.corr + blk0, 0.0f);
+      } else {
+        W8 w;
+        load_w8(expert_d(a, ue) + un * rowbytes + (int64_t)ug * (8 * Q4B), w);
+        acc = dot8_lds(w, hb.codes + blk0 * 2, hb.d + blk0, hb.corr + blk0, 0.0f);
+      }
     }
-    a.out[(int64_t)slab * RB + i] = s;
+    part[threadIdx.x] = acc;
   }
-}
-
-int pow2_le(int g, int cap) {
-  int l = 1;
-  while (l * 2 <= g && l < cap) l *= 2;
-  return l;
-}
-
-template <int A, int B>
-void launch(const DecodeArgs &a, unsigned grid, size_t lds, hipStream_t s) {
-  decode_kernel<A, B><<<dim3(grid), dim3(NT), lds, s>>>(a);
+  __syncthreads();
+  for (int r = threadIdx.x; r < rb; r += NT) {
+    const int64_t n = (int64_t)slab * rb + r;
+    if (n >= a.H) continue;
+    float o = 0.0f;
+    for (int q = 0; q < npairs; q++) {
+      int e;
+      if (!pair_valid(a, q, e)) continue;
+      float y = 0.0f;
+      for (int g = 0; g < GI; g++) y += part[(q * rb + r) * GI + g];
+      o += (q < a.k ? a.topk_w[q] : 1.0f) * y;
+    }
+    a.out[n] = o;
+  }
+  arrive(a);
 }
 
 }  // namespace
 
-// Workspace words used by the decode kernel (inside the zero-filled sync
-// region): pair counters [k + 1], slab counters [H / 32 max].
-size_t decode_sync_words(int64_t H) { return 64 + (size_t)(H / 32); }
+size_t decode_sync_words(int64_t) { return (size_t)SYNC_SLOTS * SYNC_STRIDE; }
+
+// Hand-off buffer words for T = 1.
+size_t decode_xfer_words(int64_t I, int64_t k) { return (size_t)(k + 1) * (I / 32) * 9; }
+
+bool decode_supported(int64_t H, int64_t I, int64_t k) {
+  // B items hold every pair of one down row at one unit per lane; LDS holds
+  // the staged Q8_0(x) plus 64 * H/256 partials (A) or the staged Q8_0(h) of
+  // every pair plus NT partials (B).
+  const size_t lda = act_buf_bytes((int)(H / 32)) + sizeof(float) * 64 * (H / 256);
+  const size_t ldb = act_buf_bytes((int)((k + 1) * (I / 32))) + sizeof(float) * NT;
+  return H <= 16384 && (k + 1) <= 64 && (k + 1) * (I / 256) <= NT && lda <= 48 * 1024 &&
+         ldb <= 48 * 1024;
+}
 
 int decode_forward(const float *x, const int32_t *ids, const float *topk_w, const uint8_t *w_gu,
                    const uint8_t *w_d, const uint8_t *ws_gu, const uint8_t *ws_d, float *out,
-                   int64_t H, int64_t I, int64_t E, int64_t k, uint32_t *sync, uint8_t *xq,
-                   float *h, uint8_t *hq, float *y, hipStream_t s) {
+                   int64_t H, int64_t I, int64_t E, int64_t k, uint32_t *sync, uint32_t *xfer,
+                   uint8_t *xq, float *h, uint8_t *hq, hipStream_t s) {
   DecodeArgs a;
   a.x = x; a.ids = ids; a.topk_w = topk_w;
   a.w_gu = w_gu; a.w_d = w_d; a.ws_gu = ws_gu; a.ws_d = ws_d;
   a.out = out;
-  a.pair_cnt = sync;
-  a.slab_cnt = sync + 64;
-  a.xq = xq; a.h = h; a.hq = hq; a.y = y;
+  a.sync = sync;
+  a.xfer = xfer;
+  a.xq = xq; a.h = h; a.hq = hq;
   a.H = (int)H; a.I = (int)I; a.E = (int)E; a.k = (int)k;
-  const int lpra = pow2_le((int)(H / 256), 8);
-  const int lprb = pow2_le((int)(I / 256), 8);
-  a.n_a = (int)(I / (128 / lpra));
-  a.n_b = (int)(H / (256 / lprb));
+  const int npairs = (int)k + 1;
+  const int GI = (int)(I / 256);
+  a.rb = NT / (npairs * GI);                     // >= 1 by decode_supported
+  a.n_b = (int)((H + a.rb - 1) / a.rb);
   // default wait bound: 1 ms of the 100 MHz real-time counter
   a.spin_limit = 100000;
   if (const char *env = std::getenv("W4A8_DECODE_SPIN_TICKS")) a.spin_limit = std::atoll(env);
-  const int npairs = (int)k + 1;
-  const unsigned grid = (unsigned)(npairs * (a.n_a + a.n_b));
-  const size_t lds = (size_t)((H > I ? H : I) / 32) * Q8B + 16;
-  switch (lpra * 16 + lprb) {
-#define W4A8_CASE(A, B) case A * 16 + B: launch<A, B>(a, grid, lds, s); break;
-    W4A8_CASE(1, 1) W4A8_CASE(1, 2) W4A8_CASE(1, 4) W4A8_CASE(1, 8)
-    W4A8_CASE(2, 1) W4A8_CASE(2, 2) W4A8_CASE(2, 4) W4A8_CASE(2, 8)
-    W4A8_CASE(4, 1) W4A8_CASE(4, 2) W4A8_CASE(4, 4) W4A8_CASE(4, 8)
-    W4A8_CASE(8, 1) W4A8_CASE(8, 2) W4A8_CASE(8, 4) W4A8_CASE(8, 8)
-#undef W4A8_CASE
-    default: return W4A8_ESHAPE;
-  }
+  const unsigned grid = (unsigned)(npairs * (I / 32) + a.n_b);
+  const size_t lda = act_buf_bytes((int)(H / 32)) + sizeof(float) * 64 * (H / 256);
+  const size_t ldb = act_buf_bytes(npairs * (int)(I / 32)) + sizeof(float) * NT;
+  const size_t lds = lda > ldb ? lda : ldb;
+  decode_kernel<<<dim3(grid), dim3(NT), lds, s>>>(a);
   return check_launch();
 }
 

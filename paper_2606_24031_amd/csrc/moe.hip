@@ -24,10 +24,12 @@ namespace w4a8 {
 int launch_fill_zero(void *ptr, size_t bytes, hipStream_t s);
 int launch_q8_0(const float *x, uint8_t *xq, int64_t nblocks, hipStream_t s);
 size_t decode_sync_words(int64_t H);
+size_t decode_xfer_words(int64_t I, int64_t k);
+bool decode_supported(int64_t H, int64_t I, int64_t k);
 int decode_forward(const float *x, const int32_t *ids, const float *topk_w, const uint8_t *w_gu,
                    const uint8_t *w_d, const uint8_t *ws_gu, const uint8_t *ws_d, float *out,
-                   int64_t H, int64_t I, int64_t E, int64_t k, uint32_t *sync, uint8_t *xq,
-                   float *h, uint8_t *hq, float *y, hipStream_t s);
+                   int64_t H, int64_t I, int64_t E, int64_t k, uint32_t *sync, uint32_t *xfer,
+                   uint8_t *xq, float *h, uint8_t *hq, hipStream_t s);
 
 namespace {
 
@@ -38,7 +40,7 @@ constexpr int LDS_INTS = 16000; // int32 cells of dynamic LDS for the route kern
 inline size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t meta, sync, perm, count, rank, groups, tiles, xq, h, hq, y, total;
+  size_t meta, sync, xfer, perm, count, rank, groups, tiles, xq, h, hq, y, total;
   int64_t maxtiles;
 };
 
@@ -50,6 +52,7 @@ Layout make_layout(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k) {
   size_t off = 0;
   L.meta = off;   off += 256;
   L.sync = off;   off += up256(sizeof(uint32_t) * decode_sync_words(H));
+  L.xfer = off;   off += up256(sizeof(uint32_t) * decode_xfer_words(I, k));
   L.perm = off;   off += up256(sizeof(int32_t) * P);
   L.count = off;  off += up256(sizeof(int32_t) * E);
   L.rank = off;   off += up256(sizeof(int32_t) * (T * k + 1));
@@ -374,11 +377,11 @@ int moe_forward_impl(const float *hidden, const int32_t *ids, const float *topk_
   int rc;
 
   // One token: the whole layer in a single launch (see decode.hip).
-  if (T == 1 && I / 16 < 32768 && H / 32 < 32768)
+  if (T == 1 && decode_supported(H, I, k))
     return decode_forward(hidden, ids, topk_w, w_gu, w_d, ws_gu, ws_d, out, H, I, E, k,
-                          reinterpret_cast<uint32_t *>(ws + L.sync), ws + L.xq,
-                          reinterpret_cast<float *>(ws + L.h), ws + L.hq,
-                          reinterpret_cast<float *>(ws + L.y), s);
+                          reinterpret_cast<uint32_t *>(ws + L.sync),
+                          reinterpret_cast<uint32_t *>(ws + L.xfer), ws + L.xq,
+                          reinterpret_cast<float *>(ws + L.h), ws + L.hq, s);
 
   if ((rc = launch_q8_0(hidden, ws + L.xq, T * (H / QK), s)) != W4A8_OK) return rc;
 
@@ -464,6 +467,7 @@ extern "C" int moe_w4a8_workspace_layout(int64_t T, int64_t H, int64_t I, int64_
   offsets[W4A8_WS_PERM] = L.perm;
   offsets[W4A8_WS_COUNT] = L.count;
   offsets[W4A8_WS_SYNC] = L.sync;
+  offsets[W4A8_WS_SYNC_END] = L.xfer;
   return W4A8_OK;
 }
 

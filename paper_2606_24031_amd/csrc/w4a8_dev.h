@@ -126,6 +126,30 @@ __device__ __forceinline__ float dot8(const W8 &w, const Act8 &a, float acc) {
   return acc;
 }
 
+// Activation blocks staged in LDS in an aligned layout: block i's 32 codes as
+// 8 dwords at codes[2i], codes[2i+1] (uint4), its fp32 scale d[i] and its
+// correction corr[i] = -8 * (sum of codes).  The dot reads one block at a
+// time, so only ~10 registers of activation are live.
+__device__ __forceinline__ float dot8_lds(const W8 &w, const uint4 *__restrict__ codes,
+                                          const float *__restrict__ d,
+                                          const int *__restrict__ corr, float acc) {
+#pragma unroll
+  for (int k = 0; k < 8; k++) {
+    const uint4 c0 = codes[2 * k], c1 = codes[2 * k + 1];
+    const int a_lo[4] = {(int)c0.x, (int)c0.y, (int)c0.z, (int)c0.w};
+    const int a_hi[4] = {(int)c1.x, (int)c1.y, (int)c1.z, (int)c1.w};
+    int s = corr[k];
+#pragma unroll
+    for (int c = 0; c < 4; c++) {
+      const uint32_t n = w8_nib(w, k, c);
+      s = sdot4((int)(n & 0x0F0F0F0Fu), a_lo[c], s);
+      s = sdot4((int)((n >> 4) & 0x0F0F0F0Fu), a_hi[c], s);
+    }
+    acc = fmaf((float)s, w8_scale(w, k) * d[k], acc);
+  }
+  return acc;
+}
+
 // Sum over groups of `width` consecutive lanes (width a power of two <= 64).
 template <int WIDTH>
 __device__ __forceinline__ float lane_group_sum(float v) {
