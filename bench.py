@@ -54,6 +54,9 @@ def parse():
     ap.add_argument("--no-graph", action="store_true", help="launch steps eagerly")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run a plain 256 MiB device copy 5 times (for scaling the "
+                         "rocprofv3 FETCH_SIZE / WRITE_SIZE counters)")
     return ap.parse_args()
 
 
@@ -257,6 +260,14 @@ def main():
     gbps = nbytes / (ms / 1e3) / 1e9
     bytes_per_launch = nbytes / args.steps
     log(f"decode: {ms_step * 1e3:.2f} us/step, {gbps:.0f} GB/s")
+
+    if args.calibrate_copy:
+        src = torch.randint(0, 255, (256 << 20,), dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copy calibration: 5 copies of {256 << 20} bytes")
 
     prefill = None
     if not args.no_prefill:

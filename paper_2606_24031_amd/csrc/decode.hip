@@ -253,9 +253,12 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
   if (item < na_total) {
     // ------------------------------------------------------------ A item
     const int q = item / nb_h, b = item % nb_h;
+    // x and the expert id together, both landed before the weights are
+    // issued (a wave's loads return in order)
+    const float4 x0 = load_x_first(a);
     int e;
     const bool valid = pair_valid(a, q, e);
-    const float4 x0 = load_x_first(a);                 // x first, then the weights
+    asm volatile("" ::"v"(x0.x), "v"(x0.y), "v"(x0.z), "v"(x0.w), "s"(e));
     W8 w0;
     if (valid) load_gateup_unit(a, e, b, w0);
     const ActBuf xb = act_buf(lds, nbx);
@@ -283,8 +286,12 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
   // unit u = (q * rb + r) * GI + g; one unit per lane (units <= NT)
   const int uq = threadIdx.x / (rb * GI), ur = (threadIdx.x / GI) % rb, ug = threadIdx.x % GI;
   const int64_t un = (int64_t)slab * rb + ur;
-  int ue = 0;
+  int ue = 0, ev = 0;
   const bool ulive = threadIdx.x < units && pair_valid(a, uq, ue) && un < a.H;
+  // lane q polls pair q below; its validity is read now, before the weight
+  // loads, so the poll does not wait behind them
+  const bool mine = threadIdx.x < npairs && pair_valid(a, threadIdx.x, ev);
+  asm volatile("" ::"v"(ue), "v"((int)mine));
   W8 wpre;
   if (ulive) load_w8(expert_d(a, ue) + un * rowbytes + (int64_t)ug * (8 * Q4B), wpre);
 
@@ -293,8 +300,6 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
   // under load, so polling them one after another would add up)
   {
     const uint64_t t0 = wall_clock64();
-    int ev;
-    const bool mine = threadIdx.x < npairs && pair_valid(a, threadIdx.x, ev);
     for (;;) {
       const int ready = !mine || counter_load(sync_word(a.sync, SYNC_PAIR + threadIdx.x)) >=
                                      (uint32_t)nb_h;
