@@ -23,6 +23,15 @@ namespace w4a8 {
 
 int launch_fill_zero(void *ptr, size_t bytes, hipStream_t s);
 int launch_q8_0(const float *x, uint8_t *xq, int64_t nblocks, hipStream_t s);
+int grouped_tile_rows();
+int grouped_gateup(const uint8_t *w_gu, const uint8_t *ws_gu, const uint8_t *xq,
+                   const int32_t *meta, const int32_t *perm, const int4 *groups, const int2 *tiles,
+                   float *h, uint8_t *hq, int64_t maxtiles, int64_t T, int64_t H, int64_t I,
+                   int64_t E, int64_t k, hipStream_t s);
+int grouped_down(const uint8_t *w_d, const uint8_t *ws_d, const uint8_t *hq, const int32_t *meta,
+                 const int32_t *perm, const int4 *groups, const int2 *tiles, const float *topk_w,
+                 float *y, int64_t maxtiles, int64_t T, int64_t H, int64_t I, int64_t E,
+                 int64_t k, hipStream_t s);
 size_t decode_sync_words(int64_t H);
 size_t decode_xfer_words(int64_t I, int64_t k);
 bool decode_supported(int64_t H, int64_t I, int64_t k);
@@ -33,7 +42,7 @@ int decode_forward(const float *x, const int32_t *ids, const float *topk_w, cons
 
 namespace {
 
-constexpr int MC = 4;           // token rows per tile
+constexpr int MC = 64;          // token rows per tile (one grouped MFMA tile)
 constexpr int ROUTE_T = 1024;   // threads of the route kernel
 constexpr int LDS_INTS = 16000; // int32 cells of dynamic LDS for the route kernel (< 64 KB)
 
@@ -199,143 +208,6 @@ __global__ __launch_bounds__(ROUTE_T) void route_kernel(RouteArgs a) {
   }
 }
 
-// ------------------------------------------------------------------ expert MLP
-struct MlpArgs {
-  const uint8_t *w_gu, *w_d, *ws_gu, *ws_d;
-  const float *topk_w;
-  const int32_t *meta, *perm;
-  const int4 *groups;
-  const int2 *tiles;
-  const uint8_t *xq;
-  float *h;
-  uint8_t *hq;
-  float *y;
-  int64_t T, H, I, E, k;
-};
-
-__device__ __forceinline__ float silu_f32(float g) { return g / (1.0f + expf(-g)); }
-
-// Gate/up for one (tile, 32-column h slab).  Thread (r, li): h column
-// slab*32 + r, K-groups li, li+LPR, ...  Each lane holds its gate and up row
-// group (2 x 144 bytes) and streams the tile's activation groups.
-template <int LPR>
-__global__ __launch_bounds__(32 * LPR) void gateup_kernel(MlpArgs a) {
-  const int nslab = (int)(a.I / 32);
-  const int tile = blockIdx.x / nslab, slab = blockIdx.x % nslab;
-  if (tile >= a.meta[META_NTILES]) return;
-  const int2 td = a.tiles[tile];
-  const int4 gd = a.groups[td.x];
-  const int mc = min(MC, gd.z - td.y);
-  const int r = threadIdx.x / LPR, li = threadIdx.x % LPR;
-  const int G = (int)(a.H / 256);
-  const int64_t rowbytes = (int64_t)G * 8 * Q4B;
-  const uint8_t *W = (gd.x < a.E) ? a.w_gu + (int64_t)gd.x * (2 * a.I) * rowbytes : a.ws_gu;
-  const int64_t col = (int64_t)slab * 32 + r;
-  const uint8_t *wg_row = W + col * rowbytes;
-  const uint8_t *wu_row = W + (a.I + col) * rowbytes;
-
-  int pair[MC];
-  const uint8_t *act[MC];
-  const int64_t xrow = (int64_t)G * 8 * Q8B;
-#pragma unroll
-  for (int m = 0; m < MC; m++) {
-    const int p = a.perm[gd.y + td.y + min(m, mc - 1)];
-    pair[m] = p;
-    const int64_t t = (p < a.T * a.k) ? p / a.k : p - a.T * a.k;
-    act[m] = a.xq + t * xrow;
-  }
-  float accg[MC], accu[MC];
-#pragma unroll
-  for (int m = 0; m < MC; m++) accg[m] = accu[m] = 0.0f;
-  for (int g = li; g < G; g += LPR) {
-    W8 wg, wu;
-    load_w8(wg_row + (int64_t)g * (8 * Q4B), wg);
-    load_w8(wu_row + (int64_t)g * (8 * Q4B), wu);
-#pragma unroll
-    for (int m = 0; m < MC; m++) {
-      if (m < mc) {
-        Act8 x;
-        load_act8(act[m] + (int64_t)g * (8 * Q8B), x);
-        accg[m] = dot8(wg, x, accg[m]);
-        accu[m] = dot8(wu, x, accu[m]);
-      }
-    }
-  }
-  __shared__ float sh[MC][32];
-#pragma unroll
-  for (int m = 0; m < MC; m++) {
-    const float gsum = lane_group_sum<LPR>(accg[m]);
-    const float usum = lane_group_sum<LPR>(accu[m]);
-    if (li == 0 && m < mc) {
-      const float hv = silu_f32(gsum) * usum;
-      sh[m][r] = hv;
-      a.h[(int64_t)pair[m] * a.I + col] = hv;
-    }
-  }
-  __syncthreads();
-  // Q8_0 of the 32-wide h block of each token: 8 lanes per token.
-  const int tid = threadIdx.x;
-  if (tid < 8 * MC) {
-    const int m = tid >> 3, j = tid & 7;
-    if (m < mc) {
-      float v[4] = {sh[m][4 * j], sh[m][4 * j + 1], sh[m][4 * j + 2], sh[m][4 * j + 3]};
-      uint32_t d16;
-      const uint32_t packed = q8_0_block8(v, d16);
-      uint8_t *blk = a.hq + ((int64_t)pair[m] * (a.I / QK) + slab) * Q8B;
-      store_q8_0_block8(blk, j, packed, d16);
-    }
-  }
-}
-
-// Down projection for one (tile, slab of 256/LPR output rows), scaled by the
-// routing weight of each pair (1 for the shared expert).
-template <int LPR>
-__global__ __launch_bounds__(256) void down_kernel(MlpArgs a) {
-  constexpr int RPB = 256 / LPR;
-  const int nslab = (int)(a.H / RPB);
-  const int tile = blockIdx.x / nslab, slab = blockIdx.x % nslab;
-  if (tile >= a.meta[META_NTILES]) return;
-  const int2 td = a.tiles[tile];
-  const int4 gd = a.groups[td.x];
-  const int mc = min(MC, gd.z - td.y);
-  const int r = threadIdx.x / LPR, li = threadIdx.x % LPR;
-  const int G = (int)(a.I / 256);
-  const int64_t rowbytes = (int64_t)G * 8 * Q4B;
-  const uint8_t *W = (gd.x < a.E) ? a.w_d + (int64_t)gd.x * a.H * rowbytes : a.ws_d;
-  const int64_t n = (int64_t)slab * RPB + r;
-  const uint8_t *wrow = W + n * rowbytes;
-
-  int pair[MC];
-  float wt[MC];
-  const int64_t hrow = (int64_t)G * 8 * Q8B;
-#pragma unroll
-  for (int m = 0; m < MC; m++) {
-    const int p = a.perm[gd.y + td.y + min(m, mc - 1)];
-    pair[m] = p;
-    wt[m] = (p < a.T * a.k) ? a.topk_w[p] : 1.0f;
-  }
-  float acc[MC];
-#pragma unroll
-  for (int m = 0; m < MC; m++) acc[m] = 0.0f;
-  for (int g = li; g < G; g += LPR) {
-    W8 w;
-    load_w8(wrow + (int64_t)g * (8 * Q4B), w);
-#pragma unroll
-    for (int m = 0; m < MC; m++) {
-      if (m < mc) {
-        Act8 x;
-        load_act8(a.hq + (int64_t)pair[m] * hrow + (int64_t)g * (8 * Q8B), x);
-        acc[m] = dot8(w, x, acc[m]);
-      }
-    }
-  }
-#pragma unroll
-  for (int m = 0; m < MC; m++) {
-    const float v = lane_group_sum<LPR>(acc[m]);
-    if (li == 0 && m < mc) a.y[(int64_t)pair[m] * a.H + n] = wt[m] * v;
-  }
-}
-
 // out[t] = sum_j y[t*k + j] (slots in order, skipped slots left out) + y[T*k + t].
 __global__ __launch_bounds__(256) void combine_kernel(const float *__restrict__ y,
                                                       const int32_t *__restrict__ ids,
@@ -358,12 +230,6 @@ __global__ __launch_bounds__(256) void combine_kernel(const float *__restrict__ 
     acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
   }
   reinterpret_cast<float4 *>(out)[i] = acc;
-}
-
-int pow2_floor_le(int g, int cap) {
-  int l = 1;
-  while (l * 2 <= g && l < cap) l *= 2;
-  return l;
 }
 
 }  // namespace
@@ -409,39 +275,19 @@ int moe_forward_impl(const float *hidden, const int32_t *ids, const float *topk_
   route_kernel<<<dim3(1), dim3(ROUTE_T), lds, s>>>(ra);
   if ((rc = check_launch()) != W4A8_OK) return rc;
 
-  MlpArgs ma;
-  ma.w_gu = w_gu; ma.w_d = w_d; ma.ws_gu = ws_gu; ma.ws_d = ws_d;
-  ma.topk_w = topk_w;
-  ma.meta = ra.meta; ma.perm = ra.perm; ma.groups = ra.groups; ma.tiles = ra.tiles;
-  ma.xq = ws + L.xq;
-  ma.h = reinterpret_cast<float *>(ws + L.h);
-  ma.hq = ws + L.hq;
-  ma.y = reinterpret_cast<float *>(ws + L.y);
-  ma.T = T; ma.H = H; ma.I = I; ma.E = E; ma.k = k;
-
-  const int lpr_h = pow2_floor_le((int)(H / 256), 8);
-  const unsigned grid_gu = (unsigned)(L.maxtiles * (I / 32));
-  switch (lpr_h) {
-    case 1: gateup_kernel<1><<<grid_gu, 32, 0, s>>>(ma); break;
-    case 2: gateup_kernel<2><<<grid_gu, 64, 0, s>>>(ma); break;
-    case 4: gateup_kernel<4><<<grid_gu, 128, 0, s>>>(ma); break;
-    default: gateup_kernel<8><<<grid_gu, 256, 0, s>>>(ma); break;
-  }
-  if ((rc = check_launch()) != W4A8_OK) return rc;
-
-  const int lpr_i = pow2_floor_le((int)(I / 256), 8);
-  const unsigned grid_d = (unsigned)(L.maxtiles * (H / (256 / lpr_i)));
-  switch (lpr_i) {
-    case 1: down_kernel<1><<<grid_d, 256, 0, s>>>(ma); break;
-    case 2: down_kernel<2><<<grid_d, 256, 0, s>>>(ma); break;
-    case 4: down_kernel<4><<<grid_d, 256, 0, s>>>(ma); break;
-    default: down_kernel<8><<<grid_d, 256, 0, s>>>(ma); break;
-  }
-  if ((rc = check_launch()) != W4A8_OK) return rc;
+  uint8_t *hq = ws + L.hq;
+  float *y = reinterpret_cast<float *>(ws + L.y);
+  if ((rc = grouped_gateup(w_gu, ws_gu, ws + L.xq, ra.meta, ra.perm, ra.groups, ra.tiles,
+                           reinterpret_cast<float *>(ws + L.h), hq, L.maxtiles, T, H, I, E, k,
+                           s)) != W4A8_OK)
+    return rc;
+  if ((rc = grouped_down(w_d, ws_d, hq, ra.meta, ra.perm, ra.groups, ra.tiles, topk_w, y,
+                         L.maxtiles, T, H, I, E, k, s)) != W4A8_OK)
+    return rc;
 
   const int64_t n4 = T * (H / 4);
   combine_kernel<<<dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s>>>(
-      ma.y, ids, out, T, H, (int)k, (int)E, has_shared);
+      y, ids, out, T, H, (int)k, (int)E, has_shared);
   return check_launch();
 }
 
