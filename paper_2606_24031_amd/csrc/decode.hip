@@ -3,33 +3,35 @@
 // At M = 1 the layer streams (k + 1) experts' weights (8 routed + 1 shared,
 // 15.9 MB for the Qwen3-family shape) and does almost no arithmetic, so its
 // cost is HBM latency plus the chain of hand-offs between the gate/up and the
-// down projection; an extra kernel boundary alone costs about a third of the
-// layer.  Everything therefore runs in one grid of two kinds of workgroups
-// (the routed top-k experts and the always-on shared expert of Sec. 2.2; the
-// W4A8 product of Sec. 3.3):
+// down projection; an extra kernel boundary alone costs about 1.6 us.
+// Everything therefore runs in one grid of two kinds of workgroups (the routed
+// top-k experts and the always-on shared expert of Sec. 2.2; the W4A8 product
+// of Sec. 3.3):
 //
 //   A items (pair q, 32-column block b of h): issue the 64 gate/up row loads
-//     (one 144-byte eight-block group per lane for H = 2048),
-//     quantize x to Q8_0 into LDS, take the W4A8 dots, h = SiLU(g) * u, and
-//     publish Q8_0 of the 32 h values (exactly one block); count it in the
-//     pair's counter.
+//     (one 144-byte eight-block group per lane for H = 2048), quantize x to
+//     Q8_0 into LDS, take the W4A8 dots, reduce each row over its 8 lanes
+//     with DPP (gate row and up row of one h column sit in the same wave),
+//     h = SiLU(g) * u, and publish Q8_0 of the 32 h values (one block).
 //   B items (slab of RB down rows, all pairs): issue the down weight loads of
-//     every pair first, wait until every pair's h blocks are published, read
-//     them, take the dots and write out[n] = sum_q w_q y_q[n] (slots in
-//     order, then the shared expert) -- the combine never leaves the
-//     workgroup.
+//     every pair first, collect every pair's Q8_0(h) blocks, take the dots and
+//     write out[n] = sum_q w_q y_q[n] (slots in order, then the shared
+//     expert) -- the combine never leaves the workgroup.
+//
+// Hand-off: each published word is 64 bits, the payload in the low half and
+// the call's tag in the high half, written with agent-scope (sc1) stores.  A
+// B item polls the words themselves until every one carries this call's tag,
+// so there is no counter, no store acknowledgement wait and no second read.
+// The tag is one more than the call counter kept in the hand-off region; the
+// last workgroup of the launch to arrive at a two-level counter advances the
+// call counter and clears the arrival counters, after every workgroup has
+// read it.
 //
 // The wait is bounded: after `spin_limit` ticks of the 100 MHz real-time
-// counter a B item computes the missing Q8_0(h) blocks itself (the same code,
-// so the same bytes), so progress never depends on the order in which the
-// hardware starts workgroups.  Hand-off data crosses XCDs through agent-
-// coherent (sc1) stores and loads: a writer waits until its stores are
-// acknowledged (vmcnt 0) before the workgroup barrier and the counter add; a
-// reader polls the counter and then reads with sc1 loads, so no whole-L2
-// writeback or invalidate is needed.  Every workgroup finally arrives at a
-// two-level counter (one word per XCD slot, then one top word); the last
-// arrival of the launch clears every counter, so the sync words are zero
-// again when the call completes.
+// counter a B item computes every block itself (the same code, so the same
+// bytes, also published with the same tag) straight into its own staging, so
+// progress never depends on the order in which the hardware starts
+// workgroups.
 #include <cstdlib>
 
 #include "w4a8_dev.h"
@@ -39,15 +41,15 @@ namespace w4a8 {
 
 namespace {
 
-constexpr int NT = 512;    // threads per workgroup
-constexpr int NSUB = 8;    // first-level arrival counters
+constexpr int NT = 512;          // threads per workgroup: 8 waves
+constexpr int NSUB = 8;          // first-level arrival counters
+constexpr int XW = 9;            // hand-off words per h block: scale and code sum, 8 code words
+constexpr int XFER_HDR = 64;     // uint32 words ahead of the hand-off words: the call counter
 
-// Sync words (uint32, zero between calls), each alone in its own 256-byte
-// line: same-line atomics and polls serialize in the memory system, which
-// costs microseconds at this scale.  Slots: pair counters [64], arrival
-// counters [NSUB], top arrival counter [1].
-constexpr int SYNC_STRIDE = 64;   // words between sync slots (256 bytes)
-constexpr int SYNC_PAIR = 0, SYNC_SUB = 64, SYNC_TOP = 64 + NSUB, SYNC_SLOTS = 64 + NSUB + 1;
+// Arrival counters (uint32, zero between calls), each alone in its own
+// 256-byte line: same-line atomics serialize in the memory system.
+constexpr int SYNC_STRIDE = 64;
+constexpr int SYNC_SUB = 0, SYNC_TOP = NSUB, SYNC_SLOTS = NSUB + 1;
 __device__ __forceinline__ uint32_t *sync_word(uint32_t *sync, int slot) {
   return sync + slot * SYNC_STRIDE;
 }
@@ -58,8 +60,9 @@ struct DecodeArgs {
   const float *topk_w;     // [k]
   const uint8_t *w_gu, *w_d, *ws_gu, *ws_d;
   float *out;              // [H]
-  uint32_t *sync;
-  uint32_t *xfer;          // Q8_0(h) hand-off: [(k+1)][I/32][9 words]: scale, 8 code words
+  uint32_t *sync;          // arrival counters
+  uint32_t *calls;         // call counter (tag of this call = *calls + 1)
+  uint64_t *xfer;          // Q8_0(h) hand-off: [(k+1)][I/32][XW] tagged words
   uint8_t *xq;             // documented copy of Q8_0(x)   [H/32 blocks]
   float *h;                // documented copy of h          [(k+1)][I]
   uint8_t *hq;             // documented copy of Q8_0(h)    [(k+1)][I/32 blocks]
@@ -83,18 +86,19 @@ __device__ __forceinline__ float silu_f32(float g) { return g / (1.0f + expf(-g)
 __device__ __forceinline__ uint32_t counter_add(uint32_t *p, uint32_t v) {
   return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ uint32_t counter_load(const uint32_t *p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-// agent-coherent (sc1) store and load of hand-off words
-__device__ __forceinline__ void st_agent(uint32_t *p, uint32_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 __device__ __forceinline__ uint32_t ld_agent(const uint32_t *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-// wait until this wave's stores are acknowledged (s_waitcnt vmcnt(0))
-__device__ __forceinline__ void wait_stores() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+__device__ __forceinline__ void st_agent(uint32_t *p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// agent-coherent (sc1) 64-bit store and load of tagged hand-off words
+__device__ __forceinline__ void st_agent64(uint64_t *p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t ld_agent64(const uint64_t *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 __device__ __forceinline__ const uint8_t *expert_gu(const DecodeArgs &a, int e) {
   return e < a.E ? a.w_gu + (int64_t)e * (2 * a.I) * (a.H / 256) * (8 * Q4B) : a.ws_gu;
@@ -122,11 +126,16 @@ __host__ __device__ constexpr size_t act_buf_bytes(int nblocks) {
   return ((size_t)nblocks * 40 + 15) / 16 * 16;
 }
 
+// B item LDS after the staged Q8_0(h): NT dot partials, then the weighted
+// per-pair sums [rb][npairs padded to 4].
+__host__ __device__ constexpr size_t b_part_bytes(int npairs, int rb) {
+  return sizeof(float) * ((size_t)NT + (size_t)((npairs + 3) & ~3) * rb);
+}
+
 // Q8_0 of x (fp32 [H], global) into the LDS staging; with `xq_out` also the
 // 34-byte blocks to global memory.  8 lanes per block, 4 values per lane.
 // `first` is the lane's first float4 of x, loaded by the caller ahead of the
-// weight loads (a wave's loads return in order, so x is then not stuck
-// behind the weights).
+// weight loads.
 __device__ void quantize_x_to_lds(const DecodeArgs &a, ActBuf xb, uint8_t *xq_out,
                                   float4 first) {
   const int tasks = a.H / 4;
@@ -140,9 +149,7 @@ __device__ void quantize_x_to_lds(const DecodeArgs &a, ActBuf xb, uint8_t *xq_ou
     }
     uint32_t d16;
     const uint32_t packed = q8_0_block8(v, d16);
-    int sum = sdot4((int)packed, 0x01010101, 0);
-#pragma unroll
-    for (int o = 4; o > 0; o >>= 1) sum += __shfl_xor(sum, o, 8);
+    const int sum = sum8(sdot4((int)packed, 0x01010101, 0));
     if (live) {
       const int blk = t >> 3, j = t & 7;
       reinterpret_cast<uint32_t *>(xb.codes)[blk * 8 + j] = packed;
@@ -155,68 +162,78 @@ __device__ void quantize_x_to_lds(const DecodeArgs &a, ActBuf xb, uint8_t *xq_ou
   }
 }
 
-// Gate/up for h block b of pair q with expert e: 64 rows (32 gate + 32 up) of
-// G = H/256 eight-block groups each, unit u = row * G + g over the NT lanes.
-// Publishes Q8_0 of the 32 h values to the hand-off buffer (sc1) and, for
-// inspection, h and the 34-byte block to the documented workspace regions.
-// xb must hold Q8_0(x); `w0` is the lane's first unit, already loaded.
-// Uses part[64 * G] and hv[32] in LDS.
+// Lane roles in an A item: wave w owns h columns 4w..4w+3 of the block; in a
+// wave, lanes 16c..16c+7 hold the gate row of column 4w+c and lanes
+// 16c+8..16c+15 its up row; lane g of the 8 takes the eight-block groups
+// g, g+8, ... of that row (H/256 groups per row).
+struct ARole {
+  int hcol;     // column of h within the block, 0..31
+  bool up;      // this lane's row is the up row
+  int gg;       // first group of the lane
+};
+__device__ __forceinline__ ARole a_role() {
+  ARole r;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  r.hcol = wave * 4 + (lane >> 4);
+  r.up = (lane >> 3) & 1;
+  r.gg = lane & 7;
+  return r;
+}
+__device__ __forceinline__ const uint8_t *a_row(const DecodeArgs &a, int e, int b, const ARole &r) {
+  const int64_t row = r.up ? a.I + b * 32 + r.hcol : b * 32 + r.hcol;
+  return expert_gu(a, e) + row * ((int64_t)(a.H / 256) * 8 * Q4B);
+}
+
+// Gate/up for h block b of pair q with expert e.  xb must hold Q8_0(x); with
+// PRE the lane's first group is already loaded in `w0`.  Publishes the Q8_0
+// block of the 32 h values to the hand-off words with `tag`, and, for
+// inspection, h and the 34-byte block to the documented workspace regions;
+// with `stage` also into that LDS staging (block q * I/32 + b).  Uses hv[32]
+// in LDS; every thread of the workgroup must call it.
+template <bool PRE>
 __device__ void gateup_block(const DecodeArgs &a, int q, int e, int b, ActBuf xb, const W8 &w0,
-                             float *part, float *hv) {
+                             float *hv, uint32_t tag, const ActBuf *stage) {
   const int G = a.H / 256;
-  const int units = 64 * G;
-  const uint8_t *W = expert_gu(a, e);
-  const int64_t rowbytes = (int64_t)G * 8 * Q4B;
-  for (int u = threadIdx.x, j = 0; u < units; u += NT, j++) {
-    const int row = u / G, g = u % G;
-    const uint4 *codes = xb.codes + g * 16;
-    const float *dd = xb.d + g * 8;
-    const int *cc = xb.corr + g * 8;
-    float acc;
-    if (j == 0) {
-      acc = dot8_lds(w0, codes, dd, cc, 0.0f);
-    } else {
-      const int64_t r = row < 32 ? b * 32 + row : a.I + b * 32 + (row - 32);
-      W8 w;
-      load_w8(W + r * rowbytes + (int64_t)g * (8 * Q4B), w);
-      acc = dot8_lds(w, codes, dd, cc, 0.0f);
-    }
-    part[u] = acc;
+  const ARole r = a_role();
+  const uint8_t *W = a_row(a, e, b, r);
+  float acc = 0.0f;
+  int g = r.gg;
+  if (PRE) {
+    if (g < G) acc = dot8_lds(w0, xb.codes + g * 16, xb.d + g * 8, xb.corr + g * 8, acc);
+    g += 8;
+  }
+  for (; g < G; g += 8) {
+    W8 w;
+    load_w8(W + (int64_t)g * (8 * Q4B), w);
+    acc = dot8_lds(w, xb.codes + g * 16, xb.d + g * 8, xb.corr + g * 8, acc);
+  }
+  const float s = sum8(acc);               // row sum, in every lane of the 8
+  const float other = dpp_f<DPP_ROR8>(s);  // the up row's sum, seen from a gate lane
+  if (!r.up && r.gg == 0) {
+    const float h = silu_f32(s) * other;
+    hv[r.hcol] = h;
+    a.h[(int64_t)q * a.I + b * 32 + r.hcol] = h;
   }
   __syncthreads();
-  if (threadIdx.x < 64) {               // row sums in fixed group order
-    float s = 0.0f;
-    for (int g = 0; g < G; g++) s += part[threadIdx.x * G + g];
-    part[threadIdx.x * G] = s;
-  }
-  __syncthreads();
-  if (threadIdx.x < 32) {
-    const float gsum = part[threadIdx.x * G], usum = part[(32 + threadIdx.x) * G];
-    const float h = silu_f32(gsum) * usum;
-    hv[threadIdx.x] = h;
-    a.h[(int64_t)q * a.I + b * 32 + threadIdx.x] = h;
-  }
-  __syncthreads();
-  if (threadIdx.x < 8) {                // Q8_0 of the 32-value block, 8 lanes
+  if (threadIdx.x < 8) {                   // Q8_0 of the 32-value block, 8 lanes
     const int j = threadIdx.x;
     const float v[4] = {hv[4 * j], hv[4 * j + 1], hv[4 * j + 2], hv[4 * j + 3]};
     uint32_t d16;
     const uint32_t packed = q8_0_block8(v, d16);
-    uint32_t *xf = a.xfer + ((int64_t)q * (a.I / 32) + b) * 9;
-    st_agent(xf + 1 + j, packed);
-    if (j == 0) st_agent(xf, d16);
+    const int csum = sum8(sdot4((int)packed, 0x01010101, 0));   // |csum| <= 4064
+    uint64_t *xf = a.xfer + ((int64_t)q * (a.I / 32) + b) * XW;
+    const uint64_t hi = (uint64_t)tag << 32;
+    st_agent64(xf + 1 + j, hi | packed);
+    if (j == 0) st_agent64(xf, hi | d16 | ((uint32_t)csum << 16));
     store_q8_0_block8(a.hq + ((int64_t)q * (a.I / 32) + b) * Q8B, j, packed, d16);
-  }
-}
-
-__device__ __forceinline__ void load_gateup_unit(const DecodeArgs &a, int e, int b, W8 &w0) {
-  const int G = a.H / 256;
-  const int u = threadIdx.x;
-  if (u < 64 * G) {
-    const int64_t rowbytes = (int64_t)G * 8 * Q4B;
-    const int row = u / G, g = u % G;
-    const int64_t r = row < 32 ? b * 32 + row : a.I + b * 32 + (row - 32);
-    load_w8(expert_gu(a, e) + r * rowbytes + (int64_t)g * (8 * Q4B), w0);
+    if (stage != nullptr) {
+      const int blk = q * (a.I / 32) + b;
+      reinterpret_cast<uint32_t *>(stage->codes)[blk * 8 + j] = packed;
+      if (j == 0) {
+        stage->d[blk] = f16_bits_to_f32(d16);
+        stage->corr[blk] = -8 * csum;
+      }
+    }
   }
 }
 
@@ -225,8 +242,10 @@ __device__ __forceinline__ float4 load_x_first(const DecodeArgs &a) {
                                : make_float4(0.f, 0.f, 0.f, 0.f);
 }
 
-// Last arrival of the launch clears every sync word.
-__device__ void arrive(const DecodeArgs &a) {
+// Every workgroup arrives once; the last arrival of the launch advances the
+// call counter to `tag` and clears the arrival counters.  Each workgroup has
+// read the call counter before it arrives.
+__device__ void arrive(const DecodeArgs &a, uint32_t tag) {
   if (threadIdx.x != 0) return;
   const int nblocks = (int)gridDim.x;
   const int s = blockIdx.x % NSUB;
@@ -236,14 +255,60 @@ __device__ void arrive(const DecodeArgs &a) {
   const uint32_t nsubs = (uint32_t)(nblocks < NSUB ? nblocks : NSUB);
   const uint32_t top = counter_add(sync_word(a.sync, SYNC_TOP), 1u);
   if (top + 1u != nsubs) return;
-  for (int i = 0; i < SYNC_SLOTS; i++)
-    __hip_atomic_store(sync_word(a.sync, i), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  for (int i = 0; i < SYNC_SLOTS; i++) st_agent(sync_word(a.sync, i), 0u);
+  st_agent(a.calls, tag);
+}
+
+// One staged hand-off word i of the B item's LDS staging.
+__device__ __forceinline__ void stage_word(ActBuf hb, int i, uint32_t v) {
+  const int blk = i / XW, w = i - blk * XW;
+  if (w == 0) {
+    hb.d[blk] = f16_bits_to_f32(v);
+    hb.corr[blk] = -8 * (int)(int16_t)(v >> 16);
+  } else {
+    reinterpret_cast<uint32_t *>(hb.codes)[blk * 8 + (w - 1)] = v;
+  }
+}
+
+// Collect every valid pair's tagged Q8_0(h) words into the LDS staging.
+// Returns false (uniformly) when the wait bound passed first.  Bit j of
+// `pending` marks the lane's word i = threadIdx.x + j * NT as still to be
+// collected (j < NWMAX).  Two rounds of loads are in flight: the next round
+// is issued before the current one is examined, which halves the time
+// between a word becoming visible and a load that returns it.
+constexpr int NWMAX = 8;
+__device__ bool collect_h(const DecodeArgs &a, ActBuf hb, uint32_t tag, uint32_t pending,
+                          int *tflag) {
+  const uint64_t t0 = wall_clock64();
+  const uint64_t *src = a.xfer + threadIdx.x;
+  uint64_t cur[NWMAX], nxt[NWMAX];
+#pragma unroll
+  for (int j = 0; j < NWMAX; j++) cur[j] = ((pending >> j) & 1) ? ld_agent64(src + j * NT) : 0;
+  for (int it = 0;; it++) {
+#pragma unroll
+    for (int j = 0; j < NWMAX; j++) nxt[j] = ((pending >> j) & 1) ? ld_agent64(src + j * NT) : 0;
+#pragma unroll
+    for (int j = 0; j < NWMAX; j++) {
+      if (((pending >> j) & 1) && (uint32_t)(cur[j] >> 32) == tag) {
+        stage_word(hb, threadIdx.x + j * NT, (uint32_t)cur[j]);
+        pending &= ~(1u << j);
+      }
+    }
+    if (threadIdx.x == 0) tflag[it & 1] = (int64_t)(wall_clock64() - t0) > a.spin_limit;
+    if (__syncthreads_and(pending == 0)) return true;
+    // thread 0 wrote tflag[it & 1] before the barrier and next writes that
+    // slot two barriers later, after every wave has read it
+    if (tflag[it & 1]) return false;
+#pragma unroll
+    for (int j = 0; j < NWMAX; j++) cur[j] = nxt[j];
+  }
 }
 
 __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
   extern __shared__ __align__(16) uint8_t lds[];
   __shared__ float hv[32];
-  __shared__ int flag;
+  __shared__ float wq[64];
+  __shared__ int tflag[2];
   const int npairs = a.k + 1;
   const int nb_h = a.I / 32;                  // A items per pair
   const int na_total = npairs * nb_h;
@@ -253,27 +318,23 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
   if (item < na_total) {
     // ------------------------------------------------------------ A item
     const int q = item / nb_h, b = item % nb_h;
-    // x and the expert id together, both landed before the weights are
-    // issued (a wave's loads return in order)
+    // x and the expert id land before the weights are issued: on every path
+    // the later uses of x then wait for nothing in flight behind them
     const float4 x0 = load_x_first(a);
     int e;
     const bool valid = pair_valid(a, q, e);
-    asm volatile("" ::"v"(x0.x), "v"(x0.y), "v"(x0.z), "v"(x0.w), "s"(e));
+    asm volatile("" ::"v"(x0.x), "v"(x0.y), "v"(x0.z), "v"(x0.w), "v"(e));
     W8 w0;
-    if (valid) load_gateup_unit(a, e, b, w0);
+    const ARole r = a_role();
+    if (valid && r.gg < a.H / 256) load_w8(a_row(a, e, b, r) + (int64_t)r.gg * (8 * Q4B), w0);
+    const uint32_t tag = ld_agent(a.calls) + 1u;
     const ActBuf xb = act_buf(lds, nbx);
-    float *part = reinterpret_cast<float *>(lds + act_buf_bytes(nbx));
     if (valid || item == 0) {
       quantize_x_to_lds(a, xb, item == 0 ? a.xq : nullptr, x0);
       __syncthreads();
     }
-    if (valid) {
-      gateup_block(a, q, e, b, xb, w0, part, hv);
-      wait_stores();
-      __syncthreads();
-      if (threadIdx.x == 0) counter_add(sync_word(a.sync, SYNC_PAIR + q), 1u);
-    }
-    arrive(a);
+    if (valid) gateup_block<true>(a, q, e, b, xb, w0, hv, tag, nullptr);
+    arrive(a, tag);
     return;
   }
 
@@ -286,122 +347,110 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
   // unit u = (q * rb + r) * GI + g; one unit per lane (units <= NT)
   const int uq = threadIdx.x / (rb * GI), ur = (threadIdx.x / GI) % rb, ug = threadIdx.x % GI;
   const int64_t un = (int64_t)slab * rb + ur;
-  int ue = 0, ev = 0;
+  int ue = 0;
   const bool ulive = threadIdx.x < units && pair_valid(a, uq, ue) && un < a.H;
-  // lane q polls pair q below; its validity is read now, before the weight
-  // loads, so the poll does not wait behind them
-  const bool mine = threadIdx.x < npairs && pair_valid(a, threadIdx.x, ev);
-  asm volatile("" ::"v"(ue), "v"((int)mine));
+  // validity of every pair (lane q of each wave reads slot q) and the routing
+  // weights, all landed before the weight loads are issued
+  int ev;
+  const int lq = threadIdx.x & 63;
+  const bool lane_valid = lq < npairs && pair_valid(a, lq, ev);
+  const float wl = (int)threadIdx.x < a.k ? a.topk_w[threadIdx.x] : 1.0f;
+  asm volatile("" ::"v"(ue), "v"((int)ulive), "v"((int)lane_valid), "v"(wl));
   W8 wpre;
   if (ulive) load_w8(expert_d(a, ue) + un * rowbytes + (int64_t)ug * (8 * Q4B), wpre);
+  const uint64_t vmask = __ballot(lane_valid);    // wave-uniform
+  if (threadIdx.x < npairs) wq[threadIdx.x] = wl;
+  const uint32_t tag = ld_agent(a.calls) + 1u;
 
-  // wait until every valid pair has all nb_h blocks of Q8_0(h) (bounded):
-  // lane q polls pair q, all pairs at once (a coherent poll costs ~0.3 us
-  // under load, so polling them one after another would add up)
-  {
-    const uint64_t t0 = wall_clock64();
-    for (;;) {
-      const int ready = !mine || counter_load(sync_word(a.sync, SYNC_PAIR + threadIdx.x)) >=
-                                     (uint32_t)nb_h;
-      if (__syncthreads_and(ready)) { if (threadIdx.x == 0) flag = 1; break; }
-      if (threadIdx.x == 0) flag = (int64_t)(wall_clock64() - t0) > a.spin_limit ? 0 : 2;
-      __syncthreads();
-      if (flag == 0) break;
-      __builtin_amdgcn_s_sleep(2);
-      __syncthreads();   // everyone has read flag before thread 0 rewrites it
-    }
+  const int nbh_all = npairs * nb_h;
+  const int nwords = nbh_all * XW;
+  const ActBuf hb = act_buf(lds, nbh_all);
+  float *part = reinterpret_cast<float *>(lds + act_buf_bytes(nbh_all));
+  uint32_t pending = 0;
+#pragma unroll
+  for (int j = 0; j < NWMAX; j++) {
+    const int i = threadIdx.x + j * NT;
+    if (i < nwords && ((vmask >> (i / (XW * nb_h))) & 1)) pending |= 1u << j;
   }
-  __syncthreads();
-  if (!flag) {
-    // fallback: produce every pair's Q8_0(h) here (same code, same bytes)
-    const ActBuf xb = act_buf(lds, nbx);
-    float *gpart = reinterpret_cast<float *>(lds + act_buf_bytes(nbx));
+  if (!collect_h(a, hb, tag, pending, tflag)) {
+    // fallback: compute every pair's Q8_0(h) here (same code, same bytes)
+    const ActBuf xb = act_buf(lds + act_buf_bytes(nbh_all) + b_part_bytes(npairs, rb), nbx);
     quantize_x_to_lds(a, xb, nullptr, load_x_first(a));
     __syncthreads();
     for (int q = 0; q < npairs; q++) {
+      if (!((vmask >> q) & 1)) continue;
       int e;
-      if (!pair_valid(a, q, e)) continue;
+      pair_valid(a, q, e);
       for (int b = 0; b < nb_h; b++) {
-        W8 w0;
-        load_gateup_unit(a, e, b, w0);
-        gateup_block(a, q, e, b, xb, w0, gpart, hv);
+        gateup_block<false>(a, q, e, b, xb, W8{}, hv, tag, &hb);
         __syncthreads();
       }
     }
-    wait_stores();
-    __syncthreads();
   }
-  // Q8_0(h) of every valid pair: hand-off words -> LDS staging
-  const int nbh_all = npairs * nb_h;
-  const ActBuf hb = act_buf(lds, nbh_all);
-  float *part = reinterpret_cast<float *>(lds + act_buf_bytes(nbh_all));
-  for (int i = threadIdx.x; i < nbh_all * 9; i += NT) {
-    const int blk = i / 9, w = i % 9;
-    int e;
-    if (!pair_valid(a, blk / nb_h, e)) continue;
-    const uint32_t v = ld_agent(a.xfer + i);
-    if (w == 0)
-      hb.d[blk] = f16_bits_to_f32(v);
-    else
-      reinterpret_cast<uint32_t *>(hb.codes)[blk * 8 + (w - 1)] = v;
-  }
-  __syncthreads();
-  for (int blk = threadIdx.x; blk < nbh_all; blk += NT) {
-    int e;
-    if (!pair_valid(a, blk / nb_h, e)) continue;
-    const uint32_t *c = reinterpret_cast<const uint32_t *>(hb.codes) + blk * 8;
-    int s = 0;
-#pragma unroll
-    for (int i = 0; i < 8; i++) s = sdot4((int)c[i], 0x01010101, s);
-    hb.corr[blk] = -8 * s;
-  }
-  __syncthreads();
   if (threadIdx.x < units) {
     float acc = 0.0f;
     if (ulive) {
       const int blk0 = uq * nb_h + ug * 8;
-      if (flag) {
-        acc = dot8_lds(wpre, hb.codes + blk0 * 2, hb.d + blk0, hb.corr + blk0, 0.0f);
-      } else {
-        W8 w;
-        load_w8(expert_d(a, ue) + un * rowbytes + (int64_t)ug * (8 * Q4B), w);
-        acc = dot8_lds(w, hb.codes + blk0 * 2, hb.d + blk0, hb.corr + blk0, 0.0f);
-      }
+      acc = dot8_lds(wpre, hb.codes + blk0 * 2, hb.d + blk0, hb.corr + blk0, 0.0f);
     }
     part[threadIdx.x] = acc;
   }
   __syncthreads();
+  // y_q[n] = sum over g (in order), weighted; stored transposed [r][q] with
+  // the pair count padded to a multiple of 4 (pads and skipped slots are 0)
+  const int npad = (npairs + 3) & ~3;
+  float *yw = part + NT;
+  for (int t = threadIdx.x; t < npad * rb; t += NT) {
+    const int q = t / rb, r = t - q * rb;
+    float v = 0.0f;
+    if (q < npairs && ((vmask >> q) & 1)) {
+      float y = 0.0f;
+      for (int g = 0; g < GI; g++) y += part[t * GI + g];
+      v = wq[q] * y;
+    }
+    yw[r * npad + q] = v;
+  }
+  __syncthreads();
+  // out[n] = sum over the slots in order, then the shared expert
   for (int r = threadIdx.x; r < rb; r += NT) {
     const int64_t n = (int64_t)slab * rb + r;
     if (n >= a.H) continue;
+    const float4 *row = reinterpret_cast<const float4 *>(yw + r * npad);
     float o = 0.0f;
-    for (int q = 0; q < npairs; q++) {
-      int e;
-      if (!pair_valid(a, q, e)) continue;
-      float y = 0.0f;
-      for (int g = 0; g < GI; g++) y += part[(q * rb + r) * GI + g];
-      o += (q < a.k ? a.topk_w[q] : 1.0f) * y;
+    for (int q4 = 0; q4 < npad / 4; q4++) {
+      const float4 v = row[q4];
+      o += v.x;
+      o += v.y;
+      o += v.z;
+      o += v.w;
     }
     a.out[n] = o;
   }
-  arrive(a);
+  arrive(a, tag);
 }
 
 }  // namespace
 
 size_t decode_sync_words(int64_t) { return (size_t)SYNC_SLOTS * SYNC_STRIDE; }
 
-// Hand-off buffer words for T = 1.
-size_t decode_xfer_words(int64_t I, int64_t k) { return (size_t)(k + 1) * (I / 32) * 9; }
+// Hand-off region for T = 1, in uint32 words: the call counter's line, then
+// XW 64-bit words per h block.
+size_t decode_xfer_words(int64_t I, int64_t k) {
+  return (size_t)XFER_HDR + (size_t)(k + 1) * (I / 32) * XW * 2;
+}
 
 bool decode_supported(int64_t H, int64_t I, int64_t k) {
-  // B items hold every pair of one down row at one unit per lane; LDS holds
-  // the staged Q8_0(x) plus 64 * H/256 partials (A) or the staged Q8_0(h) of
-  // every pair plus NT partials (B).
-  const size_t lda = act_buf_bytes((int)(H / 32)) + sizeof(float) * 64 * (H / 256);
-  const size_t ldb = act_buf_bytes((int)((k + 1) * (I / 32))) + sizeof(float) * NT;
-  return H <= 16384 && (k + 1) <= 64 && (k + 1) * (I / 256) <= NT && lda <= 48 * 1024 &&
-         ldb <= 48 * 1024;
+  // A items: 8 waves x 4 h columns = one 32-column block.  B items hold
+  // every pair of one down row at one unit per lane, and at most NWMAX
+  // hand-off words per lane; LDS holds the staged Q8_0(x) (A) or the staged
+  // Q8_0(h) of every pair, the partials and, for the fallback, Q8_0(x) (B).
+  if (H < 256 || I < 256 || k < 1 || H > 16384 || k + 1 > 64 || (k + 1) * (I / 256) > NT)
+    return false;
+  const int64_t nbh_all = (k + 1) * (I / 32);
+  const size_t lda = act_buf_bytes((int)(H / 32));
+  const int rb = (int)(NT / ((k + 1) * (I / 256)));
+  const size_t ldb = act_buf_bytes((int)nbh_all) + b_part_bytes((int)(k + 1), rb) + lda;
+  return nbh_all * XW <= NWMAX * NT && lda <= 48 * 1024 && ldb <= 48 * 1024;
 }
 
 int decode_forward(const float *x, const int32_t *ids, const float *topk_w, const uint8_t *w_gu,
@@ -413,7 +462,8 @@ int decode_forward(const float *x, const int32_t *ids, const float *topk_w, cons
   a.w_gu = w_gu; a.w_d = w_d; a.ws_gu = ws_gu; a.ws_d = ws_d;
   a.out = out;
   a.sync = sync;
-  a.xfer = xfer;
+  a.calls = xfer;
+  a.xfer = reinterpret_cast<uint64_t *>(xfer + XFER_HDR);
   a.xq = xq; a.h = h; a.hq = hq;
   a.H = (int)H; a.I = (int)I; a.E = (int)E; a.k = (int)k;
   const int npairs = (int)k + 1;
@@ -424,8 +474,8 @@ int decode_forward(const float *x, const int32_t *ids, const float *topk_w, cons
   a.spin_limit = 100000;
   if (const char *env = std::getenv("W4A8_DECODE_SPIN_TICKS")) a.spin_limit = std::atoll(env);
   const unsigned grid = (unsigned)(npairs * (I / 32) + a.n_b);
-  const size_t lda = act_buf_bytes((int)(H / 32)) + sizeof(float) * 64 * (H / 256);
-  const size_t ldb = act_buf_bytes(npairs * (int)(I / 32)) + sizeof(float) * NT;
+  const size_t lda = act_buf_bytes((int)(H / 32));
+  const size_t ldb = act_buf_bytes(npairs * (int)(I / 32)) + b_part_bytes(npairs, a.rb) + lda;
   const size_t lds = lda > ldb ? lda : ldb;
   decode_kernel<<<dim3(grid), dim3(NT), lds, s>>>(a);
   return check_launch();

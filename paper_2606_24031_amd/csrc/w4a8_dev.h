@@ -150,6 +150,44 @@ __device__ __forceinline__ float dot8_lds(const W8 &w, const uint4 *__restrict__
   return acc;
 }
 
+// Cross-lane moves through DPP (a VALU operand modifier, no LDS round trip).
+// quad_perm [1,0,3,2] and [2,3,0,1] exchange with lane^1 and lane^2;
+// row_half_mirror maps lane i of each 8-lane half-row to lane 7-i, which
+// pairs every lane of one quad with a lane of the other; row_ror:8 within a
+// 16-lane row gives lane^8.
+constexpr int DPP_XOR1 = 0xB1, DPP_XOR2 = 0x4E, DPP_HALF_MIRROR = 0x141, DPP_ROR8 = 0x128;
+
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __builtin_bit_cast(float, dpp_i<CTRL>(__builtin_bit_cast(int, v)));
+}
+
+// Reductions over each group of 8 consecutive lanes (all 8 must be active);
+// every lane of a group ends with the same value (fp32 addition is
+// commutative, so the mirrored partners compute identical sums).
+__device__ __forceinline__ float sum8(float v) {
+  v += dpp_f<DPP_XOR1>(v);
+  v += dpp_f<DPP_XOR2>(v);
+  v += dpp_f<DPP_HALF_MIRROR>(v);
+  return v;
+}
+__device__ __forceinline__ int sum8(int v) {
+  v += dpp_i<DPP_XOR1>(v);
+  v += dpp_i<DPP_XOR2>(v);
+  v += dpp_i<DPP_HALF_MIRROR>(v);
+  return v;
+}
+__device__ __forceinline__ float max8(float v) {
+  v = fmaxf(v, dpp_f<DPP_XOR1>(v));
+  v = fmaxf(v, dpp_f<DPP_XOR2>(v));
+  v = fmaxf(v, dpp_f<DPP_HALF_MIRROR>(v));
+  return v;
+}
+
 // Sum over groups of `width` consecutive lanes (width a power of two <= 64).
 template <int WIDTH>
 __device__ __forceinline__ float lane_group_sum(float v) {
@@ -160,13 +198,13 @@ __device__ __forceinline__ float lane_group_sum(float v) {
 
 // Q8_0 of one 32-value block held by 8 consecutive lanes, 4 values each
 // (lane j of the 8 holds elements 4j..4j+3).  Returns the four codes packed
-// in a dword and, through d16, the block's fp16 scale bits.  Same fp32 steps
+// in a dword and, through d16, the block's fp16 scale bits.  All 8 lanes of
+// the group must be active.  Same fp32 steps
 // as the format definition: amax, one division by 127, fp16 RNE, one
 // reciprocal of the stored scale, one multiply per element, round half away.
 __device__ __forceinline__ uint32_t q8_0_block8(const float v[4], uint32_t &d16) {
-  float amax = fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3])));
-#pragma unroll
-  for (int o = 4; o > 0; o >>= 1) amax = fmaxf(amax, __shfl_xor(amax, o, 8));
+  const float amax =
+      max8(fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
   const float d32 = amax / 127.0f;
   d16 = f32_to_f16_bits(d32);
   const float df = f16_bits_to_f32(d16);
