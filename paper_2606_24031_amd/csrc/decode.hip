@@ -4,31 +4,34 @@
 // 15.9 MB for the Qwen3-family shape) and does almost no arithmetic, so its
 // cost is HBM latency plus the chain of hand-offs between the gate/up and the
 // down projection; an extra kernel boundary alone costs about 1.6 us.
-// Everything therefore runs in one grid of two kinds of workgroups (the routed
-// top-k experts and the always-on shared expert of Sec. 2.2; the W4A8 product
-// of Sec. 3.3):
+// Everything therefore runs in one grid of about one workgroup per compute
+// unit, of two kinds (the routed top-k experts and the always-on shared
+// expert of Sec. 2.2; the W4A8 product of Sec. 3.3):
 //
-//   A items (pair q, 32-column block b of h): issue the 64 gate/up row loads
-//     (one 144-byte eight-block group per lane for H = 2048), quantize x to
-//     Q8_0 into LDS, take the W4A8 dots, reduce each row over its 8 lanes
-//     with DPP (gate row and up row of one h column sit in the same wave),
-//     h = SiLU(g) * u, and publish Q8_0 of the 32 h values (one block).
-//   B items (slab of RB down rows, all pairs): issue the down weight loads of
-//     every pair first, collect every pair's Q8_0(h) blocks, take the dots and
-//     write out[n] = sum_q w_q y_q[n] (slots in order, then the shared
-//     expert) -- the combine never leaves the workgroup.
+//   gate/up items (pair q, 32-column block b of h): issue the 64 gate/up row
+//     loads (one 144-byte eight-block group per lane for H = 2048), quantize
+//     x to Q8_0 into LDS, take the W4A8 dots, reduce each row over its 8
+//     lanes with DPP (gate row and up row of one h column sit in the same
+//     wave), h = SiLU(g) * u, and publish Q8_0 of the 32 h values (one block).
+//   down slabs (rb down rows, all pairs): issue the down weight loads of every
+//     pair first, collect every pair's Q8_0(h), take the dots and write
+//     out[n] = sum_q w_q y_q[n] (slots in order, then the shared expert) --
+//     the combine never leaves the workgroup.  The slabs fill the compute
+//     units the gate/up items leave free.
 //
 // Hand-off: each published word is 64 bits, the payload in the low half and
-// the call's tag in the high half, written with agent-scope (sc1) stores.  A
-// B item polls the words themselves until every one carries this call's tag,
-// so there is no counter, no store acknowledgement wait and no second read.
-// The tag is one more than the call counter kept in the hand-off region; the
-// last workgroup of the launch to arrive at a two-level counter advances the
-// call counter and clears the arrival counters, after every workgroup has
-// read it.
+// the call's tag in the high half, written with agent-scope (sc1) stores;
+// each block's words sit alone in one 128-byte line, so no line is written
+// from two XCDs.  A slab polls all the words until every one carries this
+// call's tag: one poll round trip and the store's visibility cost about
+// 0.5 us each across XCDs, so the words are read in a single pass rather
+// than a flag first and the data after.  The tag is one more than the call
+// counter kept in the hand-off region; every workgroup arrives at a
+// two-level counter once it has read the tag, and the last arrival advances
+// the call counter and clears the arrival counters.
 //
-// The wait is bounded: after `spin_limit` ticks of the 100 MHz real-time
-// counter a B item computes every block itself (the same code, so the same
+// The wait is bounded: after `spin_rounds` poll rounds (each a load round
+// trip, about 0.5-1 us) a slab computes every block itself (the same code, so the same
 // bytes, also published with the same tag) straight into its own staging, so
 // progress never depends on the order in which the hardware starts
 // workgroups.
@@ -44,6 +47,7 @@ namespace {
 constexpr int NT = 512;          // threads per workgroup: 8 waves
 constexpr int NSUB = 8;          // first-level arrival counters
 constexpr int XW = 9;            // hand-off words per h block: scale and code sum, 8 code words
+constexpr int XSTRIDE = 16;      // 64-bit words between blocks: each block alone in a 128-byte line
 constexpr int XFER_HDR = 64;     // uint32 words ahead of the hand-off words: the call counter
 
 // Arrival counters (uint32, zero between calls), each alone in its own
@@ -62,14 +66,13 @@ struct DecodeArgs {
   float *out;              // [H]
   uint32_t *sync;          // arrival counters
   uint32_t *calls;         // call counter (tag of this call = *calls + 1)
-  uint64_t *xfer;          // Q8_0(h) hand-off: [(k+1)][I/32][XW] tagged words
+  uint64_t *xfer;          // Q8_0(h) hand-off: [(k+1) * I/32][XSTRIDE] tagged words (XW used)
   uint8_t *xq;             // documented copy of Q8_0(x)   [H/32 blocks]
   float *h;                // documented copy of h          [(k+1)][I]
   uint8_t *hq;             // documented copy of Q8_0(h)    [(k+1)][I/32 blocks]
   int H, I, E, k;
-  int rb;                  // down rows per B item
-  int n_b;                 // B items
-  int64_t spin_limit;      // real-time ticks before a B item computes h itself
+  int rb;                  // down rows per slab
+  int spin_rounds;         // poll rounds before a slab computes h itself
 };
 
 __device__ __forceinline__ bool pair_valid(const DecodeArgs &a, int q, int &expert) {
@@ -107,29 +110,39 @@ __device__ __forceinline__ const uint8_t *expert_d(const DecodeArgs &a, int e) {
   return e < a.E ? a.w_d + (int64_t)e * a.H * (a.I / 256) * (8 * Q4B) : a.ws_d;
 }
 
-// LDS staging of activation blocks (see dot8_lds): codes [n][8] dwords,
-// scale [n] fp32, correction [n] int32, carved from one dynamic LDS buffer.
+// LDS staging of activation blocks (see dot8_lds): the 32 codes of each
+// block as 8 dwords, groups of 8 blocks 272 bytes apart (16 bytes of padding
+// per group), then scale [n] fp32 and correction [n] int32, carved from one
+// dynamic LDS buffer.  The lanes of a wave read up to 8 different groups at
+// once; without the padding those addresses would be 256 bytes apart and all
+// fall in the same LDS banks.
+constexpr int GROUP_U4 = 17;   // uint4 per 8-block group: 16 of codes + 1 of padding
 struct ActBuf {
   uint4 *codes;
   float *d;
   int *corr;
 };
 
+__host__ __device__ constexpr size_t act_codes_bytes(int nblocks) {
+  return (size_t)((nblocks + 7) / 8) * GROUP_U4 * 16;
+}
 __device__ __forceinline__ ActBuf act_buf(uint8_t *base, int nblocks) {
   ActBuf b;
   b.codes = reinterpret_cast<uint4 *>(base);
-  b.d = reinterpret_cast<float *>(base + (size_t)nblocks * 32);
-  b.corr = reinterpret_cast<int *>(base + (size_t)nblocks * 36);
+  b.d = reinterpret_cast<float *>(base + act_codes_bytes(nblocks));
+  b.corr = reinterpret_cast<int *>(base + act_codes_bytes(nblocks) + (size_t)nblocks * 4);
   return b;
 }
 __host__ __device__ constexpr size_t act_buf_bytes(int nblocks) {
-  return ((size_t)nblocks * 40 + 15) / 16 * 16;
+  return (act_codes_bytes(nblocks) + (size_t)nblocks * 8 + 15) / 16 * 16;
 }
-
-// B item LDS after the staged Q8_0(h): NT dot partials, then the weighted
-// per-pair sums [rb][npairs padded to 4].
-__host__ __device__ constexpr size_t b_part_bytes(int npairs, int rb) {
-  return sizeof(float) * ((size_t)NT + (size_t)((npairs + 3) & ~3) * rb);
+// dword j (0..7) of block blk's codes
+__device__ __forceinline__ uint32_t *code_word(ActBuf b, int blk, int j) {
+  return reinterpret_cast<uint32_t *>(b.codes + (blk >> 3) * GROUP_U4) + (blk & 7) * 8 + j;
+}
+// the codes of the 8-block group starting at block blk0 (a multiple of 8)
+__device__ __forceinline__ const uint4 *group_codes(ActBuf b, int blk0) {
+  return b.codes + (blk0 >> 3) * GROUP_U4;
 }
 
 // Q8_0 of x (fp32 [H], global) into the LDS staging; with `xq_out` also the
@@ -152,7 +165,7 @@ __device__ void quantize_x_to_lds(const DecodeArgs &a, ActBuf xb, uint8_t *xq_ou
     const int sum = sum8(sdot4((int)packed, 0x01010101, 0));
     if (live) {
       const int blk = t >> 3, j = t & 7;
-      reinterpret_cast<uint32_t *>(xb.codes)[blk * 8 + j] = packed;
+      *code_word(xb, blk, j) = packed;
       if (j == 0) {
         xb.d[blk] = f16_bits_to_f32(d16);
         xb.corr[blk] = -8 * sum;
@@ -199,13 +212,13 @@ __device__ void gateup_block(const DecodeArgs &a, int q, int e, int b, ActBuf xb
   float acc = 0.0f;
   int g = r.gg;
   if (PRE) {
-    if (g < G) acc = dot8_lds(w0, xb.codes + g * 16, xb.d + g * 8, xb.corr + g * 8, acc);
+    if (g < G) acc = dot8_lds(w0, group_codes(xb, g * 8), xb.d + g * 8, xb.corr + g * 8, acc);
     g += 8;
   }
   for (; g < G; g += 8) {
     W8 w;
     load_w8(W + (int64_t)g * (8 * Q4B), w);
-    acc = dot8_lds(w, xb.codes + g * 16, xb.d + g * 8, xb.corr + g * 8, acc);
+    acc = dot8_lds(w, group_codes(xb, g * 8), xb.d + g * 8, xb.corr + g * 8, acc);
   }
   const float s = sum8(acc);               // row sum, in every lane of the 8
   const float other = dpp_f<DPP_ROR8>(s);  // the up row's sum, seen from a gate lane
@@ -221,14 +234,14 @@ __device__ void gateup_block(const DecodeArgs &a, int q, int e, int b, ActBuf xb
     uint32_t d16;
     const uint32_t packed = q8_0_block8(v, d16);
     const int csum = sum8(sdot4((int)packed, 0x01010101, 0));   // |csum| <= 4064
-    uint64_t *xf = a.xfer + ((int64_t)q * (a.I / 32) + b) * XW;
+    uint64_t *xf = a.xfer + (int64_t)(q * (a.I / 32) + b) * XSTRIDE;
     const uint64_t hi = (uint64_t)tag << 32;
     st_agent64(xf + 1 + j, hi | packed);
     if (j == 0) st_agent64(xf, hi | d16 | ((uint32_t)csum << 16));
     store_q8_0_block8(a.hq + ((int64_t)q * (a.I / 32) + b) * Q8B, j, packed, d16);
     if (stage != nullptr) {
       const int blk = q * (a.I / 32) + b;
-      reinterpret_cast<uint32_t *>(stage->codes)[blk * 8 + j] = packed;
+      *code_word(*stage, blk, j) = packed;
       if (j == 0) {
         stage->d[blk] = f16_bits_to_f32(d16);
         stage->corr[blk] = -8 * csum;
@@ -259,65 +272,81 @@ __device__ void arrive(const DecodeArgs &a, uint32_t tag) {
   st_agent(a.calls, tag);
 }
 
-// One staged hand-off word i of the B item's LDS staging.
-__device__ __forceinline__ void stage_word(ActBuf hb, int i, uint32_t v) {
-  const int blk = i / XW, w = i - blk * XW;
+// Stage word w of block blk of the hand-off.
+__device__ __forceinline__ void stage_word(ActBuf hb, int blk, int w, uint32_t v) {
   if (w == 0) {
     hb.d[blk] = f16_bits_to_f32(v);
     hb.corr[blk] = -8 * (int)(int16_t)(v >> 16);
   } else {
-    reinterpret_cast<uint32_t *>(hb.codes)[blk * 8 + (w - 1)] = v;
+    *code_word(hb, blk, w - 1) = v;
   }
 }
 
-// Collect every valid pair's tagged Q8_0(h) words into the LDS staging.
-// Returns false (uniformly) when the wait bound passed first.  Bit j of
-// `pending` marks the lane's word i = threadIdx.x + j * NT as still to be
-// collected (j < NWMAX).  Two rounds of loads are in flight: the next round
-// is issued before the current one is examined, which halves the time
-// between a word becoming visible and a load that returns it.
+// Collect hand-off words [0, cnt) of the valid pairs into the staging (word
+// i is word i % XW of block i / XW); lane takes the words
+// threadIdx.x + j * NT, j < NWMAX.  One barrier per round:
+// a wave with words still missing sets notdone[round % 3] before it, everyone
+// reads it after, and thread 0 clears the slot of round + 2, which nobody
+// reads or writes until after the next barrier.  The round count is the same
+// in every wave, so the bound needs no broadcast.  Returns false (uniformly)
+// when the bound passed first; notdone[] must be zero on entry.
 constexpr int NWMAX = 8;
-__device__ bool collect_h(const DecodeArgs &a, ActBuf hb, uint32_t tag, uint32_t pending,
-                          int *tflag) {
-  const uint64_t t0 = wall_clock64();
-  const uint64_t *src = a.xfer + threadIdx.x;
-  uint64_t cur[NWMAX], nxt[NWMAX];
+__device__ bool collect(const DecodeArgs &a, ActBuf hb, uint32_t tag, int cnt, uint64_t vmask,
+                        int *notdone) {
+  const int nb_h = a.I / 32;
+  uint32_t pending = 0;
+  int blk[NWMAX], w[NWMAX];
 #pragma unroll
-  for (int j = 0; j < NWMAX; j++) cur[j] = ((pending >> j) & 1) ? ld_agent64(src + j * NT) : 0;
+  for (int j = 0; j < NWMAX; j++) {
+    const int i = (int)threadIdx.x + j * NT;
+    blk[j] = i / XW;
+    w[j] = i - blk[j] * XW;
+    if (i < cnt && ((vmask >> (blk[j] / nb_h)) & 1)) pending |= 1u << j;
+  }
   for (int it = 0;; it++) {
+    uint64_t v[NWMAX];
 #pragma unroll
-    for (int j = 0; j < NWMAX; j++) nxt[j] = ((pending >> j) & 1) ? ld_agent64(src + j * NT) : 0;
+    for (int j = 0; j < NWMAX; j++)
+      v[j] = ((pending >> j) & 1) ? ld_agent64(a.xfer + (int64_t)blk[j] * XSTRIDE + w[j]) : 0;
 #pragma unroll
     for (int j = 0; j < NWMAX; j++) {
-      if (((pending >> j) & 1) && (uint32_t)(cur[j] >> 32) == tag) {
-        stage_word(hb, threadIdx.x + j * NT, (uint32_t)cur[j]);
+      if (((pending >> j) & 1) && (uint32_t)(v[j] >> 32) == tag) {
+        stage_word(hb, blk[j], w[j], (uint32_t)v[j]);
         pending &= ~(1u << j);
       }
     }
-    if (threadIdx.x == 0) tflag[it & 1] = (int64_t)(wall_clock64() - t0) > a.spin_limit;
-    if (__syncthreads_and(pending == 0)) return true;
-    // thread 0 wrote tflag[it & 1] before the barrier and next writes that
-    // slot two barriers later, after every wave has read it
-    if (tflag[it & 1]) return false;
-#pragma unroll
-    for (int j = 0; j < NWMAX; j++) cur[j] = nxt[j];
+    const int slot = it % 3;
+    if (__ballot(pending != 0) != 0 && (threadIdx.x & 63) == 0) notdone[slot] = 1;
+    __syncthreads();
+    if (notdone[slot] == 0) return true;
+    if (threadIdx.x == 0) notdone[(it + 2) % 3] = 0;
+    if (it >= a.spin_rounds) return false;
   }
+}
+
+// LDS: Q8_0(x) staging, then Q8_0(h) staging of every pair, then the
+// weighted per-pair sums [rb][k+1 padded to 4] and, when I > 512, the down
+// partials (NT floats).
+__host__ __device__ constexpr size_t lds_x_bytes(int H) { return act_buf_bytes(H / 32); }
+__host__ __device__ constexpr size_t lds_bytes(int H, int I, int k, int rb) {
+  return lds_x_bytes(H) + act_buf_bytes((k + 1) * (I / 32)) +
+         sizeof(float) * ((size_t)rb * ((k + 1 + 3) & ~3) + (size_t)NT);
 }
 
 __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
   extern __shared__ __align__(16) uint8_t lds[];
   __shared__ float hv[32];
   __shared__ float wq[64];
-  __shared__ int tflag[2];
+  __shared__ int notdone[3];
   const int npairs = a.k + 1;
-  const int nb_h = a.I / 32;                  // A items per pair
-  const int na_total = npairs * nb_h;
-  const int item = blockIdx.x;
-  const int nbx = a.H / 32;                   // blocks of Q8_0(x)
+  const int nb_h = a.I / 32;                  // gate/up items per pair
+  const int nbh = npairs * nb_h;              // h blocks of every pair
+  const int wg = blockIdx.x;
+  const ActBuf xb = act_buf(lds, a.H / 32);
 
-  if (item < na_total) {
-    // ------------------------------------------------------------ A item
-    const int q = item / nb_h, b = item % nb_h;
+  if (wg < nbh) {
+    // --------------------------------------------------- gate/up item
+    const int q = wg / nb_h, b = wg - q * nb_h;
     // x and the expert id land before the weights are issued: on every path
     // the later uses of x then wait for nothing in flight behind them
     const float4 x0 = load_x_first(a);
@@ -328,9 +357,8 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
     const ARole r = a_role();
     if (valid && r.gg < a.H / 256) load_w8(a_row(a, e, b, r) + (int64_t)r.gg * (8 * Q4B), w0);
     const uint32_t tag = ld_agent(a.calls) + 1u;
-    const ActBuf xb = act_buf(lds, nbx);
-    if (valid || item == 0) {
-      quantize_x_to_lds(a, xb, item == 0 ? a.xq : nullptr, x0);
+    if (valid || wg == 0) {
+      quantize_x_to_lds(a, xb, wg == 0 ? a.xq : nullptr, x0);
       __syncthreads();
     }
     if (valid) gateup_block<true>(a, q, e, b, xb, w0, hv, tag, nullptr);
@@ -338,43 +366,43 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
     return;
   }
 
-  // -------------------------------------------------------------- B item
-  const int slab = item - na_total;
+  // ------------------------------------------------------ down slab
   const int rb = a.rb;
   const int GI = a.I / 256;
-  const int64_t rowbytes = (int64_t)GI * 8 * Q4B;
   const int units = npairs * rb * GI;
-  // unit u = (q * rb + r) * GI + g; one unit per lane (units <= NT)
+  // unit u = (q * rb + r) * GI + g: one 144-byte group per lane; a wave then
+  // reads the Q8_0(h) groups of one or two pairs only, so its LDS reads of
+  // them are mostly broadcasts
   const int uq = threadIdx.x / (rb * GI), ur = (threadIdx.x / GI) % rb, ug = threadIdx.x % GI;
-  const int64_t un = (int64_t)slab * rb + ur;
+  const int64_t row0 = (int64_t)(wg - nbh) * rb;
+  const int64_t un = row0 + ur;
+  // the units' experts, every pair's validity (lane q of each wave reads
+  // slot q) and the routing weights land before the weight loads are issued
   int ue = 0;
-  const bool ulive = threadIdx.x < units && pair_valid(a, uq, ue) && un < a.H;
-  // validity of every pair (lane q of each wave reads slot q) and the routing
-  // weights, all landed before the weight loads are issued
+  const bool ulive = (int)threadIdx.x < units && un < a.H && pair_valid(a, uq, ue);
   int ev;
   const int lq = threadIdx.x & 63;
   const bool lane_valid = lq < npairs && pair_valid(a, lq, ev);
   const float wl = (int)threadIdx.x < a.k ? a.topk_w[threadIdx.x] : 1.0f;
   asm volatile("" ::"v"(ue), "v"((int)ulive), "v"((int)lane_valid), "v"(wl));
   W8 wpre;
-  if (ulive) load_w8(expert_d(a, ue) + un * rowbytes + (int64_t)ug * (8 * Q4B), wpre);
+  if (ulive)
+    load_w8(expert_d(a, ue) + un * ((int64_t)GI * 8 * Q4B) + (int64_t)ug * (8 * Q4B), wpre);
   const uint64_t vmask = __ballot(lane_valid);    // wave-uniform
-  if (threadIdx.x < npairs) wq[threadIdx.x] = wl;
+  if ((int)threadIdx.x < npairs) wq[threadIdx.x] = wl;
   const uint32_t tag = ld_agent(a.calls) + 1u;
+  // a workgroup may arrive as soon as it has read the tag; here the atomic's
+  // return (which waits for this wave's weight loads) also keeps the first
+  // poll off the memory system while the gate/up weights stream
+  arrive(a, tag);
 
-  const int nbh_all = npairs * nb_h;
-  const int nwords = nbh_all * XW;
-  const ActBuf hb = act_buf(lds, nbh_all);
-  float *part = reinterpret_cast<float *>(lds + act_buf_bytes(nbh_all));
-  uint32_t pending = 0;
-#pragma unroll
-  for (int j = 0; j < NWMAX; j++) {
-    const int i = threadIdx.x + j * NT;
-    if (i < nwords && ((vmask >> (i / (XW * nb_h))) & 1)) pending |= 1u << j;
-  }
-  if (!collect_h(a, hb, tag, pending, tflag)) {
+  const ActBuf hb = act_buf(lds + lds_x_bytes(a.H), nbh);
+  float *part = reinterpret_cast<float *>(lds + lds_x_bytes(a.H) + act_buf_bytes(nbh));
+  if (threadIdx.x < 3) notdone[threadIdx.x] = 0;
+  __syncthreads();
+  const bool ok = collect(a, hb, tag, XW * nbh, vmask, notdone);
+  if (!ok) {
     // fallback: compute every pair's Q8_0(h) here (same code, same bytes)
-    const ActBuf xb = act_buf(lds + act_buf_bytes(nbh_all) + b_part_bytes(npairs, rb), nbx);
     quantize_x_to_lds(a, xb, nullptr, load_x_first(a));
     __syncthreads();
     for (int q = 0; q < npairs; q++) {
@@ -387,38 +415,47 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
       }
     }
   }
-  if (threadIdx.x < units) {
-    float acc = 0.0f;
-    if (ulive) {
-      const int blk0 = uq * nb_h + ug * 8;
-      acc = dot8_lds(wpre, hb.codes + blk0 * 2, hb.d + blk0, hb.corr + blk0, 0.0f);
-    }
-    part[threadIdx.x] = acc;
+  float acc = 0.0f;
+  if (ulive) {
+    const int blk0 = uq * nb_h + ug * 8;
+    acc = dot8_lds(wpre, group_codes(hb, blk0), hb.d + blk0, hb.corr + blk0, 0.0f);
   }
-  __syncthreads();
-  // y_q[n] = sum over g (in order), weighted; stored transposed [r][q] with
-  // the pair count padded to a multiple of 4 (pads and skipped slots are 0)
+  // weighted y_q[n] = w_q * (sum over g in order), stored transposed
+  // yw[r][q] with the pair count padded to a multiple of 4 (pads and skipped
+  // slots are 0).  For GI <= 2 the g sum stays in registers: the two groups
+  // of a row are adjacent lanes.
   const int npad = (npairs + 3) & ~3;
-  float *yw = part + NT;
-  for (int t = threadIdx.x; t < npad * rb; t += NT) {
-    const int q = t / rb, r = t - q * rb;
-    float v = 0.0f;
-    if (q < npairs && ((vmask >> q) & 1)) {
-      float y = 0.0f;
-      for (int g = 0; g < GI; g++) y += part[t * GI + g];
-      v = wq[q] * y;
+  float *yw = part;
+  if (GI <= 2) {
+    const float y = GI == 2 ? acc + dpp_f<DPP_XOR1>(acc) : acc;
+    const bool valid_q = (int)threadIdx.x < units && ((vmask >> uq) & 1);
+    if (ug == 0 && (int)threadIdx.x < units) yw[ur * npad + uq] = valid_q ? wq[uq] * y : 0.0f;
+    if ((int)threadIdx.x < (npad - npairs) * rb)       // the pads
+      yw[((int)threadIdx.x % rb) * npad + npairs + (int)threadIdx.x / rb] = 0.0f;
+  } else {
+    float *pt = part + rb * npad;
+    if ((int)threadIdx.x < units) pt[threadIdx.x] = acc;
+    __syncthreads();
+    for (int t = threadIdx.x; t < npad * rb; t += NT) {
+      const int q = t / rb, rr = t - q * rb;
+      float v = 0.0f;
+      if (q < npairs && ((vmask >> q) & 1)) {
+        float y = 0.0f;
+        for (int g = 0; g < GI; g++) y += pt[t * GI + g];
+        v = wq[q] * y;
+      }
+      yw[rr * npad + q] = v;
     }
-    yw[r * npad + q] = v;
   }
   __syncthreads();
   // out[n] = sum over the slots in order, then the shared expert
-  for (int r = threadIdx.x; r < rb; r += NT) {
-    const int64_t n = (int64_t)slab * rb + r;
+  for (int rr = threadIdx.x; rr < rb; rr += NT) {
+    const int64_t n = row0 + rr;
     if (n >= a.H) continue;
-    const float4 *row = reinterpret_cast<const float4 *>(yw + r * npad);
+    const float4 *yrow = reinterpret_cast<const float4 *>(yw + rr * npad);
     float o = 0.0f;
     for (int q4 = 0; q4 < npad / 4; q4++) {
-      const float4 v = row[q4];
+      const float4 v = yrow[q4];
       o += v.x;
       o += v.y;
       o += v.z;
@@ -426,7 +463,22 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
     }
     a.out[n] = o;
   }
-  arrive(a, tag);
+}
+
+int g_num_cus = 0;   // compute units of the device (queried once per process)
+
+// Workgroups and down rows per slab: one gate/up item per h block, then the
+// down slabs, enough of them to fill the remaining compute units but with
+// few enough rows that a slab's units fit the workgroup.  The gate/up items
+// never wait, so no slab waits for a workgroup that cannot start.
+void decode_grid(int64_t H, int64_t I, int64_t k, int ncu, int &grid, int &rb) {
+  const int64_t nbh = (k + 1) * (I / 32);
+  const int64_t rb_max = NT / ((k + 1) * (I / 256));
+  int64_t nb = (H + rb_max - 1) / rb_max;   // fewest slabs
+  if (nb < ncu - nbh) nb = ncu - nbh;
+  rb = (int)((H + nb - 1) / nb);
+  nb = (H + rb - 1) / rb;
+  grid = (int)(nbh + nb);
 }
 
 }  // namespace
@@ -434,29 +486,35 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
 size_t decode_sync_words(int64_t) { return (size_t)SYNC_SLOTS * SYNC_STRIDE; }
 
 // Hand-off region for T = 1, in uint32 words: the call counter's line, then
-// XW 64-bit words per h block.
+// one 128-byte line (XSTRIDE 64-bit words, XW used) per h block.
 size_t decode_xfer_words(int64_t I, int64_t k) {
-  return (size_t)XFER_HDR + (size_t)(k + 1) * (I / 32) * XW * 2;
+  return (size_t)XFER_HDR + (size_t)(k + 1) * (I / 32) * XSTRIDE * 2;
 }
 
 bool decode_supported(int64_t H, int64_t I, int64_t k) {
-  // A items: 8 waves x 4 h columns = one 32-column block.  B items hold
-  // every pair of one down row at one unit per lane, and at most NWMAX
-  // hand-off words per lane; LDS holds the staged Q8_0(x) (A) or the staged
-  // Q8_0(h) of every pair, the partials and, for the fallback, Q8_0(x) (B).
+  // Gate/up items: 8 waves x 4 h columns = one 32-column block.  Down slabs
+  // hold every pair of one down row at one unit per lane; a lane collects at
+  // most NWMAX hand-off words per pass; LDS holds the staged Q8_0(x), the
+  // staged Q8_0(h) of every pair and the partials.
   if (H < 256 || I < 256 || k < 1 || H > 16384 || k + 1 > 64 || (k + 1) * (I / 256) > NT)
     return false;
-  const int64_t nbh_all = (k + 1) * (I / 32);
-  const size_t lda = act_buf_bytes((int)(H / 32));
-  const int rb = (int)(NT / ((k + 1) * (I / 256)));
-  const size_t ldb = act_buf_bytes((int)nbh_all) + b_part_bytes((int)(k + 1), rb) + lda;
-  return nbh_all * XW <= NWMAX * NT && lda <= 48 * 1024 && ldb <= 48 * 1024;
+  const int64_t nbh = (k + 1) * (I / 32);
+  const int rb = (int)(NT / ((k + 1) * (I / 256)));   // the largest slab
+  return XW * nbh <= NWMAX * NT && lds_bytes((int)H, (int)I, (int)k, rb) <= 48 * 1024;
 }
 
 int decode_forward(const float *x, const int32_t *ids, const float *topk_w, const uint8_t *w_gu,
                    const uint8_t *w_d, const uint8_t *ws_gu, const uint8_t *ws_d, float *out,
                    int64_t H, int64_t I, int64_t E, int64_t k, uint32_t *sync, uint32_t *xfer,
                    uint8_t *xq, float *h, uint8_t *hq, hipStream_t s) {
+  if (g_num_cus == 0) {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n <= 0)
+      return W4A8_EHIP;
+    g_num_cus = n;
+  }
   DecodeArgs a;
   a.x = x; a.ids = ids; a.topk_w = topk_w;
   a.w_gu = w_gu; a.w_d = w_d; a.ws_gu = ws_gu; a.ws_d = ws_d;
@@ -466,18 +524,13 @@ int decode_forward(const float *x, const int32_t *ids, const float *topk_w, cons
   a.xfer = reinterpret_cast<uint64_t *>(xfer + XFER_HDR);
   a.xq = xq; a.h = h; a.hq = hq;
   a.H = (int)H; a.I = (int)I; a.E = (int)E; a.k = (int)k;
-  const int npairs = (int)k + 1;
-  const int GI = (int)(I / 256);
-  a.rb = NT / (npairs * GI);                     // >= 1 by decode_supported
-  a.n_b = (int)((H + a.rb - 1) / a.rb);
-  // default wait bound: 1 ms of the 100 MHz real-time counter
-  a.spin_limit = 100000;
-  if (const char *env = std::getenv("W4A8_DECODE_SPIN_TICKS")) a.spin_limit = std::atoll(env);
-  const unsigned grid = (unsigned)(npairs * (I / 32) + a.n_b);
-  const size_t lda = act_buf_bytes((int)(H / 32));
-  const size_t ldb = act_buf_bytes(npairs * (int)(I / 32)) + b_part_bytes(npairs, a.rb) + lda;
-  const size_t lds = lda > ldb ? lda : ldb;
-  decode_kernel<<<dim3(grid), dim3(NT), lds, s>>>(a);
+  int grid = 0;
+  decode_grid(H, I, k, g_num_cus, grid, a.rb);
+  // default wait bound: 2000 poll rounds, about 1-2 ms
+  a.spin_rounds = 2000;
+  if (const char *env = std::getenv("W4A8_DECODE_SPIN_ROUNDS")) a.spin_rounds = std::atoi(env);
+  const size_t lds = lds_bytes((int)H, (int)I, (int)k, a.rb);
+  decode_kernel<<<dim3((unsigned)grid), dim3(NT), lds, s>>>(a);
   return check_launch();
 }
 

@@ -251,9 +251,9 @@ def test_moe_decode_m1_wait_fallback(qwen_layer, monkeypatch):
     ids, wts = synth.routing(g, 1, L.E, 8)
     ws = w4.moe_workspace(1, L.H, L.I, L.E, 8)
     out, h, hq, *_ = L.run(x, ids, wts, 8, ws=ws)
-    monkeypatch.setenv("W4A8_DECODE_SPIN_TICKS", "0")
+    monkeypatch.setenv("W4A8_DECODE_SPIN_ROUNDS", "0")
     out_fb, h_fb, hq_fb, *_ = L.run(x, ids, wts, 8, ws=ws)
-    monkeypatch.delenv("W4A8_DECODE_SPIN_TICKS")
+    monkeypatch.delenv("W4A8_DECODE_SPIN_ROUNDS")
     assert np.array_equal(out, out_fb) and np.array_equal(hq, hq_fb)
     L.check(x, ids, wts, 8, out_fb, h_fb, hq_fb)
     x2 = synth.normal_f32(g, (1, L.H))
