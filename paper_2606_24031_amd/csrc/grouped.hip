@@ -3,25 +3,33 @@
 // integer products of 4-bit weight codes with 8-bit activation codes, one
 // scaling per 32-element group).
 //
-// Tile: 64 token rows (four waves x one 16-row MFMA tile) by 64 weight rows
-// (four 16-column MFMA tiles), K in chunks of eight Q-blocks.  One Q-block is
-// exactly one v_mfma_i32_16x16x32_i8, so every block's int32 dot stays
-// separate until it is scaled:
+// Tile: 32 token rows by 256 weight rows; each of the four waves owns 64
+// weight rows as two 32x32 output tiles.  One Q-block is exactly one
+// v_mfma_i32_32x32x32_i8 (K = 32), so every block's int32 dot stays separate
+// until it is scaled:
 //   * the MFMA accumulator input is the constant 0x4B400000, so the int32
 //     result read as a float is exactly 1.5*2^23 + s (|s| < 2^22);
 //   * t = fma(f, d_w, -1.5*2^23*d_w) = s*d_w rounded once, and
 //     acc = fma(t, d_x, acc): two VALU ops per (row, column, block), no
 //     int-to-float conversion.
-// Weights are staged in LDS as signed int8 codes (q - 8) with d_w and
-// -1.5*2^23*d_w precomputed; activation rows are gathered through the expert
-// permutation and staged as codes with their scale.  Row strides carry 8
-// bytes of padding (264-byte rows, 8-byte aligned) so the 16 lanes of one
-// 64-bit LDS read hit distinct banks.
-// The next chunk's global loads are issued before the current chunk's MFMAs.
+// Lane l of an MFMA holds token row l%32 of the A operand and weight row
+// l%32 of the B operand, with the block's codes 16*(l/32)..+15 in both; the
+// low nibbles of a Q4_0 block are its elements 0..15 and the high nibbles
+// 16..31, so the staged weight row of a block is [16 low codes][16 high
+// codes], each as int8 (q - 8).  Output element e of lane l is token row
+// 8*(e/4) + 4*(l/32) + e%4, weight row l%32.
 //
-// Gate/up tiles pair 32 gate rows with the 32 matching up rows, so SwiGLU and
-// Q8_0 of the 32-wide h block happen in registers; down tiles write w * y per
-// pair for the fixed-order combine.
+// Staging: each thread owns one weight row and keeps its 144-byte group of
+// eight blocks (16-byte aligned) in registers; the group is decoded into LDS
+// four blocks at a time.  Activation rows are gathered through the expert
+// permutation, one 34-byte block per thread.  LDS rows are 144 bytes apart,
+// so the 16-byte reads of 16 lanes fall in distinct banks.  About 50 KB of
+// LDS and at most 168 registers let three workgroups share a compute unit.
+//
+// Gate/up tiles pair 32 gate rows with the 32 matching up rows in each wave,
+// so SwiGLU needs no data movement; Q8_0 of each 32-wide h block goes through
+// a small LDS transpose, one row per lane.  Down tiles write w * y per pair
+// for the fixed-order combine.
 #include "w4a8_dev.h"
 #include "w4a8_host.h"
 
@@ -30,15 +38,16 @@ namespace w4a8 {
 namespace {
 
 constexpr int GT = 256;            // threads: four waves
-constexpr int BM = 64;             // token rows per tile
-constexpr int BN = 64;             // weight rows per tile
-constexpr int KC = 8;              // Q-blocks per K chunk
-constexpr int ROWB = KC * 32 + 8;  // LDS bytes per staged code row (padded)
+constexpr int BM = 32;             // token rows per tile
+constexpr int BN = 256;            // weight rows per tile (one per thread)
+constexpr int KC = 4;              // Q-blocks per K chunk
+constexpr int ROWB = KC * 32 + 16; // LDS bytes per staged code row (padded)
 constexpr int BIAS = 0x4B400000;   // float 1.5 * 2^23
 constexpr float BIASF = 12582912.0f;
 
 typedef int v4i __attribute__((ext_vector_type(4)));
-typedef float v4f __attribute__((ext_vector_type(4)));
+typedef int v16i __attribute__((ext_vector_type(16)));
+typedef float v16f __attribute__((ext_vector_type(16)));
 
 struct LdsTile {
   uint8_t wc[BN * ROWB];           // weight codes [n][block][32]
@@ -46,6 +55,8 @@ struct LdsTile {
   uint8_t ac[BM * ROWB];           // activation codes [m][block][32]
   float ad[KC * BM];               // d_x [block][m]
 };
+constexpr int HT_STRIDE = 33;      // floats per row of the h transpose
+static_assert(4 * 32 * HT_STRIDE * 4 <= BN * ROWB, "h transpose fits in the weight staging");
 
 struct GemmArgs {
   const uint8_t *w, *ws;           // routed experts [E][N][K/32] / shared [N][K/32]
@@ -65,40 +76,16 @@ __device__ __forceinline__ int64_t pair_token(const GemmArgs &a, int p) {
   return p < a.T * a.k ? p / a.k : p - a.T * a.k;
 }
 
-// Staged rows of one K chunk held in registers between the global loads and
-// the LDS writes: threads 0..63 hold one weight row group (9 x 16 bytes),
-// threads 64..127 one activation row group (17 x 16 bytes).  One raw array
-// with constant indices for both roles keeps it all in registers.
-struct Stage {
-  uint4 raw[17];
-  int n;                            // 16-byte pieces loaded (0: padding row or idle thread)
-};
-
+// Global weight row of LDS row r (= thread) for column slice `slice`.
+// Gate/up: wave w = r / 64 holds gate rows (r % 64 < 32) and up rows of the
+// 32 h columns slice*128 + 32w + (r % 32).
 template <bool GATEUP>
 __device__ __forceinline__ int64_t weight_row(const GemmArgs &a, int slice, int r) {
-  if (GATEUP) return r < 32 ? (int64_t)slice * 32 + r : a.I + (int64_t)slice * 32 + (r - 32);
-  return (int64_t)slice * BN + r;
-}
-
-template <bool GATEUP>
-__device__ __forceinline__ void stage_load(const GemmArgs &a, const uint8_t *W, int slice,
-                                           const int *rowact, int chunk, Stage &st) {
-  const int tid = threadIdx.x;
-  const int64_t gbytes_w = (a.K / 256) * (8 * Q4B), gbytes_x = (a.K / 256) * (8 * Q8B);
-  const uint4 *src = nullptr;
-  st.n = 0;
-  if (tid < BN) {
-    src = reinterpret_cast<const uint4 *>(W + weight_row<GATEUP>(a, slice, tid) * gbytes_w +
-                                          (int64_t)chunk * (8 * Q4B));
-    st.n = 9;
-  } else if (tid < BN + BM && rowact[tid - BN] >= 0) {
-    src = reinterpret_cast<const uint4 *>(a.act + (int64_t)rowact[tid - BN] * gbytes_x +
-                                          (int64_t)chunk * (8 * Q8B));
-    st.n = 17;
+  if (GATEUP) {
+    const int64_t col = (int64_t)slice * 128 + 32 * (r >> 6) + (r & 31);
+    return (r & 32) ? a.I + col : col;
   }
-#pragma unroll
-  for (int i = 0; i < 17; i++)
-    if (i < st.n) st.raw[i] = src[i];
+  return (int64_t)slice * BN + r;
 }
 
 __device__ __forceinline__ uint32_t signed_codes(uint32_t x) {
@@ -106,85 +93,102 @@ __device__ __forceinline__ uint32_t signed_codes(uint32_t x) {
   return (x + 0x78787878u) ^ 0x80808080u;
 }
 
-__device__ __forceinline__ void stage_store(LdsTile &L, const Stage &st) {
-  const int tid = threadIdx.x;
-  uint32_t D[68];
+// The thread's activation block for the current 8-block group: 9 dwords
+// around the 34-byte block (4-byte aligned), decoded at store time.
+struct ABlock {
+  uint32_t D[9];
+  bool live;
+};
+
+__device__ __forceinline__ void load_group(const GemmArgs &a, const uint8_t *wrow,
+                                           const int *rowact, int grp, W8 &w, ABlock &ab) {
+  load_w8(wrow + (int64_t)grp * (8 * Q4B), w);
+  const int m = threadIdx.x >> 3, b = threadIdx.x & 7;
+  const int ra = rowact[m];
+  ab.live = ra >= 0;
+  if (ab.live) {
+    const int64_t rowbytes = (a.K / 32) * Q8B;
+    // block 8*grp + b starts at byte 34*(8*grp + b): 4-byte aligned for even
+    // b, two bytes past a 4-byte boundary for odd b
+    const int64_t off = (int64_t)ra * rowbytes + ((int64_t)grp * 8 + b) * Q8B - ((b & 1) ? 2 : 0);
+    const uint32_t *src = reinterpret_cast<const uint32_t *>(a.act + off);
 #pragma unroll
-  for (int i = 0; i < 17; i++) {
-    D[4 * i + 0] = st.raw[i].x; D[4 * i + 1] = st.raw[i].y;
-    D[4 * i + 2] = st.raw[i].z; D[4 * i + 3] = st.raw[i].w;
-  }
-  if (tid < BN) {
-    const int n = tid;
-    W8 w;
-#pragma unroll
-    for (int i = 0; i < 36; i++) w.D[i] = D[i];
-#pragma unroll
-    for (int k = 0; k < KC; k++) {
-      uint32_t lo[4], hi[4];
-#pragma unroll
-      for (int c = 0; c < 4; c++) {
-        const uint32_t nb = w8_nib(w, k, c);
-        lo[c] = signed_codes(nb & 0x0F0F0F0Fu);
-        hi[c] = signed_codes((nb >> 4) & 0x0F0F0F0Fu);
-      }
-      uint2 *dst = reinterpret_cast<uint2 *>(L.wc + n * ROWB + k * 32);  // rows 8-byte aligned
-      dst[0] = make_uint2(lo[0], lo[1]);
-      dst[1] = make_uint2(lo[2], lo[3]);
-      dst[2] = make_uint2(hi[0], hi[1]);
-      dst[3] = make_uint2(hi[2], hi[3]);
-      const float dw = w8_scale(w, k);
-      L.wd[k * BN + n] = make_float2(dw, -BIASF * dw);
-    }
-  } else if (tid < BN + BM) {
-    const int m = tid - BN;
-    const bool live = st.n != 0;
-#pragma unroll
-    for (int k = 0; k < KC; k++) {
-      // block k of the 272-byte group: even blocks start on a dword, their
-      // codes two bytes on; odd blocks the other way round
-      const int i = k >> 1;
-      uint32_t q[8];
-      float d;
-      if ((k & 1) == 0) {
-        d = f16_bits_to_f32(D[17 * i]);
-#pragma unroll
-        for (int c = 0; c < 8; c++) q[c] = align2(D[17 * i + c + 1], D[17 * i + c]);
-      } else {
-        d = f16_bits_to_f32(D[17 * i + 8] >> 16);
-#pragma unroll
-        for (int c = 0; c < 8; c++) q[c] = D[17 * i + 9 + c];
-      }
-      uint2 *dst = reinterpret_cast<uint2 *>(L.ac + m * ROWB + k * 32);  // rows 8-byte aligned
-#pragma unroll
-      for (int c = 0; c < 4; c++) dst[c] = live ? make_uint2(q[2 * c], q[2 * c + 1]) : make_uint2(0u, 0u);
-      L.ad[k * BM + m] = live ? d : 0.0f;
-    }
+    for (int i = 0; i < 9; i++) ab.D[i] = src[i];
   }
 }
 
-// One K chunk of MFMAs for this wave's 16-row tile against the four column
-// tiles; acc[j][i] is (row 4*(lane/16)+i, column 16j + lane%16).
-__device__ __forceinline__ void chunk_mfma(const LdsTile &L, int wave, float acc[4][4]) {
+// Decode blocks 4*half .. 4*half+3 of the thread's weight group into its LDS
+// row, and, for the threads holding one of those activation blocks, the
+// activation codes and scale.
+__device__ __forceinline__ void store_half(LdsTile &L, const W8 &w, const ABlock &ab, int half) {
+  const int n = threadIdx.x;
+#pragma unroll
+  for (int kk = 0; kk < KC; kk++) {
+    const int k = 4 * half + kk;
+    uint32_t lo[4], hi[4];
+#pragma unroll
+    for (int c = 0; c < 4; c++) {
+      const uint32_t nb = w8_nib(w, k, c);
+      lo[c] = signed_codes(nb & 0x0F0F0F0Fu);
+      hi[c] = signed_codes((nb >> 4) & 0x0F0F0F0Fu);
+    }
+    uint4 *dst = reinterpret_cast<uint4 *>(L.wc + n * ROWB + kk * 32);
+    dst[0] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+    dst[1] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+    const float dw = w8_scale(w, k);
+    L.wd[kk * BN + n] = make_float2(dw, -BIASF * dw);
+  }
+  const int m = threadIdx.x >> 3, b = threadIdx.x & 7;
+  if ((b >> 2) == half) {
+    const int kk = b & 3;
+    uint32_t q[8];
+    float d;
+    if ((b & 1) == 0) {           // scale in bytes 0..1, codes from byte 2
+      d = f16_bits_to_f32(ab.D[0]);
+#pragma unroll
+      for (int c = 0; c < 8; c++) q[c] = align2(ab.D[c + 1], ab.D[c]);
+    } else {                      // two bytes before the block, codes aligned
+      d = f16_bits_to_f32(ab.D[0] >> 16);
+#pragma unroll
+      for (int c = 0; c < 8; c++) q[c] = ab.D[c + 1];
+    }
+    uint4 *dst = reinterpret_cast<uint4 *>(L.ac + m * ROWB + kk * 32);
+    dst[0] = ab.live ? make_uint4(q[0], q[1], q[2], q[3]) : make_uint4(0u, 0u, 0u, 0u);
+    dst[1] = ab.live ? make_uint4(q[4], q[5], q[6], q[7]) : make_uint4(0u, 0u, 0u, 0u);
+    L.ad[kk * BM + m] = ab.live ? d : 0.0f;
+  }
+}
+
+// One K chunk of MFMAs for this wave's two 32x32 output tiles; acc[j][e] is
+// (token row 8*(e/4) + 4*(lane/32) + e%4, weight row 64*wave + 32j + lane%32).
+__device__ __forceinline__ void chunk_mfma(const LdsTile &L, int wave, const v16i &c0,
+                                           float acc[2][16]) {
   const int lane = threadIdx.x & 63;
-  const int r16 = lane & 15, g = lane >> 4;
-  const v4i c0 = {BIAS, BIAS, BIAS, BIAS};
+  const int r32 = lane & 31, hh = lane >> 5;
+  // one block at a time: unrolling the blocks would hold four blocks'
+  // operands and MFMA results at once and spill
+#pragma unroll 1
+  for (int kk = 0; kk < KC; kk++) {
+    const v4i av = *reinterpret_cast<const v4i *>(L.ac + r32 * ROWB + kk * 32 + 16 * hh);
+    float dx[16];
 #pragma unroll
-  for (int k = 0; k < KC; k++) {
-    const long av = *reinterpret_cast<const long *>(L.ac + (wave * 16 + r16) * ROWB + k * 32 + 8 * g);
-    const float4 dx = *reinterpret_cast<const float4 *>(L.ad + k * BM + wave * 16 + 4 * g);
+    for (int q = 0; q < 4; q++) {
+      const float4 v = *reinterpret_cast<const float4 *>(L.ad + kk * BM + 8 * q + 4 * hh);
+      dx[4 * q + 0] = v.x; dx[4 * q + 1] = v.y; dx[4 * q + 2] = v.z; dx[4 * q + 3] = v.w;
+    }
 #pragma unroll
-    for (int j = 0; j < 4; j++) {
-      const long bv = *reinterpret_cast<const long *>(L.wc + (j * 16 + r16) * ROWB + k * 32 + 8 * g);
-      const float2 wd = L.wd[k * BN + j * 16 + r16];
+    for (int j = 0; j < 2; j++) {
+      const int n = 64 * wave + 32 * j + r32;
+      const v4i bv = *reinterpret_cast<const v4i *>(L.wc + n * ROWB + kk * 32 + 16 * hh);
+      const float2 wd = L.wd[kk * BN + n];
       // the whole int32 result vector reinterpreted at once (an element-wise
-      // bit cast of the vector's elements was folded to element 0)
-      const v4f f = __builtin_bit_cast(v4f, __builtin_amdgcn_mfma_i32_16x16x32_i8(av, bv, c0, 0, 0, 0));
-      const float dxv[4] = {dx.x, dx.y, dx.z, dx.w};
+      // bit cast of a vector's elements has been folded to element 0)
+      const v16f f =
+          __builtin_bit_cast(v16f, __builtin_amdgcn_mfma_i32_32x32x32_i8(av, bv, c0, 0, 0, 0));
 #pragma unroll
-      for (int i = 0; i < 4; i++) {
-        const float t = fmaf(f[i], wd.x, wd.y);
-        acc[j][i] = fmaf(t, dxv[i], acc[j][i]);
+      for (int e = 0; e < 16; e++) {
+        const float t = fmaf(f[e], wd.x, wd.y);
+        acc[j][e] = fmaf(t, dx[e], acc[j][e]);
       }
     }
   }
@@ -192,12 +196,20 @@ __device__ __forceinline__ void chunk_mfma(const LdsTile &L, int wave, float acc
 
 __device__ __forceinline__ float silu_f32(float g) { return g / (1.0f + expf(-g)); }
 
+// Q8_0 code of v for the reciprocal id of the stored scale (the same fp32
+// steps as the format definition).
+__device__ __forceinline__ uint32_t q8_code(float v, float id) {
+  int q = (int)roundf(v * id);
+  q = q > 127 ? 127 : (q < -127 ? -127 : q);
+  return (uint32_t)q & 0xFFu;
+}
+
 template <bool GATEUP>
-__global__ __launch_bounds__(GT, 2) void grouped_kernel(GemmArgs a) {
+__global__ __launch_bounds__(GT, 3) void grouped_kernel(GemmArgs a) {
   __shared__ LdsTile L;
   __shared__ int rowact[BM];       // activation row of each tile row (-1: padding)
   __shared__ int rowpair[BM];      // pair of each tile row (-1: padding)
-  const int nslices = (int)(GATEUP ? a.I / 32 : a.N / BN);
+  const int nslices = (int)(GATEUP ? a.I / 128 : a.N / BN);
   const int tile = blockIdx.x / nslices, slice = blockIdx.x % nslices;
   if (tile >= a.meta[2]) return;                     // META_NTILES
   const int2 td = a.tiles[tile];
@@ -216,84 +228,80 @@ __global__ __launch_bounds__(GT, 2) void grouped_kernel(GemmArgs a) {
   __syncthreads();
   const int64_t wexpert = (int64_t)a.N * (a.K / 32) * Q4B;
   const uint8_t *W = gd.x < a.E ? a.w + (int64_t)gd.x * wexpert : a.ws;
-  const int nchunks = (int)(a.K / 256);
-  const bool active = wave * 16 < mc;                // this wave has rows
+  const uint8_t *wrow = W + weight_row<GATEUP>(a, slice, tid) * ((a.K / 32) * Q4B);
+  const int ngroups = (int)(a.K / 256);
 
-  float acc[4][4];
+  float acc[2][16];
 #pragma unroll
-  for (int j = 0; j < 4; j++)
+  for (int j = 0; j < 2; j++)
 #pragma unroll
-    for (int i = 0; i < 4; i++) acc[j][i] = 0.0f;
+    for (int e = 0; e < 16; e++) acc[j][e] = 0.0f;
 
-  Stage st;
-  stage_load<GATEUP>(a, W, slice, rowact, 0, st);
-  for (int c = 0; c < nchunks; c++) {
-    __syncthreads();                                 // previous chunk's MFMAs done
-    stage_store(L, st);
-    __syncthreads();
-    if (c + 1 < nchunks) stage_load<GATEUP>(a, W, slice, rowact, c + 1, st);
-    if (active) chunk_mfma(L, wave, acc);
+  v16i c0;                                           // accumulator input of every MFMA
+#pragma unroll
+  for (int e = 0; e < 16; e++) c0[e] = BIAS;
+  W8 w;
+  ABlock ab;
+  load_group(a, wrow, rowact, 0, w, ab);
+  for (int g = 0; g < ngroups; g++) {
+#pragma unroll
+    for (int half = 0; half < 2; half++) {
+      __syncthreads();                               // previous chunk's MFMAs done
+      store_half(L, w, ab, half);
+      __syncthreads();
+      if (half == 1 && g + 1 < ngroups) load_group(a, wrow, rowact, g + 1, w, ab);
+      chunk_mfma(L, wave, c0, acc);
+    }
   }
 
-  const int r16 = lane & 15, g = lane >> 4;
+  const int r32 = lane & 31, hh = lane >> 5;
   if (GATEUP) {
-    // lane holds gate (j = 0, 1) and up (j = 2, 3) of h columns 16jj + r16
-    // for rows 4g + i of this wave's tile
+    // lane holds gate (j = 0) and up (j = 1) of h column slice*128 + 32*wave
+    // + r32 for token rows 8*(e/4) + 4*hh + e%4; transpose through LDS so
+    // that one lane holds a row's 32-wide h block
     __syncthreads();
-    uint8_t *hq_lds = L.ac;                          // [64 rows][34 bytes]
-    float hv[2][4];
+    float *ht = reinterpret_cast<float *>(L.wc) + wave * 32 * HT_STRIDE;
 #pragma unroll
-    for (int jj = 0; jj < 2; jj++)
-#pragma unroll
-      for (int i = 0; i < 4; i++) hv[jj][i] = silu_f32(acc[jj][i]) * acc[jj + 2][i];
-#pragma unroll
-    for (int i = 0; i < 4; i++) {
-      const int m = wave * 16 + 4 * g + i;
-      // Q8_0 of the 32 h values of row m: 16 lanes (r16) x 2 columns each
-      float amax = fmaxf(fabsf(hv[0][i]), fabsf(hv[1][i]));
-#pragma unroll
-      for (int o = 8; o > 0; o >>= 1) amax = fmaxf(amax, __shfl_xor(amax, o, 16));
-      const float d32 = amax / 127.0f;
-      const uint32_t d16 = f32_to_f16_bits(d32);
-      const float df = f16_bits_to_f32(d16);
-      const float id = df != 0.0f ? 1.0f / df : 0.0f;
-#pragma unroll
-      for (int jj = 0; jj < 2; jj++) {
-        int q = 0;
-        if (df != 0.0f) {
-          q = (int)roundf(hv[jj][i] * id);
-          q = q > 127 ? 127 : (q < -127 ? -127 : q);
-        }
-        hq_lds[m * Q8B + 2 + 16 * jj + r16] = (uint8_t)(int8_t)q;
-      }
-      if (r16 == 0) *reinterpret_cast<uint16_t *>(hq_lds + m * Q8B) = (uint16_t)d16;
-      const int p = rowpair[m];
-      if (active && p >= 0) {
-#pragma unroll
-        for (int jj = 0; jj < 2; jj++)
-          a.h[(int64_t)p * a.I + (int64_t)slice * 32 + 16 * jj + r16] = hv[jj][i];
-      }
+    for (int e = 0; e < 16; e++) {
+      const int m = 8 * (e >> 2) + 4 * hh + (e & 3);
+      ht[m * HT_STRIDE + r32] = silu_f32(acc[0][e]) * acc[1][e];
     }
     __syncthreads();
-    // copy the 64 rows' blocks out: 17 16-bit words per 34-byte block
-    for (int idx = tid; idx < BM * 17; idx += GT) {
-      const int m = idx / 17, w = idx % 17;
+    if (lane < BM) {
+      const int m = lane;
       const int p = rowpair[m];
-      if (p < 0) continue;
-      uint16_t *dst = reinterpret_cast<uint16_t *>(a.hq + ((int64_t)p * (a.I / 32) + slice) * Q8B);
-      dst[w] = reinterpret_cast<const uint16_t *>(hq_lds + m * Q8B)[w];
+      if (p >= 0) {
+        const float *hr = ht + m * HT_STRIDE;
+        float amax = 0.0f;
+        for (int c = 0; c < 32; c++) amax = fmaxf(amax, fabsf(hr[c]));
+        const float d32 = amax / 127.0f;
+        const uint32_t d16 = f32_to_f16_bits(d32);
+        const float df = f16_bits_to_f32(d16);
+        const float id = df != 0.0f ? 1.0f / df : 0.0f;
+        const int64_t hcol = (int64_t)slice * 128 + 32 * wave;
+        uint16_t *dst =
+            reinterpret_cast<uint16_t *>(a.hq + ((int64_t)p * (a.I / 32) + hcol / 32) * Q8B);
+        dst[0] = (uint16_t)d16;
+        for (int c = 0; c < 32; c += 2) {
+          const uint32_t q0 = df != 0.0f ? q8_code(hr[c], id) : 0u;
+          const uint32_t q1 = df != 0.0f ? q8_code(hr[c + 1], id) : 0u;
+          dst[1 + c / 2] = (uint16_t)(q0 | (q1 << 8));
+        }
+        float4 *hout = reinterpret_cast<float4 *>(a.h + (int64_t)p * a.I + hcol);
+        for (int c = 0; c < 32; c += 4)
+          hout[c / 4] = make_float4(hr[c], hr[c + 1], hr[c + 2], hr[c + 3]);
+      }
     }
   } else {
-    if (!active) return;
 #pragma unroll
-    for (int i = 0; i < 4; i++) {
-      const int m = wave * 16 + 4 * g + i;
+    for (int e = 0; e < 16; e++) {
+      const int m = 8 * (e >> 2) + 4 * hh + (e & 3);
       const int p = rowpair[m];
       if (p < 0) continue;
       const float wt = p < a.T * a.k ? a.topk_w[p] : 1.0f;
 #pragma unroll
-      for (int j = 0; j < 4; j++)
-        a.y[(int64_t)p * a.N + (int64_t)slice * BN + 16 * j + r16] = wt * acc[j][i];
+      for (int j = 0; j < 2; j++)
+        a.y[(int64_t)p * a.N + (int64_t)slice * BN + 64 * wave + 32 * j + r32] = wt * acc[j][e];
     }
   }
 }
@@ -312,7 +320,7 @@ int grouped_gateup(const uint8_t *w_gu, const uint8_t *ws_gu, const uint8_t *xq,
   a.h = h; a.hq = hq;
   a.T = T; a.k = k; a.E = E; a.N = 2 * I; a.K = H; a.I = I;
   a.act_by_pair = 0;
-  const unsigned grid = (unsigned)(maxtiles * (I / 32));
+  const unsigned grid = (unsigned)(maxtiles * (I / 128));
   grouped_kernel<true><<<dim3(grid), dim3(GT), 0, s>>>(a);
   return check_launch();
 }

@@ -42,7 +42,7 @@ int decode_forward(const float *x, const int32_t *ids, const float *topk_w, cons
 
 namespace {
 
-constexpr int MC = 64;          // token rows per tile (one grouped MFMA tile)
+constexpr int MC = 32;          // token rows per tile (one grouped MFMA tile)
 constexpr int ROUTE_T = 1024;   // threads of the route kernel
 constexpr int LDS_INTS = 16000; // int32 cells of dynamic LDS for the route kernel (< 64 KB)
 
