@@ -16,7 +16,9 @@ recorded on the stream the kernels run on.  `value` is algorithmic bytes
 and out, ids and weights) / time, in GB/s.
 
 The line also carries the 947-token prefill of the same layer (router bias
-~ N(0,1)) in tokens/s per layer, the roofline of the dominant kernel, and the
+~ N(0,1)) in tokens/s per layer, the same layer at batched decode (32 tokens),
+a 40-layer stack (947-token prefill, then single-token decode steps, layers
+chained by a residual RMSNorm), the roofline of the dominant kernel, and the
 CPU oracle timed on this host on a bounded sample of the decode workload.
 """
 from __future__ import annotations
@@ -54,6 +56,11 @@ def parse():
     ap.add_argument("--no-graph", action="store_true", help="launch steps eagerly")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--m32-steps", type=int, default=64)
+    ap.add_argument("--stack-layers", type=int, default=40)
+    ap.add_argument("--stack-decode-steps", type=int, default=128)
+    ap.add_argument("--no-m32", action="store_true")
+    ap.add_argument("--no-stack", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 256 MiB device copy 5 times (for scaling the "
                          "rocprofv3 FETCH_SIZE / WRITE_SIZE counters)")
@@ -195,6 +202,127 @@ def bench_prefill(torch, w4, synth, layers, args, dev):
             "hbm_peak_frac": round(sum(byts[:n]) / n / (ms / 1e3) / 1e9 / HBM_PEAK_GBPS, 4)}
 
 
+def bench_m32(torch, w4, synth, layers, args, dev):
+    """Batched decode, 32 tokens per layer call, each routed independently
+    (top-8 of 256, no router bias); the calls cycle the weight sets and are
+    replayed from one HIP graph."""
+    T, n = 32, args.m32_steps
+    rng = synth.rng(args.seed + 5)
+    ids_l, wts_l, byts = [], [], []
+    for _ in range(n):
+        ids, wts = synth.routing(rng, T, E, K_TOP)
+        ids_l.append(torch.from_numpy(ids).to(dev))
+        wts_l.append(torch.from_numpy(wts).to(dev))
+        byts.append((len(set(ids.ravel().tolist())) + 1) * EXPERT_BYTES + 2 * T * H * 4 + ids.size * 8)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(args.seed + 6)
+    xs = torch.randn((n, T, H), generator=gen, device=dev)
+    ws = w4.moe_workspace(T, H, I, E, K_TOP, device=dev)
+    out = torch.empty((T, H), dtype=torch.float32, device=dev)
+
+    def step(i):
+        L = layers[i % len(layers)]
+        w4.moe_forward(xs[i], ids_l[i], wts_l[i], L[0], L[1], L[2], L[3], H, I, E, K_TOP, ws, out=out)
+
+    for i in range(min(n, 4)):
+        step(i)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for i in range(n):
+            step(i)
+    graph.replay()
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    graph.replay()
+    ev1.record()
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / n
+    gbps = sum(byts) / n / (ms / 1e3) / 1e9
+    return {"tokens": T, "us_per_layer": round(ms * 1e3, 2),
+            "tokens_per_s_per_layer": round(T / (ms / 1e3), 1), "GBps": round(gbps, 1),
+            "hbm_peak_frac": round(gbps / HBM_PEAK_GBPS, 4), "calls": n}
+
+
+def bench_stack(torch, w4, synth, args, dev):
+    """40 chained layers (x <- x + MoE_l(RMSNorm_l(x))): a 947-token prefill,
+    then single-token decode steps through all layers; every layer has its own
+    seed-generated weights (18.2 GB of Q4_0 resident in HBM), RMSNorm gains
+    1 + N(0, 0.1^2) and its own routing per call."""
+    nl, nd, Tp = args.stack_layers, args.stack_decode_steps, 947
+    log(f"stack: generating {nl} layers of Q4_0 weights")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(args.seed + 100)
+    layers = [make_layer(torch, w4, gen, dev) for _ in range(nl)]
+    gammas = [1.0 + 0.1 * torch.randn((H,), generator=gen, device=dev) for _ in range(nl)]
+    rng = synth.rng(args.seed + 101)
+    pre = [synth.routing(rng, Tp, E, K_TOP, bias_std=1.0) for _ in range(nl)]
+    pre_ids = [torch.from_numpy(a).to(dev) for a, _ in pre]
+    pre_wts = [torch.from_numpy(b).to(dev) for _, b in pre]
+    dec_ids, dec_wts = synth.routing(rng, nd * nl, E, K_TOP)
+    dec_ids = torch.from_numpy(dec_ids).to(dev).view(nd, nl, 1, K_TOP)
+    dec_wts = torch.from_numpy(dec_wts).to(dev).view(nd, nl, 1, K_TOP)
+    ws_p = w4.moe_workspace(Tp, H, I, E, K_TOP, device=dev)
+    ws_d = w4.moe_workspace(1, H, I, E, K_TOP, device=dev)
+    x_p = torch.randn((Tp, H), generator=gen, device=dev)
+    x_p0 = x_p.clone()
+    xn_p, y_p = torch.empty_like(x_p), torch.empty_like(x_p)
+    x_d0 = torch.randn((nd, 1, H), generator=gen, device=dev)
+    x_d = torch.empty((1, H), device=dev)
+    xn_d, y_d = torch.empty_like(x_d), torch.empty_like(x_d)
+
+    def forward(x, xn, y, ids, wts, ws):
+        for l in range(nl):
+            L = layers[l]
+            w4.rmsnorm_residual(x, y if l else None, gammas[l], x_out=x, xn=xn)
+            w4.moe_forward(xn, ids(l), wts(l), L[0], L[1], L[2], L[3], H, I, E, K_TOP, ws, out=y)
+        w4.rmsnorm_residual(x, y, None, x_out=x, want_norm=False)
+
+    def prefill():
+        x_p.copy_(x_p0)
+        forward(x_p, xn_p, y_p, lambda l: pre_ids[l], lambda l: pre_wts[l], ws_p)
+
+    def decode(s):
+        x_d.copy_(x_d0[s])
+        forward(x_d, xn_d, y_d, lambda l: dec_ids[s, l], lambda l: dec_wts[s, l], ws_d)
+
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    prefill()
+    torch.cuda.synchronize()
+    ev0.record()
+    prefill()
+    ev1.record()
+    torch.cuda.synchronize()
+    ms_p = ev0.elapsed_time(ev1)
+    decode(0)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for s in range(nd):
+            decode(s)
+    graph.replay()
+    torch.cuda.synchronize()
+    ev0.record()
+    graph.replay()
+    ev1.record()
+    torch.cuda.synchronize()
+    ms_d = ev0.elapsed_time(ev1) / nd
+    ids_h = dec_ids.cpu().numpy().reshape(nd * nl, K_TOP)
+    dbytes = sum(step_bytes(ids_h[i]) for i in range(nd * nl)) / nd
+    assert torch.isfinite(x_p).all() and torch.isfinite(x_d).all()
+    del layers
+    return {"layers": nl, "weights_GB": round(nl * (E + 1) * EXPERT_BYTES / 1e9, 2),
+            "prefill_tokens": Tp, "prefill_ms": round(ms_p, 3),
+            "prefill_tokens_per_s": round(Tp / (ms_p / 1e3), 1),
+            "decode_steps": nd, "decode_ms_per_token": round(ms_d, 4),
+            "decode_tokens_per_s": round(1e3 / ms_d, 1),
+            "decode_GBps": round(dbytes / (ms_d / 1e3) / 1e9, 1),
+            "launch": "prefill eager; decode steps replayed from one HIP graph"}
+
+
 def physical_threads_note():
     try:
         out = os.popen("lscpu").read()
@@ -274,6 +402,18 @@ def main():
         prefill = bench_prefill(torch, w4, synth, layers, args, dev)
         log(f"prefill: {prefill}")
 
+    m32 = None
+    if not args.no_m32:
+        m32 = bench_m32(torch, w4, synth, layers, args, dev)
+        log(f"decode M=32: {m32}")
+
+    stack = None
+    if not args.no_stack:
+        del layers
+        torch.cuda.empty_cache()
+        stack = bench_stack(torch, w4, synth, args, dev)
+        log(f"stack: {stack}")
+
     cpu = None
     if not args.no_cpu_baseline:
         log(f"cpu baseline: oracle for ~{args.cpu_seconds:.0f} s")
@@ -306,6 +446,8 @@ def main():
                      "traffic": traffic},
         "cpu_baseline": cpu,
         "prefill_947": prefill,
+        "decode_m32": m32,
+        "stack_40": stack,
     }
     print(json.dumps(rec), flush=True)
 

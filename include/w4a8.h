@@ -34,8 +34,8 @@
  *   - Shapes are validated on the host before anything is launched; on an
  *     error nothing is enqueued and no output is touched.
  *   - Calls are thread-safe and re-entrant: the library keeps no state other
- *     than a per-device "is gfx950" check.  Concurrent calls must not share
- *     output or workspace buffers.
+ *     than a per-device "is gfx950" check and the device's compute-unit
+ *     count.  Concurrent calls must not share output or workspace buffers.
  */
 #ifndef W4A8_H
 #define W4A8_H
@@ -166,6 +166,21 @@ int moe_w4a8_forward(const float *hidden, const int32_t *topk_ids, const float *
                      const void *ws_gate_up, const void *ws_down,
                      float *out, int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
                      void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * Residual add and RMSNorm between chained MoE layers (the pre-norm chaining
+ * of the Qwen3-series model family, Sec. 2.2; the paper does not spell the
+ * norm out, so it is the standard RMSNorm).  Per row t of [T][H] fp32:
+ *   x_out = x + y          one binary32 addition (x_out = x when y is NULL)
+ *   xn    = x_out * (1 / sqrt(mean(x_out^2) + eps)) * gamma
+ * The sum of squares is taken in a fixed order (the result does not depend on
+ * scheduling).  x_out may alias x; xn must not alias x, y or x_out.  xn NULL
+ * skips the norm (then gamma may be NULL).
+ *   gamma [H] fp32.  H % 4 != 0, H <= 0, T < 0 or eps < 0 -> W4A8_ESHAPE;
+ *   T >= 2^31 -> W4A8_ERANGE.  T == 0 is a no-op.
+ */
+int rmsnorm_residual(const float *x, const float *y, const float *gamma, float *x_out,
+                     float *xn, int64_t T, int64_t H, float eps, void *stream);
 
 #ifdef __cplusplus
 }

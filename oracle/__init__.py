@@ -65,6 +65,7 @@ def _load():
     lib.orc_q8_0_candidates.argtypes = [P, P, I64, P, P, P, P]
     lib.orc_q8_0_candidates.restype = ctypes.c_int
     lib.orc_threads.restype = ctypes.c_int
+    lib.orc_rmsnorm_residual.argtypes = [P, P, P, P, P, I64, I64, ctypes.c_double]
     _lib = lib
     return lib
 
@@ -194,6 +195,20 @@ def moe(hidden, ids, wts, w_gu, w_d, ws_gu, ws_d, H, I, E, k, hq_in=None,
     if rc != 0:
         raise ValueError(f"orc_moe failed ({rc})")
     return MoeResult(out, R, gu, Rgu, h, hq)
+
+
+def rmsnorm_residual(x, y, gamma, eps: float = 1e-6, want_norm: bool = True):
+    """x_out = x + y (fp32, y may be None) and xn = RMSNorm(x_out) * gamma in
+    fp64, per row of [T, H] (see orc_rmsnorm_residual)."""
+    x = _c(x, np.float32)
+    T, H = x.shape
+    y = None if y is None else _c(y, np.float32).reshape(T, H)
+    gamma = _c(gamma, np.float32).reshape(H)
+    x_out = np.zeros((T, H), dtype=np.float32)
+    xn = np.zeros((T, H), dtype=np.float64) if want_norm else None
+    _load().orc_rmsnorm_residual(_ptr(x), _ptr(y), _ptr(gamma), _ptr(x_out), _ptr(xn), T, H,
+                                 float(eps))
+    return x_out, xn
 
 
 def q8_0_candidates(h: np.ndarray, dh: np.ndarray):

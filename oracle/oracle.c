@@ -416,6 +416,34 @@ int orc_q8_0_candidates(const float *h, const float *dh, int64_t K,
     return rc;
 }
 
+/* ------------------------------------------------------------------ */
+/* Residual add and RMSNorm between chained MoE layers.                 */
+/* ------------------------------------------------------------------ */
+
+/* Pre-norm residual chaining of the Qwen3-series model family (Sec. 2.2);
+ * the paper does not spell the norm out, so this is the standard RMSNorm.
+ * Per row t of [T][H]:
+ *   x_out = x + y   (one binary32 addition; x_out = x when y is NULL)
+ *   xn[i] = x_out[i] / sqrt(mean_i x_out[i]^2 + eps) * gamma[i]   in fp64
+ * (xn is skipped when NULL). */
+void orc_rmsnorm_residual(const float *x, const float *y, const float *gamma, float *x_out,
+                          double *xn, int64_t T, int64_t H, double eps)
+{
+    for (int64_t t = 0; t < T; t++) {
+        const float *xr = x + t * H;
+        float *vo = x_out + t * H;
+        double ss = 0.0;
+        for (int64_t i = 0; i < H; i++) {
+            const float v = y ? xr[i] + y[t * H + i] : xr[i];
+            vo[i] = v;
+            ss += (double)v * (double)v;
+        }
+        if (!xn) continue;
+        const double r = 1.0 / sqrt(ss / (double)H + eps);
+        for (int64_t i = 0; i < H; i++) xn[t * H + i] = (double)vo[i] * r * (double)gamma[i];
+    }
+}
+
 /* Number of OpenMP threads the parallel loops above use. */
 int orc_threads(void)
 {

@@ -21,7 +21,7 @@ WS_XQ, WS_H, WS_HQ, WS_PERM, WS_COUNT, WS_SYNC, WS_SYNC_END, WS_NFIELDS = 0, 1, 
 
 EXPORTS = ("w4a8_strerror", "q8_0_quantize", "q4_0_quantize", "q4q8_gemv",
            "moe_w4a8_workspace_size", "moe_w4a8_workspace_init",
-           "moe_w4a8_workspace_layout", "moe_w4a8_forward")
+           "moe_w4a8_workspace_layout", "moe_w4a8_forward", "rmsnorm_residual")
 
 _lib = None
 
@@ -57,6 +57,8 @@ def lib() -> ctypes.CDLL:
     L.moe_w4a8_workspace_layout.restype = ctypes.c_int
     L.moe_w4a8_forward.argtypes = [P, P, P, P, P, P, P, P, I64, I64, I64, I64, I64, P, SZ, P]
     L.moe_w4a8_forward.restype = ctypes.c_int
+    L.rmsnorm_residual.argtypes = [P, P, P, P, P, I64, I64, ctypes.c_float, P]
+    L.rmsnorm_residual.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -156,3 +158,20 @@ def moe_forward(hidden, topk_ids, topk_w, w_gate_up, w_down, ws_gate_up, ws_down
                                 _stream(stream))
     _check(rc, "moe_w4a8_forward")
     return out
+
+
+def rmsnorm_residual(x, y, gamma, eps=1e-6, x_out=None, xn=None, want_norm=True, stream=None):
+    """x_out = x + y (y may be None) and xn = RMSNorm(x_out) * gamma per row of
+    [T, H] fp32; returns (x_out, xn).  x_out may be x itself (in place)."""
+    import torch
+    T, H = x.shape
+    for t in (x, y, gamma):
+        assert t is None or (t.dtype == torch.float32 and t.is_contiguous())
+    if x_out is None:
+        x_out = torch.empty_like(x)
+    if want_norm and xn is None:
+        xn = torch.empty_like(x)
+    rc = lib().rmsnorm_residual(_p(x), _p(y), _p(gamma if want_norm else None), _p(x_out),
+                                _p(xn if want_norm else None), T, H, float(eps), _stream(stream))
+    _check(rc, "rmsnorm_residual")
+    return x_out, (xn if want_norm else None)

@@ -97,3 +97,17 @@ def test_moe_argument_errors():
     assert f(*args(x=_fake(A + 8)), T, H, I, E, k, p, ws, None) == w4.EALIGN
     assert f(*args(), T, H, I, E, k, p, ws - 1, None) == w4.EWORKSPACE
     assert f(*args(), 0, H, I, E, k, p, ws, None) == w4.OK                 # empty: no-op
+
+
+def test_rmsnorm_argument_errors():
+    L = w4.lib()
+    f = L.rmsnorm_residual
+    p = _fake(A)
+    assert f(None, None, p, p, p, 2, 256, 1e-6, None) == w4.ENULL
+    assert f(p, None, None, p, p, 2, 256, 1e-6, None) == w4.ENULL      # norm without gamma
+    assert f(p, None, p, p, p, 2, 258, 1e-6, None) == w4.ESHAPE        # H % 4
+    assert f(p, None, p, p, p, -1, 256, 1e-6, None) == w4.ESHAPE
+    assert f(p, None, p, p, p, 2, 256, -1.0, None) == w4.ESHAPE       # eps < 0
+    assert f(p, _fake(A + 4), p, p, p, 2, 256, 1e-6, None) == w4.EALIGN
+    assert f(p, None, p, p, p, 0, 256, 1e-6, None) == w4.OK            # empty: no-op
+    assert f(p, None, p, p, p, 1 << 31, 256, 1e-6, None) == w4.ERANGE

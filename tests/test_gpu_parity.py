@@ -301,3 +301,32 @@ def test_moe_prefill_947_sampled_tokens(qwen_layer):
     L.check(x[tokens], ids[tokens], wts[tokens], k, o, hh, qq)
     out2, *_ = L.run(x, ids, wts, k, ws=ws)
     assert np.array_equal(out, out2)
+
+
+# ------------------------------------------------------------ RMSNorm + residual
+@pytest.mark.parametrize("T,H,resid", [(1, 2048, True), (5, 256, False), (947, 2048, True), (3, 4100, True)])
+def test_rmsnorm_residual_matches_oracle(T, H, resid):
+    g = synth.rng(40 + T)
+    x = synth.normal_f32(g, (T, H))
+    y = synth.normal_f32(g, (T, H), 0.3) if resid else None
+    gamma = (np.float32(1.0) + synth.normal_f32(g, (H,), 0.1)).astype(np.float32)
+    xo_ref, xn_ref = oracle.rmsnorm_residual(x, y, gamma, eps=1e-6)
+    xo, xn = w4.rmsnorm_residual(dev(x), None if y is None else dev(y), dev(gamma), eps=1e-6)
+    assert np.array_equal(host(xo), xo_ref), "x + y must be one fp32 add"
+    # fp32 sum of squares and three fp32 roundings per element
+    err = np.abs(host(xn).astype(np.float64) - xn_ref)
+    assert np.all(err <= 2e-6 * np.abs(xn_ref) + 1e-7 * np.abs(gamma).max())
+
+
+def test_rmsnorm_residual_in_place_and_no_norm():
+    g = synth.rng(47)
+    x = synth.normal_f32(g, (4, 512))
+    y = synth.normal_f32(g, (4, 512))
+    gamma = np.ones(512, np.float32)
+    xd = dev(x)
+    xo, xn = w4.rmsnorm_residual(xd, dev(y), dev(gamma), x_out=xd)      # in place
+    ref, xn_ref = oracle.rmsnorm_residual(x, y, gamma)
+    assert np.array_equal(host(xd), ref)
+    assert np.allclose(host(xn), xn_ref, rtol=2e-6, atol=1e-7)
+    xo2, none = w4.rmsnorm_residual(dev(x), dev(y), None, want_norm=False)
+    assert none is None and np.array_equal(host(xo2), ref)

@@ -410,3 +410,41 @@ def test_q8_0_candidates_cover_perturbed_inputs():
             assert c, "scale outside the candidate set"
             c = c[0]
             assert np.all(qp[0, b] >= lo[b, c]) and np.all(qp[0, b] <= hi[b, c])
+
+
+# ------------------------------------------------------------ RMSNorm + residual
+def test_rmsnorm_hand_example():
+    # x = (3, 4): mean square 12.5, so xn = x / sqrt(12.5 + eps) * gamma
+    x = np.array([[3.0, 4.0]], np.float32)
+    g = np.array([2.0, -0.5], np.float32)
+    xo, xn = oracle.rmsnorm_residual(x, None, g, eps=0.0)
+    assert np.array_equal(xo, x)
+    r = 12.5 ** -0.5
+    assert np.allclose(xn[0], [3 * r * 2.0, 4 * r * -0.5], rtol=1e-15, atol=0)
+
+
+def test_rmsnorm_constant_row_and_scale_invariance():
+    g = np.random.default_rng(31)
+    gamma = synth.normal_f32(g, (64,), 1.0)
+    # a constant row c: xn = sign(c) * gamma (eps = 0)
+    for c in (5.0, -0.25):
+        _, xn = oracle.rmsnorm_residual(np.full((1, 64), c, np.float32), None, gamma, eps=0.0)
+        assert np.allclose(xn[0], np.sign(c) * gamma.astype(np.float64), rtol=1e-15, atol=0)
+    # a power-of-two scaling of the row leaves xn unchanged (exact in fp64)
+    x = synth.normal_f32(g, (3, 64))
+    _, a = oracle.rmsnorm_residual(x, None, gamma, eps=0.0)
+    _, b = oracle.rmsnorm_residual(x * np.float32(8.0), None, gamma, eps=0.0)
+    assert np.array_equal(a, b)
+    # eps enters under the root: a zero row stays zero, a tiny row is damped
+    _, z = oracle.rmsnorm_residual(np.zeros((1, 64), np.float32), None, gamma, eps=1e-6)
+    assert not z.any()
+
+
+def test_rmsnorm_residual_is_one_fp32_add():
+    # 1 + 2^-24 rounds to 1 in binary32 (tie to even); 1 + 3*2^-24 rounds up
+    x = np.array([[1.0, 1.0, -2.5, 0.0]], np.float32)
+    y = np.array([[2.0 ** -24, 3 * 2.0 ** -24, 2.5, -0.0]], np.float32)
+    xo, _ = oracle.rmsnorm_residual(x, y, np.ones(4, np.float32), want_norm=False)
+    assert xo[0, 0] == np.float32(1.0)
+    assert xo[0, 1] == np.float32(1.0 + 2.0 ** -22)
+    assert xo[0, 2] == 0.0 and xo[0, 3] == 0.0
