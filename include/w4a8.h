@@ -56,6 +56,7 @@ extern "C" {
 #define W4A8_EALIGN     -5  /* a base pointer is not 16-byte aligned             */
 #define W4A8_EHIP       -6  /* a HIP runtime call or kernel launch failed        */
 #define W4A8_EDEVICE    -7  /* the current device is not gfx950                  */
+#define W4A8_EALIAS     -8  /* an output shares its base address with an operand */
 
 #define W4A8_Q4_0_BLOCK_BYTES 18
 #define W4A8_Q8_0_BLOCK_BYTES 34
@@ -119,6 +120,8 @@ int moe_w4a8_workspace_init(void *workspace, size_t ws_bytes, void *stream);
  *   W4A8_WS_COUNT int32 [E]: routed pairs per expert (not written when T == 1).
  *   W4A8_WS_SYNC  start of the synchronisation words, which end at
  *                 W4A8_WS_SYNC_END: zero before and after every call.
+ *   W4A8_WS_XN    fp32 RMSNorm(x + y_prev) * gamma, [T][H] (moe_w4a8_layer
+ *                 only).
  * Pair numbering: routed slot j of token t is pair t*k + j; the shared expert
  * of token t is pair T*k + t.  Rows of skipped slots are not written.
  */
@@ -129,7 +132,8 @@ int moe_w4a8_workspace_init(void *workspace, size_t ws_bytes, void *stream);
 #define W4A8_WS_COUNT  4
 #define W4A8_WS_SYNC   5
 #define W4A8_WS_SYNC_END 6
-#define W4A8_WS_NFIELDS 7
+#define W4A8_WS_XN     7
+#define W4A8_WS_NFIELDS 8
 int moe_w4a8_workspace_layout(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
                               size_t *offsets);
 
@@ -166,6 +170,29 @@ int moe_w4a8_forward(const float *hidden, const int32_t *topk_ids, const float *
                      const void *ws_gate_up, const void *ws_down,
                      float *out, int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
                      void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * One pre-norm residual MoE step of a chained stack (the layer input is the
+ * RMSNorm of the residual stream, as in the Qwen3-series model family of
+ * Sec. 2.2; the paper does not spell the norm out, so it is the standard
+ * RMSNorm, see rmsnorm_residual):
+ *   x_out = x + y_prev              one binary32 addition per element
+ *                                   (x_out = x when y_prev is NULL)
+ *   xn    = RMSNorm(x_out) * gamma  kept in the workspace region W4A8_WS_XN
+ *   out   = moe_w4a8_forward's layer applied to xn
+ * Arguments as for moe_w4a8_forward, plus x [T][H], y_prev [T][H] or NULL,
+ * gamma [H], eps >= 0, x_out [T][H]; x_out and out must not alias x,
+ * y_prev or each other (equal base addresses -> W4A8_EALIAS).  At T = 1 the norm runs inside the single decode
+ * launch (every workgroup normalizes the row it quantizes).  gamma or x_out
+ * NULL -> W4A8_ENULL; eps < 0 -> W4A8_ESHAPE; other errors as for
+ * moe_w4a8_forward.
+ */
+int moe_w4a8_layer(const float *x, const float *y_prev, const float *gamma, float eps,
+                   float *x_out, const int32_t *topk_ids, const float *topk_w,
+                   const void *w_gate_up, const void *w_down,
+                   const void *ws_gate_up, const void *ws_down,
+                   float *out, int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
+                   void *workspace, size_t ws_bytes, void *stream);
 
 /*
  * Residual add and RMSNorm between chained MoE layers (the pre-norm chaining

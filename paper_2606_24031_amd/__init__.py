@@ -14,14 +14,16 @@ import os
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libw4a8.so")
 
-OK, ENULL, ESHAPE, ERANGE, EWORKSPACE, EALIGN, EHIP, EDEVICE = 0, -1, -2, -3, -4, -5, -6, -7
+OK, ENULL, ESHAPE, ERANGE, EWORKSPACE, EALIGN, EHIP, EDEVICE, EALIAS = 0, -1, -2, -3, -4, -5, -6, -7, -8
 Q4_0_BLOCK_BYTES = 18
 Q8_0_BLOCK_BYTES = 34
-WS_XQ, WS_H, WS_HQ, WS_PERM, WS_COUNT, WS_SYNC, WS_SYNC_END, WS_NFIELDS = 0, 1, 2, 3, 4, 5, 6, 7
+WS_XQ, WS_H, WS_HQ, WS_PERM, WS_COUNT, WS_SYNC, WS_SYNC_END, WS_XN = 0, 1, 2, 3, 4, 5, 6, 7
+WS_NFIELDS = 8
 
 EXPORTS = ("w4a8_strerror", "q8_0_quantize", "q4_0_quantize", "q4q8_gemv",
            "moe_w4a8_workspace_size", "moe_w4a8_workspace_init",
-           "moe_w4a8_workspace_layout", "moe_w4a8_forward", "rmsnorm_residual")
+           "moe_w4a8_workspace_layout", "moe_w4a8_forward", "moe_w4a8_layer",
+           "rmsnorm_residual")
 
 _lib = None
 
@@ -57,6 +59,9 @@ def lib() -> ctypes.CDLL:
     L.moe_w4a8_workspace_layout.restype = ctypes.c_int
     L.moe_w4a8_forward.argtypes = [P, P, P, P, P, P, P, P, I64, I64, I64, I64, I64, P, SZ, P]
     L.moe_w4a8_forward.restype = ctypes.c_int
+    L.moe_w4a8_layer.argtypes = [P, P, P, ctypes.c_float, P, P, P, P, P, P, P, P,
+                                 I64, I64, I64, I64, I64, P, SZ, P]
+    L.moe_w4a8_layer.restype = ctypes.c_int
     L.rmsnorm_residual.argtypes = [P, P, P, P, P, I64, I64, ctypes.c_float, P]
     L.rmsnorm_residual.restype = ctypes.c_int
     _lib = L
@@ -139,7 +144,8 @@ def moe_workspace_layout(T, H, I, E, k) -> dict:
     offs = (ctypes.c_size_t * WS_NFIELDS)()
     _check(lib().moe_w4a8_workspace_layout(T, H, I, E, k, offs), "moe_w4a8_workspace_layout")
     return {"xq": offs[WS_XQ], "h": offs[WS_H], "hq": offs[WS_HQ], "perm": offs[WS_PERM],
-            "count": offs[WS_COUNT], "sync": offs[WS_SYNC], "sync_end": offs[WS_SYNC_END]}
+            "count": offs[WS_COUNT], "sync": offs[WS_SYNC], "sync_end": offs[WS_SYNC_END],
+            "xn": offs[WS_XN]}
 
 
 def moe_forward(hidden, topk_ids, topk_w, w_gate_up, w_down, ws_gate_up, ws_down,
@@ -175,3 +181,24 @@ def rmsnorm_residual(x, y, gamma, eps=1e-6, x_out=None, xn=None, want_norm=True,
                                 _p(xn if want_norm else None), T, H, float(eps), _stream(stream))
     _check(rc, "rmsnorm_residual")
     return x_out, (xn if want_norm else None)
+
+
+def moe_layer(x, y_prev, gamma, topk_ids, topk_w, w_gate_up, w_down, ws_gate_up, ws_down,
+              H, I, E, k, workspace, eps=1e-6, x_out=None, out=None, stream=None):
+    """One pre-norm residual MoE step: x_out = x + y_prev, out = MoE(RMSNorm(x_out)
+    * gamma); returns (x_out, out)."""
+    import torch
+    T = x.shape[0]
+    for t in (x, y_prev, gamma, topk_w):
+        assert t is None or (t.dtype == torch.float32 and t.is_contiguous())
+    assert topk_ids.dtype == torch.int32 and topk_ids.is_contiguous()
+    if x_out is None:
+        x_out = torch.empty_like(x)
+    if out is None:
+        out = torch.empty_like(x)
+    rc = lib().moe_w4a8_layer(_p(x), _p(y_prev), _p(gamma), float(eps), _p(x_out), _p(topk_ids),
+                              _p(topk_w), _p(_u8(w_gate_up)), _p(_u8(w_down)), _p(ws_gate_up),
+                              _p(ws_down), _p(out), T, H, I, E, k, _p(workspace),
+                              workspace.numel(), _stream(stream))
+    _check(rc, "moe_w4a8_layer")
+    return x_out, out

@@ -14,6 +14,7 @@ extern "C" const char *w4a8_strerror(int code) {
     case W4A8_EALIGN: return "a base pointer is not 16-byte aligned";
     case W4A8_EHIP: return "HIP runtime error or kernel launch failure";
     case W4A8_EDEVICE: return "current device is not gfx950 (MI355X)";
+    case W4A8_EALIAS: return "an output buffer aliases an input or another output";
     default: return "unknown status code";
   }
 }

@@ -67,6 +67,13 @@ struct DecodeArgs {
   uint32_t *sync;          // arrival counters
   uint32_t *calls;         // call counter (tag of this call = *calls + 1)
   uint64_t *xfer;          // Q8_0(h) hand-off: [(k+1) * I/32][XSTRIDE] tagged words (XW used)
+  // pre-norm residual input (gamma != nullptr): the layer's input is
+  // xn = RMSNorm(x + resid) * gamma instead of x; workgroup 0 writes
+  // x_out = x + resid and the documented copy xn
+  const float *resid;      // [H] or nullptr
+  const float *gamma;      // [H] or nullptr (no norm)
+  float *x_out, *xn;       // [H]
+  float eps;
   uint8_t *xq;             // documented copy of Q8_0(x)   [H/32 blocks]
   float *h;                // documented copy of h          [(k+1)][I]
   uint8_t *hq;             // documented copy of Q8_0(h)    [(k+1)][I/32 blocks]
@@ -145,19 +152,57 @@ __device__ __forceinline__ const uint4 *group_codes(ActBuf b, int blk0) {
   return b.codes + (blk0 >> 3) * GROUP_U4;
 }
 
-// Q8_0 of x (fp32 [H], global) into the LDS staging; with `xq_out` also the
-// 34-byte blocks to global memory.  8 lanes per block, 4 values per lane.
-// `first` is the lane's first float4 of x, loaded by the caller ahead of the
-// weight loads.
-__device__ void quantize_x_to_lds(const DecodeArgs &a, ActBuf xb, uint8_t *xq_out,
-                                  float4 first) {
+// Element 4t..4t+3 of the layer's input: x, or x + resid in norm mode.
+__device__ __forceinline__ float4 input4(const DecodeArgs &a, int t) {
+  float4 v = reinterpret_cast<const float4 *>(a.x)[t];
+  if (a.resid) {
+    const float4 d = reinterpret_cast<const float4 *>(a.resid)[t];
+    v.x += d.x; v.y += d.y; v.z += d.z; v.w += d.w;
+  }
+  return v;
+}
+
+// Q8_0 of the layer's input (x, or RMSNorm(x + resid) * gamma) into the LDS
+// staging; with `first_wg` also the 34-byte blocks to xq and, in norm mode,
+// x + resid to x_out and the normalized row to xn.  8 lanes per block, 4
+// values per lane.  `first` is the lane's first float4 of the input, loaded
+// by the caller ahead of the weight loads.  Every thread must call it.
+__device__ void quantize_x_to_lds(const DecodeArgs &a, ActBuf xb, bool first_wg, float4 first) {
+  __shared__ float wss[NT / 64];
   const int tasks = a.H / 4;
+  float r = 1.0f;
+  if (a.gamma) {
+    // sum of squares in a fixed order: per thread in index order, a
+    // butterfly per wave, the waves in order
+    float ss = 0.0f;
+    for (int t = threadIdx.x; t < tasks; t += NT) {
+      const float4 v = t < NT ? first : input4(a, t);
+      ss = fmaf(v.x, v.x, ss);
+      ss = fmaf(v.y, v.y, ss);
+      ss = fmaf(v.z, v.z, ss);
+      ss = fmaf(v.w, v.w, ss);
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
+    if ((threadIdx.x & 63) == 0) wss[threadIdx.x >> 6] = ss;
+    __syncthreads();
+    float tot = 0.0f;
+#pragma unroll
+    for (int w = 0; w < NT / 64; w++) tot += wss[w];
+    r = 1.0f / sqrtf(tot / (float)a.H + a.eps);
+  }
   for (int t0 = 0; t0 < tasks; t0 += NT) {
     const int t = t0 + threadIdx.x;
     const bool live = t < tasks;  // tasks % 8 == 0: whole 8-lane groups agree
     float v[4] = {0.f, 0.f, 0.f, 0.f};
     if (live) {
-      const float4 f = t0 == 0 ? first : reinterpret_cast<const float4 *>(a.x)[t];
+      float4 f = t0 == 0 ? first : input4(a, t);
+      if (a.gamma) {
+        if (first_wg) reinterpret_cast<float4 *>(a.x_out)[t] = f;
+        const float4 g = reinterpret_cast<const float4 *>(a.gamma)[t];
+        f = make_float4(f.x * r * g.x, f.y * r * g.y, f.z * r * g.z, f.w * r * g.w);
+        if (first_wg) reinterpret_cast<float4 *>(a.xn)[t] = f;
+      }
       v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
     }
     uint32_t d16;
@@ -170,7 +215,7 @@ __device__ void quantize_x_to_lds(const DecodeArgs &a, ActBuf xb, uint8_t *xq_ou
         xb.d[blk] = f16_bits_to_f32(d16);
         xb.corr[blk] = -8 * sum;
       }
-      if (xq_out) store_q8_0_block8(xq_out + blk * Q8B, j, packed, d16);
+      if (first_wg) store_q8_0_block8(a.xq + blk * Q8B, j, packed, d16);
     }
   }
 }
@@ -251,8 +296,7 @@ __device__ void gateup_block(const DecodeArgs &a, int q, int e, int b, ActBuf xb
 }
 
 __device__ __forceinline__ float4 load_x_first(const DecodeArgs &a) {
-  return threadIdx.x < a.H / 4 ? reinterpret_cast<const float4 *>(a.x)[threadIdx.x]
-                               : make_float4(0.f, 0.f, 0.f, 0.f);
+  return (int)threadIdx.x < a.H / 4 ? input4(a, threadIdx.x) : make_float4(0.f, 0.f, 0.f, 0.f);
 }
 
 // Every workgroup arrives once; the last arrival of the launch advances the
@@ -358,7 +402,7 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
     if (valid && r.gg < a.H / 256) load_w8(a_row(a, e, b, r) + (int64_t)r.gg * (8 * Q4B), w0);
     const uint32_t tag = ld_agent(a.calls) + 1u;
     if (valid || wg == 0) {
-      quantize_x_to_lds(a, xb, wg == 0 ? a.xq : nullptr, x0);
+      quantize_x_to_lds(a, xb, wg == 0, x0);
       __syncthreads();
     }
     if (valid) gateup_block<true>(a, q, e, b, xb, w0, hv, tag, nullptr);
@@ -403,7 +447,7 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
   const bool ok = collect(a, hb, tag, XW * nbh, vmask, notdone);
   if (!ok) {
     // fallback: compute every pair's Q8_0(h) here (same code, same bytes)
-    quantize_x_to_lds(a, xb, nullptr, load_x_first(a));
+    quantize_x_to_lds(a, xb, false, load_x_first(a));
     __syncthreads();
     for (int q = 0; q < npairs; q++) {
       if (!((vmask >> q) & 1)) continue;
@@ -503,10 +547,11 @@ bool decode_supported(int64_t H, int64_t I, int64_t k) {
   return XW * nbh <= NWMAX * NT && lds_bytes((int)H, (int)I, (int)k, rb) <= 48 * 1024;
 }
 
-int decode_forward(const float *x, const int32_t *ids, const float *topk_w, const uint8_t *w_gu,
-                   const uint8_t *w_d, const uint8_t *ws_gu, const uint8_t *ws_d, float *out,
-                   int64_t H, int64_t I, int64_t E, int64_t k, uint32_t *sync, uint32_t *xfer,
-                   uint8_t *xq, float *h, uint8_t *hq, hipStream_t s) {
+int decode_forward(const float *x, const DecodeNorm &norm, const int32_t *ids,
+                   const float *topk_w, const uint8_t *w_gu, const uint8_t *w_d,
+                   const uint8_t *ws_gu, const uint8_t *ws_d, float *out, int64_t H, int64_t I,
+                   int64_t E, int64_t k, uint32_t *sync, uint32_t *xfer, uint8_t *xq, float *h,
+                   uint8_t *hq, hipStream_t s) {
   if (g_num_cus == 0) {
     int dev = 0, n = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
@@ -522,6 +567,8 @@ int decode_forward(const float *x, const int32_t *ids, const float *topk_w, cons
   a.sync = sync;
   a.calls = xfer;
   a.xfer = reinterpret_cast<uint64_t *>(xfer + XFER_HDR);
+  a.resid = norm.resid; a.gamma = norm.gamma; a.x_out = norm.x_out; a.xn = norm.xn;
+  a.eps = norm.eps;
   a.xq = xq; a.h = h; a.hq = hq;
   a.H = (int)H; a.I = (int)I; a.E = (int)E; a.k = (int)k;
   int grid = 0;

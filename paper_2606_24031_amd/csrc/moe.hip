@@ -35,10 +35,13 @@ int grouped_down(const uint8_t *w_d, const uint8_t *ws_d, const uint8_t *hq, con
 size_t decode_sync_words(int64_t H);
 size_t decode_xfer_words(int64_t I, int64_t k);
 bool decode_supported(int64_t H, int64_t I, int64_t k);
-int decode_forward(const float *x, const int32_t *ids, const float *topk_w, const uint8_t *w_gu,
-                   const uint8_t *w_d, const uint8_t *ws_gu, const uint8_t *ws_d, float *out,
-                   int64_t H, int64_t I, int64_t E, int64_t k, uint32_t *sync, uint32_t *xfer,
-                   uint8_t *xq, float *h, uint8_t *hq, hipStream_t s);
+int decode_forward(const float *x, const DecodeNorm &norm, const int32_t *ids,
+                   const float *topk_w, const uint8_t *w_gu, const uint8_t *w_d,
+                   const uint8_t *ws_gu, const uint8_t *ws_d, float *out, int64_t H, int64_t I,
+                   int64_t E, int64_t k, uint32_t *sync, uint32_t *xfer, uint8_t *xq, float *h,
+                   uint8_t *hq, hipStream_t s);
+int launch_rmsnorm(const float *x, const float *y, const float *gamma, float *x_out, float *xn,
+                   int64_t T, int64_t H, float eps, hipStream_t s);
 
 namespace {
 
@@ -49,7 +52,7 @@ constexpr int LDS_INTS = 16000; // int32 cells of dynamic LDS for the route kern
 inline size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t meta, sync, xfer, perm, count, rank, groups, tiles, xq, h, hq, y, total;
+  size_t meta, sync, xfer, perm, count, rank, groups, tiles, xq, h, hq, y, xn, total;
   int64_t maxtiles;
 };
 
@@ -71,6 +74,7 @@ Layout make_layout(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k) {
   L.h = off;      off += up256(sizeof(float) * (size_t)P * I);
   L.hq = off;     off += up256((size_t)P * (I / QK) * Q8B);
   L.y = off;      off += up256(sizeof(float) * (size_t)P * H);
+  L.xn = off;     off += up256(sizeof(float) * (size_t)T * H);
   L.total = off;
   return L;
 }
@@ -234,21 +238,30 @@ __global__ __launch_bounds__(256) void combine_kernel(const float *__restrict__ 
 
 }  // namespace
 
-int moe_forward_impl(const float *hidden, const int32_t *ids, const float *topk_w,
-                     const uint8_t *w_gu, const uint8_t *w_d, const uint8_t *ws_gu,
-                     const uint8_t *ws_d, float *out, int64_t T, int64_t H, int64_t I,
-                     int64_t E, int64_t k, uint8_t *ws, size_t ws_bytes, hipStream_t s) {
+int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
+                     const float *topk_w, const uint8_t *w_gu, const uint8_t *w_d,
+                     const uint8_t *ws_gu, const uint8_t *ws_d, float *out, int64_t T, int64_t H,
+                     int64_t I, int64_t E, int64_t k, uint8_t *ws, size_t ws_bytes,
+                     hipStream_t s) {
   const Layout L = make_layout(T, H, I, E, k);
   const int has_shared = ws_gu != nullptr;
   int rc;
+  if (norm.gamma) norm.xn = reinterpret_cast<float *>(ws + L.xn);
 
-  // One token: the whole layer in a single launch (see decode.hip).
+  // One token: the whole layer in a single launch, the residual RMSNorm
+  // included (see decode.hip).
   if (T == 1 && decode_supported(H, I, k))
-    return decode_forward(hidden, ids, topk_w, w_gu, w_d, ws_gu, ws_d, out, H, I, E, k,
+    return decode_forward(hidden, norm, ids, topk_w, w_gu, w_d, ws_gu, ws_d, out, H, I, E, k,
                           reinterpret_cast<uint32_t *>(ws + L.sync),
                           reinterpret_cast<uint32_t *>(ws + L.xfer), ws + L.xq,
                           reinterpret_cast<float *>(ws + L.h), ws + L.hq, s);
 
+  if (norm.gamma) {
+    if ((rc = launch_rmsnorm(hidden, norm.resid, norm.gamma, norm.x_out, norm.xn, T, H, norm.eps,
+                             s)) != W4A8_OK)
+      return rc;
+    hidden = norm.xn;
+  }
   if ((rc = launch_q8_0(hidden, ws + L.xq, T * (H / QK), s)) != W4A8_OK) return rc;
 
   RouteArgs ra;
@@ -314,6 +327,7 @@ extern "C" int moe_w4a8_workspace_layout(int64_t T, int64_t H, int64_t I, int64_
   offsets[W4A8_WS_COUNT] = L.count;
   offsets[W4A8_WS_SYNC] = L.sync;
   offsets[W4A8_WS_SYNC_END] = L.xfer;
+  offsets[W4A8_WS_XN] = L.xn;
   return W4A8_OK;
 }
 
@@ -325,11 +339,13 @@ extern "C" int moe_w4a8_workspace_init(void *workspace, size_t ws_bytes, void *s
   return launch_fill_zero(workspace, ws_bytes, as_stream(stream));
 }
 
-extern "C" int moe_w4a8_forward(const float *hidden, const int32_t *topk_ids,
-                                const float *topk_w, const void *w_gate_up, const void *w_down,
-                                const void *ws_gate_up, const void *ws_down, float *out,
-                                int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
-                                void *workspace, size_t ws_bytes, void *stream) {
+namespace w4a8 {
+namespace {
+
+int moe_args(const float *hidden, const int32_t *topk_ids, const float *topk_w,
+             const void *w_gate_up, const void *w_down, const void *ws_gate_up,
+             const void *ws_down, const float *out, int64_t T, int64_t H, int64_t I, int64_t E,
+             int64_t k, const void *workspace, size_t ws_bytes) {
   int rc = validate(T, H, I, E, k);
   if (rc != W4A8_OK) return rc;
   if (T == 0) return W4A8_OK;
@@ -341,8 +357,50 @@ extern "C" int moe_w4a8_forward(const float *hidden, const int32_t *topk_ids,
     if (!aligned16(p)) return W4A8_EALIGN;
   if (ws_gate_up && (!aligned16(ws_gate_up) || !aligned16(ws_down))) return W4A8_EALIGN;
   if (ws_bytes < make_layout(T, H, I, E, k).total) return W4A8_EWORKSPACE;
+  return W4A8_OK;
+}
+
+}  // namespace
+}  // namespace w4a8
+
+extern "C" int moe_w4a8_forward(const float *hidden, const int32_t *topk_ids,
+                                const float *topk_w, const void *w_gate_up, const void *w_down,
+                                const void *ws_gate_up, const void *ws_down, float *out,
+                                int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
+                                void *workspace, size_t ws_bytes, void *stream) {
+  int rc = moe_args(hidden, topk_ids, topk_w, w_gate_up, w_down, ws_gate_up, ws_down, out, T, H,
+                    I, E, k, workspace, ws_bytes);
+  if (rc != W4A8_OK || T == 0) return rc;
   if ((rc = check_device()) != W4A8_OK) return rc;
-  return moe_forward_impl(hidden, topk_ids, topk_w,
+  return moe_forward_impl(hidden, DecodeNorm{}, topk_ids, topk_w,
+                          reinterpret_cast<const uint8_t *>(w_gate_up),
+                          reinterpret_cast<const uint8_t *>(w_down),
+                          reinterpret_cast<const uint8_t *>(ws_gate_up),
+                          reinterpret_cast<const uint8_t *>(ws_down), out, T, H, I, E, k,
+                          reinterpret_cast<uint8_t *>(workspace), ws_bytes, as_stream(stream));
+}
+
+extern "C" int moe_w4a8_layer(const float *x, const float *y_prev, const float *gamma, float eps,
+                              float *x_out, const int32_t *topk_ids, const float *topk_w,
+                              const void *w_gate_up, const void *w_down, const void *ws_gate_up,
+                              const void *ws_down, float *out, int64_t T, int64_t H, int64_t I,
+                              int64_t E, int64_t k, void *workspace, size_t ws_bytes,
+                              void *stream) {
+  int rc = moe_args(x, topk_ids, topk_w, w_gate_up, w_down, ws_gate_up, ws_down, out, T, H, I, E,
+                    k, workspace, ws_bytes);
+  if (rc != W4A8_OK || T == 0) return rc;
+  if (!gamma || !x_out) return W4A8_ENULL;
+  if (!(eps >= 0.0f)) return W4A8_ESHAPE;
+  if (!aligned16(y_prev) || !aligned16(gamma) || !aligned16(x_out)) return W4A8_EALIGN;
+  if (x_out == x || x_out == out || out == x || (y_prev && (x_out == y_prev || out == y_prev)))
+    return W4A8_EALIAS;
+  if ((rc = check_device()) != W4A8_OK) return rc;
+  DecodeNorm norm;
+  norm.resid = y_prev;
+  norm.gamma = gamma;
+  norm.x_out = x_out;
+  norm.eps = eps;
+  return moe_forward_impl(x, norm, topk_ids, topk_w,
                           reinterpret_cast<const uint8_t *>(w_gate_up),
                           reinterpret_cast<const uint8_t *>(w_down),
                           reinterpret_cast<const uint8_t *>(ws_gate_up),

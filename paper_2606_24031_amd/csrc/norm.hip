@@ -53,6 +53,15 @@ __global__ __launch_bounds__(NT) void rmsnorm_kernel(const float4 *x, const floa
 
 }  // namespace
 
+int launch_rmsnorm(const float *x, const float *y, const float *gamma, float *x_out, float *xn,
+                   int64_t T, int64_t H, float eps, hipStream_t s) {
+  rmsnorm_kernel<<<dim3((unsigned)T), dim3(NT), 0, s>>>(
+      reinterpret_cast<const float4 *>(x), reinterpret_cast<const float4 *>(y),
+      reinterpret_cast<const float4 *>(gamma), reinterpret_cast<float4 *>(x_out),
+      reinterpret_cast<float4 *>(xn), H / 4, eps);
+  return check_launch();
+}
+
 }  // namespace w4a8
 
 extern "C" int rmsnorm_residual(const float *x, const float *y, const float *gamma, float *x_out,
@@ -65,9 +74,5 @@ extern "C" int rmsnorm_residual(const float *x, const float *y, const float *gam
     return W4A8_EALIGN;
   if (T == 0) return W4A8_OK;
   if (int rc = check_device(); rc != W4A8_OK) return rc;
-  rmsnorm_kernel<<<dim3((unsigned)T), dim3(NT), 0, as_stream(stream)>>>(
-      reinterpret_cast<const float4 *>(x), reinterpret_cast<const float4 *>(y),
-      reinterpret_cast<const float4 *>(gamma), reinterpret_cast<float4 *>(x_out),
-      reinterpret_cast<float4 *>(xn), H / 4, eps);
-  return check_launch();
+  return launch_rmsnorm(x, y, gamma, x_out, xn, T, H, eps, as_stream(stream));
 }

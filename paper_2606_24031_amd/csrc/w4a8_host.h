@@ -19,4 +19,14 @@ inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 
 
 inline hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s); }
 
+// Pre-norm residual input of a layer call: with gamma set, the layer's input
+// is xn = RMSNorm(x + resid) * gamma, and x + resid goes to x_out.
+struct DecodeNorm {
+  const float *resid = nullptr;
+  const float *gamma = nullptr;
+  float *x_out = nullptr;
+  float *xn = nullptr;
+  float eps = 0.0f;
+};
+
 }  // namespace w4a8

@@ -29,7 +29,8 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_strerror_covers_every_code():
-    for code in (w4.OK, w4.ENULL, w4.ESHAPE, w4.ERANGE, w4.EWORKSPACE, w4.EALIGN, w4.EHIP, w4.EDEVICE):
+    for code in (w4.OK, w4.ENULL, w4.ESHAPE, w4.ERANGE, w4.EWORKSPACE, w4.EALIGN, w4.EHIP, w4.EDEVICE,
+                 w4.EALIAS):
         msg = w4.strerror(code)
         assert msg and msg != "unknown status code"
     assert w4.strerror(12345) == "unknown status code"
@@ -111,3 +112,27 @@ def test_rmsnorm_argument_errors():
     assert f(p, _fake(A + 4), p, p, p, 2, 256, 1e-6, None) == w4.EALIGN
     assert f(p, None, p, p, p, 0, 256, 1e-6, None) == w4.OK            # empty: no-op
     assert f(p, None, p, p, p, 1 << 31, 256, 1e-6, None) == w4.ERANGE
+
+
+def test_moe_layer_argument_errors():
+    L = w4.lib()
+    f = L.moe_w4a8_layer
+    T, H, I, E, k = 2, 256, 256, 4, 2
+    need = L.moe_w4a8_workspace_size(T, H, I, E, k)
+    x, yp, g, xo, ids, tw, wgu, wd, out, ws = (_fake(A + 4096 * i) for i in range(10))
+
+    def call(x=x, yp=yp, g=g, eps=1e-6, xo=xo, out=out, T=T, ws_bytes=need):
+        return f(x, yp, g, eps, xo, ids, tw, wgu, wd, None, None, out, T, H, I, E, k, ws,
+                 ws_bytes, None)
+    assert call(g=None) == w4.ENULL
+    assert call(xo=None) == w4.ENULL
+    assert call(x=None) == w4.ENULL
+    assert call(eps=-1.0) == w4.ESHAPE
+    assert call(yp=_fake(A + 2)) == w4.EALIGN
+    assert call(g=_fake(A + 8)) == w4.EALIGN
+    assert call(xo=x) == w4.EALIAS
+    assert call(xo=yp) == w4.EALIAS
+    assert call(out=xo) == w4.EALIAS
+    assert call(out=yp) == w4.EALIAS
+    assert call(ws_bytes=need - 1) == w4.EWORKSPACE
+    assert call(T=0) == w4.OK                                         # empty: no-op

@@ -330,3 +330,35 @@ def test_rmsnorm_residual_in_place_and_no_norm():
     assert np.allclose(host(xn), xn_ref, rtol=2e-6, atol=1e-7)
     xo2, none = w4.rmsnorm_residual(dev(x), dev(y), None, want_norm=False)
     assert none is None and np.array_equal(host(xo2), ref)
+
+
+# ------------------------------------------------------ pre-norm residual layer
+@pytest.mark.parametrize("T,with_prev", [(1, True), (1, False), (6, True), (40, True)])
+def test_moe_layer_residual_norm(qwen_layer, T, with_prev):
+    """x_out = x + y_prev is one fp32 add, xn = RMSNorm(x_out) * gamma is within
+    fp32 rounding of the oracle, Q8_0(xn) is bit-exact for the GPU's own xn,
+    and the layer output is the MoE layer of that xn (T = 1: the norm inside
+    the single decode launch; T > 1: rmsnorm kernel, then the grouped path)."""
+    L = qwen_layer
+    g = synth.rng(60 + T)
+    x = synth.normal_f32(g, (T, L.H))
+    y_prev = synth.normal_f32(g, (T, L.H), 0.3) if with_prev else None
+    gamma = (np.float32(1.0) + synth.normal_f32(g, (L.H,), 0.1)).astype(np.float32)
+    ids, wts = synth.routing(g, T, L.E, 8)
+    ws = w4.moe_workspace(T, L.H, L.I, L.E, 8)
+    x_out, out = w4.moe_layer(dev(x), None if y_prev is None else dev(y_prev), dev(gamma),
+                              dev(ids), dev(wts), L.d_gu, L.d_d, L.d_sgu, L.d_sd,
+                              L.H, L.I, L.E, 8, ws)
+    xo_ref, xn_ref = oracle.rmsnorm_residual(x, y_prev, gamma, eps=1e-6)
+    assert np.array_equal(host(x_out), xo_ref)
+    lay = w4.moe_workspace_layout(T, L.H, L.I, L.E, 8)
+    wsn = host(ws)
+    xn = wsn[lay["xn"]:lay["xn"] + T * L.H * 4].view(np.float32).reshape(T, L.H)
+    err = np.abs(xn.astype(np.float64) - xn_ref)
+    assert np.all(err <= 2e-6 * np.abs(xn_ref) + 1e-7 * np.abs(gamma).max())
+    xq = wsn[lay["xq"]:lay["xq"] + T * (L.H // 32) * 34].reshape(T, -1)
+    assert np.array_equal(xq, oracle.q8_0_quantize(xn)), "Q8_0 of the normalized row"
+    P = T * 8 + T
+    h = wsn[lay["h"]:lay["h"] + P * L.I * 4].view(np.float32).reshape(P, L.I)
+    hq = wsn[lay["hq"]:lay["hq"] + P * (L.I // 32) * 34].reshape(P, -1)
+    L.check(xn, ids, wts, 8, host(out), h, hq)
