@@ -13,6 +13,9 @@
 //     x to Q8_0 into LDS, take the W4A8 dots, reduce each row over its 8
 //     lanes with DPP (gate row and up row of one h column sit in the same
 //     wave), h = SiLU(g) * u, and publish Q8_0 of the 32 h values (one block).
+//   The block dots run on the 4-bit dot products: activations are staged
+//   in a nibble-split form (see split_word) so that the Q4_0 payload dwords
+//   feed the dots as loaded, with no unpacking of the weight nibbles.
 //   down slabs (rb down rows, all pairs): issue the down weight loads of every
 //     pair first, collect every pair's Q8_0(h), take the dots and write
 //     out[n] = sum_q w_q y_q[n] (slots in order, then the shared expert) --
@@ -20,7 +23,8 @@
 //     units the gate/up items leave free.
 //
 // Hand-off: each published word is 64 bits, the payload in the low half and
-// the call's tag in the high half, written with agent-scope (sc1) stores;
+// the call's tag in the high half (per block: the fp16 scale and the sum of
+// the unsigned nibbles, then the 8 dwords of the nibble-split codes), written with agent-scope (sc1) stores;
 // each block's words sit alone in one 128-byte line, so no line is written
 // from two XCDs.  A slab polls all the words until every one carries this
 // call's tag: one poll round trip and the store's visibility cost about
@@ -46,7 +50,7 @@ namespace {
 
 constexpr int NT = 512;          // threads per workgroup: 8 waves
 constexpr int NSUB = 8;          // first-level arrival counters
-constexpr int XW = 9;            // hand-off words per h block: scale and code sum, 8 code words
+constexpr int XW = 9;            // hand-off words per h block: scale and nibble sum, 8 code words
 constexpr int XSTRIDE = 16;      // 64-bit words between blocks: each block alone in a 128-byte line
 constexpr int XFER_HDR = 64;     // uint32 words ahead of the hand-off words: the call counter
 
@@ -117,8 +121,8 @@ __device__ __forceinline__ const uint8_t *expert_d(const DecodeArgs &a, int e) {
   return e < a.E ? a.w_d + (int64_t)e * a.H * (a.I / 256) * (8 * Q4B) : a.ws_d;
 }
 
-// LDS staging of activation blocks (see dot8_lds): the 32 codes of each
-// block as 8 dwords, groups of 8 blocks 272 bytes apart (16 bytes of padding
+// LDS staging of activation blocks (see dot8_lds): each block's nibble-split
+// form as 8 dwords, groups of 8 blocks 272 bytes apart (16 bytes of padding
 // per group), then scale [n] fp32 and correction [n] int32, carved from one
 // dynamic LDS buffer.  The lanes of a wave read up to 8 different groups at
 // once; without the padding those addresses would be 256 bytes apart and all
@@ -143,7 +147,7 @@ __device__ __forceinline__ ActBuf act_buf(uint8_t *base, int nblocks) {
 __host__ __device__ constexpr size_t act_buf_bytes(int nblocks) {
   return (act_codes_bytes(nblocks) + (size_t)nblocks * 8 + 15) / 16 * 16;
 }
-// dword j (0..7) of block blk's codes
+// dword j (0..7) of block blk's nibble-split form
 __device__ __forceinline__ uint32_t *code_word(ActBuf b, int blk, int j) {
   return reinterpret_cast<uint32_t *>(b.codes + (blk >> 3) * GROUP_U4) + (blk & 7) * 8 + j;
 }
@@ -175,8 +179,14 @@ __device__ void quantize_x_to_lds(const DecodeArgs &a, ActBuf xb, bool first_wg,
     // sum of squares in a fixed order: per thread in index order, a
     // butterfly per wave, the waves in order
     float ss = 0.0f;
-    for (int t = threadIdx.x; t < tasks; t += NT) {
-      const float4 v = t < NT ? first : input4(a, t);
+    if ((int)threadIdx.x < tasks) {
+      ss = fmaf(first.x, first.x, ss);
+      ss = fmaf(first.y, first.y, ss);
+      ss = fmaf(first.z, first.z, ss);
+      ss = fmaf(first.w, first.w, ss);
+    }
+    for (int t = threadIdx.x + NT; t < tasks; t += NT) {
+      const float4 v = input4(a, t);
       ss = fmaf(v.x, v.x, ss);
       ss = fmaf(v.y, v.y, ss);
       ss = fmaf(v.z, v.z, ss);
@@ -207,13 +217,14 @@ __device__ void quantize_x_to_lds(const DecodeArgs &a, ActBuf xb, bool first_wg,
     }
     uint32_t d16;
     const uint32_t packed = q8_0_block8(v, d16);
-    const int sum = sum8(sdot4((int)packed, 0x01010101, 0));
+    const uint32_t word = split_word(packed, t & 7);
+    const int lsum = sum8(low_nibble_sum(packed));
     if (live) {
       const int blk = t >> 3, j = t & 7;
-      *code_word(xb, blk, j) = packed;
+      *code_word(xb, blk, j) = word;
       if (j == 0) {
         xb.d[blk] = f16_bits_to_f32(d16);
-        xb.corr[blk] = -8 * sum;
+        xb.corr[blk] = -8 * lsum;
       }
       if (first_wg) store_q8_0_block8(a.xq + blk * Q8B, j, packed, d16);
     }
@@ -278,18 +289,19 @@ __device__ void gateup_block(const DecodeArgs &a, int q, int e, int b, ActBuf xb
     const float v[4] = {hv[4 * j], hv[4 * j + 1], hv[4 * j + 2], hv[4 * j + 3]};
     uint32_t d16;
     const uint32_t packed = q8_0_block8(v, d16);
-    const int csum = sum8(sdot4((int)packed, 0x01010101, 0));   // |csum| <= 4064
+    const uint32_t word = split_word(packed, j);
+    const int lsum = sum8(low_nibble_sum(packed));              // 0..480
     uint64_t *xf = a.xfer + (int64_t)(q * (a.I / 32) + b) * XSTRIDE;
     const uint64_t hi = (uint64_t)tag << 32;
-    st_agent64(xf + 1 + j, hi | packed);
-    if (j == 0) st_agent64(xf, hi | d16 | ((uint32_t)csum << 16));
+    st_agent64(xf + 1 + j, hi | word);
+    if (j == 0) st_agent64(xf, hi | d16 | ((uint32_t)lsum << 16));
     store_q8_0_block8(a.hq + ((int64_t)q * (a.I / 32) + b) * Q8B, j, packed, d16);
     if (stage != nullptr) {
       const int blk = q * (a.I / 32) + b;
-      *code_word(*stage, blk, j) = packed;
+      *code_word(*stage, blk, j) = word;
       if (j == 0) {
         stage->d[blk] = f16_bits_to_f32(d16);
-        stage->corr[blk] = -8 * csum;
+        stage->corr[blk] = -8 * lsum;
       }
     }
   }
@@ -320,7 +332,7 @@ __device__ void arrive(const DecodeArgs &a, uint32_t tag) {
 __device__ __forceinline__ void stage_word(ActBuf hb, int blk, int w, uint32_t v) {
   if (w == 0) {
     hb.d[blk] = f16_bits_to_f32(v);
-    hb.corr[blk] = -8 * (int)(int16_t)(v >> 16);
+    hb.corr[blk] = -8 * (int)(v >> 16);
   } else {
     *code_word(hb, blk, w - 1) = v;
   }

@@ -126,30 +126,6 @@ __device__ __forceinline__ float dot8(const W8 &w, const Act8 &a, float acc) {
   return acc;
 }
 
-// Activation blocks staged in LDS in an aligned layout: block i's 32 codes as
-// 8 dwords at codes[2i], codes[2i+1] (uint4), its fp32 scale d[i] and its
-// correction corr[i] = -8 * (sum of codes).  The dot reads one block at a
-// time, so only ~10 registers of activation are live.
-__device__ __forceinline__ float dot8_lds(const W8 &w, const uint4 *__restrict__ codes,
-                                          const float *__restrict__ d,
-                                          const int *__restrict__ corr, float acc) {
-#pragma unroll
-  for (int k = 0; k < 8; k++) {
-    const uint4 c0 = codes[2 * k], c1 = codes[2 * k + 1];
-    const int a_lo[4] = {(int)c0.x, (int)c0.y, (int)c0.z, (int)c0.w};
-    const int a_hi[4] = {(int)c1.x, (int)c1.y, (int)c1.z, (int)c1.w};
-    int s = corr[k];
-#pragma unroll
-    for (int c = 0; c < 4; c++) {
-      const uint32_t n = w8_nib(w, k, c);
-      s = sdot4((int)(n & 0x0F0F0F0Fu), a_lo[c], s);
-      s = sdot4((int)((n >> 4) & 0x0F0F0F0Fu), a_hi[c], s);
-    }
-    acc = fmaf((float)s, w8_scale(w, k) * d[k], acc);
-  }
-  return acc;
-}
-
 // Cross-lane moves through DPP (a VALU operand modifier, no LDS round trip).
 // quad_perm [1,0,3,2] and [2,3,0,1] exchange with lane^1 and lane^2;
 // row_half_mirror maps lane i of each 8-lane half-row to lane 7-i, which
@@ -186,6 +162,67 @@ __device__ __forceinline__ float max8(float v) {
   v = fmaxf(v, dpp_f<DPP_XOR2>(v));
   v = fmaxf(v, dpp_f<DPP_HALF_MIRROR>(v));
   return v;
+}
+
+// Lane i of each 8-lane group receives lane i ^ 4's value: row_ror:12 (lane
+// i reads lane i + 4 of its 16-lane row) into DPP banks 0 and 2, row_ror:4
+// (lane i - 4) into banks 1 and 3.
+constexpr int DPP_ROR4 = 0x124, DPP_ROR12 = 0x12C;
+__device__ __forceinline__ uint32_t xchg4(uint32_t v) {
+  const int t = __builtin_amdgcn_update_dpp(0, (int)v, DPP_ROR12, 0xF, 0x5, false);
+  return (uint32_t)__builtin_amdgcn_update_dpp(t, (int)v, DPP_ROR4, 0xF, 0xA, false);
+}
+
+// Nibble-split form of a Q8_0 block, for the 4-bit dot products.  A code x
+// in [-127, 127] is 16 * (x >> 4) + (x & 15): a signed nibble in [-8, 7] and
+// an unsigned nibble in [0, 15].  Dwords 0..3 of the block hold the signed
+// parts, dwords 4..7 the unsigned parts, each in the nibble order of the
+// Q4_0 payload dword with the same index c: nibbles 2i and 2i+1 belong to
+// elements 4c+i and 4c+i+16.  Lane j of an 8-lane group holding the codes of
+// elements 4j..4j+3 (one byte each, `packed`) returns dword j of the form;
+// all 8 lanes must be active.
+__device__ __forceinline__ uint32_t split_word(uint32_t packed, int j) {
+  const uint32_t other = xchg4(packed);
+  return j < 4 ? (other & 0xF0F0F0F0u) | ((packed >> 4) & 0x0F0F0F0Fu)
+               : ((packed << 4) & 0xF0F0F0F0u) | (other & 0x0F0F0F0Fu);
+}
+// Sum of the unsigned nibbles of the lane's four codes (0..60).
+__device__ __forceinline__ int low_nibble_sum(uint32_t packed) {
+  return sdot4((int)(packed & 0x0F0F0F0Fu), 0x01010101, 0);
+}
+
+// Exact block dot s = sum (q_w - 8) * x over a block in nibble-split form:
+// q_w - 8 is the signed nibble q_w ^ 8, so
+//   s = 16 * sum (q_w ^ 8) * hi + sum q_w * lo - 8 * sum lo,
+// two 8-wide 4-bit dot products per payload dword and no unpacking of the
+// weights; corr = -8 * sum lo.
+__device__ __forceinline__ int blockdot_split(const W8 &w, int k, uint4 hi, uint4 lo, int corr) {
+  const uint32_t h[4] = {hi.x, hi.y, hi.z, hi.w};
+  const uint32_t l[4] = {lo.x, lo.y, lo.z, lo.w};
+  int sa = 0;
+  uint32_t sb = (uint32_t)corr;
+#pragma unroll
+  for (int c = 0; c < 4; c++) {
+    const uint32_t n = w8_nib(w, k, c);
+    sa = __builtin_amdgcn_sdot8((int)(n ^ 0x88888888u), (int)h[c], sa, false);
+    sb = __builtin_amdgcn_udot8(n, l[c], sb, false);
+  }
+  return (int)(((uint32_t)sa << 4) + sb);
+}
+
+// Activation blocks staged in LDS in nibble-split form: block i at codes[2i]
+// (signed parts) and codes[2i+1] (unsigned parts), its fp32 scale d[i] and
+// corr[i] = -8 * (sum of its unsigned parts).  acc + sum over the eight
+// blocks of d_w * d_a * s, in fp32; one block's activations live at a time.
+__device__ __forceinline__ float dot8_lds(const W8 &w, const uint4 *__restrict__ codes,
+                                          const float *__restrict__ d,
+                                          const int *__restrict__ corr, float acc) {
+#pragma unroll
+  for (int k = 0; k < 8; k++) {
+    const int s = blockdot_split(w, k, codes[2 * k], codes[2 * k + 1], corr[k]);
+    acc = fmaf((float)s, w8_scale(w, k) * d[k], acc);
+  }
+  return acc;
 }
 
 // Sum over groups of `width` consecutive lanes (width a power of two <= 64).
