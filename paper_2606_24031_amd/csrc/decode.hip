@@ -95,8 +95,6 @@ __device__ __forceinline__ bool pair_valid(const DecodeArgs &a, int q, int &expe
   return a.ws_gu != nullptr;
 }
 
-__device__ __forceinline__ float silu_f32(float g) { return g / (1.0f + expf(-g)); }
-
 __device__ __forceinline__ uint32_t counter_add(uint32_t *p, uint32_t v) {
   return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }

@@ -194,8 +194,6 @@ __device__ __forceinline__ void chunk_mfma(const LdsTile &L, int wave, const v16
   }
 }
 
-__device__ __forceinline__ float silu_f32(float g) { return g / (1.0f + expf(-g)); }
-
 // Q8_0 code of v for the reciprocal id of the stored scale (the same fp32
 // steps as the format definition).
 __device__ __forceinline__ uint32_t q8_code(float v, float id) {

@@ -10,6 +10,8 @@
 //   3. gate/up: per (row tile, 32 h columns) the gate and up rows of the
 //      expert against the tile's token rows, SwiGLU, Q8_0 of the 32-wide h
 //      block                                           -> workspace h, hq
+//      (groups of few rows: the VALU kernels of smallm.hip instead, which
+//      take the activations in nibble-split form)
 //   4. down: per (row tile, output row slab) the down rows against Q8_0(h),
 //      scaled by the routing weight                    -> workspace y
 //   5. combine: out[t] = sum over slots in slot order, then the shared pair
@@ -23,6 +25,17 @@ namespace w4a8 {
 
 int launch_fill_zero(void *ptr, size_t bytes, hipStream_t s);
 int launch_q8_0(const float *x, uint8_t *xq, int64_t nblocks, hipStream_t s);
+int launch_q8_0_split(const float *x, uint8_t *xq, SplitBlk *xs, int64_t nblocks, hipStream_t s);
+bool small_supported(int64_t H, int64_t I);
+int64_t small_max_chunks(int64_t T, int64_t E, int64_t k, int has_shared);
+int small_gateup(const uint8_t *w_gu, const uint8_t *ws_gu, const SplitBlk *xs,
+                 const int32_t *meta, const int32_t *perm, const int2 *chunks, const int4 *groups,
+                 float *h, uint8_t *hq, SplitBlk *hs, int64_t maxchunks, int64_t T, int64_t H,
+                 int64_t I, int64_t E, int64_t k, hipStream_t s);
+int small_down(const uint8_t *w_d, const uint8_t *ws_d, const SplitBlk *hs, const int32_t *meta,
+               const int32_t *perm, const int2 *chunks, const int4 *groups, const float *topk_w,
+               float *y, int64_t maxchunks, int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
+               hipStream_t s);
 int grouped_tile_rows();
 int grouped_gateup(const uint8_t *w_gu, const uint8_t *ws_gu, const uint8_t *xq,
                    const int32_t *meta, const int32_t *perm, const int4 *groups, const int2 *tiles,
@@ -52,9 +65,16 @@ constexpr int LDS_INTS = 16000; // int32 cells of dynamic LDS for the route kern
 inline size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t meta, sync, xfer, perm, count, rank, groups, tiles, xq, h, hq, y, xn, total;
-  int64_t maxtiles;
+  size_t meta, sync, xfer, perm, count, rank, groups, tiles, chunks, xq, h, hq, y, xn, xs, hs,
+      total;
+  int64_t maxtiles, maxchunks;
 };
+
+// Largest group that takes the VALU path (small_gateup / small_down, in
+// chunks of SMALL_CHUNK rows): every group of a batch of up to 32 tokens,
+// else groups of up to 8 rows, which would fill a quarter of a 32-row MFMA
+// tile at most.
+inline int small_rows(int64_t T) { return T <= 32 ? 32 : 8; }
 
 // Region sizes depend only on (T, H, I, E, k).
 Layout make_layout(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k) {
@@ -65,22 +85,26 @@ Layout make_layout(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k) {
   L.meta = off;   off += 256;
   L.sync = off;   off += up256(sizeof(uint32_t) * decode_sync_words(H));
   L.xfer = off;   off += up256(sizeof(uint32_t) * decode_xfer_words(I, k));
-  L.perm = off;   off += up256(sizeof(int32_t) * P);
+  L.perm = off;   off += up256(sizeof(int32_t) * (P + SMALL_CHUNK));
   L.count = off;  off += up256(sizeof(int32_t) * E);
   L.rank = off;   off += up256(sizeof(int32_t) * (T * k + 1));
   L.groups = off; off += up256(sizeof(int4) * (E + 1));
   L.tiles = off;  off += up256(sizeof(int2) * L.maxtiles);
+  L.maxchunks = small_max_chunks(T, E, k, 1);
+  L.chunks = off; off += up256(sizeof(int2) * L.maxchunks);
   L.xq = off;     off += up256((size_t)T * (H / QK) * Q8B);
   L.h = off;      off += up256(sizeof(float) * (size_t)P * I);
   L.hq = off;     off += up256((size_t)P * (I / QK) * Q8B);
   L.y = off;      off += up256(sizeof(float) * (size_t)P * H);
   L.xn = off;     off += up256(sizeof(float) * (size_t)T * H);
+  L.xs = off;     off += up256(sizeof(SplitBlk) * (size_t)T * (H / QK));
+  L.hs = off;     off += up256(sizeof(SplitBlk) * (size_t)P * (I / QK));
   L.total = off;
   return L;
 }
 
 // Meta words (int32) at the start of the workspace.
-enum { META_NROUTED = 0, META_NGROUPS = 1, META_NTILES = 2 };
+enum { META_NROUTED = 0, META_NGROUPS = 1, META_NTILES = 2, META_NSMALL = 3 };
 
 int validate(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k) {
   if (T < 0 || H <= 0 || I <= 0 || H % 256 != 0 || I % 256 != 0) return W4A8_ESHAPE;
@@ -121,9 +145,11 @@ __device__ int block_exscan(int *a, int n, int *wtot) {
 struct RouteArgs {
   const int32_t *ids;
   int32_t *meta, *perm, *count, *rank;
-  int4 *groups;  // {expert (E = shared), first sorted position, rows, first tile}
-  int2 *tiles;   // {group, first row within the group}
-  int T, k, E, has_shared, seg, nseg, ebits;
+  int4 *groups;     // {expert (E = shared), first sorted position, rows, first tile}
+  int2 *tiles;      // {group, first row within the group}: groups of more than ms rows
+  int2 *chunks;     // groups of at most ms rows, cut into chunks of SMALL_CHUNK
+                    // rows: {group, first row}, in group order
+  int T, k, E, has_shared, seg, nseg, ebits, ms;
 };
 
 // One workgroup.  Pairs are cut into segments of `seg` (a multiple of 64);
@@ -179,36 +205,48 @@ __global__ __launch_bounds__(ROUTE_T) void route_kernel(RouteArgs a) {
     for (int t = tid; t < a.T; t += ROUTE_T) a.perm[nrouted + t] = Pr + t;
   __syncthreads();
 
-  // counts, then the compacted list of non-empty groups (expert order) with
-  // their tile ranges; the shared expert is the last group.
-  int *gflag = hist + L;  // E + 1 entries after the histogram
+  // counts, then the compacted list of non-empty groups (expert order); a
+  // group of at most ms rows goes to the small-group list, a larger one gets
+  // its range of MFMA row tiles.  The shared expert is the last group.
+  int *gflag = hist + L;  // 3 x (E + 1) entries after the histogram
   int *gtile = gflag + a.E + 1;
-  for (int e = tid; e < a.E; e += ROUTE_T) {
-    const int start = hist[e * a.nseg];
-    const int stop = (e + 1 < a.E) ? hist[(e + 1) * a.nseg] : nrouted;
-    a.count[e] = stop - start;
-    gflag[e] = stop > start ? 1 : 0;
-    gtile[e] = (stop - start + MC - 1) / MC;
-  }
-  if (tid == 0) {
-    gflag[a.E] = (a.has_shared && a.T > 0) ? 1 : 0;
-    gtile[a.E] = a.has_shared ? (a.T + MC - 1) / MC : 0;
+  int *gsmall = gtile + a.E + 1;
+  for (int e = tid; e <= a.E; e += ROUTE_T) {
+    int rows;
+    if (e < a.E) {
+      const int start = hist[e * a.nseg];
+      const int stop = (e + 1 < a.E) ? hist[(e + 1) * a.nseg] : nrouted;
+      rows = stop - start;
+      a.count[e] = rows;
+    } else {
+      rows = a.has_shared ? a.T : 0;
+    }
+    gflag[e] = rows > 0 ? 1 : 0;
+    gsmall[e] = (rows > 0 && rows <= a.ms) ? (rows + SMALL_CHUNK - 1) / SMALL_CHUNK : 0;
+    gtile[e] = rows > a.ms ? (rows + MC - 1) / MC : 0;
   }
   __syncthreads();
   const int ngroups = block_exscan(gflag, a.E + 1, wtot);
   const int ntiles = block_exscan(gtile, a.E + 1, wtot);
+  const int nsmall = block_exscan(gsmall, a.E + 1, wtot);
   for (int e = tid; e <= a.E; e += ROUTE_T) {
     const int start = (e < a.E) ? hist[e * a.nseg] : nrouted;
     const int rows = (e < a.E) ? a.count[e] : (a.has_shared ? a.T : 0);
     if (rows == 0) continue;
     const int gi = gflag[e], t0 = gtile[e];
     a.groups[gi] = make_int4(e, start, rows, t0);
-    for (int m0 = 0, t = t0; m0 < rows; m0 += MC, t++) a.tiles[t] = make_int2(gi, m0);
+    if (rows <= a.ms) {
+      for (int m0 = 0, c = gsmall[e]; m0 < rows; m0 += SMALL_CHUNK, c++)
+        a.chunks[c] = make_int2(gi, m0);
+    } else {
+      for (int m0 = 0, t = t0; m0 < rows; m0 += MC, t++) a.tiles[t] = make_int2(gi, m0);
+    }
   }
   if (tid == 0) {
     a.meta[META_NROUTED] = nrouted;
     a.meta[META_NGROUPS] = ngroups;
     a.meta[META_NTILES] = ntiles;
+    a.meta[META_NSMALL] = nsmall;
   }
 }
 
@@ -262,7 +300,12 @@ int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
       return rc;
     hidden = norm.xn;
   }
-  if ((rc = launch_q8_0(hidden, ws + L.xq, T * (H / QK), s)) != W4A8_OK) return rc;
+  const int ms = small_supported(H, I) ? small_rows(T) : 0;
+  SplitBlk *xs = reinterpret_cast<SplitBlk *>(ws + L.xs);
+  SplitBlk *hs = reinterpret_cast<SplitBlk *>(ws + L.hs);
+  if ((rc = ms > 0 ? launch_q8_0_split(hidden, ws + L.xq, xs, T * (H / QK), s)
+                   : launch_q8_0(hidden, ws + L.xq, T * (H / QK), s)) != W4A8_OK)
+    return rc;
 
   RouteArgs ra;
   ra.ids = ids;
@@ -272,11 +315,12 @@ int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
   ra.rank = reinterpret_cast<int32_t *>(ws + L.rank);
   ra.groups = reinterpret_cast<int4 *>(ws + L.groups);
   ra.tiles = reinterpret_cast<int2 *>(ws + L.tiles);
-  ra.T = (int)T; ra.k = (int)k; ra.E = (int)E; ra.has_shared = has_shared;
+  ra.chunks = reinterpret_cast<int2 *>(ws + L.chunks);
+  ra.T = (int)T; ra.k = (int)k; ra.E = (int)E; ra.has_shared = has_shared; ra.ms = ms;
   const int64_t Pr = T * k;
   // smallest segment (multiple of 64 pairs) whose histogram fits in LDS
   int64_t seg = 64, nseg = std::max<int64_t>(1, (Pr + 63) / 64);
-  while (E * nseg + 2 * (E + 1) > LDS_INTS) {
+  while (E * nseg + 3 * (E + 1) > LDS_INTS) {
     seg += 64;
     nseg = std::max<int64_t>(1, (Pr + seg - 1) / seg);
   }
@@ -284,18 +328,27 @@ int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
   ra.nseg = (int)nseg;
   ra.ebits = 0;
   while ((1 << ra.ebits) < E) ra.ebits++;
-  const size_t lds = sizeof(int) * ((size_t)E * ra.nseg + 2 * (E + 1));
+  const size_t lds = sizeof(int) * ((size_t)E * ra.nseg + 3 * (E + 1));
   route_kernel<<<dim3(1), dim3(ROUTE_T), lds, s>>>(ra);
   if ((rc = check_launch()) != W4A8_OK) return rc;
 
   uint8_t *hq = ws + L.hq;
+  float *h = reinterpret_cast<float *>(ws + L.h);
   float *y = reinterpret_cast<float *>(ws + L.y);
-  if ((rc = grouped_gateup(w_gu, ws_gu, ws + L.xq, ra.meta, ra.perm, ra.groups, ra.tiles,
-                           reinterpret_cast<float *>(ws + L.h), hq, L.maxtiles, T, H, I, E, k,
-                           s)) != W4A8_OK)
+  const int64_t maxchunks = small_max_chunks(T, E, k, has_shared);
+  if (ms > 0 && (rc = small_gateup(w_gu, ws_gu, xs, ra.meta, ra.perm, ra.chunks, ra.groups, h, hq,
+                                   hs, maxchunks, T, H, I, E, k, s)) != W4A8_OK)
     return rc;
-  if ((rc = grouped_down(w_d, ws_d, hq, ra.meta, ra.perm, ra.groups, ra.tiles, topk_w, y,
-                         L.maxtiles, T, H, I, E, k, s)) != W4A8_OK)
+  // with ms >= T every group (at most T rows) is small: no MFMA tiles
+  const bool tiles = ms < T;
+  if (tiles && (rc = grouped_gateup(w_gu, ws_gu, ws + L.xq, ra.meta, ra.perm, ra.groups, ra.tiles,
+                                    h, hq, L.maxtiles, T, H, I, E, k, s)) != W4A8_OK)
+    return rc;
+  if (ms > 0 && (rc = small_down(w_d, ws_d, hs, ra.meta, ra.perm, ra.chunks, ra.groups, topk_w, y,
+                                 maxchunks, T, H, I, E, k, s)) != W4A8_OK)
+    return rc;
+  if (tiles && (rc = grouped_down(w_d, ws_d, hq, ra.meta, ra.perm, ra.groups, ra.tiles, topk_w,
+                                  y, L.maxtiles, T, H, I, E, k, s)) != W4A8_OK)
     return rc;
 
   const int64_t n4 = T * (H / 4);

@@ -11,8 +11,11 @@
 
 namespace w4a8 {
 
+// 8 lanes per block; with SPLIT also the nibble-split copy of each block.
+template <bool SPLIT>
 __global__ __launch_bounds__(256) void q8_0_kernel(const float *__restrict__ x,
-                                                   uint8_t *__restrict__ xq, int64_t nblocks) {
+                                                   uint8_t *__restrict__ xq,
+                                                   SplitBlk *__restrict__ xs, int64_t nblocks) {
   const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t blk = tid >> 3;
   const int j = (int)(tid & 7);
@@ -25,6 +28,17 @@ __global__ __launch_bounds__(256) void q8_0_kernel(const float *__restrict__ x,
   uint32_t d16;
   const uint32_t packed = q8_0_block8(v, d16);
   if (live) store_q8_0_block8(xq + blk * Q8B, j, packed, d16);
+  if (SPLIT) {
+    const uint32_t word = split_word(packed, j);
+    const int lsum = sum8(low_nibble_sum(packed));
+    if (live) {
+      xs[blk].w[j] = word;
+      if (j == 0) {
+        xs[blk].d = f16_bits_to_f32(d16);
+        xs[blk].corr = -8 * lsum;
+      }
+    }
+  }
 }
 
 __global__ __launch_bounds__(256) void q4_0_kernel(const float *__restrict__ w,
@@ -97,7 +111,14 @@ int launch_fill_zero(void *ptr, size_t bytes, hipStream_t s) {
 int launch_q8_0(const float *x, uint8_t *xq, int64_t nblocks, hipStream_t s) {
   if (nblocks == 0) return W4A8_OK;
   const int64_t grid = (nblocks * 8 + 255) / 256;
-  q8_0_kernel<<<dim3((unsigned)grid), dim3(256), 0, s>>>(x, xq, nblocks);
+  q8_0_kernel<false><<<dim3((unsigned)grid), dim3(256), 0, s>>>(x, xq, nullptr, nblocks);
+  return check_launch();
+}
+
+int launch_q8_0_split(const float *x, uint8_t *xq, SplitBlk *xs, int64_t nblocks, hipStream_t s) {
+  if (nblocks <= 0) return W4A8_OK;
+  const int64_t grid = (nblocks * 8 + 255) / 256;
+  q8_0_kernel<true><<<dim3((unsigned)grid), dim3(256), 0, s>>>(x, xq, xs, nblocks);
   return check_launch();
 }
 

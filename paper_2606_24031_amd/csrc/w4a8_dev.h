@@ -191,6 +191,19 @@ __device__ __forceinline__ int low_nibble_sum(uint32_t packed) {
   return sdot4((int)(packed & 0x0F0F0F0Fu), 0x01010101, 0);
 }
 
+// A nibble-split Q8_0 block in global memory: the 8 dwords of split_word,
+// the fp32 scale and -8 * (sum of the unsigned nibbles), padded to 48 bytes
+// so that blocks copy and read as 16-byte pieces.
+struct SplitBlk {
+  uint32_t w[8];
+  float d;
+  int corr;
+  int pad[2];
+};
+static_assert(sizeof(SplitBlk) == 48, "split block layout");
+
+__device__ __forceinline__ float silu_f32(float g) { return g / (1.0f + expf(-g)); }
+
 // Exact block dot s = sum (q_w - 8) * x over a block in nibble-split form:
 // q_w - 8 is the signed nibble q_w ^ 8, so
 //   s = 16 * sum (q_w ^ 8) * hi + sum q_w * lo - 8 * sum lo,

@@ -284,6 +284,28 @@ def test_moe_decode_m32(qwen_layer):
     L.check(x, ids, wts, 8, out, h, hq)
 
 
+def test_moe_group_size_boundary_between_paths(small_layer):
+    """Above 32 tokens, expert groups of up to 8 rows take the VALU path and
+    larger ones the MFMA tiles: two groups of 8 rows (VALU), groups of 9 and
+    33 rows and the shared expert's 40 (MFMA), checked token by token."""
+    L = small_layer
+    g = synth.rng(31)
+    T, k = 40, 2
+    x = synth.normal_f32(g, (T, L.H))
+    ids = np.full((T, k), -1, dtype=np.int32)
+    ids[:8, 0] = 0                       # expert 0: 8 rows
+    ids[8:17, 0] = 1                     # expert 1: 9 rows
+    ids[17:40, 0] = 2                    # expert 2: 23 + 10 = 33 rows
+    ids[:10, 1] = 2
+    ids[10:17, 1] = 3                    # expert 3: 7 rows + 1
+    ids[39, 1] = 3
+    wts = g.random((T, k), dtype=np.float32)
+    out, h, hq, perm, count, _ = L.run(x, ids, wts, k)
+    assert count.tolist() == [8, 9, 33, 8]
+    _check_route(ids, L.E, True, perm, count)
+    L.check(x, ids, wts, k, out, h, hq)
+
+
 def test_moe_prefill_947_sampled_tokens(qwen_layer):
     L = qwen_layer
     g = synth.rng(22)
