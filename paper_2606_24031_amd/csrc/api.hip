@@ -25,6 +25,7 @@ namespace {
 constexpr int kMaxDevices = 64;
 // 0 = unknown, 1 = gfx950, 2 = other architecture
 std::atomic<int> g_arch[kMaxDevices];
+std::atomic<int> g_cus[kMaxDevices];   // compute units, set with g_arch
 }  // namespace
 
 int check_device() {
@@ -36,9 +37,16 @@ int check_device() {
     hipDeviceProp_t prop;
     if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return W4A8_EHIP;
     state = (std::strncmp(prop.gcnArchName, "gfx950", 6) == 0) ? 1 : 2;
+    g_cus[dev].store(prop.multiProcessorCount, std::memory_order_relaxed);
     g_arch[dev].store(state, std::memory_order_relaxed);
   }
   return state == 1 ? W4A8_OK : W4A8_EDEVICE;
+}
+
+int device_cus() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 0;
+  return g_cus[dev].load(std::memory_order_relaxed);
 }
 
 int check_launch() {

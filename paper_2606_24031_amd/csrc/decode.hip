@@ -519,8 +519,6 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
   }
 }
 
-int g_num_cus = 0;   // compute units of the device (queried once per process)
-
 // Workgroups and down rows per slab: one gate/up item per h block, then the
 // down slabs, enough of them to fill the remaining compute units but with
 // few enough rows that a slab's units fit the workgroup.  The gate/up items
@@ -562,14 +560,8 @@ int decode_forward(const float *x, const DecodeNorm &norm, const int32_t *ids,
                    const uint8_t *ws_gu, const uint8_t *ws_d, float *out, int64_t H, int64_t I,
                    int64_t E, int64_t k, uint32_t *sync, uint32_t *xfer, uint8_t *xq, float *h,
                    uint8_t *hq, hipStream_t s) {
-  if (g_num_cus == 0) {
-    int dev = 0, n = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        n <= 0)
-      return W4A8_EHIP;
-    g_num_cus = n;
-  }
+  const int ncu = device_cus();
+  if (ncu <= 0) return W4A8_EHIP;
   DecodeArgs a;
   a.x = x; a.ids = ids; a.topk_w = topk_w;
   a.w_gu = w_gu; a.w_d = w_d; a.ws_gu = ws_gu; a.ws_d = ws_d;
@@ -582,7 +574,7 @@ int decode_forward(const float *x, const DecodeNorm &norm, const int32_t *ids,
   a.xq = xq; a.h = h; a.hq = hq;
   a.H = (int)H; a.I = (int)I; a.E = (int)E; a.k = (int)k;
   int grid = 0;
-  decode_grid(H, I, k, g_num_cus, grid, a.rb);
+  decode_grid(H, I, k, ncu, grid, a.rb);
   // default wait bound: 2000 poll rounds, about 1-2 ms
   a.spin_rounds = 2000;
   if (const char *env = std::getenv("W4A8_DECODE_SPIN_ROUNDS")) a.spin_rounds = std::atoi(env);

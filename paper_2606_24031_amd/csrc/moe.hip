@@ -29,12 +29,12 @@ int launch_q8_0_split(const float *x, uint8_t *xq, SplitBlk *xs, int64_t nblocks
 bool small_supported(int64_t H, int64_t I);
 int64_t small_max_chunks(int64_t T, int64_t E, int64_t k, int has_shared);
 int small_gateup(const uint8_t *w_gu, const uint8_t *ws_gu, const SplitBlk *xs,
-                 const int32_t *meta, const int32_t *perm, const int2 *chunks, const int4 *groups,
-                 float *h, uint8_t *hq, SplitBlk *hs, int64_t maxchunks, int64_t T, int64_t H,
-                 int64_t I, int64_t E, int64_t k, hipStream_t s);
+                 const int32_t *meta, const int32_t *perm, const int4 *chunks, float *h,
+                 uint8_t *hq, SplitBlk *hs, int64_t maxchunks, int64_t T, int64_t H, int64_t I,
+                 int64_t E, int64_t k, hipStream_t s);
 int small_down(const uint8_t *w_d, const uint8_t *ws_d, const SplitBlk *hs, const int32_t *meta,
-               const int32_t *perm, const int2 *chunks, const int4 *groups, const float *topk_w,
-               float *y, int64_t maxchunks, int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
+               const int32_t *perm, const int4 *chunks, const float *topk_w, float *y,
+               int64_t maxchunks, int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
                hipStream_t s);
 int grouped_tile_rows();
 int grouped_gateup(const uint8_t *w_gu, const uint8_t *ws_gu, const uint8_t *xq,
@@ -91,7 +91,7 @@ Layout make_layout(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k) {
   L.groups = off; off += up256(sizeof(int4) * (E + 1));
   L.tiles = off;  off += up256(sizeof(int2) * L.maxtiles);
   L.maxchunks = small_max_chunks(T, E, k, 1);
-  L.chunks = off; off += up256(sizeof(int2) * L.maxchunks);
+  L.chunks = off; off += up256(sizeof(int4) * L.maxchunks);
   L.xq = off;     off += up256((size_t)T * (H / QK) * Q8B);
   L.h = off;      off += up256(sizeof(float) * (size_t)P * I);
   L.hq = off;     off += up256((size_t)P * (I / QK) * Q8B);
@@ -147,8 +147,9 @@ struct RouteArgs {
   int32_t *meta, *perm, *count, *rank;
   int4 *groups;     // {expert (E = shared), first sorted position, rows, first tile}
   int2 *tiles;      // {group, first row within the group}: groups of more than ms rows
-  int2 *chunks;     // groups of at most ms rows, cut into chunks of SMALL_CHUNK
-                    // rows: {group, first row}, in group order
+  int4 *chunks;     // groups of at most ms rows, cut into chunks of SMALL_CHUNK
+                    // rows: {expert, first sorted position, rows, group}, in
+                    // reverse group order
   int T, k, E, has_shared, seg, nseg, ebits, ms;
 };
 
@@ -236,8 +237,9 @@ __global__ __launch_bounds__(ROUTE_T) void route_kernel(RouteArgs a) {
     const int gi = gflag[e], t0 = gtile[e];
     a.groups[gi] = make_int4(e, start, rows, t0);
     if (rows <= a.ms) {
+      // back to front: the shared expert (the largest group) comes first
       for (int m0 = 0, c = gsmall[e]; m0 < rows; m0 += SMALL_CHUNK, c++)
-        a.chunks[c] = make_int2(gi, m0);
+        a.chunks[nsmall - 1 - c] = make_int4(e, start + m0, min(SMALL_CHUNK, rows - m0), gi);
     } else {
       for (int m0 = 0, t = t0; m0 < rows; m0 += MC, t++) a.tiles[t] = make_int2(gi, m0);
     }
@@ -315,7 +317,7 @@ int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
   ra.rank = reinterpret_cast<int32_t *>(ws + L.rank);
   ra.groups = reinterpret_cast<int4 *>(ws + L.groups);
   ra.tiles = reinterpret_cast<int2 *>(ws + L.tiles);
-  ra.chunks = reinterpret_cast<int2 *>(ws + L.chunks);
+  ra.chunks = reinterpret_cast<int4 *>(ws + L.chunks);
   ra.T = (int)T; ra.k = (int)k; ra.E = (int)E; ra.has_shared = has_shared; ra.ms = ms;
   const int64_t Pr = T * k;
   // smallest segment (multiple of 64 pairs) whose histogram fits in LDS
@@ -336,16 +338,16 @@ int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
   float *h = reinterpret_cast<float *>(ws + L.h);
   float *y = reinterpret_cast<float *>(ws + L.y);
   const int64_t maxchunks = small_max_chunks(T, E, k, has_shared);
-  if (ms > 0 && (rc = small_gateup(w_gu, ws_gu, xs, ra.meta, ra.perm, ra.chunks, ra.groups, h, hq,
-                                   hs, maxchunks, T, H, I, E, k, s)) != W4A8_OK)
+  if (ms > 0 && (rc = small_gateup(w_gu, ws_gu, xs, ra.meta, ra.perm, ra.chunks, h, hq, hs,
+                                   maxchunks, T, H, I, E, k, s)) != W4A8_OK)
     return rc;
   // with ms >= T every group (at most T rows) is small: no MFMA tiles
   const bool tiles = ms < T;
   if (tiles && (rc = grouped_gateup(w_gu, ws_gu, ws + L.xq, ra.meta, ra.perm, ra.groups, ra.tiles,
                                     h, hq, L.maxtiles, T, H, I, E, k, s)) != W4A8_OK)
     return rc;
-  if (ms > 0 && (rc = small_down(w_d, ws_d, hs, ra.meta, ra.perm, ra.chunks, ra.groups, topk_w, y,
-                                 maxchunks, T, H, I, E, k, s)) != W4A8_OK)
+  if (ms > 0 && (rc = small_down(w_d, ws_d, hs, ra.meta, ra.perm, ra.chunks, topk_w, y, maxchunks,
+                                 T, H, I, E, k, s)) != W4A8_OK)
     return rc;
   if (tiles && (rc = grouped_down(w_d, ws_d, hq, ra.meta, ra.perm, ra.groups, ra.tiles, topk_w,
                                   y, L.maxtiles, T, H, I, E, k, s)) != W4A8_OK)

@@ -13,8 +13,10 @@
 // the same activation block: the chunk's activation rows (nibble-split, see
 // split_word) are loaded together with the weights and parked in LDS, so the
 // token loop waits on nothing but LDS.  The waves of a row set add their
-// partial sums through LDS in a fixed order, so results do not depend on
-// scheduling.
+// partial sums through LDS (over the activation staging) in a fixed order, so
+// results do not depend on scheduling.  A workgroup's life is mostly the wait
+// for its loads: the chunk's description is one record, so the weight loads
+// are issued after a single scalar round trip.
 //
 // gate/up: the 32 gate and the 32 matching up rows of one 32-wide block of
 //   h; per token SwiGLU, then Q8_0 of the block, written as the 34-byte
@@ -36,13 +38,15 @@ constexpr int KB_MAX = 64;         // blocks of K per row (K <= 2048)
 constexpr int PPB = sizeof(SplitBlk) / 16;   // 16-byte pieces per split block
 
 typedef __attribute__((address_space(4))) const int32_t CInt;
+// 16-byte pieces as a native vector (a copy of HIP's uint4 struct becomes a
+// memcpy, which keeps arrays of them out of registers)
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 
 struct SmallArgs {
   const uint8_t *w, *ws;      // routed experts [E][N][K/32] Q4_0 / shared [N][K/32]
   const SplitBlk *act;        // nibble-split activations [row][K/32]
   const int32_t *meta, *perm;
-  const int2 *chunks;         // {group, first row of the chunk}
-  const int4 *groups;         // {expert, first sorted position, rows, -}
+  const int4 *chunks;         // {expert, first sorted position, rows, group}
   const float *topk_w;
   float *h;                   // gate/up: fp32 h [P][I]
   uint8_t *hq;                // gate/up: Q8_0(h) [P][I/32]
@@ -54,9 +58,11 @@ struct SmallArgs {
 };
 
 struct SmallLds {
-  uint4 act[SC][KB_MAX * PPB];   // the chunk's activation rows
-  float part[SW][SC][64];        // partial row sums of each wave
-  float hv[SC][33];              // gate/up: the h block of each token row
+  union {
+    uint4 act[SC][KB_MAX * PPB];   // the chunk's activation rows
+    float part[SW][SC][64];        // then: partial row sums of each wave
+  };
+  float hv[SC][33];                // gate/up: the h block of each token row
   int pair[SC];
 };
 
@@ -70,20 +76,13 @@ __device__ __forceinline__ int pair_row(const SmallArgs &a, int p, bool by_token
   return __builtin_amdgcn_readfirstlane(r);
 }
 
+// One work item (a workgroup): chunk item / nslab, slab item % nslab.
 template <bool GATEUP>
-__global__ __launch_bounds__(SNT) __attribute__((amdgpu_waves_per_eu(4))) void small_kernel(SmallArgs a) {
-  __shared__ SmallLds L;
-  const int nchunk = ((CInt *)a.meta)[3];   // META_NSMALL
-  const int cr = (int)blockIdx.x / a.nslab, slab = (int)blockIdx.x % a.nslab;
-  if (cr >= nchunk) return;
-  // chunks are listed in group order with the shared expert last; take them
-  // from the back so its chunks start first
-  const int c = nchunk - 1 - cr;
-  CInt *cp = (CInt *)a.chunks + 2 * c;
-  const int gi = cp[0], m0 = cp[1];
-  CInt *gp = (CInt *)a.groups + 4 * gi;
-  const int expert = gp[0], start = gp[1];
-  const int rows = min(SC, gp[2] - m0);
+__device__ __forceinline__ void small_item(const SmallArgs &a, SmallLds &L, int nchunk, int item) {
+  const int c = item / a.nslab, slab = item % a.nslab;
+  (void)nchunk;
+  CInt *cp = (CInt *)a.chunks + 4 * c;
+  const int expert = cp[0], pos = cp[1], rows = cp[2];
   // the wave index, known to the compiler as wave-uniform
   const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int nrs = a.nrs, rs = wave % nrs, gg = wave / nrs;
@@ -91,7 +90,7 @@ __global__ __launch_bounds__(SNT) __attribute__((amdgpu_waves_per_eu(4))) void s
   const int nblk = (int)(a.K / 32);
   const bool live = gg < G;
 
-  // this lane's 144-byte group of its weight row
+  // this lane's 144-byte group gg of its weight row
   int64_t row;
   if (GATEUP)
     row = lane < 32 ? (int64_t)slab * 32 + lane : a.I + (int64_t)slab * 32 + (lane - 32);
@@ -99,68 +98,72 @@ __global__ __launch_bounds__(SNT) __attribute__((amdgpu_waves_per_eu(4))) void s
     row = (int64_t)slab * (64 * nrs) + rs * 64 + lane;
   const int64_t rowbytes = (int64_t)nblk * Q4B;
   const uint8_t *W = (expert < a.E ? a.w + (int64_t)expert * a.N * rowbytes : a.ws) +
-                     row * rowbytes + (int64_t)gg * (8 * Q4B);
+                     row * rowbytes + (int64_t)(live ? gg : 0) * (8 * Q4B);
   W8 w;
-  if (live) load_w8(W, w);
+  load_w8(W, w);
 
   // the chunk's pairs with one scalar read (the permutation is padded by a
-  // chunk), then every activation row: thread t loads piece t of each row,
-  // all issued behind the weights before anything waits
+  // chunk), then every activation row straight into LDS (global_load_lds:
+  // lane l's 16 bytes land 16*l past the wave's LDS address), 64 pieces per
+  // wave load, behind the weights and before anything waits
   int prs[SC];
 #pragma unroll
-  for (int m = 0; m < SC; m++) prs[m] = ((CInt *)a.perm)[start + m0 + m];
+  for (int m = 0; m < SC; m++) prs[m] = ((CInt *)a.perm)[pos + m];
   const int per_row = nblk * PPB;
-  uint4 av[SC];
-  const int piece = min((int)threadIdx.x, per_row - 1);   // clamped: loads stay unconditional
+  const int nch = (per_row + 63) / 64;                     // wave loads per row
+  for (int j = wave; j < rows * nch; j += SW) {
+    const int m = j / nch, ch = j - m * nch;
+    int pm = prs[0];
 #pragma unroll
-  for (int m = 0; m < SC; m++) {
-    const int pm = prs[m < rows ? m : 0];                   // rows past the chunk reload row 0
-    av[m] = reinterpret_cast<const uint4 *>(a.act + (int64_t)pair_row(a, pm, GATEUP) * nblk)[piece];
+    for (int mm = 1; mm < SC; mm++) pm = m == mm ? prs[mm] : pm;
+    const SplitBlk *row_src = a.act + (int64_t)pair_row(a, pm, GATEUP) * nblk;
+    const int piece = ch * 64 + lane;
+    if (piece < per_row)
+      __builtin_amdgcn_global_load_lds(
+          (const void __attribute__((address_space(1))) *)(reinterpret_cast<const uint4 *>(row_src) + piece),
+          (void __attribute__((address_space(3))) *)(&L.act[m][ch * 64]), 16, 0, 0);
   }
+  if (threadIdx.x == 0) {
 #pragma unroll
-  for (int m = 0; m < SC; m++) {
-    if (m < rows && (int)threadIdx.x < per_row) L.act[m][threadIdx.x] = av[m];
-    if (threadIdx.x == 0) L.pair[m] = prs[m];
+    for (int m = 0; m < SC; m++) L.pair[m] = prs[m];
   }
-  float *mypart = &L.part[wave][0][0];
-  if (!live)
-    for (int m = 0; m < rows; m++) mypart[m * 64 + lane] = 0.0f;
+  __builtin_amdgcn_s_waitcnt(0);   // the LDS-direct loads (and the weights) have landed
   __syncthreads();
-
+  // per token row: the 8 block dots of this lane's group (payload views of
+  // the weights taken at use: registers are the scarce resource here)
+  float acc[SC];
+#pragma unroll
+  for (int m = 0; m < SC; m++) acc[m] = 0.0f;
   if (live) {
-    uint32_t n[8][4], nx[8][4];
-    float dw[8];
 #pragma unroll
-    for (int kk = 0; kk < 8; kk++) {
+    for (int m = 0; m < SC; m++) {
+      if (m < rows) {
+        const uint4 *ar = &L.act[m][gg * 8 * PPB];
 #pragma unroll
-      for (int cc = 0; cc < 4; cc++) {
-        n[kk][cc] = w8_nib(w, kk, cc);
-        nx[kk][cc] = n[kk][cc] ^ 0x88888888u;
-      }
-      dw[kk] = w8_scale(w, kk);
-    }
-    for (int m = 0; m < rows; m++) {
-      const uint4 *ar = &L.act[m][gg * 8 * PPB];
-      float acc = 0.0f;
+        for (int kk = 0; kk < 8; kk++) {
+          const uint4 hi = ar[PPB * kk], lo = ar[PPB * kk + 1];
+          const uint2 dc = *reinterpret_cast<const uint2 *>(&ar[PPB * kk + 2]);
+          const uint32_t h4[4] = {hi.x, hi.y, hi.z, hi.w};
+          const uint32_t l4[4] = {lo.x, lo.y, lo.z, lo.w};
+          int sa = 0;
+          uint32_t sb = dc.y;
 #pragma unroll
-      for (int kk = 0; kk < 8; kk++) {
-        const uint4 hi = ar[PPB * kk], lo = ar[PPB * kk + 1];
-        const uint2 dc = *reinterpret_cast<const uint2 *>(&ar[PPB * kk + 2]);
-        const uint32_t h4[4] = {hi.x, hi.y, hi.z, hi.w};
-        const uint32_t l4[4] = {lo.x, lo.y, lo.z, lo.w};
-        int sa = 0;
-        uint32_t sb = dc.y;
-#pragma unroll
-        for (int cc = 0; cc < 4; cc++) {
-          sa = __builtin_amdgcn_sdot8((int)nx[kk][cc], (int)h4[cc], sa, false);
-          sb = __builtin_amdgcn_udot8(n[kk][cc], l4[cc], sb, false);
+          for (int cc = 0; cc < 4; cc++) {
+            const uint32_t nb = w8_nib(w, kk, cc);
+            sa = __builtin_amdgcn_sdot8((int)(nb ^ 0x88888888u), (int)h4[cc], sa, false);
+            sb = __builtin_amdgcn_udot8(nb, l4[cc], sb, false);
+          }
+          const int s = (int)(((uint32_t)sa << 4) + sb);
+          acc[m] = fmaf((float)s, w8_scale(w, kk) * __builtin_bit_cast(float, dc.x), acc[m]);
         }
-        const int s = (int)(((uint32_t)sa << 4) + sb);
-        acc = fmaf((float)s, dw[kk] * __builtin_bit_cast(float, dc.x), acc);
       }
-      mypart[m * 64 + lane] = acc;
     }
   }
+  __syncthreads();                       // every wave is done with the activations
+  float *mypart = &L.part[wave][0][0];
+#pragma unroll
+  for (int m = 0; m < SC; m++)
+    if (m < rows) mypart[m * 64 + lane] = acc[m];
   __syncthreads();
 
   if (GATEUP) {
@@ -209,6 +212,13 @@ __global__ __launch_bounds__(SNT) __attribute__((amdgpu_waves_per_eu(4))) void s
   }
 }
 
+template <bool GATEUP>
+__global__ __launch_bounds__(SNT) __attribute__((amdgpu_waves_per_eu(4))) void small_kernel(SmallArgs a) {
+  __shared__ SmallLds L;
+  const int nchunk = ((CInt *)a.meta)[3];   // META_NSMALL
+  if ((int)blockIdx.x < nchunk * a.nslab) small_item<GATEUP>(a, L, nchunk, blockIdx.x);
+}
+
 }  // namespace
 
 // Row sets per down workgroup: as many as leave each wave one eight-block
@@ -221,7 +231,7 @@ int small_down_rowsets(int64_t H, int64_t I) {
 }
 
 // Shapes the kernels cover: every wave holds at most one eight-block group
-// of its row and a row's activations fit the staging (H, I <= 2048).
+// of its row and a row's activations fit their LDS rows (H, I <= 2048).
 bool small_supported(int64_t H, int64_t I) {
   return H <= 32 * KB_MAX && I <= 32 * KB_MAX && H % 256 == 0 && I % 256 == 0;
 }
@@ -233,12 +243,12 @@ int64_t small_max_chunks(int64_t T, int64_t E, int64_t k, int has_shared) {
 }
 
 int small_gateup(const uint8_t *w_gu, const uint8_t *ws_gu, const SplitBlk *xs,
-                 const int32_t *meta, const int32_t *perm, const int2 *chunks, const int4 *groups,
-                 float *h, uint8_t *hq, SplitBlk *hs, int64_t maxchunks, int64_t T, int64_t H,
-                 int64_t I, int64_t E, int64_t k, hipStream_t s) {
+                 const int32_t *meta, const int32_t *perm, const int4 *chunks, float *h,
+                 uint8_t *hq, SplitBlk *hs, int64_t maxchunks, int64_t T, int64_t H, int64_t I,
+                 int64_t E, int64_t k, hipStream_t s) {
   SmallArgs a{};
   a.w = w_gu; a.ws = ws_gu; a.act = xs;
-  a.meta = meta; a.perm = perm; a.chunks = chunks; a.groups = groups;
+  a.meta = meta; a.perm = perm; a.chunks = chunks;
   a.h = h; a.hq = hq; a.hs = hs;
   a.T = T; a.k = k; a.E = E; a.N = 2 * I; a.K = H; a.I = I;
   a.nrs = 1; a.nslab = (int)(I / 32);
@@ -247,12 +257,12 @@ int small_gateup(const uint8_t *w_gu, const uint8_t *ws_gu, const SplitBlk *xs,
 }
 
 int small_down(const uint8_t *w_d, const uint8_t *ws_d, const SplitBlk *hs, const int32_t *meta,
-               const int32_t *perm, const int2 *chunks, const int4 *groups, const float *topk_w,
-               float *y, int64_t maxchunks, int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
+               const int32_t *perm, const int4 *chunks, const float *topk_w, float *y,
+               int64_t maxchunks, int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
                hipStream_t s) {
   SmallArgs a{};
   a.w = w_d; a.ws = ws_d; a.act = hs;
-  a.meta = meta; a.perm = perm; a.chunks = chunks; a.groups = groups;
+  a.meta = meta; a.perm = perm; a.chunks = chunks;
   a.topk_w = topk_w; a.y = y;
   a.T = T; a.k = k; a.E = E; a.N = H; a.K = I; a.I = I;
   a.nrs = small_down_rowsets(H, I);

@@ -19,12 +19,16 @@ inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 
 
 inline hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s); }
 
-// Pre-norm residual input of a layer call: with gamma set, the layer's input
-// is xn = RMSNorm(x + resid) * gamma, and x + resid goes to x_out.
+// Compute units of the current device, known once check_device has run on
+// it (0 otherwise).
+int device_cus();
+
 // Token rows per work item of the small-group (VALU) kernels; the sorted
 // pair list in the workspace is padded by this many entries.
 constexpr int SMALL_CHUNK = 8;
 
+// Pre-norm residual input of a layer call: with gamma set, the layer's input
+// is xn = RMSNorm(x + resid) * gamma, and x + resid goes to x_out.
 struct DecodeNorm {
   const float *resid = nullptr;
   const float *gamma = nullptr;
