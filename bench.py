@@ -374,8 +374,8 @@ def cpu_baseline(synth, seconds):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the layer runs "
-              "on a single MI355X and no multi-GPU path is part of this build.", file=sys.stderr)
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the library runs "
+              "a layer on a single MI355X and has no multi-GPU path.", file=sys.stderr)
         sys.exit(2)
     import torch
     import paper_2606_24031_amd as w4
