@@ -12,10 +12,12 @@ LIB = os.path.join(HERE, "libw4a8.so")
 # -ffp-contract=off: the quantizers must round every fp32 step on its own;
 # fused multiply-adds are written explicitly (fmaf) where they are wanted.
 # The target-feature flag keeps the compiler from emitting packed fp32 math.
+# -amdgpu-mfma-vgpr-form: matrix products write ordinary VGPRs, so the fp32
+# scaling reads their results without a copy out of the accumulator file.
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
     "-ffp-contract=off", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-    "-Wall",
+    "-mllvm", "-amdgpu-mfma-vgpr-form", "-Wall",
 ]
 
 

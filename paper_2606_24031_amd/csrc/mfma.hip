@@ -1,0 +1,401 @@
+// Grouped W4A8 GEMMs on int8 MFMA for expert groups of more than a few token
+// rows (paper Sec. 3.2: the token-expert pairs grouped by expert, one launch
+// over all groups; Sec. 3.3: 4-bit weight codes times 8-bit activation codes,
+// one scaling per 32 elements).
+//
+// Workgroup tile: up to 64 token rows of one group by 128 weight rows (one
+// slice).  Each of the four waves owns 32 weight rows and both 32-row halves
+// of the tokens (the second half is compiled out for tiles of at most 32
+// rows), so one weight operand feeds two v_mfma_i32_32x32x32_i8 per Q-block.
+//   * Weights: lanes l and l + 32 own the same weight row; they stream its
+//     144-byte groups of 8 blocks one group ahead, lane l the first 72 bytes
+//     (blocks 0..3), lane l + 32 the last 72 (blocks 4..7).  Each lane splits
+//     its block j into low- and high-nibble codes, each as the int8 16*(q-8)
+//     (the nibble q ^ 8 in the high half of its byte), and one swap between
+//     the wave halves (v_permlane32_swap) leaves in lanes 0..31 the low and in
+//     lanes 32..63 the high codes of block j in one register and of block
+//     j + 4 in the other: the B operands of both blocks.
+//   * Activations: the tile's aligned Q8_0 codes for 8 blocks go to LDS by
+//     direct loads (global_load_lds), the 16-byte chunks of a row XOR-swizzled
+//     by the row so the rows a half-wave reads sit in distinct banks.  With
+//     K <= 512 all of K stays resident and the workgroup runs several weight
+//     slices with no barrier; otherwise the next 8 blocks are staged while the
+//     current 8 are used, one barrier per 8 blocks.
+//   * Scaling: the accumulator input is 0x4B400000, so the int32 result read
+//     as a float is exactly 1.5*2^23 + 16 s (|16 s| < 2^22); t = fma(f, d_w,
+//     -1.5*2^23*d_w) = 16 s d_w rounded once, acc = fma(t, d_x/16, acc) (the
+//     activation scales are staged divided by 16, which is exact).
+// Output element e of an MFMA in lane l is token row 8*(e/4) + 4*(l/32) + e%4
+// of the half, weight row l%32.  Gate/up waves hold 16 gate rows and the 16
+// matching up rows, so SwiGLU is one lane exchange; Q8_0 of each 32-wide h
+// block goes through LDS.  Down tiles write w * y per pair.
+#include "w4a8_dev.h"
+#include "w4a8_host.h"
+
+namespace w4a8 {
+
+namespace {
+
+constexpr int MNT = 256;           // threads: four waves
+constexpr int MT = 64;             // token rows per tile
+constexpr int WROWS = 128;         // weight rows per slice (32 per wave)
+constexpr int SPW_MAX = 4;         // slices per workgroup when the codes are resident
+constexpr int BIAS = 0x4B400000;   // float 1.5 * 2^23
+constexpr float BIASF = 12582912.0f;
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v16i __attribute__((ext_vector_type(16)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+typedef uint32_t v2u __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(4))) const int32_t CInt;
+
+struct MArgs {
+  const uint8_t *w, *ws;           // routed experts [E][N][K/32] Q4_0 / shared [N][K/32]
+  const uint32_t *act;             // aligned Q8_0 codes [row][K/32][8 dwords]
+  const float *actd;               // their scales [row][K/32]
+  const int32_t *meta, *perm;
+  const int4 *tiles;               // {expert, first sorted position, rows, -}
+  const float *topk_w;
+  float *h;                        // gate/up: fp32 h [P][I]
+  uint8_t *hq;                     // gate/up: Q8_0(h) [P][I/32]
+  uint32_t *ha;                    // gate/up: aligned codes of Q8_0(h) [P][I/32][8]
+  float *hd;                       // gate/up: their scales [P][I/32]
+  float *y;                        // down: w * y [P][H]
+  int64_t T, k, E, N, K, I;
+  int spw;                         // slices per workgroup
+};
+
+struct MLds {
+  union {
+    uint4 a[2][MT * 16];           // codes of 8 blocks, [buffer][row][chunk ^ row%16]
+    float hv[MT][65];              // gate/up epilogue: h of the tile, [row][64 columns]
+  };
+  float dx[2][8][MT];              // activation scales of 8 blocks, [buffer][block][row]
+  int arow[MT];                    // activation row of each tile row
+  int pair[MT];                    // pair of each tile row (-1: padding)
+};
+
+// Half of a weight row's group of 8 blocks (72 bytes): blocks 0..3 in lanes
+// 0..31, blocks 4..7 in lanes 32..63.
+struct HW {
+  uint32_t D[18];
+};
+
+__device__ __forceinline__ void load_hw(const uint8_t *p, HW &w) {
+  const v2u *v = reinterpret_cast<const v2u *>(p);
+#pragma unroll
+  for (int i = 0; i < 9; i++) {
+    const v2u t = v[i];
+    w.D[2 * i] = t.x;
+    w.D[2 * i + 1] = t.y;
+  }
+}
+
+// Payload dword c of the half's block j (bytes 18j + 2 + 4c ..), and the
+// dword holding its fp16 scale (low half for even j, high half for odd j).
+__device__ __forceinline__ uint32_t hw_nib(const HW &w, int j, int c) {
+  const int i = j >> 1;
+  return (j & 1) == 0 ? align2(w.D[9 * i + c + 1], w.D[9 * i + c]) : w.D[9 * i + 5 + c];
+}
+__device__ __forceinline__ uint32_t hw_sdw(const HW &w, int j) {
+  return (j & 1) == 0 ? w.D[9 * (j >> 1)] : w.D[9 * (j >> 1) + 4];
+}
+
+// B operands and scale dwords of blocks j and j + 4 of the group.
+__device__ __forceinline__ void pair_ops(const HW &w, int j, v4i &b0, v4i &b1, uint32_t &s0,
+                                         uint32_t &s1) {
+#pragma unroll
+  for (int c = 0; c < 4; c++) {
+    // q ^ 8 read as a signed 4-bit number is q - 8; placed in the high half
+    // of a byte it is the int8 16 * (q - 8)
+    const uint32_t x8 = hw_nib(w, j, c) ^ 0x88888888u;
+    const v2u r = __builtin_amdgcn_permlane32_swap((x8 << 4) & 0xF0F0F0F0u, x8 & 0xF0F0F0F0u,
+                                                   false, false);
+    b0[c] = (int)r.x;
+    b1[c] = (int)r.y;
+  }
+  const uint32_t sd = hw_sdw(w, j);
+  const v2u r = __builtin_amdgcn_permlane32_swap(sd, sd, false, false);
+  s0 = r.x;
+  s1 = r.y;
+}
+
+// Copy the tile's codes of blocks 8g..8g+7 into buffer buf: wave w moves rows
+// 16w..16w+15 (only the first 32 rows when `two` is false), four rows per
+// instruction; lane l writes chunk position l%16 of row r0 + l/16, which holds
+// chunk (l%16) ^ (row % 16) of the row's 256 bytes.
+__device__ __forceinline__ void stage_codes(const MArgs &a, MLds &L, int g, int buf, bool two,
+                                            int wave, int lane, int nblk) {
+  if (!two && wave >= 2) return;
+#pragma unroll
+  for (int i = 0; i < 4; i++) {
+    const int r0 = wave * 16 + i * 4;
+    const int r = r0 + (lane >> 4);
+    const int c = (lane & 15) ^ (r & 15);
+    const uint32_t *src = a.act + ((int64_t)L.arow[r] * nblk + 8 * g) * 8 + c * 4;
+    __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1))) *)src,
+                                     (void __attribute__((address_space(3))) *)&L.a[buf][r0 * 16],
+                                     16, 0, 0);
+  }
+}
+
+// A operand of block kk for tile row `row`: its codes 16*hh..+15 of the
+// block, from the swizzled staging buffer.
+__device__ __forceinline__ v4i aop(const uint4 *abuf, int row, int kk, int hh) {
+  const uint4 u = abuf[row * 16 + ((2 * kk + hh) ^ (row & 15))];
+  return v4i{(int)u.x, (int)u.y, (int)u.z, (int)u.w};
+}
+
+// Integer product with the bias accumulator input, read as floats (the whole
+// vector at once: an element-wise bit cast has been folded to element 0).
+__device__ __forceinline__ v16f mm(v4i a, v4i b, v16i c) {
+  return __builtin_bit_cast(v16f, __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, c, 0, 0, 0));
+}
+
+// acc[e] += s_e * dw * dx[row of e]; dx points at the scale of output row
+// 4*(l/32) of this 32-row half (rows 8q .. 8q + 3 past it for q = 0..3).
+__device__ __forceinline__ void scale16(float acc[16], v16f f, float dw, float dwb,
+                                        const float *dx) {
+#pragma unroll
+  for (int q = 0; q < 4; q++) {
+    const float4 d = *reinterpret_cast<const float4 *>(dx + 8 * q);
+    acc[4 * q + 0] = fmaf(fmaf(f[4 * q + 0], dw, dwb), d.x, acc[4 * q + 0]);
+    acc[4 * q + 1] = fmaf(fmaf(f[4 * q + 1], dw, dwb), d.y, acc[4 * q + 1]);
+    acc[4 * q + 2] = fmaf(fmaf(f[4 * q + 2], dw, dwb), d.z, acc[4 * q + 2]);
+    acc[4 * q + 3] = fmaf(fmaf(f[4 * q + 3], dw, dwb), d.w, acc[4 * q + 3]);
+  }
+}
+
+// One block: both token halves against the weight operand b.
+template <bool TWO>
+__device__ __forceinline__ void block(float acc0[16], float acc1[16], const uint4 *abuf,
+                                      const float (*dxb)[MT], int kk, v4i b, float dw, int r32,
+                                      int hh, v16i c0) {
+  const float dwb = -BIASF * dw;
+  const v16f f0 = mm(aop(abuf, r32, kk, hh), b, c0);
+  v16f f1;
+  if (TWO) f1 = mm(aop(abuf, 32 + r32, kk, hh), b, c0);
+  scale16(acc0, f0, dw, dwb, &dxb[kk][4 * hh]);
+  if (TWO) scale16(acc1, f1, dw, dwb, &dxb[kk][32 + 4 * hh]);
+}
+
+// One tile: rows token rows (1..64) of expert's group from sorted position
+// pos, against weight slices s0 .. s0 + ns - 1 (ns > 1 only for resident
+// codes and the down projection).  TWO: the tile holds more than 32 rows (a
+// compile-time branch: a run-time one inside the block loop makes the
+// compiler keep every block's second product until the loop's end).
+template <bool GATEUP, bool TWO>
+__device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, int pos, int rows,
+                                          int s0, int ns) {
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+  const int r32 = lane & 31, hh = lane >> 5;
+  const int nblk = (int)(a.K / 32), G = (int)(a.K / 256);
+  const bool resident = G <= 2;
+
+  if (tid < MT) {
+    int p = -1, r = -1;
+    if (tid < rows) {
+      p = a.perm[pos + tid];
+      r = GATEUP ? (p < a.T * a.k ? p / (int)a.k : p - (int)(a.T * a.k)) : p;
+    }
+    L.pair[tid] = p;
+    L.arow[tid] = r;
+  }
+  __syncthreads();
+  if (tid < MT && L.arow[tid] < 0) L.arow[tid] = L.arow[0];   // padding rows read a valid row
+  __syncthreads();
+  // scales: thread t moves row t%64, blocks t/64 and t/64 + 4 of each group,
+  // divided by 16 (zero for padding rows)
+  const int dm = tid & (MT - 1), dj = tid >> 6;
+  const float dlive = L.pair[dm] >= 0 ? 0.0625f : 0.0f;
+  const float *dsrc = a.actd + (int64_t)L.arow[dm] * nblk + dj;
+  float dx0 = 0.0f, dx1 = 0.0f;
+  if (resident) {
+    for (int g = 0; g < G; g++) {
+      stage_codes(a, L, g, g, TWO, wave, lane, nblk);
+      L.dx[g][dj][dm] = dlive * dsrc[8 * g];
+      L.dx[g][dj + 4][dm] = dlive * dsrc[8 * g + 4];
+    }
+  } else {
+    stage_codes(a, L, 0, 0, TWO, wave, lane, nblk);
+    dx0 = dsrc[0];
+    dx1 = dsrc[4];
+  }
+
+  // this lane's half of its weight row in slice s
+  const int64_t rowbytes = (int64_t)nblk * Q4B;
+  const uint8_t *Wx = (expert < a.E ? a.w + (int64_t)expert * a.N * rowbytes : a.ws) + 72 * hh;
+  auto wrow = [&](int s) -> const uint8_t * {
+    int64_t grow;
+    if (GATEUP) {
+      const int64_t col = (int64_t)s * 64 + 16 * wave + (r32 & 15);
+      grow = r32 < 16 ? col : a.I + col;
+    } else {
+      grow = (int64_t)s * WROWS + 32 * wave + r32;
+    }
+    return Wx + grow * rowbytes;
+  };
+
+  float acc0[16], acc1[16];
+#pragma unroll
+  for (int e = 0; e < 16; e++) { acc0[e] = 0.0f; acc1[e] = 0.0f; }
+  v16i c0;
+#pragma unroll
+  for (int e = 0; e < 16; e++) c0[e] = BIAS;
+
+  const int J = ns * G;
+  HW w;
+  load_hw(wrow(s0), w);
+  for (int j = 0; j < J; j++) {
+    const int sj = j / G, g = j - sj * G;
+    if (!resident) {
+      // buffer g&1 was last read in group g - 2, before the previous barrier
+      L.dx[g & 1][dj][dm] = dlive * dx0;
+      L.dx[g & 1][dj + 4][dm] = dlive * dx1;
+    }
+    if (!resident || j == 0) {
+      __builtin_amdgcn_s_waitcnt(0);              // codes, scales and weights have landed
+      __syncthreads();                            // ... for every wave
+    }
+    // next group's weights (the last group reloads itself: no conditional
+    // loads into a register array)
+    const int jn = j + 1 < J ? j + 1 : j;
+    const int sn = jn / G;
+    HW wn;
+    load_hw(wrow(s0 + sn) + (int64_t)(jn - sn * G) * (8 * Q4B), wn);
+    if (!resident && g + 1 < G) {
+      stage_codes(a, L, g + 1, (g + 1) & 1, TWO, wave, lane, nblk);
+      dx0 = dsrc[8 * (g + 1)];
+      dx1 = dsrc[8 * (g + 1) + 4];
+    }
+    const int buf = resident ? g : (g & 1);
+    const float(*dxb)[MT] = L.dx[buf];
+    const uint4 *abuf = L.a[buf];
+#pragma unroll
+    for (int jj = 0; jj < 4; jj++) {
+      v4i b0, b1;
+      uint32_t sd0, sd1;
+      pair_ops(w, jj, b0, b1, sd0, sd1);
+      const float dw0 = f16_bits_to_f32((jj & 1) ? sd0 >> 16 : sd0);
+      const float dw1 = f16_bits_to_f32((jj & 1) ? sd1 >> 16 : sd1);
+      block<TWO>(acc0, acc1, abuf, dxb, jj, b0, dw0, r32, hh, c0);
+      block<TWO>(acc0, acc1, abuf, dxb, jj + 4, b1, dw1, r32, hh, c0);
+    }
+    w = wn;
+    if (g + 1 < G) continue;
+
+    const int slice = s0 + sj;
+    if (GATEUP) {
+      __syncthreads();                            // the code buffers become the h tile
+      // lane r32 < 16 holds the gate sums of column 16*wave + r32, lane
+      // r32 + 16 the matching up sums
+#pragma unroll
+      for (int e = 0; e < 16; e++) {
+        const float u0 = __shfl_xor(acc0[e], 16), u1 = __shfl_xor(acc1[e], 16);
+        if (r32 < 16) {
+          const int m = 8 * (e >> 2) + 4 * hh + (e & 3);
+          L.hv[m][16 * wave + r32] = silu_f32(acc0[e]) * u0;
+          if (TWO) L.hv[32 + m][16 * wave + r32] = silu_f32(acc1[e]) * u1;
+        }
+      }
+      __syncthreads();
+      // Q8_0 of each row's two 32-wide blocks: 8 lanes per block
+      const int nbh = (int)(a.I / 32);
+#pragma unroll
+      for (int pass = 0; pass < 4; pass++) {
+        const int idx = pass * MNT + tid;
+        const int rb = idx >> 3, jq = idx & 7, m = rb >> 1, cb = rb & 1;
+        const int p = L.pair[m];
+        if (p >= 0) {                             // whole 8-lane groups agree
+          const float v[4] = {L.hv[m][32 * cb + 4 * jq], L.hv[m][32 * cb + 4 * jq + 1],
+                              L.hv[m][32 * cb + 4 * jq + 2], L.hv[m][32 * cb + 4 * jq + 3]};
+          uint32_t d16;
+          const uint32_t packed = q8_0_block8(v, d16);
+          const int bi = 2 * slice + cb;
+          const int64_t blk = (int64_t)p * nbh + bi;
+          store_q8_0_block8(a.hq + blk * Q8B, jq, packed, d16);
+          a.ha[blk * 8 + jq] = packed;
+          if (jq == 0) a.hd[blk] = f16_bits_to_f32(d16);
+          *reinterpret_cast<float4 *>(a.h + (int64_t)p * a.I + 32 * bi + 4 * jq) =
+              make_float4(v[0], v[1], v[2], v[3]);
+        }
+      }
+    } else {
+      const int64_t n = (int64_t)slice * WROWS + 32 * wave + r32;
+#pragma unroll
+      for (int e = 0; e < 16; e++) {
+        const int m = 8 * (e >> 2) + 4 * hh + (e & 3);
+        const int p0 = L.pair[m];
+        if (p0 >= 0) a.y[(int64_t)p0 * a.N + n] = (p0 < a.T * a.k ? a.topk_w[p0] : 1.0f) * acc0[e];
+        if (TWO) {
+          const int p1 = L.pair[32 + m];
+          if (p1 >= 0)
+            a.y[(int64_t)p1 * a.N + n] = (p1 < a.T * a.k ? a.topk_w[p1] : 1.0f) * acc1[e];
+        }
+        acc0[e] = 0.0f;
+        acc1[e] = 0.0f;
+      }
+    }
+  }
+}
+
+template <bool GATEUP>
+__global__ __launch_bounds__(MNT) __attribute__((amdgpu_waves_per_eu(3))) void mfma_kernel(MArgs a) {
+  __shared__ MLds L;
+  // Work item w = tile * nch + chunk, chunk = a run of spw slices.  Workgroup
+  // b runs on XCD b % 8, so XCD x takes the contiguous items [x*C, x*C + C),
+  // C = ceil(items / 8): the slices of a tile share one L2 for its codes.
+  const int nsl = (int)(GATEUP ? a.I / 64 : a.N / WROWS);
+  const int nch = (nsl + a.spw - 1) / a.spw;
+  const int items = ((CInt *)a.meta)[2] * nch;               // META_NTILES
+  const int per = (items + 7) >> 3;
+  const int b = blockIdx.x;
+  if (b >= 8 * per) return;
+  const int w = (b & 7) * per + (b >> 3);
+  if (w >= items) return;
+  const int tile = w / nch, ch = w - tile * nch;
+  const int s0 = ch * a.spw, ns = min(a.spw, nsl - s0);
+  CInt *tp = (CInt *)a.tiles + 4 * tile;
+  const int expert = tp[0], pos = tp[1], rows = tp[2];
+  if (rows > 32)
+    mfma_tile<GATEUP, true>(a, L, expert, pos, rows, s0, ns);
+  else
+    mfma_tile<GATEUP, false>(a, L, expert, pos, rows, s0, ns);
+}
+
+}  // namespace
+
+int mfma_tile_rows() { return MT; }
+
+int mfma_gateup(const uint8_t *w_gu, const uint8_t *ws_gu, const uint32_t *xa, const float *xd,
+                const int32_t *meta, const int32_t *perm, const int4 *tiles, float *h,
+                uint8_t *hq, uint32_t *ha, float *hd, int64_t maxtiles, int64_t T, int64_t H,
+                int64_t I, int64_t E, int64_t k, hipStream_t s) {
+  MArgs a{};
+  a.w = w_gu; a.ws = ws_gu; a.act = xa; a.actd = xd;
+  a.meta = meta; a.perm = perm; a.tiles = tiles;
+  a.h = h; a.hq = hq; a.ha = ha; a.hd = hd;
+  a.T = T; a.k = k; a.E = E; a.N = 2 * I; a.K = H; a.I = I;
+  a.spw = 1;                       // the h tile reuses the code buffers
+  mfma_kernel<true><<<dim3((unsigned)((maxtiles * (I / 64) + 7) & ~7)), dim3(MNT), 0, s>>>(a);
+  return check_launch();
+}
+
+int mfma_down(const uint8_t *w_d, const uint8_t *ws_d, const uint32_t *ha, const float *hd,
+              const int32_t *meta, const int32_t *perm, const int4 *tiles, const float *topk_w,
+              float *y, int64_t maxtiles, int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
+              hipStream_t s) {
+  MArgs a{};
+  a.w = w_d; a.ws = ws_d; a.act = ha; a.actd = hd;
+  a.meta = meta; a.perm = perm; a.tiles = tiles;
+  a.topk_w = topk_w; a.y = y;
+  a.T = T; a.k = k; a.E = E; a.N = H; a.K = I; a.I = I;
+  const int64_t nsl = H / WROWS;
+  a.spw = I <= 512 ? (int)std::min<int64_t>(SPW_MAX, nsl) : 1;
+  const int64_t nch = (nsl + a.spw - 1) / a.spw;
+  mfma_kernel<false><<<dim3((unsigned)((maxtiles * nch + 7) & ~7)), dim3(MNT), 0, s>>>(a);
+  return check_launch();
+}
+
+}  // namespace w4a8

@@ -5,14 +5,16 @@
 //
 // Stages (all on the caller's stream):
 //   1. Q8_0 of the hidden rows                          -> workspace xq
+//      (plus the copies the grouped kernels read: nibble-split, aligned)
 //   2. route: stable counting sort of the T*k pairs by expert (plus the T
-//      shared pairs), the list of non-empty expert groups and of row tiles
-//   3. gate/up: per (row tile, 32 h columns) the gate and up rows of the
+//      shared pairs), the list of non-empty expert groups, the chunks of the
+//      small groups and the row tiles of the others
+//   3. gate/up: per (row tile, 64 h columns) the gate and up rows of the
 //      expert against the tile's token rows, SwiGLU, Q8_0 of the 32-wide h
-//      block                                           -> workspace h, hq
+//      blocks (mfma.hip)                               -> workspace h, hq
 //      (groups of few rows: the VALU kernels of smallm.hip instead, which
 //      take the activations in nibble-split form)
-//   4. down: per (row tile, output row slab) the down rows against Q8_0(h),
+//   4. down: per (row tile, 128 output rows) the down rows against Q8_0(h),
 //      scaled by the routing weight                    -> workspace y
 //   5. combine: out[t] = sum over slots in slot order, then the shared pair
 //      (fixed order, so the result does not depend on scheduling)
@@ -24,8 +26,8 @@
 namespace w4a8 {
 
 int launch_fill_zero(void *ptr, size_t bytes, hipStream_t s);
-int launch_q8_0(const float *x, uint8_t *xq, int64_t nblocks, hipStream_t s);
-int launch_q8_0_split(const float *x, uint8_t *xq, SplitBlk *xs, int64_t nblocks, hipStream_t s);
+int launch_q8_0_ex(const float *x, uint8_t *xq, SplitBlk *xs, uint32_t *xa, float *xd,
+                   int64_t nblocks, hipStream_t s);
 bool small_supported(int64_t H, int64_t I);
 int64_t small_max_chunks(int64_t T, int64_t E, int64_t k, int has_shared);
 int small_gateup(const uint8_t *w_gu, const uint8_t *ws_gu, const SplitBlk *xs,
@@ -36,15 +38,15 @@ int small_down(const uint8_t *w_d, const uint8_t *ws_d, const SplitBlk *hs, cons
                const int32_t *perm, const int4 *chunks, const float *topk_w, float *y,
                int64_t maxchunks, int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
                hipStream_t s);
-int grouped_tile_rows();
-int grouped_gateup(const uint8_t *w_gu, const uint8_t *ws_gu, const uint8_t *xq,
-                   const int32_t *meta, const int32_t *perm, const int4 *groups, const int2 *tiles,
-                   float *h, uint8_t *hq, int64_t maxtiles, int64_t T, int64_t H, int64_t I,
-                   int64_t E, int64_t k, hipStream_t s);
-int grouped_down(const uint8_t *w_d, const uint8_t *ws_d, const uint8_t *hq, const int32_t *meta,
-                 const int32_t *perm, const int4 *groups, const int2 *tiles, const float *topk_w,
-                 float *y, int64_t maxtiles, int64_t T, int64_t H, int64_t I, int64_t E,
-                 int64_t k, hipStream_t s);
+int mfma_tile_rows();
+int mfma_gateup(const uint8_t *w_gu, const uint8_t *ws_gu, const uint32_t *xa, const float *xd,
+                const int32_t *meta, const int32_t *perm, const int4 *tiles, float *h,
+                uint8_t *hq, uint32_t *ha, float *hd, int64_t maxtiles, int64_t T, int64_t H,
+                int64_t I, int64_t E, int64_t k, hipStream_t s);
+int mfma_down(const uint8_t *w_d, const uint8_t *ws_d, const uint32_t *ha, const float *hd,
+              const int32_t *meta, const int32_t *perm, const int4 *tiles, const float *topk_w,
+              float *y, int64_t maxtiles, int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
+              hipStream_t s);
 size_t decode_sync_words(int64_t H);
 size_t decode_xfer_words(int64_t I, int64_t k);
 bool decode_supported(int64_t H, int64_t I, int64_t k);
@@ -58,7 +60,7 @@ int launch_rmsnorm(const float *x, const float *y, const float *gamma, float *x_
 
 namespace {
 
-constexpr int MC = 32;          // token rows per tile (one grouped MFMA tile)
+constexpr int MC = 64;          // token rows per tile of the grouped MFMA kernels
 constexpr int ROUTE_T = 1024;   // threads of the route kernel
 constexpr int LDS_INTS = 16000; // int32 cells of dynamic LDS for the route kernel (< 64 KB)
 
@@ -66,7 +68,7 @@ inline size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
   size_t meta, sync, xfer, perm, count, rank, groups, tiles, chunks, xq, h, hq, y, xn, xs, hs,
-      total;
+      xa, xd, ha, hd, total;
   int64_t maxtiles, maxchunks;
 };
 
@@ -89,7 +91,7 @@ Layout make_layout(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k) {
   L.count = off;  off += up256(sizeof(int32_t) * E);
   L.rank = off;   off += up256(sizeof(int32_t) * (T * k + 1));
   L.groups = off; off += up256(sizeof(int4) * (E + 1));
-  L.tiles = off;  off += up256(sizeof(int2) * L.maxtiles);
+  L.tiles = off;  off += up256(sizeof(int4) * L.maxtiles);
   L.maxchunks = small_max_chunks(T, E, k, 1);
   L.chunks = off; off += up256(sizeof(int4) * L.maxchunks);
   L.xq = off;     off += up256((size_t)T * (H / QK) * Q8B);
@@ -99,6 +101,10 @@ Layout make_layout(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k) {
   L.xn = off;     off += up256(sizeof(float) * (size_t)T * H);
   L.xs = off;     off += up256(sizeof(SplitBlk) * (size_t)T * (H / QK));
   L.hs = off;     off += up256(sizeof(SplitBlk) * (size_t)P * (I / QK));
+  L.xa = off;     off += up256((size_t)T * H);          // aligned Q8_0 codes of x
+  L.xd = off;     off += up256(sizeof(float) * (size_t)T * (H / QK));
+  L.ha = off;     off += up256((size_t)P * I);          // aligned Q8_0 codes of h
+  L.hd = off;     off += up256(sizeof(float) * (size_t)P * (I / QK));
   L.total = off;
   return L;
 }
@@ -146,7 +152,8 @@ struct RouteArgs {
   const int32_t *ids;
   int32_t *meta, *perm, *count, *rank;
   int4 *groups;     // {expert (E = shared), first sorted position, rows, first tile}
-  int2 *tiles;      // {group, first row within the group}: groups of more than ms rows
+  int4 *tiles;      // groups of more than ms rows, cut into tiles of MC rows:
+                    // {expert, first sorted position, rows, group}
   int4 *chunks;     // groups of at most ms rows, cut into chunks of SMALL_CHUNK
                     // rows: {expert, first sorted position, rows, group}, in
                     // reverse group order
@@ -241,7 +248,8 @@ __global__ __launch_bounds__(ROUTE_T) void route_kernel(RouteArgs a) {
       for (int m0 = 0, c = gsmall[e]; m0 < rows; m0 += SMALL_CHUNK, c++)
         a.chunks[nsmall - 1 - c] = make_int4(e, start + m0, min(SMALL_CHUNK, rows - m0), gi);
     } else {
-      for (int m0 = 0, t = t0; m0 < rows; m0 += MC, t++) a.tiles[t] = make_int2(gi, m0);
+      for (int m0 = 0, t = t0; m0 < rows; m0 += MC, t++)
+        a.tiles[t] = make_int4(e, start + m0, min(MC, rows - m0), gi);
     }
   }
   if (tid == 0) {
@@ -303,10 +311,16 @@ int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
     hidden = norm.xn;
   }
   const int ms = small_supported(H, I) ? small_rows(T) : 0;
+  // with ms >= T every group (at most T rows) is small: no MFMA tiles
+  const bool tiles = ms < T;
   SplitBlk *xs = reinterpret_cast<SplitBlk *>(ws + L.xs);
   SplitBlk *hs = reinterpret_cast<SplitBlk *>(ws + L.hs);
-  if ((rc = ms > 0 ? launch_q8_0_split(hidden, ws + L.xq, xs, T * (H / QK), s)
-                   : launch_q8_0(hidden, ws + L.xq, T * (H / QK), s)) != W4A8_OK)
+  uint32_t *xa = reinterpret_cast<uint32_t *>(ws + L.xa);
+  uint32_t *ha = reinterpret_cast<uint32_t *>(ws + L.ha);
+  float *xd = reinterpret_cast<float *>(ws + L.xd);
+  float *hd = reinterpret_cast<float *>(ws + L.hd);
+  if ((rc = launch_q8_0_ex(hidden, ws + L.xq, ms > 0 ? xs : nullptr, tiles ? xa : nullptr, xd,
+                           T * (H / QK), s)) != W4A8_OK)
     return rc;
 
   RouteArgs ra;
@@ -316,7 +330,7 @@ int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
   ra.count = reinterpret_cast<int32_t *>(ws + L.count);
   ra.rank = reinterpret_cast<int32_t *>(ws + L.rank);
   ra.groups = reinterpret_cast<int4 *>(ws + L.groups);
-  ra.tiles = reinterpret_cast<int2 *>(ws + L.tiles);
+  ra.tiles = reinterpret_cast<int4 *>(ws + L.tiles);
   ra.chunks = reinterpret_cast<int4 *>(ws + L.chunks);
   ra.T = (int)T; ra.k = (int)k; ra.E = (int)E; ra.has_shared = has_shared; ra.ms = ms;
   const int64_t Pr = T * k;
@@ -341,16 +355,14 @@ int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
   if (ms > 0 && (rc = small_gateup(w_gu, ws_gu, xs, ra.meta, ra.perm, ra.chunks, h, hq, hs,
                                    maxchunks, T, H, I, E, k, s)) != W4A8_OK)
     return rc;
-  // with ms >= T every group (at most T rows) is small: no MFMA tiles
-  const bool tiles = ms < T;
-  if (tiles && (rc = grouped_gateup(w_gu, ws_gu, ws + L.xq, ra.meta, ra.perm, ra.groups, ra.tiles,
-                                    h, hq, L.maxtiles, T, H, I, E, k, s)) != W4A8_OK)
+  if (tiles && (rc = mfma_gateup(w_gu, ws_gu, xa, xd, ra.meta, ra.perm, ra.tiles, h, hq, ha, hd,
+                                 L.maxtiles, T, H, I, E, k, s)) != W4A8_OK)
     return rc;
   if (ms > 0 && (rc = small_down(w_d, ws_d, hs, ra.meta, ra.perm, ra.chunks, topk_w, y, maxchunks,
                                  T, H, I, E, k, s)) != W4A8_OK)
     return rc;
-  if (tiles && (rc = grouped_down(w_d, ws_d, hq, ra.meta, ra.perm, ra.groups, ra.tiles, topk_w,
-                                  y, L.maxtiles, T, H, I, E, k, s)) != W4A8_OK)
+  if (tiles && (rc = mfma_down(w_d, ws_d, ha, hd, ra.meta, ra.perm, ra.tiles, topk_w, y,
+                               L.maxtiles, T, H, I, E, k, s)) != W4A8_OK)
     return rc;
 
   const int64_t n4 = T * (H / 4);

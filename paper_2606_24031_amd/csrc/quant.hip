@@ -11,11 +11,15 @@
 
 namespace w4a8 {
 
-// 8 lanes per block; with SPLIT also the nibble-split copy of each block.
-template <bool SPLIT>
+// 8 lanes per block.  With SPLIT also the nibble-split copy of each block
+// (small-group kernels); with ALIGNED also its 32 codes on a 32-byte boundary
+// and its fp32 scale (grouped MFMA kernels).
+template <bool SPLIT, bool ALIGNED>
 __global__ __launch_bounds__(256) void q8_0_kernel(const float *__restrict__ x,
                                                    uint8_t *__restrict__ xq,
-                                                   SplitBlk *__restrict__ xs, int64_t nblocks) {
+                                                   SplitBlk *__restrict__ xs,
+                                                   uint32_t *__restrict__ xa,
+                                                   float *__restrict__ xd, int64_t nblocks) {
   const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t blk = tid >> 3;
   const int j = (int)(tid & 7);
@@ -38,6 +42,10 @@ __global__ __launch_bounds__(256) void q8_0_kernel(const float *__restrict__ x,
         xs[blk].corr = -8 * lsum;
       }
     }
+  }
+  if (ALIGNED && live) {
+    xa[blk * 8 + j] = packed;
+    if (j == 0) xd[blk] = f16_bits_to_f32(d16);
   }
 }
 
@@ -111,14 +119,26 @@ int launch_fill_zero(void *ptr, size_t bytes, hipStream_t s) {
 int launch_q8_0(const float *x, uint8_t *xq, int64_t nblocks, hipStream_t s) {
   if (nblocks == 0) return W4A8_OK;
   const int64_t grid = (nblocks * 8 + 255) / 256;
-  q8_0_kernel<false><<<dim3((unsigned)grid), dim3(256), 0, s>>>(x, xq, nullptr, nblocks);
+  q8_0_kernel<false, false><<<dim3((unsigned)grid), dim3(256), 0, s>>>(x, xq, nullptr, nullptr,
+                                                                        nullptr, nblocks);
   return check_launch();
 }
 
-int launch_q8_0_split(const float *x, uint8_t *xq, SplitBlk *xs, int64_t nblocks, hipStream_t s) {
+// Q8_0 with the extra copies the grouped kernels read: the nibble-split form
+// (xs) and/or the aligned codes and scales (xa, xd); either may be null.
+int launch_q8_0_ex(const float *x, uint8_t *xq, SplitBlk *xs, uint32_t *xa, float *xd,
+                   int64_t nblocks, hipStream_t s) {
   if (nblocks <= 0) return W4A8_OK;
   const int64_t grid = (nblocks * 8 + 255) / 256;
-  q8_0_kernel<true><<<dim3((unsigned)grid), dim3(256), 0, s>>>(x, xq, xs, nblocks);
+  const dim3 g((unsigned)grid), b(256);
+  if (xs && xa)
+    q8_0_kernel<true, true><<<g, b, 0, s>>>(x, xq, xs, xa, xd, nblocks);
+  else if (xs)
+    q8_0_kernel<true, false><<<g, b, 0, s>>>(x, xq, xs, nullptr, nullptr, nblocks);
+  else if (xa)
+    q8_0_kernel<false, true><<<g, b, 0, s>>>(x, xq, nullptr, xa, xd, nblocks);
+  else
+    q8_0_kernel<false, false><<<g, b, 0, s>>>(x, xq, nullptr, nullptr, nullptr, nblocks);
   return check_launch();
 }
 

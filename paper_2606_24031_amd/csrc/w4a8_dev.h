@@ -202,7 +202,11 @@ struct SplitBlk {
 };
 static_assert(sizeof(SplitBlk) == 48, "split block layout");
 
-__device__ __forceinline__ float silu_f32(float g) { return g / (1.0f + expf(-g)); }
+// SiLU(g) = g / (1 + e^-g) with the hardware base-2 exponential and
+// reciprocal (each within about one ulp).
+__device__ __forceinline__ float silu_f32(float g) {
+  return g * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(g * -1.44269504f));
+}
 
 // Exact block dot s = sum (q_w - 8) * x over a block in nibble-split form:
 // q_w - 8 is the signed nibble q_w ^ 8, so
