@@ -306,6 +306,45 @@ def test_moe_group_size_boundary_between_paths(small_layer):
     L.check(x, ids, wts, k, out, h, hq)
 
 
+def test_moe_tiles_across_64_row_boundaries(small_layer):
+    """MFMA row tiles of 64: groups of 64 (one full tile), 65 (a full tile
+    and a 1-row tile), 97 (a full tile and a 33-row tile, second half of the
+    tile in use) and 30 rows, plus the shared expert's 128 (two full tiles)."""
+    L = small_layer
+    g = synth.rng(33)
+    T, k = 128, 2
+    x = synth.normal_f32(g, (T, L.H))
+    ids = np.empty((T, k), dtype=np.int32)
+    ids[:64, 0] = 0
+    ids[64:128, 0] = 1
+    ids[:1, 1] = 1                       # expert 1: 65 rows
+    ids[1:98, 1] = 2                     # expert 2: 97 rows
+    ids[98:128, 1] = 3                   # expert 3: 30 rows
+    wts = g.random((T, k), dtype=np.float32)
+    out, h, hq, perm, count, _ = L.run(x, ids, wts, k)
+    assert count.tolist() == [64, 65, 97, 30]
+    _check_route(ids, L.E, True, perm, count)
+    L.check(x, ids, wts, k, out, h, hq)
+
+
+@pytest.mark.parametrize("seed,H,I,E,shared,T,k", [
+    (41, 768, 768, 5, True, 48, 2),      # three 8-block groups per row on both sides
+    (42, 512, 256, 3, False, 40, 2),     # no shared expert; down K = 256 (one group)
+    (43, 2560, 256, 2, True, 40, 1),     # K = 2560: ten staged groups for gate/up
+])
+def test_moe_mfma_path_shapes(seed, H, I, E, shared, T, k):
+    """Shapes other than the paper's layer with groups large enough for the
+    MFMA tiles (more than 8 rows at T > 32)."""
+    L = Layer(seed, H, I, E, shared=shared)
+    g = synth.rng(seed + 100)
+    x = synth.normal_f32(g, (T, L.H))
+    ids, wts = synth.routing(g, T, L.E, k)
+    out, h, hq, perm, count, _ = L.run(x, ids, wts, k)
+    assert count.max() > 8
+    _check_route(ids, L.E, shared, perm, count)
+    L.check(x, ids, wts, k, out, h, hq)
+
+
 def test_moe_prefill_947_sampled_tokens(qwen_layer):
     L = qwen_layer
     g = synth.rng(22)
