@@ -120,33 +120,49 @@ int validate(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k) {
 }
 
 // ------------------------------------------------------------------ route
-// Exclusive scan of a[0..n) in LDS by all ROUTE_T threads; returns the total.
-__device__ int block_exscan(int *a, int n, int *wtot) {
+// Exclusive scans of NA arrays a[j][0..n) in LDS at once by all ROUTE_T
+// threads; tot[j] receives the total of array j.
+template <int NA>
+__device__ void block_exscan(int *const (&a)[NA], int n, int (*wtot)[ROUTE_T / 64 + 1],
+                             int (&tot)[NA]) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int per = (n + ROUTE_T - 1) / ROUTE_T;
   const int lo = min(tid * per, n), hi = min(lo + per, n);
-  int s = 0;
-  for (int i = lo; i < hi; i++) s += a[i];
-  int x = s;
+  int s[NA], x[NA];
+#pragma unroll
+  for (int j = 0; j < NA; j++) {
+    s[j] = 0;
+    for (int i = lo; i < hi; i++) s[j] += a[j][i];
+    x[j] = s[j];
+  }
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o);
-    if (lane >= o) x += y;
+#pragma unroll
+    for (int j = 0; j < NA; j++) {
+      const int y = __shfl_up(x[j], o);
+      if (lane >= o) x[j] += y;
+    }
   }
-  if (lane == 63) wtot[wave] = x;
+  if (lane == 63)
+#pragma unroll
+    for (int j = 0; j < NA; j++) wtot[j][wave] = x[j];
   __syncthreads();
-  if (tid == 0) {
+  if (tid < NA) {
     int run = 0;
-    for (int w = 0; w < ROUTE_T / 64; w++) { const int v = wtot[w]; wtot[w] = run; run += v; }
-    wtot[ROUTE_T / 64] = run;
+    for (int w = 0; w < ROUTE_T / 64; w++) { const int v = wtot[tid][w]; wtot[tid][w] = run; run += v; }
+    wtot[tid][ROUTE_T / 64] = run;
   }
   __syncthreads();
-  int base = wtot[wave] + x - s;
-  for (int i = lo; i < hi; i++) { const int v = a[i]; a[i] = base; base += v; }
-  const int total = wtot[ROUTE_T / 64];
+#pragma unroll
+  for (int j = 0; j < NA; j++) {
+    int base = wtot[j][wave] + x[j] - s[j];
+    for (int i = lo; i < hi; i++) { const int v = a[j][i]; a[j][i] = base; base += v; }
+    tot[j] = wtot[j][ROUTE_T / 64];
+  }
   __syncthreads();
-  return total;
 }
+
+constexpr int RCH = 16;   // chunks of 64 pairs a wave keeps in registers
 
 struct RouteArgs {
   const int32_t *ids;
@@ -160,86 +176,152 @@ struct RouteArgs {
   int T, k, E, has_shared, seg, nseg, ebits, ms;
 };
 
+// Rank of this lane's pair among the earlier pairs of the same expert in its
+// 64-pair chunk (lanes agreeing on every bit of the expert id), plus the
+// pairs of that expert in the segment's earlier chunks (hist[e][s], advanced
+// by the chunk's first lane of each expert).  e < 0: no pair.
+__device__ __forceinline__ int chunk_rank(int e, int s, int *hist, const RouteArgs &a,
+                                          int lane) {
+  uint64_t peers = __ballot(e >= 0);
+  for (int bit = 0; bit < a.ebits; bit++) {
+    const int mine = (e >> bit) & 1;
+    const uint64_t b = __ballot(mine);
+    peers &= mine ? b : ~b;
+  }
+  int r = 0;
+  if (e >= 0) {
+    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    const int idx = e * a.nseg + s;
+    const int before = hist[idx];
+    r = before + __popcll(peers & lt);
+    if ((peers & lt) == 0) hist[idx] = before + __popcll(peers);
+  }
+  return r;
+}
+
 // One workgroup.  Pairs are cut into segments of `seg` (a multiple of 64);
 // wave w owns segments w, w+16, ...  For every pair, its rank among the
-// earlier pairs of the same expert inside its segment comes from wave ballots
-// (lanes agreeing on every bit of the expert id); the per-(expert, segment)
-// counts, laid out expert-major, are then scanned once, which yields at the
-// same time each expert's offset and each segment's base inside it.  The
-// resulting order is stable in pair index.
+// earlier pairs of the same expert inside its segment comes from wave ballots;
+// the per-(expert, segment) counts, laid out expert-major, are then scanned
+// once, which yields at the same time each expert's offset and each segment's
+// base inside it.  The resulting order is stable in pair index.  REG: every
+// wave's chunks fit in RCH registers, so the ids are loaded in one batch and
+// the ranks stay in registers until the scatter (otherwise they go through
+// the workspace).
+template <bool REG>
 __global__ __launch_bounds__(ROUTE_T) void route_kernel(RouteArgs a) {
-  extern __shared__ int hist[];  // [E][nseg]
-  __shared__ int wtot[ROUTE_T / 64 + 1];
+  extern __shared__ int hist[];  // [E][nseg], later the group counters
+  __shared__ int wtot[3][ROUTE_T / 64 + 1];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int Pr = a.T * a.k;
   const int L = a.E * a.nseg;
   for (int i = tid; i < L; i += ROUTE_T) hist[i] = 0;
+
+  const int cps = a.seg >> 6;    // chunks per segment
+  int er[RCH], rr[RCH];
+  if (REG) {
+    // chunk i of this wave: segment wave + 16 (i / cps), its chunk i % cps
+#pragma unroll
+    for (int i = 0; i < RCH; i++) {
+      const int j = i / cps, sg = wave + 16 * j;
+      const int p = sg * a.seg + 64 * (i - j * cps) + lane;
+      const bool live = sg < a.nseg && p < Pr;
+      const int e = a.ids[live ? p : 0];
+      er[i] = (live && e >= 0 && e < a.E) ? e : -1;
+    }
+  }
   __syncthreads();
 
-  for (int s = wave; s < a.nseg; s += ROUTE_T / 64) {
-    const int end = min((s + 1) * a.seg, Pr);
-    for (int base = s * a.seg; base < end; base += 64) {
-      const int p = base + lane;
-      int e = -1;
-      if (p < end) {
-        e = a.ids[p];
-        if (e < 0 || e >= a.E) e = -1;
-      }
-      const uint64_t valid = __ballot(e >= 0);
-      uint64_t peers = valid;
-      for (int bit = 0; bit < a.ebits; bit++) {
-        const int mine = (e >> bit) & 1;
-        const uint64_t b = __ballot(mine);
-        peers &= mine ? b : ~b;
-      }
-      if (e >= 0) {
-        const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-        const int idx = e * a.nseg + s;
-        const int before = hist[idx];
-        a.rank[p] = before + __popcll(peers & lt);
-        if ((peers & lt) == 0) hist[idx] = before + __popcll(peers);
+  if (REG) {
+#pragma unroll
+    for (int i = 0; i < RCH; i++) {
+      const int sg = wave + 16 * (i / cps);
+      rr[i] = sg < a.nseg ? chunk_rank(er[i], sg, hist, a, lane) : 0;
+    }
+  } else {
+    for (int sg = wave; sg < a.nseg; sg += ROUTE_T / 64) {
+      const int end = (int)min((int64_t)(sg + 1) * a.seg, (int64_t)Pr);
+      for (int base = sg * a.seg; base < end; base += 64) {
+        const int p = base + lane;
+        int e = -1;
+        if (p < end) {
+          e = a.ids[p];
+          if (e < 0 || e >= a.E) e = -1;
+        }
+        const int r = chunk_rank(e, sg, hist, a, lane);
+        if (e >= 0) a.rank[p] = r;
       }
     }
   }
   __syncthreads();
-  const int nrouted = block_exscan(hist, L, wtot);
+  int nrouted;
+  {
+    int *const arr[1] = {hist};
+    int tot[1];
+    block_exscan<1>(arr, L, wtot, tot);
+    nrouted = tot[0];
+  }
 
-  for (int p = tid; p < Pr; p += ROUTE_T) {
-    const int e = a.ids[p];
-    if (e < 0 || e >= a.E) continue;
-    a.perm[hist[e * a.nseg + p / a.seg] + a.rank[p]] = p;
+  if (REG) {
+#pragma unroll
+    for (int i = 0; i < RCH; i++) {
+      const int j = i / cps, sg = wave + 16 * j;
+      const int p = sg * a.seg + 64 * (i - j * cps) + lane;
+      if (er[i] >= 0) a.perm[hist[er[i] * a.nseg + sg] + rr[i]] = p;
+    }
+  } else {
+    for (int p = tid; p < Pr; p += ROUTE_T) {
+      const int e = a.ids[p];
+      if (e < 0 || e >= a.E) continue;
+      a.perm[hist[e * a.nseg + p / a.seg] + a.rank[p]] = p;
+    }
   }
   if (a.has_shared)
     for (int t = tid; t < a.T; t += ROUTE_T) a.perm[nrouted + t] = Pr + t;
-  __syncthreads();
 
   // counts, then the compacted list of non-empty groups (expert order); a
   // group of at most ms rows goes to the small-group list, a larger one gets
-  // its range of MFMA row tiles.  The shared expert is the last group.
-  int *gflag = hist + L;  // 3 x (E + 1) entries after the histogram
+  // its range of MFMA row tiles.  The shared expert is the last group.  Each
+  // thread keeps the start and size of its experts (e = tid + j*ROUTE_T) in
+  // registers, and the histogram's space then holds the three group counters.
+  constexpr int EPT = 5;         // (E + 1) <= EPT * ROUTE_T for E <= 4096
+  int gst[EPT], grw[EPT];
+#pragma unroll
+  for (int j = 0; j < EPT; j++) {
+    const int e = tid + j * ROUTE_T;
+    gst[j] = nrouted;
+    grw[j] = 0;
+    if (e < a.E) {
+      gst[j] = hist[e * a.nseg];
+      grw[j] = ((e + 1 < a.E) ? hist[(e + 1) * a.nseg] : nrouted) - gst[j];
+      a.count[e] = grw[j];
+    } else if (e == a.E) {
+      grw[j] = a.has_shared ? a.T : 0;
+    }
+  }
+  __syncthreads();
+  int *gflag = hist;             // 3 x (E + 1) entries
   int *gtile = gflag + a.E + 1;
   int *gsmall = gtile + a.E + 1;
-  for (int e = tid; e <= a.E; e += ROUTE_T) {
-    int rows;
-    if (e < a.E) {
-      const int start = hist[e * a.nseg];
-      const int stop = (e + 1 < a.E) ? hist[(e + 1) * a.nseg] : nrouted;
-      rows = stop - start;
-      a.count[e] = rows;
-    } else {
-      rows = a.has_shared ? a.T : 0;
-    }
+#pragma unroll
+  for (int j = 0; j < EPT; j++) {
+    const int e = tid + j * ROUTE_T, rows = grw[j];
+    if (e > a.E) break;
     gflag[e] = rows > 0 ? 1 : 0;
     gsmall[e] = (rows > 0 && rows <= a.ms) ? (rows + SMALL_CHUNK - 1) / SMALL_CHUNK : 0;
     gtile[e] = rows > a.ms ? (rows + MC - 1) / MC : 0;
   }
   __syncthreads();
-  const int ngroups = block_exscan(gflag, a.E + 1, wtot);
-  const int ntiles = block_exscan(gtile, a.E + 1, wtot);
-  const int nsmall = block_exscan(gsmall, a.E + 1, wtot);
-  for (int e = tid; e <= a.E; e += ROUTE_T) {
-    const int start = (e < a.E) ? hist[e * a.nseg] : nrouted;
-    const int rows = (e < a.E) ? a.count[e] : (a.has_shared ? a.T : 0);
+  int tot[3];
+  {
+    int *const arr[3] = {gflag, gtile, gsmall};
+    block_exscan<3>(arr, a.E + 1, wtot, tot);
+  }
+  const int ngroups = tot[0], ntiles = tot[1], nsmall = tot[2];
+#pragma unroll
+  for (int j = 0; j < EPT; j++) {
+    const int e = tid + j * ROUTE_T, start = gst[j], rows = grw[j];
+    if (e > a.E) break;
     if (rows == 0) continue;
     const int gi = gflag[e], t0 = gtile[e];
     a.groups[gi] = make_int4(e, start, rows, t0);
@@ -335,17 +417,19 @@ int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
   ra.T = (int)T; ra.k = (int)k; ra.E = (int)E; ra.has_shared = has_shared; ra.ms = ms;
   const int64_t Pr = T * k;
   // smallest segment (multiple of 64 pairs) whose histogram fits in LDS
-  int64_t seg = 64, nseg = std::max<int64_t>(1, (Pr + 63) / 64);
-  while (E * nseg + 3 * (E + 1) > LDS_INTS) {
-    seg += 64;
-    nseg = std::max<int64_t>(1, (Pr + seg - 1) / seg);
-  }
+  const int64_t nseg_max = std::max<int64_t>(1, LDS_INTS / E);
+  const int64_t seg = std::max<int64_t>(64, ((Pr + nseg_max - 1) / nseg_max + 63) / 64 * 64);
+  const int64_t nseg = std::max<int64_t>(1, (Pr + seg - 1) / seg);
   ra.seg = (int)seg;
   ra.nseg = (int)nseg;
   ra.ebits = 0;
   while ((1 << ra.ebits) < E) ra.ebits++;
-  const size_t lds = sizeof(int) * ((size_t)E * ra.nseg + 3 * (E + 1));
-  route_kernel<<<dim3(1), dim3(ROUTE_T), lds, s>>>(ra);
+  const size_t lds = sizeof(int) * std::max<size_t>((size_t)E * ra.nseg, 3 * (E + 1));
+  // every wave's chunks fit the register arrays: at most RCH per wave
+  if ((ra.nseg + 15) / 16 * (seg / 64) <= RCH)
+    route_kernel<true><<<dim3(1), dim3(ROUTE_T), lds, s>>>(ra);
+  else
+    route_kernel<false><<<dim3(1), dim3(ROUTE_T), lds, s>>>(ra);
   if ((rc = check_launch()) != W4A8_OK) return rc;
 
   uint8_t *hq = ws + L.hq;

@@ -345,6 +345,23 @@ def test_moe_mfma_path_shapes(seed, H, I, E, shared, T, k):
     L.check(x, ids, wts, k, out, h, hq)
 
 
+def test_moe_route_4096_experts():
+    """The largest expert count the library accepts: the route kernel's
+    histogram then holds one segment per expert and the group counters reuse
+    its space.  Tokens spread over few experts so some groups reach the MFMA
+    tiles."""
+    L = Layer(44, 256, 256, 4096)
+    g = synth.rng(144)
+    T, k = 96, 3
+    x = synth.normal_f32(g, (T, L.H))
+    ids, wts = synth.routing(g, T, L.E, k)
+    ids[:40, 0] = 4095                   # one group of 40 rows (MFMA)
+    ids[40:52, 1] = 17                   # one of 12 (MFMA) beside single rows
+    out, h, hq, perm, count, _ = L.run(x, ids, wts, k)
+    _check_route(ids, L.E, True, perm, count)
+    L.check(x, ids, wts, k, out, h, hq)
+
+
 def test_moe_prefill_947_sampled_tokens(qwen_layer):
     L = qwen_layer
     g = synth.rng(22)
