@@ -338,12 +338,11 @@ __device__ __forceinline__ void stage_word(ActBuf hb, int blk, int w, uint32_t v
 
 // Collect hand-off words [0, cnt) of the valid pairs into the staging (word
 // i is word i % XW of block i / XW); lane takes the words
-// threadIdx.x + j * NT, j < NWMAX.  One barrier per round:
-// a wave with words still missing sets notdone[round % 3] before it, everyone
-// reads it after, and thread 0 clears the slot of round + 2, which nobody
-// reads or writes until after the next barrier.  The round count is the same
-// in every wave, so the bound needs no broadcast.  Returns false (uniformly)
-// when the bound passed first; notdone[] must be zero on entry.
+// threadIdx.x + j * NT, j < NWMAX.  Every wave polls its own words with two
+// rounds of loads in flight (a word seen twice is staged twice, with the same
+// value) and no barrier between rounds; a wave that passes the round bound
+// sets notdone[0].  One barrier at the end; returns false (uniformly) when
+// some wave passed the bound.  notdone[0] must be zero on entry.
 constexpr int NWMAX = 8;
 __device__ bool collect(const DecodeArgs &a, ActBuf hb, uint32_t tag, int cnt, uint64_t vmask,
                         int *notdone) {
@@ -357,11 +356,12 @@ __device__ bool collect(const DecodeArgs &a, ActBuf hb, uint32_t tag, int cnt, u
     w[j] = i - blk[j] * XW;
     if (i < cnt && ((vmask >> (blk[j] / nb_h)) & 1)) pending |= 1u << j;
   }
-  for (int it = 0;; it++) {
-    uint64_t v[NWMAX];
+  auto issue = [&](uint64_t (&v)[NWMAX]) {
 #pragma unroll
     for (int j = 0; j < NWMAX; j++)
       v[j] = ((pending >> j) & 1) ? ld_agent64(a.xfer + (int64_t)blk[j] * XSTRIDE + w[j]) : 0;
+  };
+  auto take = [&](const uint64_t (&v)[NWMAX]) {
 #pragma unroll
     for (int j = 0; j < NWMAX; j++) {
       if (((pending >> j) & 1) && (uint32_t)(v[j] >> 32) == tag) {
@@ -369,13 +369,16 @@ __device__ bool collect(const DecodeArgs &a, ActBuf hb, uint32_t tag, int cnt, u
         pending &= ~(1u << j);
       }
     }
-    const int slot = it % 3;
-    if (__ballot(pending != 0) != 0 && (threadIdx.x & 63) == 0) notdone[slot] = 1;
-    __syncthreads();
-    if (notdone[slot] == 0) return true;
-    if (threadIdx.x == 0) notdone[(it + 2) % 3] = 0;
-    if (it >= a.spin_rounds) return false;
+    return __ballot(pending != 0) == 0;         // this wave has all its words
+  };
+  uint64_t va[NWMAX];
+  for (int it = 0;; it++) {
+    issue(va);
+    if (take(va)) break;
+    if (it + 1 > a.spin_rounds) { if ((threadIdx.x & 63) == 0) notdone[0] = 1; break; }
   }
+  __syncthreads();
+  return notdone[0] == 0;
 }
 
 // LDS: Q8_0(x) staging, then Q8_0(h) staging of every pair, then the
