@@ -8,7 +8,8 @@
 //      (plus the copies the grouped kernels read: nibble-split, aligned)
 //   2. route: stable counting sort of the T*k pairs by expert (plus the T
 //      shared pairs), the list of non-empty expert groups, the chunks of the
-//      small groups and the row tiles of the others
+//      small groups and the row tiles of the others (one workgroup, in the
+//      same launch as stage 1)
 //   3. gate/up: per (row tile, 64 h columns) the gate and up rows of the
 //      expert against the tile's token rows, SwiGLU, Q8_0 of the 32-wide h
 //      blocks (mfma.hip)                               -> workspace h, hq
@@ -26,8 +27,6 @@
 namespace w4a8 {
 
 int launch_fill_zero(void *ptr, size_t bytes, hipStream_t s);
-int launch_q8_0_ex(const float *x, uint8_t *xq, SplitBlk *xs, uint32_t *xa, float *xd,
-                   int64_t nblocks, hipStream_t s);
 bool small_supported(int64_t H, int64_t I);
 int64_t small_max_chunks(int64_t T, int64_t E, int64_t k, int has_shared);
 int small_gateup(const uint8_t *w_gu, const uint8_t *ws_gu, const SplitBlk *xs,
@@ -120,6 +119,14 @@ int validate(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k) {
 }
 
 // ------------------------------------------------------------------ route
+// Workgroup barrier that orders LDS only: unlike __syncthreads it does not
+// wait for this wave's global stores (the route kernel's count and
+// permutation stores), which nothing in the workgroup reads back (the
+// workspace ranks of the path without register ranks use __syncthreads).
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 // Exclusive scans of NA arrays a[j][0..n) in LDS at once by all ROUTE_T
 // threads; tot[j] receives the total of array j.
 template <int NA>
@@ -146,20 +153,29 @@ __device__ void block_exscan(int *const (&a)[NA], int n, int (*wtot)[ROUTE_T / 6
   if (lane == 63)
 #pragma unroll
     for (int j = 0; j < NA; j++) wtot[j][wave] = x[j];
-  __syncthreads();
-  if (tid < NA) {
-    int run = 0;
-    for (int w = 0; w < ROUTE_T / 64; w++) { const int v = wtot[tid][w]; wtot[tid][w] = run; run += v; }
-    wtot[tid][ROUTE_T / 64] = run;
+  lds_barrier();
+  // the wave totals: exclusive scan by the first wave, 16 lanes per array
+  constexpr int NW = ROUTE_T / 64;
+  if (tid < NA * NW) {
+    const int j = tid / NW, w = tid - j * NW;
+    const int v = wtot[j][w];
+    int c = v;
+#pragma unroll
+    for (int o = 1; o < NW; o <<= 1) {
+      const int y = __shfl_up(c, o, NW);
+      if (w >= o) c += y;
+    }
+    wtot[j][w] = c - v;
+    if (w == NW - 1) wtot[j][NW] = c;
   }
-  __syncthreads();
+  lds_barrier();
 #pragma unroll
   for (int j = 0; j < NA; j++) {
     int base = wtot[j][wave] + x[j] - s[j];
     for (int i = lo; i < hi; i++) { const int v = a[j][i]; a[j][i] = base; base += v; }
     tot[j] = wtot[j][ROUTE_T / 64];
   }
-  __syncthreads();
+  lds_barrier();
 }
 
 constexpr int RCH = 16;   // chunks of 64 pairs a wave keeps in registers
@@ -174,6 +190,7 @@ struct RouteArgs {
                     // rows: {expert, first sorted position, rows, group}, in
                     // reverse group order
   int T, k, E, has_shared, seg, nseg, ebits, ms;
+  int stage;        // REG path: the permutation goes through LDS (it fits)
 };
 
 // Rank of this lane's pair among the earlier pairs of the same expert in its
@@ -209,7 +226,7 @@ __device__ __forceinline__ int chunk_rank(int e, int s, int *hist, const RouteAr
 // the ranks stay in registers until the scatter (otherwise they go through
 // the workspace).
 template <bool REG>
-__global__ __launch_bounds__(ROUTE_T) void route_kernel(RouteArgs a) {
+__device__ __forceinline__ void route_body(const RouteArgs &a) {
   extern __shared__ int hist[];  // [E][nseg], later the group counters
   __shared__ int wtot[3][ROUTE_T / 64 + 1];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -230,7 +247,7 @@ __global__ __launch_bounds__(ROUTE_T) void route_kernel(RouteArgs a) {
       er[i] = (live && e >= 0 && e < a.E) ? e : -1;
     }
   }
-  __syncthreads();
+  lds_barrier();
 
   if (REG) {
 #pragma unroll
@@ -253,7 +270,11 @@ __global__ __launch_bounds__(ROUTE_T) void route_kernel(RouteArgs a) {
       }
     }
   }
-  __syncthreads();
+  // the workspace ranks are read back by other threads in the scatter
+  if (REG)
+    lds_barrier();
+  else
+    __syncthreads();
   int nrouted;
   {
     int *const arr[1] = {hist};
@@ -262,12 +283,17 @@ __global__ __launch_bounds__(ROUTE_T) void route_kernel(RouteArgs a) {
     nrouted = tot[0];
   }
 
+  // sorted position of each register-held pair; written straight to the
+  // workspace, or (stage) through LDS so that the permutation leaves in
+  // coalesced stores
+  int dst[RCH];
   if (REG) {
 #pragma unroll
     for (int i = 0; i < RCH; i++) {
       const int j = i / cps, sg = wave + 16 * j;
       const int p = sg * a.seg + 64 * (i - j * cps) + lane;
-      if (er[i] >= 0) a.perm[hist[er[i] * a.nseg + sg] + rr[i]] = p;
+      dst[i] = er[i] >= 0 ? hist[er[i] * a.nseg + sg] + rr[i] : -1;
+      if (!a.stage && dst[i] >= 0) a.perm[dst[i]] = p;
     }
   } else {
     for (int p = tid; p < Pr; p += ROUTE_T) {
@@ -276,7 +302,7 @@ __global__ __launch_bounds__(ROUTE_T) void route_kernel(RouteArgs a) {
       a.perm[hist[e * a.nseg + p / a.seg] + a.rank[p]] = p;
     }
   }
-  if (a.has_shared)
+  if (a.has_shared && !a.stage)
     for (int t = tid; t < a.T; t += ROUTE_T) a.perm[nrouted + t] = Pr + t;
 
   // counts, then the compacted list of non-empty groups (expert order); a
@@ -299,8 +325,20 @@ __global__ __launch_bounds__(ROUTE_T) void route_kernel(RouteArgs a) {
       grw[j] = a.has_shared ? a.T : 0;
     }
   }
-  __syncthreads();
-  int *gflag = hist;             // 3 x (E + 1) entries
+  lds_barrier();
+  if (REG && a.stage) {
+#pragma unroll
+    for (int i = 0; i < RCH; i++) {
+      const int j = i / cps, sg = wave + 16 * j;
+      if (dst[i] >= 0) hist[dst[i]] = sg * a.seg + 64 * (i - j * cps) + lane;
+    }
+    if (a.has_shared)
+      for (int t = tid; t < a.T; t += ROUTE_T) hist[nrouted + t] = Pr + t;
+    lds_barrier();
+    const int ptot = nrouted + (a.has_shared ? a.T : 0);
+    for (int i = tid; i < ptot; i += ROUTE_T) a.perm[i] = hist[i];
+  }
+  int *gflag = hist + (a.stage ? Pr + a.T : 0);   // 3 x (E + 1) entries
   int *gtile = gflag + a.E + 1;
   int *gsmall = gtile + a.E + 1;
 #pragma unroll
@@ -311,7 +349,7 @@ __global__ __launch_bounds__(ROUTE_T) void route_kernel(RouteArgs a) {
     gsmall[e] = (rows > 0 && rows <= a.ms) ? (rows + SMALL_CHUNK - 1) / SMALL_CHUNK : 0;
     gtile[e] = rows > a.ms ? (rows + MC - 1) / MC : 0;
   }
-  __syncthreads();
+  lds_barrier();
   int tot[3];
   {
     int *const arr[3] = {gflag, gtile, gsmall};
@@ -340,6 +378,27 @@ __global__ __launch_bounds__(ROUTE_T) void route_kernel(RouteArgs a) {
     a.meta[META_NTILES] = ntiles;
     a.meta[META_NSMALL] = nsmall;
   }
+}
+
+struct Q8Args {
+  const float *x;
+  uint8_t *xq;
+  SplitBlk *xs;     // nibble-split copy (small-group kernels), or null
+  uint32_t *xa;     // aligned codes and fp32 scales (MFMA kernels), or null
+  float *xd;
+  int64_t nblocks;
+};
+
+// Stages 1 and 2 in one launch (they are independent): workgroup 0 routes,
+// the others quantize the hidden rows, ROUTE_T / 8 blocks each.
+template <bool REG>
+__global__ __launch_bounds__(ROUTE_T) void prep_kernel(RouteArgs a, Q8Args q) {
+  if (blockIdx.x == 0) {
+    route_body<REG>(a);
+    return;
+  }
+  q8_0_lane(q.x, q.xq, q.xs, q.xa, q.xd, q.nblocks,
+            (int64_t)(blockIdx.x - 1) * ROUTE_T + threadIdx.x);
 }
 
 // out[t] = sum_j y[t*k + j] (slots in order, skipped slots left out) + y[T*k + t].
@@ -401,9 +460,13 @@ int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
   uint32_t *ha = reinterpret_cast<uint32_t *>(ws + L.ha);
   float *xd = reinterpret_cast<float *>(ws + L.xd);
   float *hd = reinterpret_cast<float *>(ws + L.hd);
-  if ((rc = launch_q8_0_ex(hidden, ws + L.xq, ms > 0 ? xs : nullptr, tiles ? xa : nullptr, xd,
-                           T * (H / QK), s)) != W4A8_OK)
-    return rc;
+  Q8Args qa;
+  qa.x = hidden;
+  qa.xq = ws + L.xq;
+  qa.xs = ms > 0 ? xs : nullptr;
+  qa.xa = tiles ? xa : nullptr;
+  qa.xd = xd;
+  qa.nblocks = T * (H / QK);
 
   RouteArgs ra;
   ra.ids = ids;
@@ -424,12 +487,16 @@ int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
   ra.nseg = (int)nseg;
   ra.ebits = 0;
   while ((1 << ra.ebits) < E) ra.ebits++;
-  const size_t lds = sizeof(int) * std::max<size_t>((size_t)E * ra.nseg, 3 * (E + 1));
   // every wave's chunks fit the register arrays: at most RCH per wave
-  if ((ra.nseg + 15) / 16 * (seg / 64) <= RCH)
-    route_kernel<true><<<dim3(1), dim3(ROUTE_T), lds, s>>>(ra);
+  const bool reg = (ra.nseg + 15) / 16 * (seg / 64) <= RCH;
+  ra.stage = reg && Pr + T + 3 * (E + 1) <= LDS_INTS;
+  const size_t lds = sizeof(int) * std::max<size_t>((size_t)E * ra.nseg,
+                                                    (ra.stage ? Pr + T : 0) + 3 * (E + 1));
+  const unsigned grid = (unsigned)(1 + (qa.nblocks * 8 + ROUTE_T - 1) / ROUTE_T);
+  if (reg)
+    prep_kernel<true><<<dim3(grid), dim3(ROUTE_T), lds, s>>>(ra, qa);
   else
-    route_kernel<false><<<dim3(1), dim3(ROUTE_T), lds, s>>>(ra);
+    prep_kernel<false><<<dim3(grid), dim3(ROUTE_T), lds, s>>>(ra, qa);
   if ((rc = check_launch()) != W4A8_OK) return rc;
 
   uint8_t *hq = ws + L.hq;

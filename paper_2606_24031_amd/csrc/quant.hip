@@ -11,42 +11,13 @@
 
 namespace w4a8 {
 
-// 8 lanes per block.  With SPLIT also the nibble-split copy of each block
-// (small-group kernels); with ALIGNED also its 32 codes on a 32-byte boundary
-// and its fp32 scale (grouped MFMA kernels).
-template <bool SPLIT, bool ALIGNED>
+// 8 lanes per block (q8_0_lane); xs and xa may be null.
 __global__ __launch_bounds__(256) void q8_0_kernel(const float *__restrict__ x,
                                                    uint8_t *__restrict__ xq,
                                                    SplitBlk *__restrict__ xs,
                                                    uint32_t *__restrict__ xa,
                                                    float *__restrict__ xd, int64_t nblocks) {
-  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t blk = tid >> 3;
-  const int j = (int)(tid & 7);
-  float v[4] = {0.f, 0.f, 0.f, 0.f};
-  const bool live = blk < nblocks;
-  if (live) {
-    const float4 t = reinterpret_cast<const float4 *>(x + blk * QK)[j];
-    v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
-  }
-  uint32_t d16;
-  const uint32_t packed = q8_0_block8(v, d16);
-  if (live) store_q8_0_block8(xq + blk * Q8B, j, packed, d16);
-  if (SPLIT) {
-    const uint32_t word = split_word(packed, j);
-    const int lsum = sum8(low_nibble_sum(packed));
-    if (live) {
-      xs[blk].w[j] = word;
-      if (j == 0) {
-        xs[blk].d = f16_bits_to_f32(d16);
-        xs[blk].corr = -8 * lsum;
-      }
-    }
-  }
-  if (ALIGNED && live) {
-    xa[blk * 8 + j] = packed;
-    if (j == 0) xd[blk] = f16_bits_to_f32(d16);
-  }
+  q8_0_lane(x, xq, xs, xa, xd, nblocks, (int64_t)blockIdx.x * blockDim.x + threadIdx.x);
 }
 
 __global__ __launch_bounds__(256) void q4_0_kernel(const float *__restrict__ w,
@@ -119,26 +90,8 @@ int launch_fill_zero(void *ptr, size_t bytes, hipStream_t s) {
 int launch_q8_0(const float *x, uint8_t *xq, int64_t nblocks, hipStream_t s) {
   if (nblocks == 0) return W4A8_OK;
   const int64_t grid = (nblocks * 8 + 255) / 256;
-  q8_0_kernel<false, false><<<dim3((unsigned)grid), dim3(256), 0, s>>>(x, xq, nullptr, nullptr,
-                                                                        nullptr, nblocks);
-  return check_launch();
-}
-
-// Q8_0 with the extra copies the grouped kernels read: the nibble-split form
-// (xs) and/or the aligned codes and scales (xa, xd); either may be null.
-int launch_q8_0_ex(const float *x, uint8_t *xq, SplitBlk *xs, uint32_t *xa, float *xd,
-                   int64_t nblocks, hipStream_t s) {
-  if (nblocks <= 0) return W4A8_OK;
-  const int64_t grid = (nblocks * 8 + 255) / 256;
-  const dim3 g((unsigned)grid), b(256);
-  if (xs && xa)
-    q8_0_kernel<true, true><<<g, b, 0, s>>>(x, xq, xs, xa, xd, nblocks);
-  else if (xs)
-    q8_0_kernel<true, false><<<g, b, 0, s>>>(x, xq, xs, nullptr, nullptr, nblocks);
-  else if (xa)
-    q8_0_kernel<false, true><<<g, b, 0, s>>>(x, xq, nullptr, xa, xd, nblocks);
-  else
-    q8_0_kernel<false, false><<<g, b, 0, s>>>(x, xq, nullptr, nullptr, nullptr, nblocks);
+  q8_0_kernel<<<dim3((unsigned)grid), dim3(256), 0, s>>>(x, xq, nullptr, nullptr, nullptr,
+                                                          nblocks);
   return check_launch();
 }
 

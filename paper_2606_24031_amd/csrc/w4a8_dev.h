@@ -285,4 +285,40 @@ __device__ __forceinline__ void store_q8_0_block8(uint8_t *blk, int j, uint32_t 
   if (j == 0) *reinterpret_cast<uint16_t *>(blk) = (uint16_t)d16;
 }
 
+// Q8_0 of one 32-element block of x by 8 lanes (thread tid: block tid / 8,
+// elements 4 (tid % 8) .. + 3): the 34-byte block, and when the pointers are
+// set its nibble-split form (xs) and its 32 codes on a 32-byte boundary with
+// the fp32 scale (xa, xd).  Lanes past nblocks take part in the exchanges and
+// store nothing.
+__device__ __forceinline__ void q8_0_lane(const float *__restrict__ x, uint8_t *__restrict__ xq,
+                                          SplitBlk *__restrict__ xs, uint32_t *__restrict__ xa,
+                                          float *__restrict__ xd, int64_t nblocks, int64_t tid) {
+  const int64_t blk = tid >> 3;
+  const int j = (int)(tid & 7);
+  float v[4] = {0.f, 0.f, 0.f, 0.f};
+  const bool live = blk < nblocks;
+  if (live) {
+    const float4 t = reinterpret_cast<const float4 *>(x + blk * QK)[j];
+    v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+  }
+  uint32_t d16;
+  const uint32_t packed = q8_0_block8(v, d16);
+  if (live) store_q8_0_block8(xq + blk * Q8B, j, packed, d16);
+  if (xs) {
+    const uint32_t word = split_word(packed, j);
+    const int lsum = sum8(low_nibble_sum(packed));
+    if (live) {
+      xs[blk].w[j] = word;
+      if (j == 0) {
+        xs[blk].d = f16_bits_to_f32(d16);
+        xs[blk].corr = -8 * lsum;
+      }
+    }
+  }
+  if (xa && live) {
+    xa[blk * 8 + j] = packed;
+    if (j == 0) xd[blk] = f16_bits_to_f32(d16);
+  }
+}
+
 }  // namespace w4a8
