@@ -119,14 +119,6 @@ int validate(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k) {
 }
 
 // ------------------------------------------------------------------ route
-// Workgroup barrier that orders LDS only: unlike __syncthreads it does not
-// wait for this wave's global stores (the route kernel's count and
-// permutation stores), which nothing in the workgroup reads back (the
-// workspace ranks of the path without register ranks use __syncthreads).
-__device__ __forceinline__ void lds_barrier() {
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
-
 // Exclusive scans of NA arrays a[j][0..n) in LDS at once by all ROUTE_T
 // threads; tot[j] receives the total of array j.
 template <int NA>
@@ -153,7 +145,7 @@ __device__ void block_exscan(int *const (&a)[NA], int n, int (*wtot)[ROUTE_T / 6
   if (lane == 63)
 #pragma unroll
     for (int j = 0; j < NA; j++) wtot[j][wave] = x[j];
-  lds_barrier();
+  __syncthreads();
   // the wave totals: exclusive scan by the first wave, 16 lanes per array
   constexpr int NW = ROUTE_T / 64;
   if (tid < NA * NW) {
@@ -168,14 +160,14 @@ __device__ void block_exscan(int *const (&a)[NA], int n, int (*wtot)[ROUTE_T / 6
     wtot[j][w] = c - v;
     if (w == NW - 1) wtot[j][NW] = c;
   }
-  lds_barrier();
+  __syncthreads();
 #pragma unroll
   for (int j = 0; j < NA; j++) {
     int base = wtot[j][wave] + x[j] - s[j];
     for (int i = lo; i < hi; i++) { const int v = a[j][i]; a[j][i] = base; base += v; }
     tot[j] = wtot[j][ROUTE_T / 64];
   }
-  lds_barrier();
+  __syncthreads();
 }
 
 constexpr int RCH = 16;   // chunks of 64 pairs a wave keeps in registers
@@ -247,7 +239,7 @@ __device__ __forceinline__ void route_body(const RouteArgs &a) {
       er[i] = (live && e >= 0 && e < a.E) ? e : -1;
     }
   }
-  lds_barrier();
+  __syncthreads();
 
   if (REG) {
 #pragma unroll
@@ -270,11 +262,7 @@ __device__ __forceinline__ void route_body(const RouteArgs &a) {
       }
     }
   }
-  // the workspace ranks are read back by other threads in the scatter
-  if (REG)
-    lds_barrier();
-  else
-    __syncthreads();
+  __syncthreads();
   int nrouted;
   {
     int *const arr[1] = {hist};
@@ -325,7 +313,7 @@ __device__ __forceinline__ void route_body(const RouteArgs &a) {
       grw[j] = a.has_shared ? a.T : 0;
     }
   }
-  lds_barrier();
+  __syncthreads();
   if (REG && a.stage) {
 #pragma unroll
     for (int i = 0; i < RCH; i++) {
@@ -334,7 +322,7 @@ __device__ __forceinline__ void route_body(const RouteArgs &a) {
     }
     if (a.has_shared)
       for (int t = tid; t < a.T; t += ROUTE_T) hist[nrouted + t] = Pr + t;
-    lds_barrier();
+    __syncthreads();
     const int ptot = nrouted + (a.has_shared ? a.T : 0);
     for (int i = tid; i < ptot; i += ROUTE_T) a.perm[i] = hist[i];
   }
@@ -349,7 +337,7 @@ __device__ __forceinline__ void route_body(const RouteArgs &a) {
     gsmall[e] = (rows > 0 && rows <= a.ms) ? (rows + SMALL_CHUNK - 1) / SMALL_CHUNK : 0;
     gtile[e] = rows > a.ms ? (rows + MC - 1) / MC : 0;
   }
-  lds_barrier();
+  __syncthreads();
   int tot[3];
   {
     int *const arr[3] = {gflag, gtile, gsmall};
