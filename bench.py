@@ -246,6 +246,38 @@ def bench_m32(torch, w4, synth, layers, args, dev):
             "hbm_peak_frac": round(gbps / HBM_PEAK_GBPS, 4), "calls": n}
 
 
+def bench_router(torch, w4, synth, args, dev):
+    """Router top-k on fp32 logits ~ N(0,1) (plus the per-expert bias for the
+    947-token case): 947 tokens and 1 token, E = 256, k = 8."""
+    res = {}
+    for T, bias in ((947, 1.0), (1, 0.0)):
+        g = synth.rng(args.seed + 7)
+        b = synth.normal_f32(g, (E,), bias) if bias > 0 else 0.0
+        logits = torch.from_numpy(synth.normal_f32(g, (T, E)) + b).to(dev)
+        ids = torch.empty((T, K_TOP), dtype=torch.int32, device=dev)
+        wts = torch.empty((T, K_TOP), dtype=torch.float32, device=dev)
+        n = 200
+        for _ in range(5):
+            w4.router_topk(logits, K_TOP, ids, wts)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for _ in range(n):
+                w4.router_topk(logits, K_TOP, ids, wts)
+        graph.replay()
+        torch.cuda.synchronize()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        ev0.record()
+        graph.replay()
+        ev1.record()
+        torch.cuda.synchronize()
+        us = ev0.elapsed_time(ev1) / n * 1e3
+        res[f"T{T}"] = {"us_per_call": round(us, 2), "tokens_per_s": round(T / (us / 1e6), 1),
+                        "launch": "hipGraph"}
+    return res
+
+
 def bench_stack(torch, w4, synth, args, dev):
     """40 chained pre-norm residual layers (x <- x + MoE_l(RMSNorm_l(x)), one
     moe_w4a8_layer call each, the residual add and norm fused into the layer
@@ -414,6 +446,9 @@ def main():
         m32 = bench_m32(torch, w4, synth, layers, args, dev)
         log(f"decode M=32: {m32}")
 
+    router = bench_router(torch, w4, synth, args, dev)
+    log(f"router top-k: {router}")
+
     stack = None
     if not args.no_stack:
         del layers
@@ -455,6 +490,7 @@ def main():
         "prefill_947": prefill,
         "decode_m32": m32,
         "stack_40": stack,
+        "router_topk": router,
     }
     print(json.dumps(rec), flush=True)
 

@@ -138,6 +138,28 @@ int moe_w4a8_workspace_layout(int64_t T, int64_t H, int64_t I, int64_t E, int64_
                               size_t *offsets);
 
 /*
+ * Router top-k (Sec. 2.2: the sparsely gated MoE layer sends each token to
+ * its top-k of E routed experts; the k gate values are the softmax
+ * probabilities renormalized over the selection, as the Qwen3-series models
+ * of Sec. 2.2 do).  Per token t of logits [T][E] fp32 (finite values):
+ *   ids[t][0..k)   the k largest logits in descending order, equal logits
+ *                  in increasing expert index.  Softmax is monotone, so this
+ *                  is the order of the probabilities; it is decided on the
+ *                  fp32 logits themselves, with no rounding in between.
+ *   weights[t][j]  exp(l_j - l_max) / sum over the selection of
+ *                  exp(l_i - l_max): the softmax over E restricted to the
+ *                  selection and renormalized (its full denominator
+ *                  cancels).  fp32, within a few ulps of the exact value.
+ *   ids [T][k] int32 and weights [T][k] fp32 are overwritten; they feed
+ *   moe_w4a8_forward / moe_w4a8_layer directly.
+ * NULL pointer -> W4A8_ENULL; a pointer not 4-byte aligned -> W4A8_EALIGN;
+ * T < 0 -> W4A8_ESHAPE; E < 1, E > 4096, k < 1, k > 32, k > E or
+ * T >= 2^31 -> W4A8_ERANGE.  T == 0 is a no-op.
+ */
+int moe_router_topk(const float *logits, int32_t *ids, float *weights, int64_t T, int64_t E,
+                    int64_t k, void *stream);
+
+/*
  * One routed + shared MoE feed-forward layer in W4A8 (Sec. 2.2: top-k routed
  * experts plus an always-on shared expert; Sec. 3.2: one grouped pass over
  * all routed token-expert pairs; Sec. 3.3: W4A8 integer products):

@@ -66,6 +66,7 @@ def _load():
     lib.orc_q8_0_candidates.restype = ctypes.c_int
     lib.orc_threads.restype = ctypes.c_int
     lib.orc_rmsnorm_residual.argtypes = [P, P, P, P, P, I64, I64, ctypes.c_double]
+    lib.orc_router_topk.argtypes = [P, P, P, I64, I64, I64, P]
     _lib = lib
     return lib
 
@@ -209,6 +210,19 @@ def rmsnorm_residual(x, y, gamma, eps: float = 1e-6, want_norm: bool = True):
     _load().orc_rmsnorm_residual(_ptr(x), _ptr(y), _ptr(gamma), _ptr(x_out), _ptr(xn), T, H,
                                  float(eps))
     return x_out, xn
+
+
+def router_topk(logits: np.ndarray, k: int):
+    """Router top-k of fp32 logits [T, E] (see orc_router_topk): ids int32
+    [T, k] in descending logit order (equal logits by increasing index) and
+    the renormalized softmax weights fp64 [T, k]."""
+    logits = _c(logits, np.float32)
+    T, E = logits.shape
+    ids = np.zeros((T, k), dtype=np.int32)
+    w = np.zeros((T, k), dtype=np.float64)
+    taken = np.zeros(E, dtype=np.uint8)
+    _load().orc_router_topk(_ptr(logits), _ptr(ids), _ptr(w), T, E, k, _ptr(taken))
+    return ids, w
 
 
 def q8_0_candidates(h: np.ndarray, dh: np.ndarray):

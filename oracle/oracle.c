@@ -444,6 +444,38 @@ void orc_rmsnorm_residual(const float *x, const float *y, const float *gamma, fl
     }
 }
 
+/* ------------------------------------------------------------------ */
+/* Router top-k (Sec. 2.2: each token goes to its top-k routed experts). */
+/* ------------------------------------------------------------------ */
+
+/* Per token t of logits [T][E]: k times, the largest logit not yet taken
+ * (scanning in index order and keeping the first of equal values, so equal
+ * logits go in increasing index) -> ids[t][j].  Softmax is monotone, so this
+ * is the order of the probabilities.  weights[t][j] = the softmax
+ * probability of ids[t][j] divided by the sum of the selected
+ * probabilities, evaluated in fp64 as exp(l_j - l_max) / sum over the
+ * selection of exp(l_i - l_max).  taken: E bytes of scratch. */
+void orc_router_topk(const float *logits, int32_t *ids, double *weights, int64_t T, int64_t E,
+                     int64_t k, unsigned char *taken)
+{
+    for (int64_t t = 0; t < T; t++) {
+        const float *l = logits + t * E;
+        memset(taken, 0, (size_t)E);
+        for (int64_t j = 0; j < k; j++) {
+            int64_t best = -1;
+            for (int64_t e = 0; e < E; e++)
+                if (!taken[e] && (best < 0 || l[e] > l[best])) best = e;
+            taken[best] = 1;
+            ids[t * k + j] = (int32_t)best;
+        }
+        const double lmax = (double)l[ids[t * k]];
+        double sum = 0.0;
+        for (int64_t j = 0; j < k; j++) sum += exp((double)l[ids[t * k + j]] - lmax);
+        for (int64_t j = 0; j < k; j++)
+            weights[t * k + j] = exp((double)l[ids[t * k + j]] - lmax) / sum;
+    }
+}
+
 /* Number of OpenMP threads the parallel loops above use. */
 int orc_threads(void)
 {

@@ -23,7 +23,7 @@ WS_NFIELDS = 8
 EXPORTS = ("w4a8_strerror", "q8_0_quantize", "q4_0_quantize", "q4q8_gemv",
            "moe_w4a8_workspace_size", "moe_w4a8_workspace_init",
            "moe_w4a8_workspace_layout", "moe_w4a8_forward", "moe_w4a8_layer",
-           "rmsnorm_residual")
+           "rmsnorm_residual", "moe_router_topk")
 
 _lib = None
 
@@ -64,6 +64,8 @@ def lib() -> ctypes.CDLL:
     L.moe_w4a8_layer.restype = ctypes.c_int
     L.rmsnorm_residual.argtypes = [P, P, P, P, P, I64, I64, ctypes.c_float, P]
     L.rmsnorm_residual.restype = ctypes.c_int
+    L.moe_router_topk.argtypes = [P, P, P, I64, I64, I64, P]
+    L.moe_router_topk.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -123,6 +125,22 @@ def q4q8_gemv(w, xq, N, K, y=None, stream=None):
         y = torch.empty(N, dtype=torch.float32, device=w.device)
     _check(lib().q4q8_gemv(_p(_u8(w)), _p(_u8(xq)), _p(y), N, K, _stream(stream)), "q4q8_gemv")
     return y
+
+
+def router_topk(logits, k, ids=None, weights=None, stream=None):
+    """Top-k of fp32 logits [T, E] (descending, equal logits by increasing
+    index) and the softmax weights renormalized over the selection; returns
+    (ids int32 [T, k], weights fp32 [T, k])."""
+    import torch
+    assert logits.dtype == torch.float32 and logits.is_contiguous() and logits.dim() == 2
+    T, E = logits.shape
+    if ids is None:
+        ids = torch.empty((T, k), dtype=torch.int32, device=logits.device)
+    if weights is None:
+        weights = torch.empty((T, k), dtype=torch.float32, device=logits.device)
+    _check(lib().moe_router_topk(_p(logits), _p(ids), _p(weights), T, E, k, _stream(stream)),
+           "moe_router_topk")
+    return ids, weights
 
 
 def moe_workspace_size(T, H, I, E, k) -> int:

@@ -136,3 +136,19 @@ def test_moe_layer_argument_errors():
     assert call(out=yp) == w4.EALIAS
     assert call(ws_bytes=need - 1) == w4.EWORKSPACE
     assert call(T=0) == w4.OK                                         # empty: no-op
+
+
+def test_router_argument_errors():
+    f = w4.lib().moe_router_topk
+    p = _fake(A)
+    assert f(None, p, p, 4, 256, 8, None) == w4.ENULL
+    assert f(p, p, None, 4, 256, 8, None) == w4.ENULL
+    assert f(p, p, p, -1, 256, 8, None) == w4.ESHAPE
+    assert f(p, p, p, 4, 0, 1, None) == w4.ERANGE          # E < 1
+    assert f(p, p, p, 4, 4097, 8, None) == w4.ERANGE       # E > 4096
+    assert f(p, p, p, 4, 256, 0, None) == w4.ERANGE        # k < 1
+    assert f(p, p, p, 4, 256, 33, None) == w4.ERANGE       # k > 32
+    assert f(p, p, p, 4, 6, 7, None) == w4.ERANGE          # k > E
+    assert f(p, p, p, 1 << 31, 256, 8, None) == w4.ERANGE
+    assert f(p, _fake(A + 2), p, 4, 256, 8, None) == w4.EALIGN
+    assert f(p, p, p, 0, 256, 8, None) == w4.OK            # empty: no-op

@@ -440,3 +440,39 @@ def test_moe_layer_residual_norm(qwen_layer, T, with_prev):
     h = wsn[lay["h"]:lay["h"] + P * L.I * 4].view(np.float32).reshape(P, L.I)
     hq = wsn[lay["hq"]:lay["hq"] + P * (L.I // 32) * 34].reshape(P, -1)
     L.check(xn, ids, wts, 8, host(out), h, hq)
+
+
+# ------------------------------------------------------------ router top-k
+@pytest.mark.parametrize("T,E,k", [(1, 256, 8), (947, 256, 8), (5, 7, 7), (33, 4096, 32),
+                                   (64, 64, 1), (3, 130, 32), (2, 10, 4)])
+def test_router_topk_matches_oracle(T, E, k):
+    """ids bit-exact (the selection compares the fp32 logits on both sides);
+    weights within 4e-6 relative: fp32 rounding of l - l_max (|l - l_max| of
+    at most ~10 here, 2^-24 each), of expf (2 ulp), of the k-term sum and of
+    the division."""
+    g = synth.rng(70 + T + E + k)
+    logits = synth.normal_f32(g, (T, E))
+    logits[0] = np.round(logits[0] * 2.0) / 2.0            # many equal logits
+    if E == 10:
+        logits[:] = 0.0                                    # all equal
+    ids, w = w4.router_topk(dev(logits), k)
+    ids_r, w_r = oracle.router_topk(logits, k)
+    assert np.array_equal(host(ids), ids_r)
+    err = np.abs(host(w).astype(np.float64) - w_r)
+    assert np.all(err <= 4e-6 * w_r), f"max rel err {np.max(err / w_r):.3g}"
+
+
+def test_router_output_feeds_the_layer(small_layer):
+    """The router's ids and weights drive a 40-token layer as given."""
+    L = small_layer
+    g = synth.rng(77)
+    T, k = 40, 2
+    x = synth.normal_f32(g, (T, L.H))
+    logits = synth.normal_f32(g, (T, L.E))
+    ids_d, w_d = w4.router_topk(dev(logits), k)
+    ids, wts = host(ids_d), host(w_d)
+    ids_r, _ = oracle.router_topk(logits, k)
+    assert np.array_equal(ids, ids_r)
+    out, h, hq, perm, count, _ = L.run(x, ids, wts, k)
+    _check_route(ids, L.E, True, perm, count)
+    L.check(x, ids, wts, k, out, h, hq)

@@ -2,6 +2,7 @@
 than itself -- a library routine (numpy's IEEE fp16 conversion, BLAS matmul),
 exact rational arithmetic, brute-force search over all codes, hand-built
 blocks (tests/golden/), closed forms and invariants.  CPU only."""
+import math
 import os
 from fractions import Fraction
 
@@ -448,3 +449,53 @@ def test_rmsnorm_residual_is_one_fp32_add():
     assert xo[0, 0] == np.float32(1.0)
     assert xo[0, 1] == np.float32(1.0 + 2.0 ** -22)
     assert xo[0, 2] == 0.0 and xo[0, 3] == 0.0
+
+
+# ------------------------------------------------------------------ router top-k
+def test_router_hand_example_with_tie():
+    """Logits [1, 3, 2, 3], k = 3: the two 3s first (lower index first), then
+    the 2; weights e^3 : e^3 : e^2 renormalized, i.e. 1 / (2 + e^-1) twice and
+    e^-1 / (2 + e^-1)."""
+    ids, w = oracle.router_topk(np.array([[1.0, 3.0, 2.0, 3.0]], np.float32), 3)
+    assert ids.tolist() == [[1, 3, 2]]
+    c = 2.0 + math.exp(-1.0)
+    assert np.allclose(w[0], [1.0 / c, 1.0 / c, math.exp(-1.0) / c], rtol=0, atol=1e-15)
+
+
+def test_router_matches_library_softmax_and_stable_sort():
+    """Against scipy's softmax over all E and numpy's stable argsort: the
+    selection is the top k of the probabilities (ties by index) and the
+    weights are those probabilities renormalized."""
+    from scipy.special import softmax
+    g = synth.rng(61)
+    for T, E, k in ((9, 256, 8), (5, 7, 7), (3, 130, 32), (4, 64, 1)):
+        logits = synth.normal_f32(g, (T, E))
+        logits[0, :] = np.round(logits[0, :])          # many equal logits in one row
+        ids, w = oracle.router_topk(logits, k)
+        p = softmax(logits.astype(np.float64), axis=1)
+        order = np.argsort(-logits.astype(np.float64), axis=1, kind="stable")[:, :k]
+        assert np.array_equal(ids, order)
+        ref = np.take_along_axis(p, order, axis=1)
+        ref /= ref.sum(axis=1, keepdims=True)
+        assert np.allclose(w, ref, rtol=1e-12, atol=0)
+
+
+def test_router_invariants_and_special_cases():
+    g = synth.rng(62)
+    logits = synth.normal_f32(g, (16, 256))
+    ids, w = oracle.router_topk(logits, 8)
+    assert np.allclose(w.sum(axis=1), 1.0, rtol=0, atol=1e-14)
+    for t in range(16):
+        assert len(set(ids[t].tolist())) == 8
+        sel = logits[t, ids[t]]
+        assert np.all(np.diff(sel) <= 0) and np.all(np.diff(w[t]) <= 0)
+        assert sel[-1] >= np.max(np.delete(logits[t], ids[t]))
+    # shift invariance (a power-of-two shift keeps the fp32 differences exact)
+    ids2, w2 = oracle.router_topk(logits + np.float32(4.0), 8)
+    assert np.array_equal(ids, ids2)
+    assert np.allclose(w, w2, rtol=1e-6, atol=0)
+    # equal logits: the first k experts, uniform weights; k = 1: weight 1
+    ids3, w3 = oracle.router_topk(np.zeros((2, 10), np.float32), 4)
+    assert ids3.tolist() == [[0, 1, 2, 3]] * 2 and np.all(w3 == 0.25)
+    ids4, w4 = oracle.router_topk(logits, 1)
+    assert np.array_equal(ids4[:, 0], np.argmax(logits, axis=1)) and np.all(w4 == 1.0)
