@@ -217,6 +217,27 @@ int moe_w4a8_layer(const float *x, const float *y_prev, const float *gamma, floa
                    void *workspace, size_t ws_bytes, void *stream);
 
 /*
+ * moe_w4a8_layer with the router in front (the sparsely gated layer of
+ * Sec. 2.2 from its router logits on): moe_router_topk(router_logits) writes
+ * topk_ids [T][k] and topk_w [T][k] (caller buffers, kept as outputs), then
+ * the layer runs on them.  shared_gate [T] fp32 (or NULL): the shared
+ * expert's output of token t is scaled by sigmoid(shared_gate[t]), computed
+ * in fp32 (1 / (1 + exp(-g))); NULL keeps it always on with weight 1.
+ *   router_logits [T][E] fp32, finite; k > E -> W4A8_ERANGE.
+ *   router_logits or shared_gate not 4-byte aligned -> W4A8_EALIGN;
+ *   router_logits NULL, or shared_gate without a shared expert -> W4A8_ENULL.
+ * Other arguments and errors as for moe_w4a8_layer.  Two launches at T = 1
+ * (router, then the single-launch layer).
+ */
+int moe_w4a8_layer_routed(const float *x, const float *y_prev, const float *gamma, float eps,
+                          float *x_out, const float *router_logits, const float *shared_gate,
+                          const void *w_gate_up, const void *w_down,
+                          const void *ws_gate_up, const void *ws_down,
+                          float *out, int32_t *topk_ids, float *topk_w,
+                          int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
+                          void *workspace, size_t ws_bytes, void *stream);
+
+/*
  * Residual add and RMSNorm between chained MoE layers (the pre-norm chaining
  * of the Qwen3-series model family, Sec. 2.2; the paper does not spell the
  * norm out, so it is the standard RMSNorm).  Per row t of [T][H] fp32:

@@ -60,7 +60,7 @@ def _load():
     lib.orc_gemv.argtypes = [P, P, I64, I64, P, P]
     lib.orc_gemv_dequant.argtypes = [P, P, I64, I64, P]
     lib.orc_moe.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, I64, I64, P,
-                            P, P, P, P, P, P]
+                            P, P, P, P, P, P, P]
     lib.orc_moe.restype = ctypes.c_int
     lib.orc_q8_0_candidates.argtypes = [P, P, I64, P, P, P, P]
     lib.orc_q8_0_candidates.restype = ctypes.c_int
@@ -160,13 +160,15 @@ class MoeResult:
 
 
 def moe(hidden, ids, wts, w_gu, w_d, ws_gu, ws_d, H, I, E, k, hq_in=None,
-        want_intermediates=True) -> MoeResult:
+        want_intermediates=True, shared_w=None) -> MoeResult:
     """Routed + shared W4A8 MoE layer, one token at a time (see orc_moe).
 
     hidden [T,H] fp32; ids [T,k] int32 (-1 = skipped slot); wts [T,k] fp32;
     w_gu [E, 2I, H/32*18] and w_d [E, H, I/32*18] uint8 (any shape with that
     many bytes); ws_gu/ws_d the shared expert (None = no shared expert).
     hq_in: optional [P, I/32*34] codes for h to use in the down projection.
+    shared_w: optional [T] fp64 weights of the shared expert's output (its
+    gate); None = 1.
     """
     hidden = _c(hidden, np.float32).reshape(-1, H)
     T = hidden.shape[0]
@@ -190,9 +192,12 @@ def moe(hidden, ids, wts, w_gu, w_d, ws_gu, ws_d, H, I, E, k, hq_in=None,
         hq = np.zeros((P, I // QK * Q8_BYTES), dtype=np.uint8)
     if hq_in is not None:
         hq_in = _c(hq_in, np.uint8).reshape(P, I // QK * Q8_BYTES)
+    if shared_w is not None:
+        shared_w = _c(shared_w, np.float64).reshape(T)
     rc = _load().orc_moe(_ptr(hidden), _ptr(ids), _ptr(wts), _ptr(w_gu), _ptr(w_d),
                          _ptr(ws_gu), _ptr(ws_d), T, H, I, E, k, _ptr(hq_in),
-                         _ptr(out), _ptr(R), _ptr(gu), _ptr(Rgu), _ptr(h), _ptr(hq))
+                         _ptr(out), _ptr(R), _ptr(gu), _ptr(Rgu), _ptr(h), _ptr(hq),
+                         _ptr(shared_w))
     if rc != 0:
         raise ValueError(f"orc_moe failed ({rc})")
     return MoeResult(out, R, gu, Rgu, h, hq)

@@ -275,8 +275,10 @@ static double silu_d(double g) { return g / (1.0 + exp(-g)); }
  *     h     = fp32( silu(gu[0:I]) * gu[I:2I] ), evaluated in fp64
  *     hq    = Q8_0(h)                (or hq_in for the pair, when given)
  *     y     = W4A8 gemv of W_d[e] with hq  (fp64, unrounded)
- *   out[t]  = sum_j w[t,j] * y_j + y_shared, accumulated in fp64
- *   R[t]    = sum_j |w[t,j]| * R_y_j + R_y_shared
+ *   out[t]  = sum_j w[t,j] * y_j + s[t] * y_shared, accumulated in fp64
+ *   R[t]    = sum_j |w[t,j]| * R_y_j + |s[t]| * R_y_shared
+ * s[t] = shared_w[t] when shared_w is given (the sigmoid gate of a gated
+ * shared expert, evaluated by the caller), else 1 (always on, Sec. 2.2).
  *
  * hq_in (may be NULL): Q8_0 codes to use for h, one 34-byte block row per pair
  * (a choice among results the oracle itself accepts; see the tests).
@@ -291,7 +293,8 @@ int orc_moe(const float *hidden, const int32_t *ids, const float *wts,
             int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
             const uint8_t *hq_in,
             double *out, double *R,
-            float *gu_out, double *Rgu_out, float *h_out, uint8_t *hq_out)
+            float *gu_out, double *Rgu_out, float *h_out, uint8_t *hq_out,
+            const double *shared_w)
 {
     int64_t nbH = H / QK, nbI = I / QK;
     size_t gu_bytes = (size_t)(2 * I) * nbH * Q4_BYTES;    /* one expert's gate/up */
@@ -329,7 +332,7 @@ int orc_moe(const float *hidden, const int32_t *ids, const float *wts,
                 if (!ws_gu || !ws_d) continue;
                 Wgu = ws_gu;
                 Wd = ws_d;
-                wj = 1.0;
+                wj = shared_w ? shared_w[t] : 1.0;
                 pair = T * k + t;
             }
             orc_gemv(Wgu, xq, 2 * I, H, gu, rgu);

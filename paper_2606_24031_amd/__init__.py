@@ -23,7 +23,7 @@ WS_NFIELDS = 8
 EXPORTS = ("w4a8_strerror", "q8_0_quantize", "q4_0_quantize", "q4q8_gemv",
            "moe_w4a8_workspace_size", "moe_w4a8_workspace_init",
            "moe_w4a8_workspace_layout", "moe_w4a8_forward", "moe_w4a8_layer",
-           "rmsnorm_residual", "moe_router_topk")
+           "rmsnorm_residual", "moe_router_topk", "moe_w4a8_layer_routed")
 
 _lib = None
 
@@ -66,6 +66,9 @@ def lib() -> ctypes.CDLL:
     L.rmsnorm_residual.restype = ctypes.c_int
     L.moe_router_topk.argtypes = [P, P, P, I64, I64, I64, P]
     L.moe_router_topk.restype = ctypes.c_int
+    L.moe_w4a8_layer_routed.argtypes = [P, P, P, ctypes.c_float, P, P, P, P, P, P, P, P, P, P,
+                                        I64, I64, I64, I64, I64, P, SZ, P]
+    L.moe_w4a8_layer_routed.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -220,3 +223,30 @@ def moe_layer(x, y_prev, gamma, topk_ids, topk_w, w_gate_up, w_down, ws_gate_up,
                               workspace.numel(), _stream(stream))
     _check(rc, "moe_w4a8_layer")
     return x_out, out
+
+
+def moe_layer_routed(x, y_prev, gamma, router_logits, w_gate_up, w_down, ws_gate_up, ws_down,
+                     H, I, E, k, workspace, shared_gate=None, eps=1e-6, x_out=None, out=None,
+                     topk_ids=None, topk_w=None, stream=None):
+    """moe_layer with the router in front: top-k of router_logits [T, E] and
+    the renormalized softmax weights, an optional sigmoid gate [T] on the
+    shared expert; returns (x_out, out, topk_ids, topk_w)."""
+    import torch
+    T = x.shape[0]
+    for t in (x, y_prev, gamma, router_logits, shared_gate):
+        assert t is None or (t.dtype == torch.float32 and t.is_contiguous())
+    if x_out is None:
+        x_out = torch.empty_like(x)
+    if out is None:
+        out = torch.empty_like(x)
+    if topk_ids is None:
+        topk_ids = torch.empty((T, k), dtype=torch.int32, device=x.device)
+    if topk_w is None:
+        topk_w = torch.empty((T, k), dtype=torch.float32, device=x.device)
+    rc = lib().moe_w4a8_layer_routed(_p(x), _p(y_prev), _p(gamma), float(eps), _p(x_out),
+                                     _p(router_logits), _p(shared_gate), _p(_u8(w_gate_up)),
+                                     _p(_u8(w_down)), _p(ws_gate_up), _p(ws_down), _p(out),
+                                     _p(topk_ids), _p(topk_w), T, H, I, E, k, _p(workspace),
+                                     workspace.numel(), _stream(stream))
+    _check(rc, "moe_w4a8_layer_routed")
+    return x_out, out, topk_ids, topk_w

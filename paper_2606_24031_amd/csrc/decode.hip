@@ -66,6 +66,7 @@ struct DecodeArgs {
   const float *x;          // [H]
   const int32_t *ids;      // [k]
   const float *topk_w;     // [k]
+  const float *shared_w;   // the shared expert's weight [1], or null (1)
   const uint8_t *w_gu, *w_d, *ws_gu, *ws_d;
   float *out;              // [H]
   uint32_t *sync;          // arrival counters
@@ -440,7 +441,8 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
   int ev;
   const int lq = threadIdx.x & 63;
   const bool lane_valid = lq < npairs && pair_valid(a, lq, ev);
-  const float wl = (int)threadIdx.x < a.k ? a.topk_w[threadIdx.x] : 1.0f;
+  const float wl = (int)threadIdx.x < a.k ? a.topk_w[threadIdx.x]
+                                           : (a.shared_w ? a.shared_w[0] : 1.0f);
   asm volatile("" ::"v"(ue), "v"((int)ulive), "v"((int)lane_valid), "v"(wl));
   W8 wpre;
   if (ulive)
@@ -559,14 +561,15 @@ bool decode_supported(int64_t H, int64_t I, int64_t k) {
 }
 
 int decode_forward(const float *x, const DecodeNorm &norm, const int32_t *ids,
-                   const float *topk_w, const uint8_t *w_gu, const uint8_t *w_d,
+                   const float *topk_w, const float *shared_w, const uint8_t *w_gu,
+                   const uint8_t *w_d,
                    const uint8_t *ws_gu, const uint8_t *ws_d, float *out, int64_t H, int64_t I,
                    int64_t E, int64_t k, uint32_t *sync, uint32_t *xfer, uint8_t *xq, float *h,
                    uint8_t *hq, hipStream_t s) {
   const int ncu = device_cus();
   if (ncu <= 0) return W4A8_EHIP;
   DecodeArgs a;
-  a.x = x; a.ids = ids; a.topk_w = topk_w;
+  a.x = x; a.ids = ids; a.topk_w = topk_w; a.shared_w = shared_w;
   a.w_gu = w_gu; a.w_d = w_d; a.ws_gu = ws_gu; a.ws_d = ws_d;
   a.out = out;
   a.sync = sync;

@@ -56,6 +56,7 @@ struct MArgs {
   const int32_t *meta, *perm;
   const int4 *tiles;               // {expert, first sorted position, rows, -}
   const float *topk_w;
+  const float *shared_w;           // down: the shared expert's weight per token, or null (1)
   float *h;                        // gate/up: fp32 h [P][I]
   uint8_t *hq;                     // gate/up: Q8_0(h) [P][I/32]
   uint32_t *ha;                    // gate/up: aligned codes of Q8_0(h) [P][I/32][8]
@@ -64,6 +65,13 @@ struct MArgs {
   int64_t T, k, E, N, K, I;
   int spw;                         // slices per workgroup
 };
+
+// Weight of pair p in the combine: its routing weight, or for the shared
+// pair of token t = p - T*k the shared expert's weight (1 without a gate).
+__device__ __forceinline__ float pair_weight(const MArgs &a, int p) {
+  const int64_t pr = a.T * a.k;
+  return p < pr ? a.topk_w[p] : (a.shared_w ? a.shared_w[p - pr] : 1.0f);
+}
 
 struct MLds {
   union {
@@ -327,11 +335,11 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
       for (int e = 0; e < 16; e++) {
         const int m = 8 * (e >> 2) + 4 * hh + (e & 3);
         const int p0 = L.pair[m];
-        if (p0 >= 0) a.y[(int64_t)p0 * a.N + n] = (p0 < a.T * a.k ? a.topk_w[p0] : 1.0f) * acc0[e];
+        if (p0 >= 0) a.y[(int64_t)p0 * a.N + n] = pair_weight(a, p0) * acc0[e];
         if (TWO) {
           const int p1 = L.pair[32 + m];
           if (p1 >= 0)
-            a.y[(int64_t)p1 * a.N + n] = (p1 < a.T * a.k ? a.topk_w[p1] : 1.0f) * acc1[e];
+            a.y[(int64_t)p1 * a.N + n] = pair_weight(a, p1) * acc1[e];
         }
         acc0[e] = 0.0f;
         acc1[e] = 0.0f;
@@ -384,12 +392,12 @@ int mfma_gateup(const uint8_t *w_gu, const uint8_t *ws_gu, const uint32_t *xa, c
 
 int mfma_down(const uint8_t *w_d, const uint8_t *ws_d, const uint32_t *ha, const float *hd,
               const int32_t *meta, const int32_t *perm, const int4 *tiles, const float *topk_w,
-              float *y, int64_t maxtiles, int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
-              hipStream_t s) {
+              const float *shared_w, float *y, int64_t maxtiles, int64_t T, int64_t H, int64_t I,
+              int64_t E, int64_t k, hipStream_t s) {
   MArgs a{};
   a.w = w_d; a.ws = ws_d; a.act = ha; a.actd = hd;
   a.meta = meta; a.perm = perm; a.tiles = tiles;
-  a.topk_w = topk_w; a.y = y;
+  a.topk_w = topk_w; a.shared_w = shared_w; a.y = y;
   a.T = T; a.k = k; a.E = E; a.N = H; a.K = I; a.I = I;
   const int64_t nsl = H / WROWS;
   a.spw = I <= 512 ? (int)std::min<int64_t>(SPW_MAX, nsl) : 1;

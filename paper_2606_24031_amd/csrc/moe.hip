@@ -34,9 +34,9 @@ int small_gateup(const uint8_t *w_gu, const uint8_t *ws_gu, const SplitBlk *xs,
                  uint8_t *hq, SplitBlk *hs, int64_t maxchunks, int64_t T, int64_t H, int64_t I,
                  int64_t E, int64_t k, hipStream_t s);
 int small_down(const uint8_t *w_d, const uint8_t *ws_d, const SplitBlk *hs, const int32_t *meta,
-               const int32_t *perm, const int4 *chunks, const float *topk_w, float *y,
-               int64_t maxchunks, int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
-               hipStream_t s);
+               const int32_t *perm, const int4 *chunks, const float *topk_w,
+               const float *shared_w, float *y, int64_t maxchunks, int64_t T, int64_t H,
+               int64_t I, int64_t E, int64_t k, hipStream_t s);
 int mfma_tile_rows();
 int mfma_gateup(const uint8_t *w_gu, const uint8_t *ws_gu, const uint32_t *xa, const float *xd,
                 const int32_t *meta, const int32_t *perm, const int4 *tiles, float *h,
@@ -44,18 +44,21 @@ int mfma_gateup(const uint8_t *w_gu, const uint8_t *ws_gu, const uint32_t *xa, c
                 int64_t I, int64_t E, int64_t k, hipStream_t s);
 int mfma_down(const uint8_t *w_d, const uint8_t *ws_d, const uint32_t *ha, const float *hd,
               const int32_t *meta, const int32_t *perm, const int4 *tiles, const float *topk_w,
-              float *y, int64_t maxtiles, int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
-              hipStream_t s);
+              const float *shared_w, float *y, int64_t maxtiles, int64_t T, int64_t H, int64_t I,
+              int64_t E, int64_t k, hipStream_t s);
 size_t decode_sync_words(int64_t H);
 size_t decode_xfer_words(int64_t I, int64_t k);
 bool decode_supported(int64_t H, int64_t I, int64_t k);
 int decode_forward(const float *x, const DecodeNorm &norm, const int32_t *ids,
-                   const float *topk_w, const uint8_t *w_gu, const uint8_t *w_d,
+                   const float *topk_w, const float *shared_w, const uint8_t *w_gu,
+                   const uint8_t *w_d,
                    const uint8_t *ws_gu, const uint8_t *ws_d, float *out, int64_t H, int64_t I,
                    int64_t E, int64_t k, uint32_t *sync, uint32_t *xfer, uint8_t *xq, float *h,
                    uint8_t *hq, hipStream_t s);
 int launch_rmsnorm(const float *x, const float *y, const float *gamma, float *x_out, float *xn,
                    int64_t T, int64_t H, float eps, hipStream_t s);
+int router_launch(const float *logits, int32_t *ids, float *weights, const float *gate,
+                  float *gate_w, int64_t T, int64_t E, int64_t k, hipStream_t s);
 
 namespace {
 
@@ -67,7 +70,7 @@ inline size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
   size_t meta, sync, xfer, perm, count, rank, groups, tiles, chunks, xq, h, hq, y, xn, xs, hs,
-      xa, xd, ha, hd, total;
+      xa, xd, ha, hd, sw, total;
   int64_t maxtiles, maxchunks;
 };
 
@@ -104,6 +107,7 @@ Layout make_layout(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k) {
   L.xd = off;     off += up256(sizeof(float) * (size_t)T * (H / QK));
   L.ha = off;     off += up256((size_t)P * I);          // aligned Q8_0 codes of h
   L.hd = off;     off += up256(sizeof(float) * (size_t)P * (I / QK));
+  L.sw = off;     off += up256(sizeof(float) * (size_t)T);   // shared expert's gate weights
   L.total = off;
   return L;
 }
@@ -416,7 +420,8 @@ __global__ __launch_bounds__(256) void combine_kernel(const float *__restrict__ 
 }  // namespace
 
 int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
-                     const float *topk_w, const uint8_t *w_gu, const uint8_t *w_d,
+                     const float *topk_w, const float *shared_w, const uint8_t *w_gu,
+                     const uint8_t *w_d,
                      const uint8_t *ws_gu, const uint8_t *ws_d, float *out, int64_t T, int64_t H,
                      int64_t I, int64_t E, int64_t k, uint8_t *ws, size_t ws_bytes,
                      hipStream_t s) {
@@ -428,7 +433,8 @@ int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
   // One token: the whole layer in a single launch, the residual RMSNorm
   // included (see decode.hip).
   if (T == 1 && decode_supported(H, I, k))
-    return decode_forward(hidden, norm, ids, topk_w, w_gu, w_d, ws_gu, ws_d, out, H, I, E, k,
+    return decode_forward(hidden, norm, ids, topk_w, shared_w, w_gu, w_d, ws_gu, ws_d, out, H, I,
+                          E, k,
                           reinterpret_cast<uint32_t *>(ws + L.sync),
                           reinterpret_cast<uint32_t *>(ws + L.xfer), ws + L.xq,
                           reinterpret_cast<float *>(ws + L.h), ws + L.hq, s);
@@ -497,11 +503,11 @@ int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
   if (tiles && (rc = mfma_gateup(w_gu, ws_gu, xa, xd, ra.meta, ra.perm, ra.tiles, h, hq, ha, hd,
                                  L.maxtiles, T, H, I, E, k, s)) != W4A8_OK)
     return rc;
-  if (ms > 0 && (rc = small_down(w_d, ws_d, hs, ra.meta, ra.perm, ra.chunks, topk_w, y, maxchunks,
-                                 T, H, I, E, k, s)) != W4A8_OK)
+  if (ms > 0 && (rc = small_down(w_d, ws_d, hs, ra.meta, ra.perm, ra.chunks, topk_w, shared_w, y,
+                                 maxchunks, T, H, I, E, k, s)) != W4A8_OK)
     return rc;
-  if (tiles && (rc = mfma_down(w_d, ws_d, ha, hd, ra.meta, ra.perm, ra.tiles, topk_w, y,
-                               L.maxtiles, T, H, I, E, k, s)) != W4A8_OK)
+  if (tiles && (rc = mfma_down(w_d, ws_d, ha, hd, ra.meta, ra.perm, ra.tiles, topk_w, shared_w,
+                               y, L.maxtiles, T, H, I, E, k, s)) != W4A8_OK)
     return rc;
 
   const int64_t n4 = T * (H / 4);
@@ -566,6 +572,23 @@ int moe_args(const float *hidden, const int32_t *topk_ids, const float *topk_w,
   return W4A8_OK;
 }
 
+// moe_w4a8_layer's arguments (see include/w4a8.h).
+int layer_args(const float *x, const float *y_prev, const float *gamma, float eps,
+               const float *x_out, const int32_t *topk_ids, const float *topk_w,
+               const void *w_gate_up, const void *w_down, const void *ws_gate_up,
+               const void *ws_down, const float *out, int64_t T, int64_t H, int64_t I, int64_t E,
+               int64_t k, const void *workspace, size_t ws_bytes) {
+  int rc = moe_args(x, topk_ids, topk_w, w_gate_up, w_down, ws_gate_up, ws_down, out, T, H, I, E,
+                    k, workspace, ws_bytes);
+  if (rc != W4A8_OK || T == 0) return rc;
+  if (!gamma || !x_out) return W4A8_ENULL;
+  if (!(eps >= 0.0f)) return W4A8_ESHAPE;
+  if (!aligned16(y_prev) || !aligned16(gamma) || !aligned16(x_out)) return W4A8_EALIGN;
+  if (x_out == x || x_out == out || out == x || (y_prev && (x_out == y_prev || out == y_prev)))
+    return W4A8_EALIAS;
+  return W4A8_OK;
+}
+
 }  // namespace
 }  // namespace w4a8
 
@@ -578,7 +601,7 @@ extern "C" int moe_w4a8_forward(const float *hidden, const int32_t *topk_ids,
                     I, E, k, workspace, ws_bytes);
   if (rc != W4A8_OK || T == 0) return rc;
   if ((rc = check_device()) != W4A8_OK) return rc;
-  return moe_forward_impl(hidden, DecodeNorm{}, topk_ids, topk_w,
+  return moe_forward_impl(hidden, DecodeNorm{}, topk_ids, topk_w, nullptr,
                           reinterpret_cast<const uint8_t *>(w_gate_up),
                           reinterpret_cast<const uint8_t *>(w_down),
                           reinterpret_cast<const uint8_t *>(ws_gate_up),
@@ -592,24 +615,54 @@ extern "C" int moe_w4a8_layer(const float *x, const float *y_prev, const float *
                               const void *ws_down, float *out, int64_t T, int64_t H, int64_t I,
                               int64_t E, int64_t k, void *workspace, size_t ws_bytes,
                               void *stream) {
-  int rc = moe_args(x, topk_ids, topk_w, w_gate_up, w_down, ws_gate_up, ws_down, out, T, H, I, E,
-                    k, workspace, ws_bytes);
+  int rc = layer_args(x, y_prev, gamma, eps, x_out, topk_ids, topk_w, w_gate_up, w_down,
+                      ws_gate_up, ws_down, out, T, H, I, E, k, workspace, ws_bytes);
   if (rc != W4A8_OK || T == 0) return rc;
-  if (!gamma || !x_out) return W4A8_ENULL;
-  if (!(eps >= 0.0f)) return W4A8_ESHAPE;
-  if (!aligned16(y_prev) || !aligned16(gamma) || !aligned16(x_out)) return W4A8_EALIGN;
-  if (x_out == x || x_out == out || out == x || (y_prev && (x_out == y_prev || out == y_prev)))
-    return W4A8_EALIAS;
   if ((rc = check_device()) != W4A8_OK) return rc;
   DecodeNorm norm;
   norm.resid = y_prev;
   norm.gamma = gamma;
   norm.x_out = x_out;
   norm.eps = eps;
-  return moe_forward_impl(x, norm, topk_ids, topk_w,
+  return moe_forward_impl(x, norm, topk_ids, topk_w, nullptr,
                           reinterpret_cast<const uint8_t *>(w_gate_up),
                           reinterpret_cast<const uint8_t *>(w_down),
                           reinterpret_cast<const uint8_t *>(ws_gate_up),
                           reinterpret_cast<const uint8_t *>(ws_down), out, T, H, I, E, k,
                           reinterpret_cast<uint8_t *>(workspace), ws_bytes, as_stream(stream));
+}
+
+extern "C" int moe_w4a8_layer_routed(const float *x, const float *y_prev, const float *gamma,
+                                     float eps, float *x_out, const float *router_logits,
+                                     const float *shared_gate, const void *w_gate_up,
+                                     const void *w_down, const void *ws_gate_up,
+                                     const void *ws_down, float *out, int32_t *topk_ids,
+                                     float *topk_w, int64_t T, int64_t H, int64_t I, int64_t E,
+                                     int64_t k, void *workspace, size_t ws_bytes, void *stream) {
+  int rc = layer_args(x, y_prev, gamma, eps, x_out, topk_ids, topk_w, w_gate_up, w_down,
+                      ws_gate_up, ws_down, out, T, H, I, E, k, workspace, ws_bytes);
+  if (rc != W4A8_OK || T == 0) return rc;
+  if (k > E) return W4A8_ERANGE;
+  if (!router_logits || (shared_gate && !ws_gate_up)) return W4A8_ENULL;
+  if ((reinterpret_cast<uintptr_t>(router_logits) | reinterpret_cast<uintptr_t>(shared_gate)) & 3u)
+    return W4A8_EALIGN;
+  if ((rc = check_device()) != W4A8_OK) return rc;
+  const Layout L = make_layout(T, H, I, E, k);
+  uint8_t *ws = reinterpret_cast<uint8_t *>(workspace);
+  float *sw = shared_gate ? reinterpret_cast<float *>(ws + L.sw) : nullptr;
+  hipStream_t s = as_stream(stream);
+  if ((rc = router_launch(router_logits, topk_ids, topk_w, shared_gate, sw, T, E, k, s)) !=
+      W4A8_OK)
+    return rc;
+  DecodeNorm norm;
+  norm.resid = y_prev;
+  norm.gamma = gamma;
+  norm.x_out = x_out;
+  norm.eps = eps;
+  return moe_forward_impl(x, norm, topk_ids, topk_w, sw,
+                          reinterpret_cast<const uint8_t *>(w_gate_up),
+                          reinterpret_cast<const uint8_t *>(w_down),
+                          reinterpret_cast<const uint8_t *>(ws_gate_up),
+                          reinterpret_cast<const uint8_t *>(ws_down), out, T, H, I, E, k, ws,
+                          ws_bytes, s);
 }

@@ -45,7 +45,9 @@ __device__ __forceinline__ void wave_argmax(float &v, int &i) {
 
 __global__ __launch_bounds__(RT) void router_kernel(const float *__restrict__ logits,
                                                     int32_t *__restrict__ ids,
-                                                    float *__restrict__ weights, int64_t T, int E,
+                                                    float *__restrict__ weights,
+                                                    const float *__restrict__ gate,
+                                                    float *__restrict__ gate_w, int64_t T, int E,
                                                     int k) {
   extern __shared__ float lv[];    // [RT / 64][E]
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -76,9 +78,21 @@ __global__ __launch_bounds__(RT) void router_kernel(const float *__restrict__ lo
     ids[t * k + lane] = seli;
     weights[t * k + lane] = ex / s;
   }
+  // the shared expert's sigmoid gate
+  if (gate != nullptr && lane == 0) gate_w[t] = 1.0f / (1.0f + expf(-gate[t]));
 }
 
 }  // namespace
+
+// Validated arguments; gate and gate_w may be null (no shared-expert gate).
+int router_launch(const float *logits, int32_t *ids, float *weights, const float *gate,
+                  float *gate_w, int64_t T, int64_t E, int64_t k, hipStream_t s) {
+  const int64_t grid = (T + RT / 64 - 1) / (RT / 64);
+  const size_t lds = sizeof(float) * (RT / 64) * (size_t)E;
+  router_kernel<<<dim3((unsigned)grid), dim3(RT), lds, s>>>(logits, ids, weights, gate, gate_w, T,
+                                                            (int)E, (int)k);
+  return check_launch();
+}
 
 }  // namespace w4a8
 
@@ -96,9 +110,5 @@ extern "C" int moe_router_topk(const float *logits, int32_t *ids, float *weights
   if (T == 0) return W4A8_OK;
   int rc = check_device();
   if (rc != W4A8_OK) return rc;
-  const int64_t grid = (T + RT / 64 - 1) / (RT / 64);
-  const size_t lds = sizeof(float) * (RT / 64) * (size_t)E;
-  router_kernel<<<dim3((unsigned)grid), dim3(RT), lds, as_stream(stream)>>>(
-      logits, ids, weights, T, (int)E, (int)k);
-  return check_launch();
+  return router_launch(logits, ids, weights, nullptr, nullptr, T, E, k, as_stream(stream));
 }

@@ -48,6 +48,7 @@ struct SmallArgs {
   const int32_t *meta, *perm;
   const int4 *chunks;         // {expert, first sorted position, rows, group}
   const float *topk_w;
+  const float *shared_w;      // down: the shared expert's weight per token, or null (1)
   float *h;                   // gate/up: fp32 h [P][I]
   uint8_t *hq;                // gate/up: Q8_0(h) [P][I/32]
   SplitBlk *hs;               // gate/up: nibble-split Q8_0(h) [P][I/32]
@@ -206,7 +207,8 @@ __device__ __forceinline__ void small_item(const SmallArgs &a, SmallLds &L, int 
       float v = 0.0f;
       for (int wv = rset; wv < SW; wv += nrs) v += L.part[wv][m][rl];
       const int p = L.pair[m];
-      const float wt = p < a.T * a.k ? a.topk_w[p] : 1.0f;
+      const int64_t pr = a.T * a.k;
+      const float wt = p < pr ? a.topk_w[p] : (a.shared_w ? a.shared_w[p - pr] : 1.0f);
       a.y[(int64_t)p * a.N + (int64_t)slab * R + r] = wt * v;
     }
   }
@@ -257,13 +259,13 @@ int small_gateup(const uint8_t *w_gu, const uint8_t *ws_gu, const SplitBlk *xs,
 }
 
 int small_down(const uint8_t *w_d, const uint8_t *ws_d, const SplitBlk *hs, const int32_t *meta,
-               const int32_t *perm, const int4 *chunks, const float *topk_w, float *y,
-               int64_t maxchunks, int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
-               hipStream_t s) {
+               const int32_t *perm, const int4 *chunks, const float *topk_w,
+               const float *shared_w, float *y, int64_t maxchunks, int64_t T, int64_t H,
+               int64_t I, int64_t E, int64_t k, hipStream_t s) {
   SmallArgs a{};
   a.w = w_d; a.ws = ws_d; a.act = hs;
   a.meta = meta; a.perm = perm; a.chunks = chunks;
-  a.topk_w = topk_w; a.y = y;
+  a.topk_w = topk_w; a.shared_w = shared_w; a.y = y;
   a.T = T; a.k = k; a.E = E; a.N = H; a.K = I; a.I = I;
   a.nrs = small_down_rowsets(H, I);
   a.nslab = (int)(H / (64 * a.nrs));

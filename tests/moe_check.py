@@ -41,12 +41,14 @@ def valid_pairs(ids: np.ndarray, E: int, shared: bool):
     return routed + ([T * k + t for t in range(T)] if shared else [])
 
 
-def check_layer(out_gpu, h_gpu, hq_gpu, x, ids, wts, w_gu, w_d, ws_gu, ws_d, H, I, E, k):
+def check_layer(out_gpu, h_gpu, hq_gpu, x, ids, wts, w_gu, w_d, ws_gu, ws_d, H, I, E, k,
+                shared_w=None):
     """All GPU arrays in the oracle's pair numbering for these T tokens:
-    out_gpu [T,H] fp32, h_gpu [P,I] fp32, hq_gpu [P, I/32*34] uint8."""
+    out_gpu [T,H] fp32, h_gpu [P,I] fp32, hq_gpu [P, I/32*34] uint8.
+    shared_w: the shared expert's per-token weight (fp64 [T]), None = 1."""
     T = x.shape[0]
     shared = ws_gu is not None
-    r = oracle.moe(x, ids, wts, w_gu, w_d, ws_gu, ws_d, H, I, E, k)
+    r = oracle.moe(x, ids, wts, w_gu, w_d, ws_gu, ws_d, H, I, E, k, shared_w=shared_w)
     pairs = valid_pairs(ids, E, shared)
     nb = I // 32
     sel = r.hq.copy()
@@ -70,7 +72,7 @@ def check_layer(out_gpu, h_gpu, hq_gpu, x, ids, wts, w_gu, w_d, ws_gu, ws_d, H, 
                 flips += 1
         sel[p] = hq_gpu[p]
     r2 = oracle.moe(x, ids, wts, w_gu, w_d, ws_gu, ws_d, H, I, E, k, hq_in=sel,
-                    want_intermediates=False)
+                    want_intermediates=False, shared_w=shared_w)
     err = np.abs(out_gpu.astype(np.float64) - r2.out)
     bound = EPS * r2.R
     bad = err > bound

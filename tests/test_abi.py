@@ -152,3 +152,27 @@ def test_router_argument_errors():
     assert f(p, p, p, 1 << 31, 256, 8, None) == w4.ERANGE
     assert f(p, _fake(A + 2), p, 4, 256, 8, None) == w4.EALIGN
     assert f(p, p, p, 0, 256, 8, None) == w4.OK            # empty: no-op
+
+
+def test_layer_routed_argument_errors():
+    f = w4.lib().moe_w4a8_layer_routed
+    H, I, E, k, T = 256, 256, 4, 2, 3
+    need = w4.moe_workspace_size(T, H, I, E, k)
+    x, yp, g, xo, lg, gt, wgu, wd, sgu, sd, out, ids, tw, ws = (_fake(A + 4096 * i)
+                                                                for i in range(14))
+    def call(**kw):
+        a = dict(x=x, yp=yp, g=g, eps=1e-6, xo=xo, lg=lg, gt=gt, wgu=wgu, wd=wd, sgu=sgu, sd=sd,
+                 out=out, ids=ids, tw=tw, T=T, E=E, k=k, ws=ws, n=need)
+        a.update(kw)
+        return f(a["x"], a["yp"], a["g"], a["eps"], a["xo"], a["lg"], a["gt"], a["wgu"], a["wd"],
+                 a["sgu"], a["sd"], a["out"], a["ids"], a["tw"], a["T"], H, I, a["E"], a["k"],
+                 a["ws"], a["n"], None)
+    assert call(lg=None) == w4.ENULL
+    assert call(sgu=None, sd=None) == w4.ENULL          # a gate for a missing shared expert
+    assert call(ids=None) == w4.ENULL
+    assert call(lg=_fake(A + 2)) == w4.EALIGN
+    assert call(gt=_fake(A + 1)) == w4.EALIGN
+    assert call(k=5, n=w4.moe_workspace_size(T, H, I, E, 5)) == w4.ERANGE   # k > E
+    assert call(xo=x) == w4.EALIAS
+    assert call(n=need - 1) == w4.EWORKSPACE
+    assert call(T=0) == w4.OK

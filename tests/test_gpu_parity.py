@@ -140,9 +140,9 @@ class Layer:
         assert np.array_equal(xq, oracle.q8_0_quantize(x)), "workspace Q8_0(x)"
         return host(out), h, hq, perm, count, ws
 
-    def check(self, x, ids, wts, k, out, h, hq):
+    def check(self, x, ids, wts, k, out, h, hq, shared_w=None):
         return moe_check.check_layer(out, h, hq, x, ids, wts, self.w_gu, self.w_d, self.ws_gu,
-                                     self.ws_d, self.H, self.I, self.E, k)
+                                     self.ws_d, self.H, self.I, self.E, k, shared_w=shared_w)
 
 
 def _check_route(ids, E, shared, perm, count):
@@ -440,6 +440,45 @@ def test_moe_layer_residual_norm(qwen_layer, T, with_prev):
     h = wsn[lay["h"]:lay["h"] + P * L.I * 4].view(np.float32).reshape(P, L.I)
     hq = wsn[lay["hq"]:lay["hq"] + P * (L.I // 32) * 34].reshape(P, -1)
     L.check(xn, ids, wts, 8, host(out), h, hq)
+
+
+@pytest.mark.parametrize("T,gated", [(1, True), (1, False), (6, True), (40, True), (40, False)])
+def test_moe_layer_routed(qwen_layer, T, gated):
+    """Router in front of the residual layer: ids bit-exact with the oracle's
+    top-k of the logits and weights within 4e-6; x_out, the normalized row
+    and its Q8_0 as for moe_layer; the output through the MoE check, with the
+    GPU's own routing weights for the routed slots (they are the layer's
+    input) and the oracle's fp64 sigmoid of the gate for the shared expert
+    (T = 1: router launch, then the single decode launch; T = 6: VALU path;
+    T = 40: MFMA tiles as well)."""
+    L = qwen_layer
+    g = synth.rng(80 + T)
+    x = synth.normal_f32(g, (T, L.H))
+    y_prev = synth.normal_f32(g, (T, L.H), 0.3)
+    gamma = (np.float32(1.0) + synth.normal_f32(g, (L.H,), 0.1)).astype(np.float32)
+    logits = synth.normal_f32(g, (T, L.E))
+    logits[:, :16] += np.float32(1.5)              # a few popular experts
+    gate = synth.normal_f32(g, (T,), 2.0) if gated else None
+    ws = w4.moe_workspace(T, L.H, L.I, L.E, 8)
+    x_out, out, ids_d, w_d = w4.moe_layer_routed(
+        dev(x), dev(y_prev), dev(gamma), dev(logits), L.d_gu, L.d_d, L.d_sgu, L.d_sd,
+        L.H, L.I, L.E, 8, ws, shared_gate=dev(gate) if gated else None)
+    ids, wts = host(ids_d), host(w_d)
+    ids_r, w_r = oracle.router_topk(logits, 8)
+    assert np.array_equal(ids, ids_r)
+    assert np.all(np.abs(wts.astype(np.float64) - w_r) <= 4e-6 * w_r)
+    xo_ref, xn_ref = oracle.rmsnorm_residual(x, y_prev, gamma, eps=1e-6)
+    assert np.array_equal(host(x_out), xo_ref)
+    lay = w4.moe_workspace_layout(T, L.H, L.I, L.E, 8)
+    wsn = host(ws)
+    xn = wsn[lay["xn"]:lay["xn"] + T * L.H * 4].view(np.float32).reshape(T, L.H)
+    err = np.abs(xn.astype(np.float64) - xn_ref)
+    assert np.all(err <= 2e-6 * np.abs(xn_ref) + 1e-7 * np.abs(gamma).max())
+    P = T * 8 + T
+    h = wsn[lay["h"]:lay["h"] + P * L.I * 4].view(np.float32).reshape(P, L.I)
+    hq = wsn[lay["hq"]:lay["hq"] + P * (L.I // 32) * 34].reshape(P, -1)
+    sw = 1.0 / (1.0 + np.exp(-gate.astype(np.float64))) if gated else None
+    L.check(xn, ids, wts, 8, host(out), h, hq, shared_w=sw)
 
 
 # ------------------------------------------------------------ router top-k

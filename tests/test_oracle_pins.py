@@ -499,3 +499,24 @@ def test_router_invariants_and_special_cases():
     assert ids3.tolist() == [[0, 1, 2, 3]] * 2 and np.all(w3 == 0.25)
     ids4, w4 = oracle.router_topk(logits, 1)
     assert np.array_equal(ids4[:, 0], np.argmax(logits, axis=1)) and np.all(w4 == 1.0)
+
+
+def test_moe_shared_weight_is_linear():
+    """out(s) = out(s=0) + s * (out(s=1) - out(s=0)) per token for the shared
+    expert's weight s, and s = 1 is the ungated layer."""
+    g = synth.rng(63)
+    T, H, I, E, k = 3, 256, 256, 4, 2
+    w_gu = synth.q4_0_random_blocks(g, E * 2 * I, H)
+    w_d = synth.q4_0_random_blocks(g, E * H, I)
+    ws_gu = synth.q4_0_random_blocks(g, 2 * I, H)
+    ws_d = synth.q4_0_random_blocks(g, H, I)
+    x = synth.normal_f32(g, (T, H))
+    ids, wts = synth.routing(g, T, E, k)
+    f = lambda s: oracle.moe(x, ids, wts, w_gu, w_d, ws_gu, ws_d, H, I, E, k, shared_w=s,
+                             want_intermediates=False)
+    base = f(None)
+    r0, r1 = f(np.zeros(T)), f(np.ones(T))
+    s = np.array([0.25, 0.5, 2.0])
+    rs = f(s)
+    assert np.array_equal(r1.out, base.out) and np.array_equal(r1.R, base.R)
+    assert np.allclose(rs.out, r0.out + s[:, None] * (r1.out - r0.out), rtol=0, atol=1e-12 * base.R.max())
