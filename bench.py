@@ -349,6 +349,42 @@ def bench_stack(torch, w4, synth, args, dev):
     ev1.record()
     torch.cuda.synchronize()
     ms_d = ev0.elapsed_time(ev1) / nd
+
+    # the same decode steps with the router in front of every layer: fresh
+    # N(0,1) logits and a sigmoid gate on the shared expert per layer and step
+    # (moe_w4a8_layer_routed: a router launch, then the layer's launch)
+    dec_logits = torch.randn((nd, nl, 1, E), generator=gen, device=dev)
+    dec_gate = torch.randn((nd, nl, 1), generator=gen, device=dev)
+    r_ids = torch.empty((1, K_TOP), dtype=torch.int32, device=dev)
+    r_wts = torch.empty((1, K_TOP), dtype=torch.float32, device=dev)
+
+    def decode_routed(s):
+        xs, ys = xs_d, ys_d
+        xs[0].copy_(x_d0[s])
+        for l in range(nl):
+            L = layers[l]
+            w4.moe_layer_routed(xs[l % 2], ys[(l + 1) % 2] if l else None, gammas[l],
+                                dec_logits[s, l], L[0], L[1], L[2], L[3], H, I, E, K_TOP, ws_d,
+                                shared_gate=dec_gate[s, l], x_out=xs[(l + 1) % 2],
+                                out=ys[l % 2], topk_ids=r_ids, topk_w=r_wts)
+        x = xs[nl % 2]
+        w4.rmsnorm_residual(x, ys[(nl - 1) % 2], None, x_out=x, want_norm=False)
+        return x
+
+    decode_routed(0)
+    torch.cuda.synchronize()
+    graph_r = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph_r):
+        for s in range(nd):
+            x_r = decode_routed(s)
+    graph_r.replay()
+    torch.cuda.synchronize()
+    ev0.record()
+    graph_r.replay()
+    ev1.record()
+    torch.cuda.synchronize()
+    ms_r = ev0.elapsed_time(ev1) / nd
+    assert torch.isfinite(x_r).all()
     ids_h = dec_ids.cpu().numpy().reshape(nd * nl, K_TOP)
     dbytes = sum(step_bytes(ids_h[i]) for i in range(nd * nl)) / nd
     assert torch.isfinite(x_p).all() and torch.isfinite(x_d).all()
@@ -359,6 +395,8 @@ def bench_stack(torch, w4, synth, args, dev):
             "decode_steps": nd, "decode_ms_per_token": round(ms_d, 4),
             "decode_tokens_per_s": round(1e3 / ms_d, 1),
             "decode_GBps": round(dbytes / (ms_d / 1e3) / 1e9, 1),
+            "decode_routed_ms_per_token": round(ms_r, 4),
+            "decode_routed_tokens_per_s": round(1e3 / ms_r, 1),
             "launch": "prefill eager; decode steps replayed from one HIP graph"}
 
 
