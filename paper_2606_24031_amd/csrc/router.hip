@@ -2,12 +2,13 @@
 // to its top-k of E routed experts; the k gate values are renormalized over
 // the selection, as the Qwen3-series models do).
 //
-// One wave per token.  The token's logits are staged in LDS; k rounds each
-// take the wave's largest remaining logit (a lane scans its strided share in
-// index order, then DPP exchanges and four lane reads keep the larger value,
-// or on equal values the lower index) and mark it taken.  The selection compares the fp32
-// logits themselves: softmax is monotone, so this is the order of the
-// probabilities without any rounding in the decision.  The weights are
+// One wave per token.  The token's logits sit in registers (E <= 512) or in
+// LDS; k rounds each take the wave's largest remaining logit (a lane scans
+// its strided share in index order, then DPP exchanges and row broadcasts
+// keep the larger value, or on equal values the lower index) and mark it
+// taken.  The selection compares the fp32 logits themselves: softmax is
+// monotone, so this is the order of the probabilities without any rounding
+// in the decision.  The weights are
 // exp(l_j - l_max) over their sum across the selection (the full softmax
 // denominator cancels in the renormalization), summed in a fixed butterfly.
 #include "w4a8_dev.h"
@@ -21,53 +22,96 @@ constexpr int RT = 256;            // threads: four waves, one token each
 
 // (av, ai) replaced by (bv, bi) when that is larger, or equal with a lower index.
 __device__ __forceinline__ void take_better(float &av, int &ai, float bv, int bi) {
-  if (bv > av || (bv == av && bi < ai)) { av = bv; ai = bi; }
+  // bitwise on the conditions: a branch-free select
+  const bool take = (bv > av) | ((bv == av) & (bi < ai));
+  av = take ? bv : av;
+  ai = take ? bi : ai;
 }
 
-// Largest (value, index) over the wave, equal values by the lower index, in
-// every lane: DPP exchanges inside each 16-lane row (lane^1, lane^2, the
-// half-row mirror, lane^8), then the four row results read out in row order.
+// Largest (value, index) over the wave, equal values by the lower index:
+// DPP exchanges inside each 16-lane row (lane^1, lane^2, the half-row
+// mirror, lane^8), then row broadcasts (row 0's result into row 1 and row
+// 2's into row 3, then row 1's into rows 2 and 3), and lane 63 read out.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ void dpp_better(float &v, int &i) {
+  const float ov = __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, v), __builtin_bit_cast(int, v),
+                                         CTRL, ROWS, 0xF, false));
+  const int oi = __builtin_amdgcn_update_dpp(i, i, CTRL, ROWS, 0xF, false);
+  take_better(v, i, ov, oi);
+}
+
 __device__ __forceinline__ void wave_argmax(float &v, int &i) {
-  take_better(v, i, dpp_f<DPP_XOR1>(v), dpp_i<DPP_XOR1>(i));
-  take_better(v, i, dpp_f<DPP_XOR2>(v), dpp_i<DPP_XOR2>(i));
-  take_better(v, i, dpp_f<DPP_HALF_MIRROR>(v), dpp_i<DPP_HALF_MIRROR>(i));
-  take_better(v, i, dpp_f<DPP_ROR8>(v), dpp_i<DPP_ROR8>(i));
-  float bv = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
-  int bi = __builtin_amdgcn_readlane(i, 0);
-#pragma unroll
-  for (int r = 1; r < 4; r++)
-    take_better(bv, bi,
-                __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16 * r)),
-                __builtin_amdgcn_readlane(i, 16 * r));
-  v = bv;
-  i = bi;
+  dpp_better<DPP_XOR1, 0xF>(v, i);
+  dpp_better<DPP_XOR2, 0xF>(v, i);
+  dpp_better<DPP_HALF_MIRROR, 0xF>(v, i);
+  dpp_better<DPP_ROR8, 0xF>(v, i);
+  dpp_better<0x142, 0xA>(v, i);    // row_bcast:15 into rows 1 and 3
+  dpp_better<0x143, 0xC>(v, i);    // row_bcast:31 into rows 2 and 3
+  v = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+  i = __builtin_amdgcn_readlane(i, 63);
 }
 
+// RV > 0: the token's logits live in registers, RV per lane (E <= 64 * RV);
+// RV == 0: in LDS.
+template <int RV>
 __global__ __launch_bounds__(RT) void router_kernel(const float *__restrict__ logits,
                                                     int32_t *__restrict__ ids,
                                                     float *__restrict__ weights,
                                                     const float *__restrict__ gate,
                                                     float *__restrict__ gate_w, int64_t T, int E,
                                                     int k) {
-  extern __shared__ float lv[];    // [RT / 64][E]
+  extern __shared__ float lv[];    // [RT / 64][E] (LDS form only)
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t t = (int64_t)blockIdx.x * (RT / 64) + wave;
   if (t >= T) return;              // whole waves; no workgroup barrier below
-  float *v = lv + (size_t)wave * E;
   const float *row = logits + t * E;
-  for (int e = lane; e < E; e += 64) v[e] = row[e];
   float selv = 0.0f;
   int seli = 0;                    // lane j < k: the j-th selection
-  for (int j = 0; j < k; j++) {
-    float bv = -INFINITY;
-    int bi = 0x7fffffff;
-    for (int e = lane; e < E; e += 64) {
-      const float x = v[e];
-      if (x > bv) { bv = x; bi = e; }
+  if (RV > 0) {
+    float x[RV > 0 ? RV : 1];
+#pragma unroll
+    for (int r = 0; r < RV; r++) {
+      const int e = lane + 64 * r;
+      x[r] = e < E ? row[e] : -INFINITY;
     }
-    wave_argmax(bv, bi);
-    if (lane == j) { selv = bv; seli = bi; }
-    if (lane == (bi & 63)) v[bi] = -INFINITY;   // taken (the logits are finite)
+    for (int j = 0; j < k; j++) {
+      // this lane's largest remaining logit, a pairwise tree in which the
+      // left (lower index) side keeps equal values
+      float tv[RV > 0 ? RV : 1];
+      int ti[RV > 0 ? RV : 1];
+#pragma unroll
+      for (int r = 0; r < RV; r++) { tv[r] = x[r]; ti[r] = lane + 64 * r; }
+#pragma unroll
+      for (int w = 1; w < RV; w *= 2)
+#pragma unroll
+        for (int r = 0; r + w < RV; r += 2 * w) {
+          const bool take = tv[r + w] > tv[r];
+          tv[r] = take ? tv[r + w] : tv[r];
+          ti[r] = take ? ti[r + w] : ti[r];
+        }
+      float bv = tv[0];
+      int bi = ti[0];
+      wave_argmax(bv, bi);
+      if (lane == j) { selv = bv; seli = bi; }
+#pragma unroll
+      for (int r = 0; r < RV; r++)
+        if (bi == lane + 64 * r) x[r] = -INFINITY;   // taken (the logits are finite)
+    }
+  } else {
+    float *v = lv + (size_t)wave * E;
+    for (int e = lane; e < E; e += 64) v[e] = row[e];
+    for (int j = 0; j < k; j++) {
+      float bv = -INFINITY;
+      int bi = 0x7fffffff;
+      for (int e = lane; e < E; e += 64) {
+        const float xv = v[e];
+        if (xv > bv) { bv = xv; bi = e; }
+      }
+      wave_argmax(bv, bi);
+      if (lane == j) { selv = bv; seli = bi; }
+      if (lane == (bi & 63)) v[bi] = -INFINITY;
+    }
   }
   const float lmax = __shfl(selv, 0);
   const float ex = lane < k ? expf(selv - lmax) : 0.0f;
@@ -88,9 +132,17 @@ __global__ __launch_bounds__(RT) void router_kernel(const float *__restrict__ lo
 int router_launch(const float *logits, int32_t *ids, float *weights, const float *gate,
                   float *gate_w, int64_t T, int64_t E, int64_t k, hipStream_t s) {
   const int64_t grid = (T + RT / 64 - 1) / (RT / 64);
-  const size_t lds = sizeof(float) * (RT / 64) * (size_t)E;
-  router_kernel<<<dim3((unsigned)grid), dim3(RT), lds, s>>>(logits, ids, weights, gate, gate_w, T,
-                                                            (int)E, (int)k);
+  if (E <= 256) {
+    router_kernel<4><<<dim3((unsigned)grid), dim3(RT), 0, s>>>(logits, ids, weights, gate, gate_w,
+                                                               T, (int)E, (int)k);
+  } else if (E <= 512) {
+    router_kernel<8><<<dim3((unsigned)grid), dim3(RT), 0, s>>>(logits, ids, weights, gate, gate_w,
+                                                               T, (int)E, (int)k);
+  } else {
+    const size_t lds = sizeof(float) * (RT / 64) * (size_t)E;
+    router_kernel<0><<<dim3((unsigned)grid), dim3(RT), lds, s>>>(logits, ids, weights, gate,
+                                                                 gate_w, T, (int)E, (int)k);
+  }
   return check_launch();
 }
 
