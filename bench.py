@@ -278,6 +278,40 @@ def bench_router(torch, w4, synth, args, dev):
     return res
 
 
+def bench_lm_head(torch, w4, synth, args, dev):
+    """The dense W4A8 GEMV at the output projection's shape (N = 151936
+    vocabulary rows, K = H = 2048; random Q4_0 blocks, 175 MB), two weight
+    copies alternated so successive calls stream from HBM."""
+    N, K = 151936, H
+    g = synth.rng(args.seed + 9)
+    ws = [torch.from_numpy(synth.q4_0_random_blocks(g, N, K)).to(dev) for _ in range(2)]
+    xq = w4.q8_0_quantize(torch.from_numpy(synth.normal_f32(g, (1, K))).to(dev))
+    y = torch.empty(N, dtype=torch.float32, device=dev)
+    n = 40
+    for i in range(4):
+        w4.q4q8_gemv(ws[i % 2], xq, N, K, y=y)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for i in range(n):
+            w4.q4q8_gemv(ws[i % 2], xq, N, K, y=y)
+    graph.replay()
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    graph.replay()
+    ev1.record()
+    torch.cuda.synchronize()
+    us = ev0.elapsed_time(ev1) / n * 1e3
+    nbytes = N * (K // 32) * 18 + (K // 32) * 34 + N * 4
+    del ws
+    return {"N": N, "K": K, "us_per_call": round(us, 2),
+            "GBps": round(nbytes / (us / 1e6) / 1e9, 1),
+            "hbm_peak_frac": round(nbytes / (us / 1e6) / 1e9 / HBM_PEAK_GBPS, 4),
+            "launch": "hipGraph"}
+
+
 def bench_stack(torch, w4, synth, args, dev):
     """40 chained pre-norm residual layers (x <- x + MoE_l(RMSNorm_l(x)), one
     moe_w4a8_layer call each, the residual add and norm fused into the layer
@@ -486,6 +520,8 @@ def main():
 
     router = bench_router(torch, w4, synth, args, dev)
     log(f"router top-k: {router}")
+    lm_head = bench_lm_head(torch, w4, synth, args, dev)
+    log(f"lm-head gemv: {lm_head}")
 
     stack = None
     if not args.no_stack:
@@ -529,6 +565,7 @@ def main():
         "decode_m32": m32,
         "stack_40": stack,
         "router_topk": router,
+        "gemv_lm_head": lm_head,
     }
     print(json.dumps(rec), flush=True)
 

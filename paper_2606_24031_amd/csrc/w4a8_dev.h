@@ -321,4 +321,39 @@ __device__ __forceinline__ void q8_0_lane(const float *__restrict__ x, uint8_t *
   }
 }
 
+// LDS staging of activation blocks (see dot8_lds): each block's nibble-split
+// form as 8 dwords, groups of 8 blocks 272 bytes apart (16 bytes of padding
+// per group), then scale [n] fp32 and correction [n] int32, carved from one
+// dynamic LDS buffer.  The lanes of a wave read up to 8 different groups at
+// once; without the padding those addresses would be 256 bytes apart and all
+// fall in the same LDS banks.
+constexpr int GROUP_U4 = 17;   // uint4 per 8-block group: 16 of codes + 1 of padding
+struct ActBuf {
+  uint4 *codes;
+  float *d;
+  int *corr;
+};
+
+__host__ __device__ constexpr size_t act_codes_bytes(int nblocks) {
+  return (size_t)((nblocks + 7) / 8) * GROUP_U4 * 16;
+}
+__device__ __forceinline__ ActBuf act_buf(uint8_t *base, int nblocks) {
+  ActBuf b;
+  b.codes = reinterpret_cast<uint4 *>(base);
+  b.d = reinterpret_cast<float *>(base + act_codes_bytes(nblocks));
+  b.corr = reinterpret_cast<int *>(base + act_codes_bytes(nblocks) + (size_t)nblocks * 4);
+  return b;
+}
+__host__ __device__ constexpr size_t act_buf_bytes(int nblocks) {
+  return (act_codes_bytes(nblocks) + (size_t)nblocks * 8 + 15) / 16 * 16;
+}
+// dword j (0..7) of block blk's nibble-split form
+__device__ __forceinline__ uint32_t *code_word(ActBuf b, int blk, int j) {
+  return reinterpret_cast<uint32_t *>(b.codes + (blk >> 3) * GROUP_U4) + (blk & 7) * 8 + j;
+}
+// the codes of the 8-block group starting at block blk0 (a multiple of 8)
+__device__ __forceinline__ const uint4 *group_codes(ActBuf b, int blk0) {
+  return b.codes + (blk0 >> 3) * GROUP_U4;
+}
+
 }  // namespace w4a8

@@ -98,6 +98,21 @@ def test_gemv_unit_scales_give_exact_integer_dots(N, K):
     assert np.array_equal(y.astype(np.float64), y_ref)
 
 
+def test_gemv_lm_head_shape_sampled_rows():
+    """The output projection's shape (N = 151936 vocabulary rows, K = 2048):
+    random Q4_0 blocks made on the host, 200 sampled rows and the first and
+    last rows against the oracle."""
+    N, K = 151936, 2048
+    g = synth.rng(500)
+    w = synth.q4_0_random_blocks(g, N, K).reshape(N, K // 32 * 18)
+    x = synth.normal_f32(g, (K,))
+    xq = oracle.q8_0_quantize(x)
+    y = host(w4.q4q8_gemv(dev(w), dev(xq), N, K))
+    rows = np.unique(np.concatenate([[0, N - 1], g.choice(N, 200, replace=False)]))
+    y_ref, R = oracle.gemv(w[rows], xq, len(rows), K)
+    assert np.all(np.abs(y[rows] - y_ref) <= 1e-5 * R)
+
+
 def test_gemv_zero_codes_give_zero():
     N, K = 100, 512
     w = np.zeros((N, K // 32, 18), np.uint8)
