@@ -29,11 +29,11 @@ namespace w4a8 {
 int launch_fill_zero(void *ptr, size_t bytes, hipStream_t s);
 bool small_supported(int64_t H, int64_t I);
 int64_t small_max_chunks(int64_t T, int64_t E, int64_t k, int has_shared);
-int small_gateup(const uint8_t *w_gu, const uint8_t *ws_gu, const SplitBlk *xs,
+int small_gateup(const uint8_t *w_gu, const uint8_t *ws_gu, const uint8_t *xs,
                  const int32_t *meta, const int32_t *perm, const int4 *chunks, float *h,
-                 uint8_t *hq, SplitBlk *hs, int64_t maxchunks, int64_t T, int64_t H, int64_t I,
+                 uint8_t *hq, uint8_t *hs, int64_t maxchunks, int64_t T, int64_t H, int64_t I,
                  int64_t E, int64_t k, hipStream_t s);
-int small_down(const uint8_t *w_d, const uint8_t *ws_d, const SplitBlk *hs, const int32_t *meta,
+int small_down(const uint8_t *w_d, const uint8_t *ws_d, const uint8_t *hs, const int32_t *meta,
                const int32_t *perm, const int4 *chunks, const float *topk_w,
                const float *shared_w, float *y, int64_t maxchunks, int64_t T, int64_t H,
                int64_t I, int64_t E, int64_t k, hipStream_t s);
@@ -101,8 +101,8 @@ Layout make_layout(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k) {
   L.hq = off;     off += up256((size_t)P * (I / QK) * Q8B);
   L.y = off;      off += up256(sizeof(float) * (size_t)P * H);
   L.xn = off;     off += up256(sizeof(float) * (size_t)T * H);
-  L.xs = off;     off += up256(sizeof(SplitBlk) * (size_t)T * (H / QK));
-  L.hs = off;     off += up256(sizeof(SplitBlk) * (size_t)P * (I / QK));
+  L.xs = off;     off += up256((size_t)T * split_row_bytes(H / QK));
+  L.hs = off;     off += up256((size_t)P * split_row_bytes(I / QK));
   L.xa = off;     off += up256((size_t)T * H);          // aligned Q8_0 codes of x
   L.xd = off;     off += up256(sizeof(float) * (size_t)T * (H / QK));
   L.ha = off;     off += up256((size_t)P * I);          // aligned Q8_0 codes of h
@@ -375,10 +375,10 @@ __device__ __forceinline__ void route_body(const RouteArgs &a) {
 struct Q8Args {
   const float *x;
   uint8_t *xq;
-  SplitBlk *xs;     // nibble-split copy (small-group kernels), or null
+  uint8_t *xs;      // nibble-split copy (small-group kernels, split_blk rows), or null
   uint32_t *xa;     // aligned codes and fp32 scales (MFMA kernels), or null
   float *xd;
-  int64_t nblocks;
+  int64_t nblocks, nbrow;   // blocks in all, per row
 };
 
 // Stages 1 and 2 in one launch (they are independent): workgroup 0 routes,
@@ -389,7 +389,7 @@ __global__ __launch_bounds__(ROUTE_T) void prep_kernel(RouteArgs a, Q8Args q) {
     route_body<REG>(a);
     return;
   }
-  q8_0_lane(q.x, q.xq, q.xs, q.xa, q.xd, q.nblocks,
+  q8_0_lane(q.x, q.xq, q.xs, q.xa, q.xd, q.nblocks, q.nbrow,
             (int64_t)(blockIdx.x - 1) * ROUTE_T + threadIdx.x);
 }
 
@@ -448,8 +448,8 @@ int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
   const int ms = small_supported(H, I) ? small_rows(T) : 0;
   // with ms >= T every group (at most T rows) is small: no MFMA tiles
   const bool tiles = ms < T;
-  SplitBlk *xs = reinterpret_cast<SplitBlk *>(ws + L.xs);
-  SplitBlk *hs = reinterpret_cast<SplitBlk *>(ws + L.hs);
+  uint8_t *xs = ws + L.xs;
+  uint8_t *hs = ws + L.hs;
   uint32_t *xa = reinterpret_cast<uint32_t *>(ws + L.xa);
   uint32_t *ha = reinterpret_cast<uint32_t *>(ws + L.ha);
   float *xd = reinterpret_cast<float *>(ws + L.xd);
@@ -461,6 +461,7 @@ int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
   qa.xa = tiles ? xa : nullptr;
   qa.xd = xd;
   qa.nblocks = T * (H / QK);
+  qa.nbrow = H / QK;
 
   RouteArgs ra;
   ra.ids = ids;

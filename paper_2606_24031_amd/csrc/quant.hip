@@ -11,13 +11,11 @@
 
 namespace w4a8 {
 
-// 8 lanes per block (q8_0_lane); xs and xa may be null.
+// 8 lanes per block (q8_0_lane).
 __global__ __launch_bounds__(256) void q8_0_kernel(const float *__restrict__ x,
-                                                   uint8_t *__restrict__ xq,
-                                                   SplitBlk *__restrict__ xs,
-                                                   uint32_t *__restrict__ xa,
-                                                   float *__restrict__ xd, int64_t nblocks) {
-  q8_0_lane(x, xq, xs, xa, xd, nblocks, (int64_t)blockIdx.x * blockDim.x + threadIdx.x);
+                                                   uint8_t *__restrict__ xq, int64_t nblocks) {
+  q8_0_lane(x, xq, nullptr, nullptr, nullptr, nblocks, 1,
+            (int64_t)blockIdx.x * blockDim.x + threadIdx.x);
 }
 
 __global__ __launch_bounds__(256) void q4_0_kernel(const float *__restrict__ w,
@@ -90,8 +88,7 @@ int launch_fill_zero(void *ptr, size_t bytes, hipStream_t s) {
 int launch_q8_0(const float *x, uint8_t *xq, int64_t nblocks, hipStream_t s) {
   if (nblocks == 0) return W4A8_OK;
   const int64_t grid = (nblocks * 8 + 255) / 256;
-  q8_0_kernel<<<dim3((unsigned)grid), dim3(256), 0, s>>>(x, xq, nullptr, nullptr, nullptr,
-                                                          nblocks);
+  q8_0_kernel<<<dim3((unsigned)grid), dim3(256), 0, s>>>(x, xq, nblocks);
   return check_launch();
 }
 

@@ -202,6 +202,20 @@ struct SplitBlk {
 };
 static_assert(sizeof(SplitBlk) == 48, "split block layout");
 
+// Rows of SplitBlk in global memory (the small-group kernels' activations):
+// every group of 8 blocks takes 8 records (384 bytes) and 16 bytes of
+// padding, so that in an LDS copy of a row the lanes reading different
+// groups hit different banks.  nblk (blocks per row) is a multiple of 8.
+constexpr int SPLIT_GROUP_BYTES = 400;
+__host__ __device__ constexpr size_t split_row_bytes(int64_t nblk) {
+  return (size_t)(nblk / 8) * SPLIT_GROUP_BYTES;
+}
+__device__ __forceinline__ SplitBlk *split_blk(uint8_t *base, int64_t row, int64_t nblk,
+                                               int64_t blk) {
+  return reinterpret_cast<SplitBlk *>(base + row * (int64_t)split_row_bytes(nblk) +
+                                      (blk >> 3) * SPLIT_GROUP_BYTES + (blk & 7) * 48);
+}
+
 // SiLU(g) = g / (1 + e^-g) with the hardware base-2 exponential and
 // reciprocal (each within about one ulp).
 __device__ __forceinline__ float silu_f32(float g) {
@@ -287,12 +301,13 @@ __device__ __forceinline__ void store_q8_0_block8(uint8_t *blk, int j, uint32_t 
 
 // Q8_0 of one 32-element block of x by 8 lanes (thread tid: block tid / 8,
 // elements 4 (tid % 8) .. + 3): the 34-byte block, and when the pointers are
-// set its nibble-split form (xs) and its 32 codes on a 32-byte boundary with
-// the fp32 scale (xa, xd).  Lanes past nblocks take part in the exchanges and
-// store nothing.
+// set its nibble-split form (xs, rows of nbrow blocks, see split_blk) and its
+// 32 codes on a 32-byte boundary with the fp32 scale (xa, xd).  Lanes past
+// nblocks take part in the exchanges and store nothing.
 __device__ __forceinline__ void q8_0_lane(const float *__restrict__ x, uint8_t *__restrict__ xq,
-                                          SplitBlk *__restrict__ xs, uint32_t *__restrict__ xa,
-                                          float *__restrict__ xd, int64_t nblocks, int64_t tid) {
+                                          uint8_t *__restrict__ xs, uint32_t *__restrict__ xa,
+                                          float *__restrict__ xd, int64_t nblocks, int64_t nbrow,
+                                          int64_t tid) {
   const int64_t blk = tid >> 3;
   const int j = (int)(tid & 7);
   float v[4] = {0.f, 0.f, 0.f, 0.f};
@@ -308,10 +323,12 @@ __device__ __forceinline__ void q8_0_lane(const float *__restrict__ x, uint8_t *
     const uint32_t word = split_word(packed, j);
     const int lsum = sum8(low_nibble_sum(packed));
     if (live) {
-      xs[blk].w[j] = word;
+      const int64_t r = blk / nbrow;
+      SplitBlk *sb = split_blk(xs, r, nbrow, blk - r * nbrow);
+      sb->w[j] = word;
       if (j == 0) {
-        xs[blk].d = f16_bits_to_f32(d16);
-        xs[blk].corr = -8 * lsum;
+        sb->d = f16_bits_to_f32(d16);
+        sb->corr = -8 * lsum;
       }
     }
   }
