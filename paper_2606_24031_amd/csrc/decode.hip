@@ -39,9 +39,16 @@
 // bytes, also published with the same tag) straight into its own staging, so
 // progress never depends on the order in which the hardware starts
 // workgroups.
+//
+// With the router in front (router logits instead of ids and weights), every
+// workgroup first takes the token's top-k itself in one wave (wave_topk, the
+// router kernel's own code, so the same decisions and bits) into LDS; the
+// first workgroup also writes the ids, weights and gate value out.  The
+// selection costs a few hundred ns on each workgroup's path to its weight
+// loads, less than a launch of its own and the gap behind it.
 #include <cstdlib>
 
-#include "w4a8_dev.h"
+#include "router_dev.h"
 #include "w4a8_host.h"
 
 namespace w4a8 {
@@ -82,6 +89,13 @@ struct DecodeArgs {
   uint8_t *xq;             // documented copy of Q8_0(x)   [H/32 blocks]
   float *h;                // documented copy of h          [(k+1)][I]
   uint8_t *hq;             // documented copy of Q8_0(h)    [(k+1)][I/32 blocks]
+  // router in front (logits != nullptr): ids, topk_w and shared_w are
+  // taken in the launch (see route_in_wg) and written out by workgroup 0
+  const float *logits;     // [E] or nullptr
+  const float *gate;       // the shared expert's gate logit [1], or nullptr
+  int32_t *route_ids;      // [k]
+  float *route_w;          // [k]
+  float *route_gate;       // [1]
   int H, I, E, k;
   int rb;                  // down rows per slab
   int spin_rounds;         // poll rounds before a slab computes h itself
@@ -274,6 +288,25 @@ __device__ void gateup_block(const DecodeArgs &a, int q, int e, int b, ActBuf xb
 __device__ __forceinline__ float4 load_x_first(const DecodeArgs &a) {
   return (int)threadIdx.x < a.H / 4 ? input4(a, threadIdx.x) : make_float4(0.f, 0.f, 0.f, 0.f);
 }
+// The same in two halves: the loads of x and resid issued, the sum taken later.
+struct XFirst {
+  float4 x, r;
+};
+__device__ __forceinline__ XFirst issue_x_first(const DecodeArgs &a) {
+  XFirst f{make_float4(0.f, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f)};
+  if ((int)threadIdx.x < a.H / 4) {
+    f.x = reinterpret_cast<const float4 *>(a.x)[threadIdx.x];
+    if (a.resid) f.r = reinterpret_cast<const float4 *>(a.resid)[threadIdx.x];
+  }
+  return f;
+}
+__device__ __forceinline__ float4 x_first(const DecodeArgs &a, const XFirst &f) {
+  float4 v = f.x;
+  if (a.resid) {
+    v.x += f.r.x; v.y += f.r.y; v.z += f.r.z; v.w += f.r.w;
+  }
+  return v;
+}
 
 // Every workgroup arrives once; the last arrival of the launch advances the
 // call counter to `tag` and clears the arrival counters.  Each workgroup has
@@ -347,6 +380,55 @@ __device__ bool collect(const DecodeArgs &a, ActBuf hb, uint32_t tag, int cnt, u
   return notdone[0] == 0;
 }
 
+// The router's inputs, loaded by wave 0 at the start of the launch (RV
+// logits per lane, E <= 64 * RV, clamped addresses masked afterwards, and
+// the gate logit) so that they are first in the wave's load queue.
+template <int RV>
+__device__ __forceinline__ void route_issue(const DecodeArgs &a, float (&x)[RV], float &g) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int r = 0; r < RV; r++) x[r] = a.logits[min(lane + 64 * r, a.E - 1)];
+  // a vector load (an index the compiler cannot see through): a scalar load
+  // would be waited for before the loads issued after it
+  int zero = 0;
+  asm volatile("" : "+v"(zero));
+  g = a.gate ? a.gate[zero] : 0.0f;
+}
+
+// The token's top-k in wave 0 into the LDS arrays rid[k] and rw[k + 1] (the
+// shared expert's weight last), which then stand in for the ids and
+// weights; workgroup 0 also writes them out.  Every thread must call it.
+template <int RV>
+__device__ void route_finish(DecodeArgs &a, float (&x)[RV], float g, int32_t *rid, float *rw) {
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+#pragma unroll
+    for (int r = 0; r < RV; r++)
+      if (lane + 64 * r >= a.E) x[r] = -INFINITY;
+    float selv;
+    int seli;
+    wave_topk<RV>(x, a.k, selv, seli);
+    const float wt = topk_weight(selv, a.k);
+    const float gw = a.gate ? shared_gate(g) : 1.0f;
+    if (lane < a.k) {
+      rid[lane] = seli;
+      rw[lane] = wt;
+    }
+    if (lane == 0) rw[a.k] = gw;
+    if (blockIdx.x == 0) {
+      if (lane < a.k) {
+        a.route_ids[lane] = seli;
+        a.route_w[lane] = wt;
+      }
+      if (lane == 0 && a.gate) a.route_gate[0] = gw;
+    }
+  }
+  __syncthreads();
+  a.ids = rid;
+  a.topk_w = rw;
+  a.shared_w = rw + a.k;
+}
+
 // LDS: Q8_0(x) staging, then Q8_0(h) staging of every pair, then the
 // weighted per-pair sums [rb][k+1 padded to 4] and, when I > 512, the down
 // partials (NT floats).
@@ -356,23 +438,36 @@ __host__ __device__ constexpr size_t lds_bytes(int H, int I, int k, int rb) {
          sizeof(float) * ((size_t)rb * ((k + 1 + 3) & ~3) + (size_t)NT);
 }
 
+// RV > 0: the router in front, RV logits per lane (see route_in_wg).
+template <int RV>
 __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
   extern __shared__ __align__(16) uint8_t lds[];
   __shared__ float hv[32];
   __shared__ float wq[64];
   __shared__ int notdone[3];
+  __shared__ int32_t rid[64];
+  __shared__ float rw[64];
   const int npairs = a.k + 1;
   const int nb_h = a.I / 32;                  // gate/up items per pair
   const int nbh = npairs * nb_h;              // h blocks of every pair
   const int wg = blockIdx.x;
   const ActBuf xb = act_buf(lds, a.H / 32);
+  // the router's inputs first, then a gate/up item's x, all in flight
+  // before anything waits
+  constexpr int RVX = RV > 0 ? RV : 1;
+  float lx[RVX];
+  float lg = 0.0f;
+  if (RV > 0 && threadIdx.x < 64) route_issue<RVX>(a, lx, lg);
+  XFirst xf{make_float4(0.f, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f)};
+  if (wg < nbh) xf = issue_x_first(a);
+  if (RV > 0) route_finish<RVX>(a, lx, lg, rid, rw);
+  const float4 x0 = x_first(a, xf);
 
   if (wg < nbh) {
     // --------------------------------------------------- gate/up item
     const int q = wg / nb_h, b = wg - q * nb_h;
     // x and the expert id land before the weights are issued: on every path
     // the later uses of x then wait for nothing in flight behind them
-    const float4 x0 = load_x_first(a);
     int e;
     const bool valid = pair_valid(a, q, e);
     asm volatile("" ::"v"(x0.x), "v"(x0.y), "v"(x0.z), "v"(x0.w), "v"(e));
@@ -513,6 +608,10 @@ size_t decode_xfer_words(int64_t I, int64_t k) {
   return (size_t)XFER_HDR + (size_t)(k + 1) * (I / 32) * XSTRIDE * 2;
 }
 
+// Router in front of the launch: the logits of E experts fit wave 0's
+// registers.
+bool decode_routes(int64_t E, int64_t k) { return E <= 512 && k <= 32 && k <= E; }
+
 bool decode_supported(int64_t H, int64_t I, int64_t k) {
   // Gate/up items: 8 waves x 4 h columns = one 32-column block.  Down slabs
   // hold every pair of one down row at one unit per lane; a lane collects at
@@ -525,7 +624,8 @@ bool decode_supported(int64_t H, int64_t I, int64_t k) {
   return XW * nbh <= NWMAX * NT && lds_bytes((int)H, (int)I, (int)k, rb) <= 48 * 1024;
 }
 
-int decode_forward(const float *x, const DecodeNorm &norm, const int32_t *ids,
+int decode_forward(const float *x, const DecodeNorm &norm, const DecodeRoute *route,
+                   const int32_t *ids,
                    const float *topk_w, const float *shared_w, const uint8_t *w_gu,
                    const uint8_t *w_d,
                    const uint8_t *ws_gu, const uint8_t *ws_d, float *out, int64_t H, int64_t I,
@@ -543,6 +643,13 @@ int decode_forward(const float *x, const DecodeNorm &norm, const int32_t *ids,
   a.resid = norm.resid; a.gamma = norm.gamma; a.x_out = norm.x_out; a.xn = norm.xn;
   a.eps = norm.eps;
   a.xq = xq; a.h = h; a.hq = hq;
+  a.logits = nullptr; a.gate = nullptr;
+  a.route_ids = nullptr; a.route_w = nullptr; a.route_gate = nullptr;
+  if (route != nullptr) {
+    if (!decode_routes(E, k)) return W4A8_ERANGE;
+    a.logits = route->logits; a.gate = route->gate;
+    a.route_ids = route->ids; a.route_w = route->w; a.route_gate = route->gate_w;
+  }
   a.H = (int)H; a.I = (int)I; a.E = (int)E; a.k = (int)k;
   int grid = 0;
   decode_grid(H, I, k, ncu, grid, a.rb);
@@ -550,7 +657,12 @@ int decode_forward(const float *x, const DecodeNorm &norm, const int32_t *ids,
   a.spin_rounds = 2000;
   if (const char *env = std::getenv("W4A8_DECODE_SPIN_ROUNDS")) a.spin_rounds = std::atoi(env);
   const size_t lds = lds_bytes((int)H, (int)I, (int)k, a.rb);
-  decode_kernel<<<dim3((unsigned)grid), dim3(NT), lds, s>>>(a);
+  if (route == nullptr)
+    decode_kernel<0><<<dim3((unsigned)grid), dim3(NT), lds, s>>>(a);
+  else if (E <= 256)
+    decode_kernel<4><<<dim3((unsigned)grid), dim3(NT), lds, s>>>(a);
+  else
+    decode_kernel<8><<<dim3((unsigned)grid), dim3(NT), lds, s>>>(a);
   return check_launch();
 }
 

@@ -49,7 +49,9 @@ int mfma_down(const uint8_t *w_d, const uint8_t *ws_d, const uint32_t *ha, const
 size_t decode_sync_words(int64_t H);
 size_t decode_xfer_words(int64_t I, int64_t k);
 bool decode_supported(int64_t H, int64_t I, int64_t k);
-int decode_forward(const float *x, const DecodeNorm &norm, const int32_t *ids,
+bool decode_routes(int64_t E, int64_t k);
+int decode_forward(const float *x, const DecodeNorm &norm, const DecodeRoute *route,
+                   const int32_t *ids,
                    const float *topk_w, const float *shared_w, const uint8_t *w_gu,
                    const uint8_t *w_d,
                    const uint8_t *ws_gu, const uint8_t *ws_d, float *out, int64_t H, int64_t I,
@@ -433,7 +435,7 @@ int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
   // One token: the whole layer in a single launch, the residual RMSNorm
   // included (see decode.hip).
   if (T == 1 && decode_supported(H, I, k))
-    return decode_forward(hidden, norm, ids, topk_w, shared_w, w_gu, w_d, ws_gu, ws_d, out, H, I,
+    return decode_forward(hidden, norm, nullptr, ids, topk_w, shared_w, w_gu, w_d, ws_gu, ws_d, out, H, I,
                           E, k,
                           reinterpret_cast<uint32_t *>(ws + L.sync),
                           reinterpret_cast<uint32_t *>(ws + L.xfer), ws + L.xq,
@@ -652,6 +654,29 @@ extern "C" int moe_w4a8_layer_routed(const float *x, const float *y_prev, const 
   uint8_t *ws = reinterpret_cast<uint8_t *>(workspace);
   float *sw = shared_gate ? reinterpret_cast<float *>(ws + L.sw) : nullptr;
   hipStream_t s = as_stream(stream);
+  if (T == 1 && decode_supported(H, I, k) && decode_routes(E, k)) {
+    // one launch: the routing runs inside the single-token layer kernel
+    DecodeNorm norm;
+    norm.resid = y_prev;
+    norm.gamma = gamma;
+    norm.x_out = x_out;
+    norm.eps = eps;
+    if (gamma) norm.xn = reinterpret_cast<float *>(ws + L.xn);
+    DecodeRoute route;
+    route.logits = router_logits;
+    route.gate = shared_gate;
+    route.ids = topk_ids;
+    route.w = topk_w;
+    route.gate_w = sw;
+    return decode_forward(x, norm, &route, nullptr, nullptr, nullptr,
+                          reinterpret_cast<const uint8_t *>(w_gate_up),
+                          reinterpret_cast<const uint8_t *>(w_down),
+                          reinterpret_cast<const uint8_t *>(ws_gate_up),
+                          reinterpret_cast<const uint8_t *>(ws_down), out, H, I, E, k,
+                          reinterpret_cast<uint32_t *>(ws + L.sync),
+                          reinterpret_cast<uint32_t *>(ws + L.xfer), ws + L.xq,
+                          reinterpret_cast<float *>(ws + L.h), ws + L.hq, s);
+  }
   if ((rc = router_launch(router_logits, topk_ids, topk_w, shared_gate, sw, T, E, k, s)) !=
       W4A8_OK)
     return rc;

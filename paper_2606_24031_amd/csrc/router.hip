@@ -2,16 +2,11 @@
 // to its top-k of E routed experts; the k gate values are renormalized over
 // the selection, as the Qwen3-series models do).
 //
-// One wave per token.  The token's logits sit in registers (E <= 512) or in
-// LDS; k rounds each take the wave's largest remaining logit (a lane scans
-// its strided share in index order, then DPP exchanges and row broadcasts
-// keep the larger value, or on equal values the lower index) and mark it
-// taken.  The selection compares the fp32 logits themselves: softmax is
-// monotone, so this is the order of the probabilities without any rounding
-// in the decision.  The weights are
-// exp(l_j - l_max) over their sum across the selection (the full softmax
-// denominator cancels in the renormalization), summed in a fixed butterfly.
-#include "w4a8_dev.h"
+// One wave per token.  The token's logits sit in registers (E <= 512, see
+// wave_topk) or in LDS (larger E: k rounds in which each lane scans its
+// strided share in index order and DPP exchanges and row broadcasts keep the
+// larger value, or on equal values the lower index).
+#include "router_dev.h"
 #include "w4a8_host.h"
 
 namespace w4a8 {
@@ -46,8 +41,8 @@ __device__ __forceinline__ void wave_argmax(float &v, int &i) {
   dpp_better<DPP_XOR2, 0xF>(v, i);
   dpp_better<DPP_HALF_MIRROR, 0xF>(v, i);
   dpp_better<DPP_ROR8, 0xF>(v, i);
-  dpp_better<0x142, 0xA>(v, i);    // row_bcast:15 into rows 1 and 3
-  dpp_better<0x143, 0xC>(v, i);    // row_bcast:31 into rows 2 and 3
+  dpp_better<DPP_ROW_BCAST15, 0xA>(v, i);   // into rows 1 and 3
+  dpp_better<DPP_ROW_BCAST31, 0xC>(v, i);   // into rows 2 and 3
   v = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
   i = __builtin_amdgcn_readlane(i, 63);
 }
@@ -68,36 +63,18 @@ __global__ __launch_bounds__(RT) void router_kernel(const float *__restrict__ lo
   const float *row = logits + t * E;
   float selv = 0.0f;
   int seli = 0;                    // lane j < k: the j-th selection
+  float gv = 0.0f;                 // the gate logit (lane 0)
   if (RV > 0) {
     float x[RV > 0 ? RV : 1];
+    // every load in flight at once (clamped addresses, masked afterwards),
+    // the gate logit's too
 #pragma unroll
-    for (int r = 0; r < RV; r++) {
-      const int e = lane + 64 * r;
-      x[r] = e < E ? row[e] : -INFINITY;
-    }
-    for (int j = 0; j < k; j++) {
-      // this lane's largest remaining logit, a pairwise tree in which the
-      // left (lower index) side keeps equal values
-      float tv[RV > 0 ? RV : 1];
-      int ti[RV > 0 ? RV : 1];
+    for (int r = 0; r < RV; r++) x[r] = row[min(lane + 64 * r, E - 1)];
+    gv = gate != nullptr && lane == 0 ? gate[t] : 0.0f;
 #pragma unroll
-      for (int r = 0; r < RV; r++) { tv[r] = x[r]; ti[r] = lane + 64 * r; }
-#pragma unroll
-      for (int w = 1; w < RV; w *= 2)
-#pragma unroll
-        for (int r = 0; r + w < RV; r += 2 * w) {
-          const bool take = tv[r + w] > tv[r];
-          tv[r] = take ? tv[r + w] : tv[r];
-          ti[r] = take ? ti[r + w] : ti[r];
-        }
-      float bv = tv[0];
-      int bi = ti[0];
-      wave_argmax(bv, bi);
-      if (lane == j) { selv = bv; seli = bi; }
-#pragma unroll
-      for (int r = 0; r < RV; r++)
-        if (bi == lane + 64 * r) x[r] = -INFINITY;   // taken (the logits are finite)
-    }
+    for (int r = 0; r < RV; r++)
+      if (lane + 64 * r >= E) x[r] = -INFINITY;
+    wave_topk<(RV > 0 ? RV : 1)>(x, k, selv, seli);
   } else {
     float *v = lv + (size_t)wave * E;
     for (int e = lane; e < E; e += 64) v[e] = row[e];
@@ -113,17 +90,13 @@ __global__ __launch_bounds__(RT) void router_kernel(const float *__restrict__ lo
       if (lane == (bi & 63)) v[bi] = -INFINITY;
     }
   }
-  const float lmax = __shfl(selv, 0);
-  const float ex = lane < k ? expf(selv - lmax) : 0.0f;
-  float s = ex;
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+  const float wt = topk_weight(selv, k);
   if (lane < k) {
     ids[t * k + lane] = seli;
-    weights[t * k + lane] = ex / s;
+    weights[t * k + lane] = wt;
   }
   // the shared expert's sigmoid gate
-  if (gate != nullptr && lane == 0) gate_w[t] = 1.0f / (1.0f + expf(-gate[t]));
+  if (gate != nullptr && lane == 0) gate_w[t] = shared_gate(RV > 0 ? gv : gate[t]);
 }
 
 }  // namespace

@@ -37,4 +37,15 @@ struct DecodeNorm {
   float eps = 0.0f;
 };
 
+// Router in front of the single-token layer: the top-k of the token's logits
+// (and the shared expert's sigmoid gate) taken inside the layer's launch;
+// ids, weights and the gate value are also written out.
+struct DecodeRoute {
+  const float *logits = nullptr;   // [E]
+  const float *gate = nullptr;     // [1] or null (shared expert weight 1)
+  int32_t *ids = nullptr;          // [k]
+  float *w = nullptr;              // [k]
+  float *gate_w = nullptr;         // [1], written when gate is set
+};
+
 }  // namespace w4a8

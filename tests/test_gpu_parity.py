@@ -464,7 +464,7 @@ def test_moe_layer_routed(qwen_layer, T, gated):
     and its Q8_0 as for moe_layer; the output through the MoE check, with the
     GPU's own routing weights for the routed slots (they are the layer's
     input) and the oracle's fp64 sigmoid of the gate for the shared expert
-    (T = 1: router launch, then the single decode launch; T = 6: VALU path;
+    (T = 1: the routing inside the single decode launch; T = 6: VALU path;
     T = 40: MFMA tiles as well)."""
     L = qwen_layer
     g = synth.rng(80 + T)
@@ -494,6 +494,41 @@ def test_moe_layer_routed(qwen_layer, T, gated):
     hq = wsn[lay["hq"]:lay["hq"] + P * (L.I // 32) * 34].reshape(P, -1)
     sw = 1.0 / (1.0 + np.exp(-gate.astype(np.float64))) if gated else None
     L.check(xn, ids, wts, 8, host(out), h, hq, shared_w=sw)
+
+
+@pytest.mark.parametrize("E,k,ties,gated", [(256, 8, True, True), (300, 8, False, False),
+                                             (512, 32, True, True), (8, 8, True, False)])
+def test_routed_decode_matches_router_kernel(E, k, ties, gated):
+    """T = 1: the top-k taken inside the single-token launch gives the router
+    kernel's ids and weights bit for bit (the same wave top-k on both), with
+    equal logits, with 256 < E <= 512 (eight logits per lane) and with k = E;
+    ids also against the oracle, the layer output through the MoE check."""
+    L = Layer(90 + E, 256, 256, E)
+    g = synth.rng(91 + E + k)
+    x = synth.normal_f32(g, (1, L.H))
+    y_prev = synth.normal_f32(g, (1, L.H), 0.3)
+    gamma = np.ones(L.H, np.float32)
+    logits = synth.normal_f32(g, (1, E))
+    if ties:
+        logits = (np.round(logits * 2.0) / 2.0).astype(np.float32)
+    gate = synth.normal_f32(g, (1,), 2.0) if gated else None
+    ws = w4.moe_workspace(1, L.H, L.I, E, k)
+    x_out, out, ids_d, w_d = w4.moe_layer_routed(
+        dev(x), dev(y_prev), dev(gamma), dev(logits), L.d_gu, L.d_d, L.d_sgu, L.d_sd,
+        L.H, L.I, E, k, ws, shared_gate=dev(gate) if gated else None)
+    ids_k, w_k = w4.router_topk(dev(logits), k)
+    ids, wts = host(ids_d), host(w_d)
+    assert np.array_equal(ids, host(ids_k))
+    assert np.array_equal(wts.view(np.uint32), host(w_k).view(np.uint32))
+    assert np.array_equal(ids, oracle.router_topk(logits, k)[0])
+    lay = w4.moe_workspace_layout(1, L.H, L.I, E, k)
+    wsn = host(ws)
+    xn = wsn[lay["xn"]:lay["xn"] + L.H * 4].view(np.float32).reshape(1, L.H)
+    P = k + 1
+    h = wsn[lay["h"]:lay["h"] + P * L.I * 4].view(np.float32).reshape(P, L.I)
+    hq = wsn[lay["hq"]:lay["hq"] + P * (L.I // 32) * 34].reshape(P, -1)
+    sw = 1.0 / (1.0 + np.exp(-gate.astype(np.float64))) if gated else None
+    L.check(xn, ids, wts, k, host(out), h, hq, shared_w=sw)
 
 
 # ------------------------------------------------------------ router top-k
