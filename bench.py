@@ -162,6 +162,51 @@ def bench_decode(torch, w4, synth, layers, args, dev):
     return ms, nbytes
 
 
+def bench_decode_invariants(torch, w4, synth, layers, args, dev, n=500):
+    """Single-token layer at E = 128 (the first 128 experts of the same
+    weight sets: the bytes per step are those of E = 256, so the time should
+    be too) and at k = 4 (5 experts per step instead of 9)."""
+    res = {}
+    for name, e_, k_ in (("E128_k8", 128, 8), ("E256_k4", 256, 4)):
+        rng = synth.rng(args.seed + 11)
+        ids_all, wts_all = synth.routing(rng, n, e_, k_)
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(args.seed + 12)
+        x_all = torch.randn((n, 1, H), generator=gen, device=dev)
+        ids_d = torch.from_numpy(ids_all).to(dev).view(n, 1, k_)
+        wts_d = torch.from_numpy(wts_all).to(dev).view(n, 1, k_)
+        ws = w4.moe_workspace(1, H, I, e_, k_, device=dev)
+        out = torch.empty((1, H), dtype=torch.float32, device=dev)
+
+        def step(i):
+            L = layers[i % len(layers)]
+            w4.moe_forward(x_all[i], ids_d[i], wts_d[i], L[0], L[1], L[2], L[3], H, I, e_, k_,
+                           ws, out=out)
+
+        for i in range(20):
+            step(i)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for i in range(n):
+                step(i)
+        graph.replay()
+        torch.cuda.synchronize()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        ev0.record()
+        graph.replay()
+        ev1.record()
+        torch.cuda.synchronize()
+        ms = ev0.elapsed_time(ev1)
+        nbytes = sum((len({int(e) for e in ids_all[i]}) + 1) * EXPERT_BYTES + 2 * H * 4 + k_ * 8
+                     for i in range(n))
+        gbps = nbytes / (ms * 1e-3) / 1e9
+        res[name] = {"us_per_step": round(ms * 1e3 / n, 2), "GBps": round(gbps, 1),
+                     "hbm_peak_frac": round(gbps / HBM_PEAK_GBPS, 4), "launch": "hipGraph"}
+    return res
+
+
 def bench_prefill(torch, w4, synth, layers, args, dev):
     T = 947
     rng = synth.rng(args.seed + 3)
@@ -518,6 +563,8 @@ def main():
         m32 = bench_m32(torch, w4, synth, layers, args, dev)
         log(f"decode M=32: {m32}")
 
+    invariants = bench_decode_invariants(torch, w4, synth, layers, args, dev)
+    log(f"decode invariants: {invariants}")
     router = bench_router(torch, w4, synth, args, dev)
     log(f"router top-k: {router}")
     lm_head = bench_lm_head(torch, w4, synth, args, dev)
@@ -564,6 +611,7 @@ def main():
         "prefill_947": prefill,
         "decode_m32": m32,
         "stack_40": stack,
+        "decode_invariants": invariants,
         "router_topk": router,
         "gemv_lm_head": lm_head,
     }

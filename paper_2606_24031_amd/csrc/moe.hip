@@ -125,6 +125,29 @@ int validate(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k) {
 }
 
 // ------------------------------------------------------------------ route
+// Inclusive prefix sum over each 16-lane row (ROW16) or over the whole wave,
+// all lanes active, on DPP: the row_shr 1, 2, 3 partials of the original
+// values, then row_shr 4 and 8 (into the lanes of banks 1-3 and 2-3), then
+// row 0's total into row 1 and row 2's into row 3, then row 1's into rows 2
+// and 3.  Integer sums, so exact in any order.
+template <int CTRL, int ROWS, int BANKS, bool BOUND>
+__device__ __forceinline__ int dpp_or0(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, ROWS, BANKS, BOUND);
+}
+template <bool ROW16>
+__device__ __forceinline__ int scan_incl(int v) {
+  int s = v + dpp_or0<0x111, 0xF, 0xF, true>(v);   // row_shr:1
+  s += dpp_or0<0x112, 0xF, 0xF, true>(v);            // row_shr:2
+  s += dpp_or0<0x113, 0xF, 0xF, true>(v);            // row_shr:3
+  s += dpp_or0<0x114, 0xF, 0xE, true>(s);            // row_shr:4, banks 1-3
+  s += dpp_or0<0x118, 0xF, 0xC, true>(s);            // row_shr:8, banks 2-3
+  if (!ROW16) {
+    s += dpp_or0<0x142, 0xA, 0xF, false>(s);         // row_bcast:15 into rows 1, 3
+    s += dpp_or0<0x143, 0xC, 0xF, false>(s);         // row_bcast:31 into rows 2, 3
+  }
+  return s;
+}
+
 // Exclusive scans of NA arrays a[j][0..n) in LDS at once by all ROUTE_T
 // threads; tot[j] receives the total of array j.
 template <int NA>
@@ -138,33 +161,24 @@ __device__ void block_exscan(int *const (&a)[NA], int n, int (*wtot)[ROUTE_T / 6
   for (int j = 0; j < NA; j++) {
     s[j] = 0;
     for (int i = lo; i < hi; i++) s[j] += a[j][i];
-    x[j] = s[j];
-  }
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-#pragma unroll
-    for (int j = 0; j < NA; j++) {
-      const int y = __shfl_up(x[j], o);
-      if (lane >= o) x[j] += y;
-    }
+    x[j] = scan_incl<false>(s[j]);
   }
   if (lane == 63)
 #pragma unroll
     for (int j = 0; j < NA; j++) wtot[j][wave] = x[j];
   __syncthreads();
-  // the wave totals: exclusive scan by the first wave, 16 lanes per array
+  // the wave totals: exclusive scan in the first NA rows of 16 lanes, one
+  // array per row (whole rows stay active)
   constexpr int NW = ROUTE_T / 64;
-  if (tid < NA * NW) {
+  static_assert(NW == 16 && NA <= 4, "one 16-lane row per array");
+  if (tid < 64) {
     const int j = tid / NW, w = tid - j * NW;
-    const int v = wtot[j][w];
-    int c = v;
-#pragma unroll
-    for (int o = 1; o < NW; o <<= 1) {
-      const int y = __shfl_up(c, o, NW);
-      if (w >= o) c += y;
+    const int v = j < NA ? wtot[j][w] : 0;
+    const int c = scan_incl<true>(v);
+    if (j < NA) {
+      wtot[j][w] = c - v;
+      if (w == NW - 1) wtot[j][NW] = c;
     }
-    wtot[j][w] = c - v;
-    if (w == NW - 1) wtot[j][NW] = c;
   }
   __syncthreads();
 #pragma unroll
@@ -405,16 +419,28 @@ __global__ __launch_bounds__(256) void combine_kernel(const float *__restrict__ 
   if (i >= T * h4) return;
   const int64_t t = i / h4, c = i % h4;
   const float4 *y4 = reinterpret_cast<const float4 *>(y);
+  // every load of a group of 8 slots in flight before any is waited for (a
+  // skipped slot's row is read and left out), the shared expert's first
+  const float4 vs = has_shared ? y4[(T * k + t) * h4 + c] : make_float4(0.f, 0.f, 0.f, 0.f);
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int j = 0; j < k; j++) {
-    const int e = ids[t * k + j];
-    if (e < 0 || e >= E) continue;
-    const float4 v = y4[(t * k + j) * h4 + c];
-    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+  for (int j0 = 0; j0 < k; j0 += 8) {
+    int e[8];
+    float4 v[8];
+#pragma unroll
+    for (int jj = 0; jj < 8; jj++) {
+      const int j = min(j0 + jj, k - 1);
+      e[jj] = ids[t * k + j];
+      v[jj] = y4[(t * k + j) * h4 + c];
+    }
+#pragma unroll
+    for (int jj = 0; jj < 8; jj++) {
+      if (j0 + jj < k && e[jj] >= 0 && e[jj] < E) {
+        acc.x += v[jj].x; acc.y += v[jj].y; acc.z += v[jj].z; acc.w += v[jj].w;
+      }
+    }
   }
   if (has_shared) {
-    const float4 v = y4[(T * k + t) * h4 + c];
-    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+    acc.x += vs.x; acc.y += vs.y; acc.z += vs.z; acc.w += vs.w;
   }
   reinterpret_cast<float4 *>(out)[i] = acc;
 }
