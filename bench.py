@@ -96,7 +96,8 @@ def source_sha(files) -> str:
     return h.hexdigest()[:16]
 
 
-DECODE_SOURCES = ["paper_2606_24031_amd/csrc/decode.hip", "paper_2606_24031_amd/csrc/w4a8_dev.h"]
+DECODE_SOURCES = ["paper_2606_24031_amd/csrc/decode.hip", "paper_2606_24031_amd/csrc/w4a8_dev.h",
+                  "paper_2606_24031_amd/csrc/router_dev.h"]
 
 
 def measured_traffic():
