@@ -61,6 +61,8 @@ def parse():
     ap.add_argument("--stack-decode-steps", type=int, default=128)
     ap.add_argument("--no-m32", action="store_true")
     ap.add_argument("--no-stack", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the E/k invariants, router, LM-head and 1024x1024 GEMV lines")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 256 MiB device copy 5 times (for scaling the "
                          "rocprofv3 FETCH_SIZE / WRITE_SIZE counters)")
@@ -324,6 +326,57 @@ def bench_router(torch, w4, synth, args, dev):
     return res
 
 
+def bench_gemv_1024(torch, w4, synth, args, dev, copies=2048, n=2048):
+    """The single W4A8 GEMV of 1024 x 1024 (Q4_0 weights from N(0, 0.02^2),
+    one Q8_0 vector from N(0, 1)).  Its 0.59 MB of weights fit in L2, so the
+    streaming rate is taken over `copies` distinct weight copies (1.2 GB,
+    several times the last-level cache) replayed from one HIP graph; the
+    latency of repeated calls on one copy (cache-resident) is reported
+    beside it."""
+    N = K = 1024
+    g = synth.rng(args.seed)
+    W = torch.from_numpy(synth.normal_f32(g, (N, K), 0.02)).to(dev)
+    wq0 = w4.q4_0_quantize(W)
+    blk = synth.q4_0_random_blocks(g, N, K)
+    wbytes = N * (K // 32) * 18
+    pool = torch.empty((copies, wbytes), dtype=torch.uint8, device=dev)
+    pool[0].copy_(wq0.reshape(-1))
+    src = torch.from_numpy(blk.reshape(-1)).to(dev)
+    for c in range(1, copies):
+        pool[c].copy_(src)
+    xq = w4.q8_0_quantize(torch.from_numpy(synth.normal_f32(g, (1, K))).to(dev))
+    y = torch.empty(N, dtype=torch.float32, device=dev)
+    nbytes = wbytes + (K // 32) * 34 + N * 4
+
+    def timed(sel):
+        for i in range(8):
+            w4.q4q8_gemv(pool[sel(i)], xq, N, K, y=y)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for i in range(n):
+                w4.q4q8_gemv(pool[sel(i)], xq, N, K, y=y)
+        graph.replay()
+        torch.cuda.synchronize()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        ev0.record()
+        graph.replay()
+        ev1.record()
+        torch.cuda.synchronize()
+        return ev0.elapsed_time(ev1) / n * 1e3
+
+    us_stream = timed(lambda i: i % copies)
+    us_hot = timed(lambda i: 0)
+    del pool
+    return {"N": N, "K": K, "bytes_per_call": nbytes, "weight_copies": copies,
+            "us_per_call": round(us_stream, 3),
+            "GBps": round(nbytes / (us_stream / 1e6) / 1e9, 1),
+            "hbm_peak_frac": round(nbytes / (us_stream / 1e6) / 1e9 / HBM_PEAK_GBPS, 4),
+            "us_per_call_cache_resident": round(us_hot, 3),
+            "launch": "hipGraph"}
+
+
 def bench_lm_head(torch, w4, synth, args, dev):
     """The dense W4A8 GEMV at the output projection's shape (N = 151936
     vocabulary rows, K = H = 2048; random Q4_0 blocks, 175 MB), two weight
@@ -564,12 +617,16 @@ def main():
         m32 = bench_m32(torch, w4, synth, layers, args, dev)
         log(f"decode M=32: {m32}")
 
-    invariants = bench_decode_invariants(torch, w4, synth, layers, args, dev)
-    log(f"decode invariants: {invariants}")
-    router = bench_router(torch, w4, synth, args, dev)
-    log(f"router top-k: {router}")
-    lm_head = bench_lm_head(torch, w4, synth, args, dev)
-    log(f"lm-head gemv: {lm_head}")
+    invariants = router = lm_head = gemv_1024 = None
+    if not args.no_extras:
+        invariants = bench_decode_invariants(torch, w4, synth, layers, args, dev)
+        log(f"decode invariants: {invariants}")
+        router = bench_router(torch, w4, synth, args, dev)
+        log(f"router top-k: {router}")
+        lm_head = bench_lm_head(torch, w4, synth, args, dev)
+        log(f"lm-head gemv: {lm_head}")
+        gemv_1024 = bench_gemv_1024(torch, w4, synth, args, dev)
+        log(f"gemv 1024x1024: {gemv_1024}")
 
     stack = None
     if not args.no_stack:
@@ -615,6 +672,7 @@ def main():
         "decode_invariants": invariants,
         "router_topk": router,
         "gemv_lm_head": lm_head,
+        "gemv_1024": gemv_1024,
     }
     print(json.dumps(rec), flush=True)
 
