@@ -81,6 +81,7 @@ struct MLds {
   float dx[2][8][MT];              // activation scales of 8 blocks, [buffer][block][row]
   int arow[MT];                    // activation row of each tile row
   int pair[MT];                    // pair of each tile row (-1: padding)
+  float pw[MT];                    // down: combine weight of the row's pair
 };
 
 // Half of a weight row's group of 8 blocks (72 bytes): blocks 0..3 in lanes
@@ -128,6 +129,25 @@ __device__ __forceinline__ void pair_ops(const HW &w, int j, v4i &b0, v4i &b1, u
   s1 = r.y;
 }
 
+// Direct load of 16 bytes per lane into LDS at dst + 16 * lane.  Written as
+// an instruction the compiler does not model: through the builtin it cannot
+// tell a copy into one staging buffer from reads of the other, and waits for
+// every outstanding load (the prefetched weights with it) before reading
+// LDS.  The copies are ordered by the explicit wait and barrier at the top
+// of the group that reads them.
+// M0 is named as clobbered; nothing else in these kernels keeps a value in it.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void lds_dma16(const uint32_t *src, const void *dst) {
+  const uint32_t m0 =
+      (uint32_t)(uintptr_t)(const void __attribute__((address_space(3))) *)dst;
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(src), "s"(m0)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
 // Copy the tile's codes of blocks 8g..8g+7 into buffer buf: wave w moves rows
 // 16w..16w+15 (only the first 32 rows when `two` is false), four rows per
 // instruction; lane l writes chunk position l%16 of row r0 + l/16, which holds
@@ -141,9 +161,7 @@ __device__ __forceinline__ void stage_codes(const MArgs &a, MLds &L, int g, int 
     const int r = r0 + (lane >> 4);
     const int c = (lane & 15) ^ (r & 15);
     const uint32_t *src = a.act + ((int64_t)L.arow[r] * nblk + 8 * g) * 8 + c * 4;
-    __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1))) *)src,
-                                     (void __attribute__((address_space(3))) *)&L.a[buf][r0 * 16],
-                                     16, 0, 0);
+    lds_dma16(src, &L.a[buf][r0 * 16]);
   }
 }
 
@@ -192,14 +210,14 @@ __device__ __forceinline__ void block(float acc0[16], float acc1[16], const uint
 // codes and the down projection).  TWO: the tile holds more than 32 rows (a
 // compile-time branch: a run-time one inside the block loop makes the
 // compiler keep every block's second product until the loop's end).
-template <bool GATEUP, bool TWO>
+template <bool GATEUP, bool TWO, bool RES>
 __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, int pos, int rows,
                                           int s0, int ns) {
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int r32 = lane & 31, hh = lane >> 5;
   const int nblk = (int)(a.K / 32), G = (int)(a.K / 256);
-  const bool resident = G <= 2;
+  constexpr bool resident = RES;                  // G <= 2: every group staged once
 
   if (tid < MT) {
     int p = -1, r = -1;
@@ -209,6 +227,7 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
     }
     L.pair[tid] = p;
     L.arow[tid] = r;
+    if (!GATEUP) L.pw[tid] = p >= 0 ? pair_weight(a, p) : 0.0f;
   }
   __syncthreads();
   if (tid < MT && L.arow[tid] < 0) L.arow[tid] = L.arow[0];   // padding rows read a valid row
@@ -266,17 +285,20 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
       __builtin_amdgcn_s_waitcnt(0);              // codes, scales and weights have landed
       __syncthreads();                            // ... for every wave
     }
-    // next group's weights (the last group reloads itself: no conditional
-    // loads into a register array)
-    const int jn = j + 1 < J ? j + 1 : j;
-    const int sn = jn / G;
-    HW wn;
-    load_hw(wrow(s0 + sn) + (int64_t)(jn - sn * G) * (8 * Q4B), wn);
+    // next group's codes, then its weights (the last group reloads itself:
+    // no conditional loads into a register array).  The codes go first: the
+    // compiler cannot tell the direct loads into the other buffer from the
+    // reads of this one and waits for them before this group's products,
+    // so only loads issued after them stay in flight across the group.
     if (!resident && g + 1 < G) {
       stage_codes(a, L, g + 1, (g + 1) & 1, TWO, wave, lane, nblk);
       dx0 = dsrc[8 * (g + 1)];
       dx1 = dsrc[8 * (g + 1) + 4];
     }
+    const int jn = j + 1 < J ? j + 1 : j;
+    const int sn = jn / G;
+    HW wn;
+    load_hw(wrow(s0 + sn) + (int64_t)(jn - sn * G) * (8 * Q4B), wn);
     const int buf = resident ? g : (g & 1);
     const float(*dxb)[MT] = L.dx[buf];
     const uint4 *abuf = L.a[buf];
@@ -335,11 +357,10 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
       for (int e = 0; e < 16; e++) {
         const int m = 8 * (e >> 2) + 4 * hh + (e & 3);
         const int p0 = L.pair[m];
-        if (p0 >= 0) a.y[(int64_t)p0 * a.N + n] = pair_weight(a, p0) * acc0[e];
+        if (p0 >= 0) a.y[(int64_t)p0 * a.N + n] = L.pw[m] * acc0[e];
         if (TWO) {
           const int p1 = L.pair[32 + m];
-          if (p1 >= 0)
-            a.y[(int64_t)p1 * a.N + n] = pair_weight(a, p1) * acc1[e];
+          if (p1 >= 0) a.y[(int64_t)p1 * a.N + n] = L.pw[32 + m] * acc1[e];
         }
         acc0[e] = 0.0f;
         acc1[e] = 0.0f;
@@ -366,10 +387,17 @@ __global__ __launch_bounds__(MNT) __attribute__((amdgpu_waves_per_eu(3))) void m
   const int s0 = ch * a.spw, ns = min(a.spw, nsl - s0);
   CInt *tp = (CInt *)a.tiles + 4 * tile;
   const int expert = tp[0], pos = tp[1], rows = tp[2];
-  if (rows > 32)
-    mfma_tile<GATEUP, true>(a, L, expert, pos, rows, s0, ns);
-  else
-    mfma_tile<GATEUP, false>(a, L, expert, pos, rows, s0, ns);
+  if (a.K <= 512) {
+    if (rows > 32)
+      mfma_tile<GATEUP, true, true>(a, L, expert, pos, rows, s0, ns);
+    else
+      mfma_tile<GATEUP, false, true>(a, L, expert, pos, rows, s0, ns);
+  } else {
+    if (rows > 32)
+      mfma_tile<GATEUP, true, false>(a, L, expert, pos, rows, s0, ns);
+    else
+      mfma_tile<GATEUP, false, false>(a, L, expert, pos, rows, s0, ns);
+  }
 }
 
 }  // namespace
