@@ -372,18 +372,22 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
 template <bool GATEUP>
 __global__ __launch_bounds__(MNT) __attribute__((amdgpu_waves_per_eu(3))) void mfma_kernel(MArgs a) {
   __shared__ MLds L;
-  // Work item w = tile * nch + chunk, chunk = a run of spw slices.  Workgroup
-  // b runs on XCD b % 8, so XCD x takes the contiguous items [x*C, x*C + C),
-  // C = ceil(items / 8): the slices of a tile share one L2 for its codes.
+  // Work items are (tile, chunk), chunk = a run of spw slices.  Workgroup b
+  // runs on XCD b % 8 and is the (b / 8)-th item there.  Each XCD takes an
+  // even share of the long tiles (more than 32 rows), then an even share of
+  // the short ones, each share a contiguous run of tiles (neighbouring tiles
+  // of one expert share its weights in that XCD's L2), and all chunks of a
+  // tile in a row (they share the tile's codes).
   const int nsl = (int)(GATEUP ? a.I / 64 : a.N / WROWS);
   const int nch = (nsl + a.spw - 1) / a.spw;
-  const int items = ((CInt *)a.meta)[2] * nch;               // META_NTILES
-  const int per = (items + 7) >> 3;
-  const int b = blockIdx.x;
-  if (b >= 8 * per) return;
-  const int w = (b & 7) * per + (b >> 3);
-  if (w >= items) return;
-  const int tile = w / nch, ch = w - tile * nch;
+  const int ntiles = ((CInt *)a.meta)[2], nlong = ((CInt *)a.meta)[4];   // META_NTILES, META_NLONG
+  const int x = blockIdx.x & 7, q = blockIdx.x >> 3;
+  const int qt = q / nch, ch = q - qt * nch;
+  const int l0 = x * nlong / 8, nl = (x + 1) * nlong / 8 - l0;
+  const int nshort = ntiles - nlong;
+  const int s0t = nlong + x * nshort / 8, ns_ = nlong + (x + 1) * nshort / 8 - s0t;
+  if (qt >= nl + ns_) return;
+  const int tile = qt < nl ? l0 + qt : s0t + (qt - nl);
   const int s0 = ch * a.spw, ns = min(a.spw, nsl - s0);
   CInt *tp = (CInt *)a.tiles + 4 * tile;
   const int expert = tp[0], pos = tp[1], rows = tp[2];
@@ -414,7 +418,8 @@ int mfma_gateup(const uint8_t *w_gu, const uint8_t *ws_gu, const uint32_t *xa, c
   a.h = h; a.hq = hq; a.ha = ha; a.hd = hd;
   a.T = T; a.k = k; a.E = E; a.N = 2 * I; a.K = H; a.I = I;
   a.spw = 1;                       // the h tile reuses the code buffers
-  mfma_kernel<true><<<dim3((unsigned)((maxtiles * (I / 64) + 7) & ~7)), dim3(MNT), 0, s>>>(a);
+  // an XCD takes at most ceil(long/8) + ceil(short/8) <= ceil(maxtiles/8) + 1 tiles
+  mfma_kernel<true><<<dim3((unsigned)(8 * ((maxtiles + 7) / 8 + 1) * (I / 64))), dim3(MNT), 0, s>>>(a);
   return check_launch();
 }
 
@@ -430,7 +435,7 @@ int mfma_down(const uint8_t *w_d, const uint8_t *ws_d, const uint32_t *ha, const
   const int64_t nsl = H / WROWS;
   a.spw = I <= 512 ? (int)std::min<int64_t>(SPW_MAX, nsl) : 1;
   const int64_t nch = (nsl + a.spw - 1) / a.spw;
-  mfma_kernel<false><<<dim3((unsigned)((maxtiles * nch + 7) & ~7)), dim3(MNT), 0, s>>>(a);
+  mfma_kernel<false><<<dim3((unsigned)(8 * ((maxtiles + 7) / 8 + 1) * nch)), dim3(MNT), 0, s>>>(a);
   return check_launch();
 }
 

@@ -115,7 +115,7 @@ Layout make_layout(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k) {
 }
 
 // Meta words (int32) at the start of the workspace.
-enum { META_NROUTED = 0, META_NGROUPS = 1, META_NTILES = 2, META_NSMALL = 3 };
+enum { META_NROUTED = 0, META_NGROUPS = 1, META_NTILES = 2, META_NSMALL = 3, META_NLONG = 4 };
 
 int validate(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k) {
   if (T < 0 || H <= 0 || I <= 0 || H % 256 != 0 || I % 256 != 0) return W4A8_ESHAPE;
@@ -315,7 +315,12 @@ __device__ __forceinline__ void route_body(const RouteArgs &a) {
 
   // counts, then the compacted list of non-empty groups (expert order); a
   // group of at most ms rows goes to the small-group list, a larger one gets
-  // its range of MFMA row tiles.  The shared expert is the last group.  Each
+  // its MFMA row tiles: those of more than MC/2 rows (full cost) first, in
+  // expert order, then the tiles of at most MC/2 rows (half cost), so each
+  // XCD can take an even share of both kinds, the longer work first.  The
+  // small-chunk and short-tile counts share one scanned word (low and high
+  // 16 bits: each total is at most E + 1).  The shared expert is the last
+  // group.  Each
   // thread keeps the start and size of its experts (e = tid + j*ROUTE_T) in
   // registers, and the histogram's space then holds the three group counters.
   constexpr int EPT = 5;         // (E + 1) <= EPT * ROUTE_T for E <= 4096
@@ -354,8 +359,11 @@ __device__ __forceinline__ void route_body(const RouteArgs &a) {
     const int e = tid + j * ROUTE_T, rows = grw[j];
     if (e > a.E) break;
     gflag[e] = rows > 0 ? 1 : 0;
-    gsmall[e] = (rows > 0 && rows <= a.ms) ? (rows + SMALL_CHUNK - 1) / SMALL_CHUNK : 0;
-    gtile[e] = rows > a.ms ? (rows + MC - 1) / MC : 0;
+    const int rem = rows % MC;
+    const bool tiled = rows > a.ms;
+    gsmall[e] = ((rows > 0 && !tiled) ? (rows + SMALL_CHUNK - 1) / SMALL_CHUNK : 0) |
+                ((tiled && rem > 0 && rem <= MC / 2) ? 1 << 16 : 0);
+    gtile[e] = tiled ? rows / MC + (rem > MC / 2 ? 1 : 0) : 0;
   }
   __syncthreads();
   int tot[3];
@@ -363,7 +371,8 @@ __device__ __forceinline__ void route_body(const RouteArgs &a) {
     int *const arr[3] = {gflag, gtile, gsmall};
     block_exscan<3>(arr, a.E + 1, wtot, tot);
   }
-  const int ngroups = tot[0], ntiles = tot[1], nsmall = tot[2];
+  const int ngroups = tot[0], nlong = tot[1], nsmall = tot[2] & 0xFFFF;
+  const int ntiles = nlong + (tot[2] >> 16);
 #pragma unroll
   for (int j = 0; j < EPT; j++) {
     const int e = tid + j * ROUTE_T, start = gst[j], rows = grw[j];
@@ -373,11 +382,13 @@ __device__ __forceinline__ void route_body(const RouteArgs &a) {
     a.groups[gi] = make_int4(e, start, rows, t0);
     if (rows <= a.ms) {
       // back to front: the shared expert (the largest group) comes first
-      for (int m0 = 0, c = gsmall[e]; m0 < rows; m0 += SMALL_CHUNK, c++)
+      for (int m0 = 0, c = gsmall[e] & 0xFFFF; m0 < rows; m0 += SMALL_CHUNK, c++)
         a.chunks[nsmall - 1 - c] = make_int4(e, start + m0, min(SMALL_CHUNK, rows - m0), gi);
     } else {
-      for (int m0 = 0, t = t0; m0 < rows; m0 += MC, t++)
-        a.tiles[t] = make_int4(e, start + m0, min(MC, rows - m0), gi);
+      for (int m0 = 0, t = t0; m0 < rows; m0 += MC) {
+        const int r = min(MC, rows - m0);
+        a.tiles[r > MC / 2 ? t++ : nlong + (gsmall[e] >> 16)] = make_int4(e, start + m0, r, gi);
+      }
     }
   }
   if (tid == 0) {
@@ -385,6 +396,7 @@ __device__ __forceinline__ void route_body(const RouteArgs &a) {
     a.meta[META_NGROUPS] = ngroups;
     a.meta[META_NTILES] = ntiles;
     a.meta[META_NSMALL] = nsmall;
+    a.meta[META_NLONG] = nlong;
   }
 }
 
