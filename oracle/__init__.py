@@ -28,6 +28,8 @@ _lib = None
 QK = 32
 Q4_BYTES = 18
 Q8_BYTES = 34
+Q4S_BYTES = 20      # the paper's symmetric 4-bit block: fp32 scale + 16 bytes
+Q8F_BYTES = 36      # 8-bit activations with an fp32 scale: fp32 scale + 32 codes
 
 
 def build() -> str:
@@ -58,6 +60,11 @@ def _load():
     lib.orc_blockdot.argtypes = [P, P]
     lib.orc_blockdot.restype = ctypes.c_int32
     lib.orc_gemv.argtypes = [P, P, I64, I64, P, P]
+    lib.orc_q4_sym_quantize.argtypes = [P, P, I64, I64]
+    lib.orc_q8_f32_quantize.argtypes = [P, P, I64, I64]
+    lib.orc_blockdot_sym.argtypes = [P, P]
+    lib.orc_blockdot_sym.restype = ctypes.c_int32
+    lib.orc_gemv_sym.argtypes = [P, P, I64, I64, P, P]
     lib.orc_gemv_dequant.argtypes = [P, P, I64, I64, P]
     lib.orc_moe.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, I64, I64, P,
                             P, P, P, P, P, P, P]
@@ -269,3 +276,48 @@ def q4_0_split(wq: np.ndarray):
     nib = b[..., 2:]
     q = np.concatenate([nib & 0x0F, nib >> 4], axis=-1)
     return d, q
+
+
+# ------------------------------------------- the paper's own block format
+def q4_sym_quantize(w: np.ndarray) -> np.ndarray:
+    """Symmetric 4-bit weights in {-7..7} with an fp32 scale per 32 (Sec. 2.3),
+    fp32 rows [rows, K] -> uint8 [rows, K/32*20]."""
+    w = _c(w, np.float32)
+    if w.ndim == 1:
+        w = w[None, :]
+    rows, K = w.shape
+    assert K % QK == 0
+    out = np.empty((rows, K // QK * Q4S_BYTES), dtype=np.uint8)
+    _load().orc_q4_sym_quantize(_ptr(w), _ptr(out), rows, K)
+    return out
+
+
+def q8_f32_quantize(x: np.ndarray) -> np.ndarray:
+    """8-bit activations with an fp32 scale per 32 (Sec. 3.3), fp32 rows
+    [rows, K] -> uint8 [rows, K/32*36]."""
+    x = _c(x, np.float32)
+    if x.ndim == 1:
+        x = x[None, :]
+    rows, K = x.shape
+    assert K % QK == 0
+    out = np.empty((rows, K // QK * Q8F_BYTES), dtype=np.uint8)
+    _load().orc_q8_f32_quantize(_ptr(x), _ptr(out), rows, K)
+    return out
+
+
+def blockdot_sym(wblock: np.ndarray, ablock: np.ndarray) -> int:
+    wb = _c(wblock, np.uint8)
+    ab = _c(ablock, np.uint8)
+    assert wb.size == Q4S_BYTES and ab.size == Q8F_BYTES
+    return int(_load().orc_blockdot_sym(_ptr(wb), _ptr(ab)))
+
+
+def gemv_sym(w: np.ndarray, xq: np.ndarray, N: int, K: int):
+    """Product in the paper's format: returns (y fp64 [N], R fp64 [N])."""
+    w = _c(w, np.uint8)
+    xq = _c(xq, np.uint8)
+    assert w.size == N * (K // QK) * Q4S_BYTES and xq.size == (K // QK) * Q8F_BYTES
+    y = np.empty(N, dtype=np.float64)
+    R = np.empty(N, dtype=np.float64)
+    _load().orc_gemv_sym(_ptr(w), _ptr(xq), N, K, _ptr(y), _ptr(R))
+    return y, R

@@ -490,3 +490,122 @@ int orc_threads(void)
     }
     return n;
 }
+
+/* ------------------------------------------------------------------ */
+/* The paper's own block format (Sec. 2.3 "Weight quantization": each  */
+/* weight an integer in {-7..7} with one FP32 scale per group, two per  */
+/* byte; Sec. 3.3: activations quantized per group to 8 bits with an    */
+/* FP32 scale, each 4-bit weight held as the unsigned value in {1..15}).*/
+/* Readings: 32 per group; weight scale d = amax / 7 and activation     */
+/* scale d = amax / 127, each one correctly rounded fp32 division;      */
+/* codes round-half-away(v * (1 / d)) clamped to +-7 / +-127; a zero    */
+/* scale, or one whose reciprocal overflows fp32, gives zero codes.     */
+/* Q4_SYM block, 20 bytes: fp32 d (little endian), then byte j holding  */
+/* q_j + 8 in its low and q_{j+16} + 8 in its high nibble.  Q8_F32      */
+/* block, 36 bytes: fp32 d, then 32 int8 codes.                         */
+/* ------------------------------------------------------------------ */
+
+#define Q4S_BYTES 20
+#define Q8F_BYTES 36
+
+static void wrf32(uint8_t *p, float f) { memcpy(p, &f, 4); }
+static float rdf32(const uint8_t *p) { float f; memcpy(&f, p, 4); return f; }
+
+/* the fp32 reciprocal of a scale, or 0 when codes are all zero */
+static float sym_inverse(float d)
+{
+    if (d == 0.0f) return 0.0f;
+    float id = 1.0f / d;
+    return isinf(id) ? 0.0f : id;
+}
+
+static int round_clamp(float v, int lim)
+{
+    int q = (int)roundf(v);                   /* half away from zero */
+    if (q > lim) q = lim;
+    if (q < -lim) q = -lim;
+    return q;
+}
+
+void orc_q4_sym_block(const float *w, uint8_t *out)
+{
+    float amax = 0.0f;
+    for (int i = 0; i < QK; i++) {
+        float a = fabsf(w[i]);
+        if (a > amax) amax = a;
+    }
+    float d = amax / 7.0f;
+    float id = sym_inverse(d);
+    int q[QK];
+    for (int i = 0; i < QK; i++)
+        q[i] = (id == 0.0f) ? 0 : round_clamp(w[i] * id, 7);
+    wrf32(out, d);
+    for (int j = 0; j < 16; j++)
+        out[4 + j] = (uint8_t)((q[j] + 8) | ((q[j + 16] + 8) << 4));
+}
+
+void orc_q8_f32_block(const float *x, uint8_t *out)
+{
+    float amax = 0.0f;
+    for (int i = 0; i < QK; i++) {
+        float a = fabsf(x[i]);
+        if (a > amax) amax = a;
+    }
+    float d = amax / 127.0f;
+    float id = sym_inverse(d);
+    wrf32(out, d);
+    for (int i = 0; i < QK; i++)
+        out[4 + i] = (uint8_t)(int8_t)((id == 0.0f) ? 0 : round_clamp(x[i] * id, 127));
+}
+
+void orc_q4_sym_quantize(const float *w, uint8_t *out, int64_t rows, int64_t K)
+{
+    int64_t nb = K / QK;
+    #pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < rows; r++)
+        for (int64_t b = 0; b < nb; b++)
+            orc_q4_sym_block(w + r * K + b * QK, out + (r * nb + b) * Q4S_BYTES);
+}
+
+void orc_q8_f32_quantize(const float *x, uint8_t *out, int64_t rows, int64_t K)
+{
+    int64_t nb = K / QK;
+    #pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < rows; r++)
+        for (int64_t b = 0; b < nb; b++)
+            orc_q8_f32_block(x + r * K + b * QK, out + (r * nb + b) * Q8F_BYTES);
+}
+
+/* s = sum_i (nibble_i - 8) * q_a,i over one block of the paper's format. */
+int32_t orc_blockdot_sym(const uint8_t *wb, const uint8_t *ab)
+{
+    const int8_t *qa = (const int8_t *)(ab + 4);
+    int32_t s = 0;
+    for (int j = 0; j < 16; j++) {
+        int lo = (wb[4 + j] & 0x0F) - 8;
+        int hi = (wb[4 + j] >> 4) - 8;
+        s += lo * qa[j] + hi * qa[j + 16];
+    }
+    return s;
+}
+
+/* y[n] = sum_b d_w[n,b] * d_a[b] * s[n,b] in fp64, block order; R[n] = sum
+ * of |term|.  Either output pointer may be NULL. */
+void orc_gemv_sym(const uint8_t *w, const uint8_t *xq, int64_t N, int64_t K,
+                  double *y, double *R)
+{
+    int64_t nb = K / QK;
+    #pragma omp parallel for schedule(static)
+    for (int64_t n = 0; n < N; n++) {
+        double acc = 0.0, mag = 0.0;
+        for (int64_t b = 0; b < nb; b++) {
+            const uint8_t *wb = w + (n * nb + b) * Q4S_BYTES;
+            const uint8_t *ab = xq + b * Q8F_BYTES;
+            double t = (double)rdf32(wb) * (double)rdf32(ab) * (double)orc_blockdot_sym(wb, ab);
+            acc += t;
+            mag += fabs(t);
+        }
+        if (y) y[n] = acc;
+        if (R) R[n] = mag;
+    }
+}
