@@ -377,6 +377,50 @@ def bench_gemv_1024(torch, w4, synth, args, dev, copies=2048, n=2048):
             "launch": "hipGraph"}
 
 
+def bench_gemv_sym(torch, w4, synth, args, dev):
+    """The GEMV in the paper's own block format (symmetric 4-bit weights with an
+    fp32 scale per 32, 20-byte blocks; 8-bit activations with an fp32 scale)
+    at the output projection's shape (N = 151936, K = 2048, 195 MB), two
+    weight copies alternated so successive calls stream from HBM."""
+    N, K = 151936, H
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(args.seed + 10)
+    ws = []
+    for _ in range(2):
+        wq = torch.empty((N, K // 32 * 20), dtype=torch.uint8, device=dev)
+        for r0 in range(0, N, 16384):   # quantize in slabs: bounded fp32 staging
+            r1 = min(N, r0 + 16384)
+            W = torch.randn((r1 - r0, K), generator=gen, device=dev) * 0.02
+            w4.q4_sym_quantize(W, out=wq[r0:r1])
+        ws.append(wq)
+    xq = w4.q8_f32_quantize(torch.randn((1, K), generator=gen, device=dev))
+    y = torch.empty(N, dtype=torch.float32, device=dev)
+    n = 40
+    for i in range(4):
+        w4.q4sym_q8f32_gemv(ws[i % 2], xq, N, K, y=y)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for i in range(n):
+            w4.q4sym_q8f32_gemv(ws[i % 2], xq, N, K, y=y)
+    graph.replay()
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    graph.replay()
+    ev1.record()
+    torch.cuda.synchronize()
+    us = ev0.elapsed_time(ev1) / n * 1e3
+    nbytes = N * (K // 32) * 20 + (K // 32) * 36 + N * 4
+    del ws
+    return {"N": N, "K": K, "format": "q4_sym x q8_f32 (fp32 scales)",
+            "us_per_call": round(us, 2),
+            "GBps": round(nbytes / (us / 1e6) / 1e9, 1),
+            "hbm_peak_frac": round(nbytes / (us / 1e6) / 1e9 / HBM_PEAK_GBPS, 4),
+            "launch": "hipGraph"}
+
+
 def bench_lm_head(torch, w4, synth, args, dev):
     """The dense W4A8 GEMV at the output projection's shape (N = 151936
     vocabulary rows, K = H = 2048; random Q4_0 blocks, 175 MB), two weight
@@ -617,7 +661,7 @@ def main():
         m32 = bench_m32(torch, w4, synth, layers, args, dev)
         log(f"decode M=32: {m32}")
 
-    invariants = router = lm_head = gemv_1024 = None
+    invariants = router = lm_head = gemv_1024 = gemv_sym = None
     if not args.no_extras:
         invariants = bench_decode_invariants(torch, w4, synth, layers, args, dev)
         log(f"decode invariants: {invariants}")
@@ -627,6 +671,8 @@ def main():
         log(f"lm-head gemv: {lm_head}")
         gemv_1024 = bench_gemv_1024(torch, w4, synth, args, dev)
         log(f"gemv 1024x1024: {gemv_1024}")
+        gemv_sym = bench_gemv_sym(torch, w4, synth, args, dev)
+        log(f"gemv, paper's fp32-scale format: {gemv_sym}")
 
     stack = None
     if not args.no_stack:
@@ -673,6 +719,7 @@ def main():
         "router_topk": router,
         "gemv_lm_head": lm_head,
         "gemv_1024": gemv_1024,
+        "gemv_lm_head_paper_format": gemv_sym,
     }
     print(json.dumps(rec), flush=True)
 

@@ -60,6 +60,8 @@ extern "C" {
 
 #define W4A8_Q4_0_BLOCK_BYTES 18
 #define W4A8_Q8_0_BLOCK_BYTES 34
+#define W4A8_Q4_SYM_BLOCK_BYTES 20
+#define W4A8_Q8_F32_BLOCK_BYTES 36
 #define W4A8_BLOCK 32
 
 /* Static, NUL-terminated description of a status code (never NULL). */
@@ -93,6 +95,37 @@ int q4_0_quantize(const float *w, void *wq, int64_t rows, int64_t K, void *strea
  * -> W4A8_ESHAPE.
  */
 int q4q8_gemv(const void *w, const void *xq, float *y, int64_t N, int64_t K, void *stream);
+
+/*
+ * The paper's own block format (Sec. 2.3 "Weight quantization": each weight
+ * an integer in {-7..7} with one FP32 scale per group, two per byte;
+ * Sec. 3.3: activations quantized per group to 8 bits with an FP32 scale,
+ * every 4-bit weight held as the unsigned value in {1..15}).  32 per group:
+ *   Q4_SYM block, 20 bytes: fp32 scale d (little endian), then 16 bytes in
+ *     the Q4_0 nibble order (byte j: element j low, element j+16 high), each
+ *     nibble q + 8 with q in -7..7; weight value = q * d.  Quantizer:
+ *     d = amax / 7, q = clamp(round_half_away(w * (1/d)), -7, 7).
+ *   Q8_F32 block, 36 bytes: fp32 scale d, then 32 int8 codes; d = amax / 127,
+ *     q = clamp(round_half_away(x * (1/d)), -127, 127).
+ *   In both, every step is one IEEE binary32 operation, and a zero scale, or
+ *   one whose reciprocal overflows fp32 (below 2^-128), gives zero codes.
+ * Quantizers: w or x [rows][K] fp32 -> [rows][K/32] blocks.  K % 32 != 0,
+ * rows < 0 or K <= 0 -> W4A8_ESHAPE; rows == 0 is a no-op.  Bit-identical to
+ * the definitions above.
+ */
+int q4_sym_quantize(const float *w, void *wq, int64_t rows, int64_t K, void *stream);
+int q8_f32_quantize(const float *x, void *xq, int64_t rows, int64_t K, void *stream);
+
+/*
+ * Matrix-vector product in the paper's format (Sec. 3.3):
+ *   y[n] = sum_b d_w[n,b] * d_x[b] * s[n,b],  s[n,b] = sum_i q_w * q_x
+ * with s exact in int32 and the scaled sum in fp32.
+ *   w  [N][K/32] Q4_SYM blocks;  xq [K/32] Q8_F32 blocks;  y [N] fp32.
+ * K % 256 != 0, N <= 0 or K <= 0 -> W4A8_ESHAPE; K > 32768 -> W4A8_ERANGE
+ * (the activation vector is staged whole in LDS).
+ */
+int q4sym_q8f32_gemv(const void *w, const void *xq, float *y, int64_t N, int64_t K,
+                     void *stream);
 
 /*
  * Bytes of device workspace moe_w4a8_forward needs for these sizes, or 0 if

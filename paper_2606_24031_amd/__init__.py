@@ -17,13 +17,16 @@ LIB_PATH = os.path.join(HERE, "libw4a8.so")
 OK, ENULL, ESHAPE, ERANGE, EWORKSPACE, EALIGN, EHIP, EDEVICE, EALIAS = 0, -1, -2, -3, -4, -5, -6, -7, -8
 Q4_0_BLOCK_BYTES = 18
 Q8_0_BLOCK_BYTES = 34
+Q4_SYM_BLOCK_BYTES = 20
+Q8_F32_BLOCK_BYTES = 36
 WS_XQ, WS_H, WS_HQ, WS_PERM, WS_COUNT, WS_SYNC, WS_SYNC_END, WS_XN = 0, 1, 2, 3, 4, 5, 6, 7
 WS_NFIELDS = 8
 
 EXPORTS = ("w4a8_strerror", "q8_0_quantize", "q4_0_quantize", "q4q8_gemv",
            "moe_w4a8_workspace_size", "moe_w4a8_workspace_init",
            "moe_w4a8_workspace_layout", "moe_w4a8_forward", "moe_w4a8_layer",
-           "rmsnorm_residual", "moe_router_topk", "moe_w4a8_layer_routed")
+           "rmsnorm_residual", "moe_router_topk", "moe_w4a8_layer_routed",
+           "q4_sym_quantize", "q8_f32_quantize", "q4sym_q8f32_gemv")
 
 _lib = None
 
@@ -46,11 +49,13 @@ def lib() -> ctypes.CDLL:
     P, I64, SZ = ctypes.c_void_p, ctypes.c_int64, ctypes.c_size_t
     L.w4a8_strerror.argtypes = [ctypes.c_int]
     L.w4a8_strerror.restype = ctypes.c_char_p
-    for name in ("q8_0_quantize", "q4_0_quantize"):
+    for name in ("q8_0_quantize", "q4_0_quantize", "q4_sym_quantize", "q8_f32_quantize"):
         getattr(L, name).argtypes = [P, P, I64, I64, P]
         getattr(L, name).restype = ctypes.c_int
     L.q4q8_gemv.argtypes = [P, P, P, I64, I64, P]
     L.q4q8_gemv.restype = ctypes.c_int
+    L.q4sym_q8f32_gemv.argtypes = [P, P, P, I64, I64, P]
+    L.q4sym_q8f32_gemv.restype = ctypes.c_int
     L.moe_w4a8_workspace_size.argtypes = [I64, I64, I64, I64, I64]
     L.moe_w4a8_workspace_size.restype = SZ
     L.moe_w4a8_workspace_init.argtypes = [P, SZ, P]
@@ -127,6 +132,40 @@ def q4q8_gemv(w, xq, N, K, y=None, stream=None):
     if y is None:
         y = torch.empty(N, dtype=torch.float32, device=w.device)
     _check(lib().q4q8_gemv(_p(_u8(w)), _p(_u8(xq)), _p(y), N, K, _stream(stream)), "q4q8_gemv")
+    return y
+
+
+def q4_sym_quantize(w, out=None, stream=None):
+    """The paper's symmetric 4-bit weights ({-7..7}, fp32 scale per 32) of fp32
+    rows w [rows, K] -> uint8 [rows, K/32*20] on w's device."""
+    import torch
+    assert w.dtype == torch.float32 and w.is_contiguous()
+    rows, K = (1, w.numel()) if w.dim() == 1 else (w.numel() // w.shape[-1], w.shape[-1])
+    if out is None:
+        out = torch.empty((rows, K // 32 * Q4_SYM_BLOCK_BYTES), dtype=torch.uint8, device=w.device)
+    _check(lib().q4_sym_quantize(_p(w), _p(_u8(out)), rows, K, _stream(stream)), "q4_sym_quantize")
+    return out
+
+
+def q8_f32_quantize(x, out=None, stream=None):
+    """8-bit activations with an fp32 scale per 32 of fp32 rows x [rows, K] ->
+    uint8 [rows, K/32*36] on x's device."""
+    import torch
+    assert x.dtype == torch.float32 and x.is_contiguous()
+    rows, K = (1, x.numel()) if x.dim() == 1 else (x.numel() // x.shape[-1], x.shape[-1])
+    if out is None:
+        out = torch.empty((rows, K // 32 * Q8_F32_BLOCK_BYTES), dtype=torch.uint8, device=x.device)
+    _check(lib().q8_f32_quantize(_p(x), _p(_u8(out)), rows, K, _stream(stream)), "q8_f32_quantize")
+    return out
+
+
+def q4sym_q8f32_gemv(w, xq, N, K, y=None, stream=None):
+    """y[N] = product of w [N, K/32 Q4_SYM blocks] and xq [K/32 Q8_F32 blocks]."""
+    import torch
+    if y is None:
+        y = torch.empty(N, dtype=torch.float32, device=w.device)
+    _check(lib().q4sym_q8f32_gemv(_p(_u8(w)), _p(_u8(xq)), _p(y), N, K, _stream(stream)),
+           "q4sym_q8f32_gemv")
     return y
 
 

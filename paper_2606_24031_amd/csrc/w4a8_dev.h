@@ -227,18 +227,23 @@ __device__ __forceinline__ float silu_f32(float g) {
 //   s = 16 * sum (q_w ^ 8) * hi + sum q_w * lo - 8 * sum lo,
 // two 8-wide 4-bit dot products per payload dword and no unpacking of the
 // weights; corr = -8 * sum lo.
-__device__ __forceinline__ int blockdot_split(const W8 &w, int k, uint4 hi, uint4 lo, int corr) {
+// n: the block's four payload dwords (stored nibbles q_w).
+__device__ __forceinline__ int blockdot_nib(const uint32_t n[4], uint4 hi, uint4 lo, int corr) {
   const uint32_t h[4] = {hi.x, hi.y, hi.z, hi.w};
   const uint32_t l[4] = {lo.x, lo.y, lo.z, lo.w};
   int sa = 0;
   uint32_t sb = (uint32_t)corr;
 #pragma unroll
   for (int c = 0; c < 4; c++) {
-    const uint32_t n = w8_nib(w, k, c);
-    sa = __builtin_amdgcn_sdot8((int)(n ^ 0x88888888u), (int)h[c], sa, false);
-    sb = __builtin_amdgcn_udot8(n, l[c], sb, false);
+    sa = __builtin_amdgcn_sdot8((int)(n[c] ^ 0x88888888u), (int)h[c], sa, false);
+    sb = __builtin_amdgcn_udot8(n[c], l[c], sb, false);
   }
   return (int)(((uint32_t)sa << 4) + sb);
+}
+// The same for block k of a Q4_0 group.
+__device__ __forceinline__ int blockdot_split(const W8 &w, int k, uint4 hi, uint4 lo, int corr) {
+  const uint32_t n[4] = {w8_nib(w, k, 0), w8_nib(w, k, 1), w8_nib(w, k, 2), w8_nib(w, k, 3)};
+  return blockdot_nib(n, hi, lo, corr);
 }
 
 // Activation blocks staged in LDS in nibble-split form: block i at codes[2i]

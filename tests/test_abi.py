@@ -45,7 +45,7 @@ A = 0x10000   # an aligned fake device address (never dereferenced: validation f
 
 def test_quantize_argument_errors():
     L = w4.lib()
-    for fn in (L.q8_0_quantize, L.q4_0_quantize):
+    for fn in (L.q8_0_quantize, L.q4_0_quantize, L.q4_sym_quantize, L.q8_f32_quantize):
         assert fn(None, _fake(A), 4, 64, None) == w4.ENULL
         assert fn(_fake(A), None, 4, 64, None) == w4.ENULL
         assert fn(_fake(A), _fake(A), 4, 48, None) == w4.ESHAPE
@@ -63,6 +63,13 @@ def test_gemv_argument_errors():
     assert L.q4q8_gemv(_fake(A), _fake(A), y, 8, 128, None) == w4.ESHAPE   # K % 256
     assert L.q4q8_gemv(_fake(A), _fake(A), y, 0, 256, None) == w4.ESHAPE
     assert L.q4q8_gemv(_fake(A), _fake(A + 2), y, 8, 256, None) == w4.EALIGN
+    G = L.q4sym_q8f32_gemv
+    assert G(None, _fake(A), y, 8, 256, None) == w4.ENULL
+    assert G(_fake(A), _fake(A), None, 8, 256, None) == w4.ENULL
+    assert G(_fake(A), _fake(A), y, 8, 128, None) == w4.ESHAPE            # K % 256
+    assert G(_fake(A), _fake(A), y, 0, 256, None) == w4.ESHAPE
+    assert G(_fake(A), _fake(A), y, 8, 32768 + 256, None) == w4.ERANGE    # staged whole in LDS
+    assert G(_fake(A + 4), _fake(A), y, 8, 256, None) == w4.EALIGN
 
 
 def test_moe_workspace_size_and_layout():
