@@ -618,6 +618,30 @@ def cpu_baseline(synth, seconds):
                       f"{physical_threads_note()} physical cores on this host"}
 
 
+def hbm_copy_rate(torch, dev, nbytes=2 << 30, reps=10):
+    """Practical HBM rate on this machine: a plain device-to-device copy of 2 GiB
+    (bytes read plus bytes written over time), beside the 8 TB/s
+    specification.  A measured reference, not a ceiling: the read-only GEMV
+    at the output projection's shape streams faster (a reduction such as
+    torch.sum reads at only about 4 TB/s here)."""
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    ev1.record()
+    torch.cuda.synchronize()
+    s = ev0.elapsed_time(ev1) / reps / 1e3
+    del src, dst
+    return {"GBps": round(2 * nbytes / s / 1e9, 1), "kernel": "device copy of 2 GiB (read + write)",
+            "frac_of_spec": round(2 * nbytes / s / 1e9 / HBM_PEAK_GBPS, 4)}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -688,6 +712,8 @@ def main():
         log(f"cpu baseline: {cpu}")
 
     traffic = measured_traffic()
+    copy_rate = hbm_copy_rate(torch, dev)
+    log(f"hbm copy rate: {copy_rate}")
     rec = {
         "metric": METRIC,
         "value": round(gbps, 1),
@@ -712,6 +738,7 @@ def main():
                      "frac": round(bytes_per_launch / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBPS, 4),
                      "traffic": traffic},
         "cpu_baseline": cpu,
+        "hbm_copy_rate": dict(copy_rate, decode_frac_of_copy_rate=round(gbps / copy_rate["GBps"], 4)),
         "prefill_947": prefill,
         "decode_m32": m32,
         "stack_40": stack,
