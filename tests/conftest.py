@@ -26,3 +26,18 @@ def oracle_lib():
     import oracle
     oracle.build()
     return oracle
+
+
+def pytest_terminal_summary(terminalreporter):
+    """Flip counts of every MoE-layer check of the run: Q8_0(h) blocks that
+    differ from the oracle's own choice (each within the valid set)."""
+    try:
+        from tests import moe_check
+    except Exception:
+        return
+    if not moe_check.STATS:
+        return
+    tr = terminalreporter
+    tr.write_sep("-", "MoE-layer checks: Q8_0(h) flips / blocks, max |out - ref| / sum|terms|")
+    for name, st in moe_check.STATS:
+        tr.write_line(f"{st['flips']:4d} / {st['blocks']:6d}  {st['max_rel_err']:.2e}  {name}")

@@ -156,8 +156,11 @@ class Layer:
         return host(out), h, hq, perm, count, ws
 
     def check(self, x, ids, wts, k, out, h, hq, shared_w=None):
+        """The MoE check; at one token no Q8_0(h) block may differ from the
+        oracle's own choice (flips are counted and reported otherwise)."""
         return moe_check.check_layer(out, h, hq, x, ids, wts, self.w_gu, self.w_d, self.ws_gu,
-                                     self.ws_d, self.H, self.I, self.E, k, shared_w=shared_w)
+                                     self.ws_d, self.H, self.I, self.E, k, shared_w=shared_w,
+                                     max_flips=0 if x.shape[0] == 1 else None)
 
 
 def _check_route(ids, E, shared, perm, count):
@@ -377,7 +380,11 @@ def test_moe_route_4096_experts():
     L.check(x, ids, wts, k, out, h, hq)
 
 
-def test_moe_prefill_947_sampled_tokens(qwen_layer):
+def test_moe_prefill_947_all_tokens(qwen_layer):
+    """The 947-token prefill with biased routing (skewed expert load: empty
+    experts, groups of a few rows on the VALU kernels, groups of hundreds of
+    rows on the MFMA tiles, the 947-row shared group): every token and every
+    pair through the MoE check, and a second call bit-identical."""
     L = qwen_layer
     g = synth.rng(22)
     T, k = 947, 8
@@ -385,13 +392,9 @@ def test_moe_prefill_947_sampled_tokens(qwen_layer):
     ids, wts = synth.routing(g, T, L.E, k, bias_std=1.0)
     out, h, hq, perm, count, ws = L.run(x, ids, wts, k)
     _check_route(ids, L.E, True, perm, count)
-    # tokens through the heaviest expert, the first and last token, and a few more
-    heavy = int(np.argmax(count))
-    through_heavy = np.nonzero((ids == heavy).any(axis=1))[0]
-    tokens = sorted(set([0, T - 1] + through_heavy[:4].tolist() + through_heavy[-2:].tolist()
-                        + g.choice(T, 8, replace=False).tolist()))
-    o, hh, qq, Ts = moe_check.gather_tokens(tokens, T, k, out, h, hq)
-    L.check(x[tokens], ids[tokens], wts[tokens], k, o, hh, qq)
+    assert count.max() > 64 and (count[count > 0] <= 8).any()
+    st = L.check(x, ids, wts, k, out, h, hq)
+    assert st["pairs"] == T * (k + 1)
     out2, *_ = L.run(x, ids, wts, k, ws=ws)
     assert np.array_equal(out, out2)
 

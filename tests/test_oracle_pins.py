@@ -520,3 +520,106 @@ def test_moe_shared_weight_is_linear():
     rs = f(s)
     assert np.array_equal(r1.out, base.out) and np.array_equal(r1.R, base.R)
     assert np.allclose(rs.out, r0.out + s[:, None] * (r1.out - r0.out), rtol=0, atol=1e-12 * base.R.max())
+
+
+def _f32_values(lo, hi):
+    """Every fp32 value v with lo <= v <= hi (both fp32), in order."""
+    def key(v):
+        i = int(np.array([v], np.float32).view(np.int32)[0])
+        return i if i >= 0 else -(i & 0x7FFFFFFF)
+    k0, k1 = key(lo), key(hi)
+    keys = np.arange(k0, k1 + 1, dtype=np.int64)
+    bits = np.where(keys >= 0, keys, (-keys) | 0x80000000).astype(np.uint32)
+    return bits.view(np.float32)
+
+
+def _code_f32(v, df):
+    """Q8_0 code of fp32 values v for the fp32 scale df, written from the
+    format definition in numpy fp32: one multiply by 1/df, round half away
+    from zero, clamp to +-127."""
+    idf = np.float32(1.0) / np.float32(df)
+    p = (v.astype(np.float32) * idf).astype(np.float64)
+    r = np.sign(p) * np.floor(np.abs(p) + 0.5)
+    return np.clip(r, -127, 127).astype(np.int64)
+
+
+def test_q8_0_candidates_are_tight():
+    """Tightness, not only coverage: for boxes of a few ulps placed on code
+    ties (x / d at c + 1/2) and on fp16 rounding boundaries of the scale, the
+    scale set and every per-element code interval equal what an independent
+    enumeration of every fp32 value in the box gives (numpy fp16 conversion,
+    numpy fp32 arithmetic): no listed scale or code is unreachable and none
+    reachable is missing."""
+    g = np.random.default_rng(15)
+    nb = 24
+    h = synth.normal_f32(g, (nb * 32,), 0.5)
+    dh = np.zeros_like(h)
+    ulp = lambda v: np.spacing(np.abs(np.float32(v))).astype(np.float32)
+    d0, _ = oracle.q8_0_split(oracle.q8_0_quantize(h))
+    for b in range(nb):
+        blk = slice(32 * b, 32 * b + 32)
+        x = h[blk]
+        df = float(np.array([d0[0, b]], np.uint16).view(np.float16)[0])
+        amax_i = int(np.argmax(np.abs(x)))
+        # three elements on code ties c + 1/2, boxes of a few ulps
+        for i in g.choice([j for j in range(32) if j != amax_i], 3, replace=False):
+            c = int(g.integers(-100, 100))
+            x[i] = np.float32((c + 0.5) * df)
+            dh[32 * b + i] = np.float32(int(g.integers(1, 5))) * ulp(x[i])
+        # three elements whose box of n ulps stops one ulp short of a tie
+        # (a box even slightly too wide would reach it)
+        for i in g.choice([j for j in range(32) if j != amax_i and dh[32 * b + j] == 0], 3,
+                          replace=False):
+            c = int(g.integers(-100, 100))
+            tie = np.float32((c + 0.5) * df)
+            n = int(g.integers(1, 4))
+            side = 1 if g.random() < 0.5 else -1
+            v = tie
+            for _ in range(n + 1):
+                v = np.nextafter(v, np.float32(side * np.inf))
+            x[i] = v
+            dh[32 * b + i] = np.float32(n) * ulp(v)
+        # some other elements get a one-ulp box, the rest none
+        for i in g.choice(32, 6, replace=False):
+            if dh[32 * b + i] == 0 and i != amax_i:
+                dh[32 * b + i] = ulp(x[i])
+        if b % 2 == 0:
+            # amax on an fp16 rounding boundary of amax / 127: two scales
+            s = np.float16(np.float32(abs(x[amax_i])) / np.float32(127))
+            s_next = np.nextafter(s, np.float16(np.inf))
+            mid = (float(s) + float(s_next)) / 2.0
+            x[amax_i] = np.float32(np.sign(x[amax_i]) * mid * 127.0)
+            dh[32 * b + amax_i] = np.float32(3) * ulp(x[amax_i])
+        elif b % 4 == 1:
+            # amax two ulps past an fp16 rounding boundary, a one-ulp box:
+            # one scale, unless the box is too wide
+            s = np.float16(np.float32(abs(x[amax_i])) / np.float32(127))
+            s_next = np.nextafter(s, np.float16(np.inf))
+            mid = np.float32((float(s) + float(s_next)) / 2.0 * 127.0)
+            while np.float16(mid / np.float32(127)) == s:      # first fp32 past the boundary
+                mid = np.nextafter(mid, np.float32(np.inf))
+            v = np.nextafter(np.nextafter(mid, np.float32(np.inf)), np.float32(np.inf))
+            x[amax_i] = np.float32(np.sign(x[amax_i]) * v)
+            dh[32 * b + amax_i] = ulp(v)
+        h[blk] = x
+    scales, qlo, qhi, ns = oracle.q8_0_candidates(h, dh)
+    lo_box = (h.astype(np.float64) - dh.astype(np.float64)).astype(np.float32)
+    hi_box = (h.astype(np.float64) + dh.astype(np.float64)).astype(np.float32)
+    multi = 0
+    for b in range(nb):
+        el = range(32 * b, 32 * b + 32)
+        vals = [_f32_values(lo_box[i], hi_box[i]) for i in el]
+        amin = max(float(np.min(np.abs(v))) for v in vals)
+        amaxv = max(float(np.max(np.abs(v))) for v in vals)
+        a = _f32_values(np.float32(amin), np.float32(amaxv))
+        s_enum = np.unique((a / np.float32(127)).astype(np.float32).astype(np.float16).view(np.uint16))
+        assert list(s_enum) == list(scales[b, :ns[b]]), f"block {b}: scale set"
+        multi += ns[b] > 1
+        for c in range(ns[b]):
+            df = np.array([scales[b, c]], np.uint16).view(np.float16).astype(np.float32)[0]
+            for j, i in enumerate(el):
+                codes = np.unique(_code_f32(vals[j], df))
+                want = np.arange(int(qlo[b, c, j]), int(qhi[b, c, j]) + 1)
+                assert np.array_equal(codes, want), f"block {b} scale {c} element {j}"
+    assert multi >= nb // 2 - 2, "the boxes were meant to straddle scale boundaries"
+    assert (qhi > qlo).sum() >= 2 * nb, "the boxes were meant to straddle code ties"
