@@ -34,8 +34,9 @@
  *   - Shapes are validated on the host before anything is launched; on an
  *     error nothing is enqueued and no output is touched.
  *   - Calls are thread-safe and re-entrant: the library keeps no state other
- *     than a per-device "is gfx950" check and the device's compute-unit
- *     count.  Concurrent calls must not share output or workspace buffers.
+ *     than a per-device "is gfx950" check, the device's compute-unit count
+ *     and the wait bound of w4a8_decode_wait_bound.  Concurrent calls must
+ *     not share output or workspace buffers.
  */
 #ifndef W4A8_H
 #define W4A8_H
@@ -132,7 +133,10 @@ int q4sym_q8f32_gemv(const void *w, const void *xq, float *y, int64_t N, int64_t
  * the sizes are invalid.  The workspace must be zero-filled once before its
  * first use (moe_w4a8_workspace_init does that); the library leaves its
  * synchronisation words zero again when each call completes, so it can be
- * reused by later calls with sizes up to the ones it was sized for.
+ * reused by later calls of any sizes whose moe_w4a8_workspace_size is at most
+ * ws_bytes.  The single-token hand-off region has the same offset and size
+ * for every shape, and no other region of any call overlaps it.  Calls that
+ * overlap in time must not share a workspace.
  */
 size_t moe_w4a8_workspace_size(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k);
 
@@ -149,7 +153,8 @@ int moe_w4a8_workspace_init(void *workspace, size_t ws_bytes, void *stream);
  *   W4A8_WS_H     fp32 h = SiLU(gate) * up, [P][I], P = T*k + T pairs.
  *   W4A8_WS_HQ    Q8_0(h), [P][I/32] blocks.
  *   W4A8_WS_PERM  int32 [T*k + T]: pairs sorted by expert (stable in pair
- *                 index), routed pairs first, then the T shared pairs.
+ *                 index), routed pairs first, then the T shared pairs (not
+ *                 written when T == 1: the single-token kernel needs no sort).
  *   W4A8_WS_COUNT int32 [E]: routed pairs per expert (not written when T == 1).
  *   W4A8_WS_SYNC  start of the synchronisation words, which end at
  *                 W4A8_WS_SYNC_END: zero before and after every call.
@@ -216,7 +221,8 @@ int moe_router_topk(const float *logits, int32_t *ids, float *weights, int64_t T
  *   workspace  ws_bytes >= moe_w4a8_workspace_size(T,H,I,E,k), zero-filled
  *              before its first use.
  * Shapes: H % 256, I % 256 != 0, T < 0 -> W4A8_ESHAPE; k < 1, k > 32, E < 1,
- * E > 4096 or T*(k+1) >= 2^31 -> W4A8_ERANGE.  T == 0 is a no-op.
+ * E > 4096 or T*(k+1) >= 2^31 -> W4A8_ERANGE.  T == 0 is a no-op.  out equal
+ * to hidden -> W4A8_EALIAS (no in-place calls).
  * Results: Q8_0 stages bit-exact with the format definition for the fp32
  * values they receive; float outputs within fp32 rounding of the exact sums.
  */
@@ -259,8 +265,8 @@ int moe_w4a8_layer(const float *x, const float *y_prev, const float *gamma, floa
  *   router_logits [T][E] fp32, finite; k > E -> W4A8_ERANGE.
  *   router_logits or shared_gate not 4-byte aligned -> W4A8_EALIGN;
  *   router_logits NULL, or shared_gate without a shared expert -> W4A8_ENULL.
- * Other arguments and errors as for moe_w4a8_layer.  Two launches at T = 1
- * (router, then the single-launch layer).
+ * Other arguments and errors as for moe_w4a8_layer.  At T = 1 (E <= 512) the
+ * routing runs inside the single launch of the layer.
  */
 int moe_w4a8_layer_routed(const float *x, const float *y_prev, const float *gamma, float eps,
                           float *x_out, const float *router_logits, const float *shared_gate,
@@ -284,6 +290,17 @@ int moe_w4a8_layer_routed(const float *x, const float *y_prev, const float *gamm
  */
 int rmsnorm_residual(const float *x, const float *y, const float *gamma, float *x_out,
                      float *xn, int64_t T, int64_t H, float eps, void *stream);
+
+/*
+ * Bound on the poll rounds of the single-token kernel's wait for the h blocks
+ * of other workgroups (each round one load round trip, about 0.5-1 us); past
+ * it a workgroup computes the blocks itself (same code, same bytes), so
+ * progress never depends on the order in which workgroups start.  Process
+ * wide: rounds >= 0 sets it, rounds < 0 leaves it; returns the previous
+ * value.  Default 2000, or W4A8_DECODE_SPIN_ROUNDS when set in the
+ * environment at the library's first use.
+ */
+int w4a8_decode_wait_bound(int64_t rounds);
 
 #ifdef __cplusplus
 }

@@ -26,7 +26,8 @@ EXPORTS = ("w4a8_strerror", "q8_0_quantize", "q4_0_quantize", "q4q8_gemv",
            "moe_w4a8_workspace_size", "moe_w4a8_workspace_init",
            "moe_w4a8_workspace_layout", "moe_w4a8_forward", "moe_w4a8_layer",
            "rmsnorm_residual", "moe_router_topk", "moe_w4a8_layer_routed",
-           "q4_sym_quantize", "q8_f32_quantize", "q4sym_q8f32_gemv")
+           "q4_sym_quantize", "q8_f32_quantize", "q4sym_q8f32_gemv",
+           "w4a8_decode_wait_bound")
 
 _lib = None
 
@@ -74,6 +75,8 @@ def lib() -> ctypes.CDLL:
     L.moe_w4a8_layer_routed.argtypes = [P, P, P, ctypes.c_float, P, P, P, P, P, P, P, P, P, P,
                                         I64, I64, I64, I64, I64, P, SZ, P]
     L.moe_w4a8_layer_routed.restype = ctypes.c_int
+    L.w4a8_decode_wait_bound.argtypes = [I64]
+    L.w4a8_decode_wait_bound.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -289,3 +292,10 @@ def moe_layer_routed(x, y_prev, gamma, router_logits, w_gate_up, w_down, ws_gate
                                      workspace.numel(), _stream(stream))
     _check(rc, "moe_w4a8_layer_routed")
     return x_out, out, topk_ids, topk_w
+
+
+def decode_wait_bound(rounds: int = -1) -> int:
+    """Set the single-token kernel's bound on poll rounds (rounds >= 0);
+    returns the previous bound."""
+    return int(lib().w4a8_decode_wait_bound(int(rounds)))
+

@@ -46,6 +46,8 @@
 // first workgroup also writes the ids, weights and gate value out.  The
 // selection costs a few hundred ns on each workgroup's path to its weight
 // loads, less than a launch of its own and the gap behind it.
+#include <algorithm>
+#include <atomic>
 #include <cstdlib>
 
 #include "router_dev.h"
@@ -602,10 +604,32 @@ void decode_grid(int64_t H, int64_t I, int64_t k, int ncu, int &grid, int &rb) {
 
 size_t decode_sync_words(int64_t) { return (size_t)SYNC_SLOTS * SYNC_STRIDE; }
 
+// Largest number of h blocks a single-token call hands off (decode_supported
+// bounds (k + 1) * I/32 by it).
+constexpr int XBLK_MAX = NWMAX * NT / XW;
+
 // Hand-off region for T = 1, in uint32 words: the call counter's line, then
-// one 128-byte line (XSTRIDE 64-bit words, XW used) per h block.
-size_t decode_xfer_words(int64_t I, int64_t k) {
-  return (size_t)XFER_HDR + (size_t)(k + 1) * (I / 32) * XSTRIDE * 2;
+// one 128-byte line (XSTRIDE 64-bit words, XW used) per h block, sized for
+// the largest supported (I, k).  Its size does not depend on the call's
+// shape, so no region of any other call's layout ever overlaps it: every
+// word in it was last written by a single-token call, with that call's tag,
+// which is below the current tag (the counter only grows; it would take 2^32
+// calls for a tag to come back).
+size_t decode_xfer_words() { return (size_t)XFER_HDR + (size_t)XBLK_MAX * XSTRIDE * 2; }
+
+// Bound on the poll rounds of the hand-off wait: W4A8_DECODE_SPIN_ROUNDS if
+// set when the library first needs it, else 2000 (about 1-2 ms);
+// w4a8_decode_wait_bound changes it.
+std::atomic<int> g_spin_rounds{-1};
+
+int spin_rounds() {
+  int v = g_spin_rounds.load(std::memory_order_relaxed);
+  if (v >= 0) return v;
+  int d = 2000;
+  if (const char *env = std::getenv("W4A8_DECODE_SPIN_ROUNDS")) d = std::max(0, std::atoi(env));
+  int expected = -1;
+  g_spin_rounds.compare_exchange_strong(expected, d, std::memory_order_relaxed);
+  return g_spin_rounds.load(std::memory_order_relaxed);
 }
 
 // Router in front of the launch: the logits of E experts fit wave 0's
@@ -621,7 +645,7 @@ bool decode_supported(int64_t H, int64_t I, int64_t k) {
     return false;
   const int64_t nbh = (k + 1) * (I / 32);
   const int rb = (int)(NT / ((k + 1) * (I / 256)));   // the largest slab
-  return XW * nbh <= NWMAX * NT && lds_bytes((int)H, (int)I, (int)k, rb) <= 48 * 1024;
+  return nbh <= XBLK_MAX && lds_bytes((int)H, (int)I, (int)k, rb) <= 48 * 1024;
 }
 
 int decode_forward(const float *x, const DecodeNorm &norm, const DecodeRoute *route,
@@ -653,9 +677,7 @@ int decode_forward(const float *x, const DecodeNorm &norm, const DecodeRoute *ro
   a.H = (int)H; a.I = (int)I; a.E = (int)E; a.k = (int)k;
   int grid = 0;
   decode_grid(H, I, k, ncu, grid, a.rb);
-  // default wait bound: 2000 poll rounds, about 1-2 ms
-  a.spin_rounds = 2000;
-  if (const char *env = std::getenv("W4A8_DECODE_SPIN_ROUNDS")) a.spin_rounds = std::atoi(env);
+  a.spin_rounds = spin_rounds();
   const size_t lds = lds_bytes((int)H, (int)I, (int)k, a.rb);
   if (route == nullptr)
     decode_kernel<0><<<dim3((unsigned)grid), dim3(NT), lds, s>>>(a);
@@ -667,3 +689,10 @@ int decode_forward(const float *x, const DecodeNorm &norm, const DecodeRoute *ro
 }
 
 }  // namespace w4a8
+
+extern "C" int w4a8_decode_wait_bound(int64_t rounds) {
+  const int prev = w4a8::spin_rounds();
+  if (rounds >= 0) w4a8::g_spin_rounds.store((int)std::min<int64_t>(rounds, 1 << 30),
+                                             std::memory_order_relaxed);
+  return prev;
+}

@@ -47,7 +47,7 @@ int mfma_down(const uint8_t *w_d, const uint8_t *ws_d, const uint32_t *ha, const
               const float *shared_w, float *y, int64_t maxtiles, int64_t T, int64_t H, int64_t I,
               int64_t E, int64_t k, hipStream_t s);
 size_t decode_sync_words(int64_t H);
-size_t decode_xfer_words(int64_t I, int64_t k);
+size_t decode_xfer_words();
 bool decode_supported(int64_t H, int64_t I, int64_t k);
 bool decode_routes(int64_t E, int64_t k);
 int decode_forward(const float *x, const DecodeNorm &norm, const DecodeRoute *route,
@@ -90,7 +90,7 @@ Layout make_layout(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k) {
   size_t off = 0;
   L.meta = off;   off += 256;
   L.sync = off;   off += up256(sizeof(uint32_t) * decode_sync_words(H));
-  L.xfer = off;   off += up256(sizeof(uint32_t) * decode_xfer_words(I, k));
+  L.xfer = off;   off += up256(sizeof(uint32_t) * decode_xfer_words());
   L.perm = off;   off += up256(sizeof(int32_t) * (P + SMALL_CHUNK));
   L.count = off;  off += up256(sizeof(int32_t) * E);
   L.rank = off;   off += up256(sizeof(int32_t) * (T * k + 1));
@@ -595,6 +595,22 @@ extern "C" int moe_w4a8_workspace_init(void *workspace, size_t ws_bytes, void *s
 namespace w4a8 {
 namespace {
 
+// Arguments of a layer call other than the workspace.
+int layer_core_args(const float *hidden, const int32_t *topk_ids, const float *topk_w,
+                    const void *w_gate_up, const void *w_down, const void *ws_gate_up,
+                    const void *ws_down, const float *out) {
+  if (!hidden || !topk_ids || !topk_w || !w_gate_up || !w_down || !out) return W4A8_ENULL;
+  if ((ws_gate_up == nullptr) != (ws_down == nullptr)) return W4A8_ENULL;
+  const void *ptrs[] = {hidden, topk_ids, topk_w, w_gate_up, w_down, out};
+  for (const void *p : ptrs)
+    if (!aligned16(p)) return W4A8_EALIGN;
+  if (ws_gate_up && (!aligned16(ws_gate_up) || !aligned16(ws_down))) return W4A8_EALIGN;
+  // the single-token kernel reads the input row after other workgroups have
+  // begun writing the output: no in-place calls
+  if (static_cast<const void *>(out) == static_cast<const void *>(hidden)) return W4A8_EALIAS;
+  return W4A8_OK;
+}
+
 int moe_args(const float *hidden, const int32_t *topk_ids, const float *topk_w,
              const void *w_gate_up, const void *w_down, const void *ws_gate_up,
              const void *ws_down, const float *out, int64_t T, int64_t H, int64_t I, int64_t E,
@@ -602,13 +618,11 @@ int moe_args(const float *hidden, const int32_t *topk_ids, const float *topk_w,
   int rc = validate(T, H, I, E, k);
   if (rc != W4A8_OK) return rc;
   if (T == 0) return W4A8_OK;
-  if (!hidden || !topk_ids || !topk_w || !w_gate_up || !w_down || !out || !workspace)
-    return W4A8_ENULL;
-  if ((ws_gate_up == nullptr) != (ws_down == nullptr)) return W4A8_ENULL;
-  const void *ptrs[] = {hidden, topk_ids, topk_w, w_gate_up, w_down, out, workspace};
-  for (const void *p : ptrs)
-    if (!aligned16(p)) return W4A8_EALIGN;
-  if (ws_gate_up && (!aligned16(ws_gate_up) || !aligned16(ws_down))) return W4A8_EALIGN;
+  if (!workspace) return W4A8_ENULL;
+  if ((rc = layer_core_args(hidden, topk_ids, topk_w, w_gate_up, w_down, ws_gate_up, ws_down,
+                            out)) != W4A8_OK)
+    return rc;
+  if (!aligned16(workspace)) return W4A8_EALIGN;
   if (ws_bytes < make_layout(T, H, I, E, k).total) return W4A8_EWORKSPACE;
   return W4A8_OK;
 }

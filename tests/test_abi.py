@@ -93,7 +93,8 @@ def test_moe_argument_errors():
     T, H, I, E, k = 2, 256, 256, 4, 2
     ws = w4.moe_workspace_size(T, H, I, E, k)
     p = _fake(A)
-    args = lambda **kw: [kw.get(n, p) for n in ("x", "ids", "w", "wgu", "wd", "sgu", "sd", "out")]
+    names = ("x", "ids", "w", "wgu", "wd", "sgu", "sd", "out")
+    args = lambda **kw: [kw.get(n, _fake(A + 0x1000 * i)) for i, n in enumerate(names)]
     assert f(*args(x=None), T, H, I, E, k, p, ws, None) == w4.ENULL
     assert f(*args(sgu=None), T, H, I, E, k, p, ws, None) == w4.ENULL      # one shared ptr alone
     assert f(*args(), T, 255, I, E, k, p, ws, None) == w4.ESHAPE
@@ -104,7 +105,17 @@ def test_moe_argument_errors():
     assert f(*args(), T, H, I, 0, k, p, ws, None) == w4.ERANGE
     assert f(*args(x=_fake(A + 8)), T, H, I, E, k, p, ws, None) == w4.EALIGN
     assert f(*args(), T, H, I, E, k, p, ws - 1, None) == w4.EWORKSPACE
+    assert f(*args(out=_fake(A)), T, H, I, E, k, p, ws, None) == w4.EALIAS   # out == hidden
     assert f(*args(), 0, H, I, E, k, p, ws, None) == w4.OK                 # empty: no-op
+
+
+def test_decode_wait_bound_set_and_restore():
+    prev = w4.decode_wait_bound(-1)        # query
+    assert prev >= 0
+    assert w4.decode_wait_bound(7) == prev
+    assert w4.decode_wait_bound(-5) == 7   # negative leaves it
+    assert w4.decode_wait_bound(prev) == 7
+    assert w4.decode_wait_bound(-1) == prev
 
 
 def test_rmsnorm_argument_errors():

@@ -258,26 +258,47 @@ def test_moe_decode_m1_many_steps_one_workspace(qwen_layer):
         L.check(x, ids, wts, 8, out, h, hq)
 
 
-def test_moe_decode_m1_wait_fallback(qwen_layer, monkeypatch):
+def test_moe_decode_m1_wait_fallback(qwen_layer):
     """Force the bounded wait of the single-launch decode kernel to expire at
-    once (spin limit 0 set from the host): every down-projection workgroup
-    then computes its pair's h itself.  Same bytes as the normal path, and the
-    counters still return to zero."""
+    once (poll bound 0 set from the host through w4a8_decode_wait_bound):
+    every down-projection workgroup then computes its pair's h itself.  Same
+    bytes as the normal path, and the counters still return to zero."""
     L = qwen_layer
     g = synth.rng(24)
     x = synth.normal_f32(g, (1, L.H))
     ids, wts = synth.routing(g, 1, L.E, 8)
     ws = w4.moe_workspace(1, L.H, L.I, L.E, 8)
     out, h, hq, *_ = L.run(x, ids, wts, 8, ws=ws)
-    monkeypatch.setenv("W4A8_DECODE_SPIN_ROUNDS", "0")
-    out_fb, h_fb, hq_fb, *_ = L.run(x, ids, wts, 8, ws=ws)
-    monkeypatch.delenv("W4A8_DECODE_SPIN_ROUNDS")
+    prev = w4.decode_wait_bound(0)
+    try:
+        out_fb, h_fb, hq_fb, *_ = L.run(x, ids, wts, 8, ws=ws)
+    finally:
+        assert w4.decode_wait_bound(prev) == 0
     assert np.array_equal(out, out_fb) and np.array_equal(hq, hq_fb)
     L.check(x, ids, wts, 8, out_fb, h_fb, hq_fb)
     x2 = synth.normal_f32(g, (1, L.H))
     ids2, wts2 = synth.routing(g, 1, L.E, 8)
     out2, h2, hq2, *_ = L.run(x2, ids2, wts2, 8, ws=ws)
     L.check(x2, ids2, wts2, 8, out2, h2, hq2)
+
+
+def test_moe_workspace_reused_across_shapes(qwen_layer):
+    """One workspace for a 32-token call with k = 4 (the grouped path writes
+    its sort, tile and activation regions), then single-token calls with
+    k = 8, whose hand-off region lies in the same workspace: each checked
+    against the oracle (no stale hand-off word may be taken as this call's)."""
+    L = qwen_layer
+    g = synth.rng(27)
+    ws = w4.moe_workspace(32, L.H, L.I, L.E, 8)
+    x = synth.normal_f32(g, (32, L.H))
+    ids, wts = synth.routing(g, 32, L.E, 4)
+    out, h, hq, *_ = L.run(x, ids, wts, 4, ws=ws)
+    L.check(x, ids, wts, 4, out, h, hq)
+    for _ in range(3):
+        x = synth.normal_f32(g, (1, L.H))
+        ids, wts = synth.routing(g, 1, L.E, 8)
+        out, h, hq, *_ = L.run(x, ids, wts, 8, ws=ws)
+        L.check(x, ids, wts, 8, out, h, hq)
 
 
 def test_moe_decode_m1_no_shared_small_shapes():
