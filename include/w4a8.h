@@ -34,9 +34,10 @@
  *   - Shapes are validated on the host before anything is launched; on an
  *     error nothing is enqueued and no output is touched.
  *   - Calls are thread-safe and re-entrant: the library keeps no state other
- *     than a per-device "is gfx950" check, the device's compute-unit count
- *     and the wait bound of w4a8_decode_wait_bound.  Concurrent calls must
- *     not share output or workspace buffers.
+ *     than a per-device "is gfx950" check, the device's compute-unit count,
+ *     the wait bound of w4a8_decode_wait_bound and, per device, the scratch
+ *     array of moe_w4a8_forward_noalloc.  Concurrent calls must not share
+ *     output or workspace buffers.
  */
 #ifndef W4A8_H
 #define W4A8_H
@@ -58,6 +59,8 @@ extern "C" {
 #define W4A8_EHIP       -6  /* a HIP runtime call or kernel launch failed        */
 #define W4A8_EDEVICE    -7  /* the current device is not gfx950                  */
 #define W4A8_EALIAS     -8  /* an output shares its base address with an operand */
+#define W4A8_ESCRATCH   -9  /* sizes beyond the fixed scratch of the no-allocation
+                               entry point (W4A8_NOALLOC_SCRATCH_BYTES)           */
 
 #define W4A8_Q4_0_BLOCK_BYTES 18
 #define W4A8_Q8_0_BLOCK_BYTES 34
@@ -301,6 +304,26 @@ int rmsnorm_residual(const float *x, const float *y, const float *gamma, float *
  * environment at the library's first use.
  */
 int w4a8_decode_wait_bound(int64_t rounds);
+
+/*
+ * moe_w4a8_forward for callers that cannot allocate device memory or pass a
+ * workspace: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc.  Same arguments and results as moe_w4a8_forward
+ * without the workspace, which is instead a fixed array of
+ * W4A8_NOALLOC_SCRATCH_BYTES in device memory, one per GPU, held by the
+ * library until the process ends (8 MiB: at the paper's layer shape, H =
+ * 2048, I = 512, E = 256, k = 8, up to T = 66 tokens).  Sizes whose
+ * moe_w4a8_workspace_size exceeds it -> W4A8_ESCRATCH.  The call allocates
+ * nothing (no hipMalloc, no library allocation).  All calls on one GPU share
+ * that GPU's array: calls that overlap in time on one GPU (other streams,
+ * other threads) race and give undefined results.
+ */
+#define W4A8_NOALLOC_SCRATCH_BYTES ((size_t)8 << 20)
+int moe_w4a8_forward_noalloc(const float *hidden, const int32_t *topk_ids, const float *topk_w,
+                             const void *w_gate_up, const void *w_down,
+                             const void *ws_gate_up, const void *ws_down,
+                             float *out, int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
+                             void *stream);
 
 #ifdef __cplusplus
 }

@@ -14,7 +14,9 @@ import os
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libw4a8.so")
 
-OK, ENULL, ESHAPE, ERANGE, EWORKSPACE, EALIGN, EHIP, EDEVICE, EALIAS = 0, -1, -2, -3, -4, -5, -6, -7, -8
+OK, ENULL, ESHAPE, ERANGE, EWORKSPACE, EALIGN, EHIP, EDEVICE, EALIAS, ESCRATCH = \
+    0, -1, -2, -3, -4, -5, -6, -7, -8, -9
+NOALLOC_SCRATCH_BYTES = 8 << 20
 Q4_0_BLOCK_BYTES = 18
 Q8_0_BLOCK_BYTES = 34
 Q4_SYM_BLOCK_BYTES = 20
@@ -27,7 +29,7 @@ EXPORTS = ("w4a8_strerror", "q8_0_quantize", "q4_0_quantize", "q4q8_gemv",
            "moe_w4a8_workspace_layout", "moe_w4a8_forward", "moe_w4a8_layer",
            "rmsnorm_residual", "moe_router_topk", "moe_w4a8_layer_routed",
            "q4_sym_quantize", "q8_f32_quantize", "q4sym_q8f32_gemv",
-           "w4a8_decode_wait_bound")
+           "w4a8_decode_wait_bound", "moe_w4a8_forward_noalloc")
 
 _lib = None
 
@@ -77,6 +79,8 @@ def lib() -> ctypes.CDLL:
     L.moe_w4a8_layer_routed.restype = ctypes.c_int
     L.w4a8_decode_wait_bound.argtypes = [I64]
     L.w4a8_decode_wait_bound.restype = ctypes.c_int
+    L.moe_w4a8_forward_noalloc.argtypes = [P, P, P, P, P, P, P, P, I64, I64, I64, I64, I64, P]
+    L.moe_w4a8_forward_noalloc.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -299,3 +303,21 @@ def decode_wait_bound(rounds: int = -1) -> int:
     returns the previous bound."""
     return int(lib().w4a8_decode_wait_bound(int(rounds)))
 
+
+def moe_forward_noalloc(hidden, topk_ids, topk_w, w_gate_up, w_down, ws_gate_up, ws_down,
+                        H, I, E, k, out=None, stream=None):
+    """moe_forward without a workspace argument: the library's fixed per-GPU
+    scratch array serves as the workspace (moe_w4a8_forward_noalloc).  With
+    `out` given, nothing is allocated."""
+    import torch
+    T = hidden.shape[0]
+    assert hidden.dtype == torch.float32 and hidden.is_contiguous()
+    assert topk_ids.dtype == torch.int32 and topk_ids.is_contiguous()
+    assert topk_w.dtype == torch.float32 and topk_w.is_contiguous()
+    if out is None:
+        out = torch.empty((T, H), dtype=torch.float32, device=hidden.device)
+    rc = lib().moe_w4a8_forward_noalloc(_p(hidden), _p(topk_ids), _p(topk_w), _p(_u8(w_gate_up)),
+                                        _p(_u8(w_down)), _p(ws_gate_up), _p(ws_down), _p(out),
+                                        T, H, I, E, k, _stream(stream))
+    _check(rc, "moe_w4a8_forward_noalloc")
+    return out

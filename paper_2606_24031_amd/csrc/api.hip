@@ -15,6 +15,9 @@ extern "C" const char *w4a8_strerror(int code) {
     case W4A8_EHIP: return "HIP runtime error or kernel launch failure";
     case W4A8_EDEVICE: return "current device is not gfx950 (MI355X)";
     case W4A8_EALIAS: return "an output buffer aliases an input or another output";
+    case W4A8_ESCRATCH:
+      return "these sizes need more workspace than the fixed scratch of the no-allocation "
+             "entry point holds (W4A8_NOALLOC_SCRATCH_BYTES)";
     default: return "unknown status code";
   }
 }

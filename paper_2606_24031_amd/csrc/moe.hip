@@ -20,6 +20,7 @@
 //   5. combine: out[t] = sum over slots in slot order, then the shared pair
 //      (fixed order, so the result does not depend on scheduling)
 #include <algorithm>
+#include <mutex>
 
 #include "w4a8_dev.h"
 #include "w4a8_host.h"
@@ -743,4 +744,70 @@ extern "C" int moe_w4a8_layer_routed(const float *x, const float *y_prev, const 
                           reinterpret_cast<const uint8_t *>(ws_gate_up),
                           reinterpret_cast<const uint8_t *>(ws_down), out, T, H, I, E, k, ws,
                           ws_bytes, s);
+}
+
+// ------------------------------------------------------------ no allocation
+// moe_w4a8_forward for callers that cannot allocate (code under graph
+// capture, tight serving loops): the workspace is a fixed array in device
+// memory, one per GPU, that the library owns for the life of the process.
+namespace w4a8 {
+namespace {
+
+static __device__ __align__(256) uint8_t scratch[W4A8_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mutex;
+void *g_scratch_ptr[kMaxScratchDevices];   // device address of `scratch`, per device
+
+// The device address of this device's scratch array, looked up once per
+// device with the device current (in host code the array's name is only a
+// host-side stand-in).  The array is zero when the code object is loaded; the
+// first call on a device also clears it on the caller's stream (unless that
+// stream is being captured), before its own kernels.
+int scratch_for_device(hipStream_t s, uint8_t **out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return W4A8_EHIP;
+  if (dev < 0 || dev >= kMaxScratchDevices) return W4A8_EDEVICE;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr)
+      return W4A8_EHIP;
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(s, &cs) != hipSuccess) return W4A8_EHIP;
+    if (cs == hipStreamCaptureStatusNone) {
+      const int rc = launch_fill_zero(p, W4A8_NOALLOC_SCRATCH_BYTES, s);
+      if (rc != W4A8_OK) return rc;
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  *out = reinterpret_cast<uint8_t *>(g_scratch_ptr[dev]);
+  return W4A8_OK;
+}
+
+}  // namespace
+}  // namespace w4a8
+
+extern "C" int moe_w4a8_forward_noalloc(const float *hidden, const int32_t *topk_ids,
+                                        const float *topk_w, const void *w_gate_up,
+                                        const void *w_down, const void *ws_gate_up,
+                                        const void *ws_down, float *out, int64_t T, int64_t H,
+                                        int64_t I, int64_t E, int64_t k, void *stream) {
+  int rc = validate(T, H, I, E, k);
+  if (rc != W4A8_OK || T == 0) return rc;
+  if ((rc = layer_core_args(hidden, topk_ids, topk_w, w_gate_up, w_down, ws_gate_up, ws_down,
+                            out)) != W4A8_OK)
+    return rc;
+  const size_t need = make_layout(T, H, I, E, k).total;
+  if (need > W4A8_NOALLOC_SCRATCH_BYTES) return W4A8_ESCRATCH;
+  if ((rc = check_device()) != W4A8_OK) return rc;
+  hipStream_t s = as_stream(stream);
+  uint8_t *ws = nullptr;
+  if ((rc = scratch_for_device(s, &ws)) != W4A8_OK) return rc;
+  return moe_forward_impl(hidden, DecodeNorm{}, topk_ids, topk_w, nullptr,
+                          reinterpret_cast<const uint8_t *>(w_gate_up),
+                          reinterpret_cast<const uint8_t *>(w_down),
+                          reinterpret_cast<const uint8_t *>(ws_gate_up),
+                          reinterpret_cast<const uint8_t *>(ws_down), out, T, H, I, E, k, ws, need,
+                          s);
 }

@@ -30,7 +30,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_strerror_covers_every_code():
     for code in (w4.OK, w4.ENULL, w4.ESHAPE, w4.ERANGE, w4.EWORKSPACE, w4.EALIGN, w4.EHIP, w4.EDEVICE,
-                 w4.EALIAS):
+                 w4.EALIAS, w4.ESCRATCH):
         msg = w4.strerror(code)
         assert msg and msg != "unknown status code"
     assert w4.strerror(12345) == "unknown status code"
@@ -107,6 +107,27 @@ def test_moe_argument_errors():
     assert f(*args(), T, H, I, E, k, p, ws - 1, None) == w4.EWORKSPACE
     assert f(*args(out=_fake(A)), T, H, I, E, k, p, ws, None) == w4.EALIAS   # out == hidden
     assert f(*args(), 0, H, I, E, k, p, ws, None) == w4.OK                 # empty: no-op
+
+
+def test_moe_noalloc_argument_errors():
+    """The no-allocation entry point validates like moe_w4a8_forward, and
+    sizes whose workspace exceeds its fixed scratch give W4A8_ESCRATCH (all
+    before any device call)."""
+    f = w4.lib().moe_w4a8_forward_noalloc
+    names = ("x", "ids", "w", "wgu", "wd", "sgu", "sd", "out")
+    args = lambda **kw: [kw.get(n, _fake(A + 0x1000 * i)) for i, n in enumerate(names)]
+    H, I, E, k = 2048, 512, 256, 8
+    assert w4.moe_workspace_size(66, H, I, E, k) <= w4.NOALLOC_SCRATCH_BYTES
+    assert w4.moe_workspace_size(67, H, I, E, k) > w4.NOALLOC_SCRATCH_BYTES
+    assert f(*args(), 67, H, I, E, k, None) == w4.ESCRATCH
+    assert f(*args(), 947, H, I, E, k, None) == w4.ESCRATCH
+    assert f(*args(x=None), 1, H, I, E, k, None) == w4.ENULL
+    assert f(*args(sd=None), 1, H, I, E, k, None) == w4.ENULL
+    assert f(*args(), 1, 2000, I, E, k, None) == w4.ESHAPE
+    assert f(*args(), 1, H, I, E, 0, None) == w4.ERANGE
+    assert f(*args(ids=_fake(A + 4)), 1, H, I, E, k, None) == w4.EALIGN
+    assert f(*args(out=_fake(A)), 1, H, I, E, k, None) == w4.EALIAS
+    assert f(*args(), 0, H, I, E, k, None) == w4.OK                      # empty: no-op
 
 
 def test_decode_wait_bound_set_and_restore():
