@@ -23,13 +23,66 @@ CPU oracle timed on this host on a bounded sample of the decode workload.
 """
 from __future__ import annotations
 
-import argparse
-import hashlib
-import json
 import os
 import re
-import sys
-import time
+
+
+def _host_setup():
+    """Runs before torch or the CPU oracle load (OpenMP reads its settings
+    when it starts): one OpenMP thread per physical core -- at most the CPU
+    share the host gives this process, an OMP_NUM_THREADS already set --
+    bound close, and, when more than one NUMA node is allowed, page
+    interleaving over them for this process (the paper interleaves its expert
+    block over both sockets, Sec. 4.3; hyper-threads hurt, Sec. 5.5)."""
+    info = {}
+    try:
+        out = os.popen("lscpu").read()
+        soc = int(re.search(r"Socket\(s\):\s+(\d+)", out).group(1))
+        cps = int(re.search(r"Core\(s\) per socket:\s+(\d+)", out).group(1))
+        info["physical_cores"] = soc * cps
+    except Exception:
+        info["physical_cores"] = os.cpu_count() or 1
+    n = info["physical_cores"]
+    share = os.environ.get("OMP_NUM_THREADS", "")
+    if share.isdigit() and int(share) > 0:
+        n = min(n, int(share))
+        info["cpu_share"] = int(share)
+    os.environ["OMP_NUM_THREADS"] = str(n)
+    os.environ["OMP_PROC_BIND"] = "close"
+    os.environ["OMP_PLACES"] = "cores"
+    info["omp_threads"] = n
+    nodes = []
+    try:
+        with open("/proc/self/status") as f:
+            for line in f:
+                if line.startswith("Mems_allowed_list:"):
+                    for part in line.split(":", 1)[1].strip().split(","):
+                        a, _, b = part.partition("-")
+                        nodes += list(range(int(a), int(b or a) + 1))
+    except Exception:
+        pass
+    info["numa_nodes"] = len(nodes) or 1
+    info["numa_policy"] = "default"
+    if len(nodes) > 1:
+        import ctypes
+        mask = 0
+        for nd in nodes:
+            mask |= 1 << nd
+        words = (ctypes.c_ulong * 16)(*[(mask >> (64 * i)) & ((1 << 64) - 1) for i in range(16)])
+        libc = ctypes.CDLL(None, use_errno=True)
+        MPOL_INTERLEAVE, SYS_set_mempolicy = 3, 238
+        rc = libc.syscall(SYS_set_mempolicy, MPOL_INTERLEAVE, words, ctypes.c_ulong(16 * 64))
+        info["numa_policy"] = "interleave" if rc == 0 else f"interleave failed (errno {ctypes.get_errno()})"
+    return info
+
+
+HOST = _host_setup()
+
+import argparse   # noqa: E402
+import hashlib    # noqa: E402
+import json       # noqa: E402
+import sys        # noqa: E402
+import time       # noqa: E402
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
@@ -577,45 +630,121 @@ def bench_stack(torch, w4, synth, args, dev):
             "launch": "prefill eager; decode steps replayed from one HIP graph"}
 
 
-def physical_threads_note():
-    try:
-        out = os.popen("lscpu").read()
-        soc = int(re.search(r"Socket\(s\):\s+(\d+)", out).group(1))
-        cps = int(re.search(r"Core\(s\) per socket:\s+(\d+)", out).group(1))
-        return soc * cps
-    except Exception:
-        return None
-
-
 def cpu_baseline(synth, seconds):
-    """The oracle on this host: independent single-token decode steps of the
-    same layer shape, OpenMP across tokens, until `seconds` have elapsed."""
+    """The oracle as it stands (plain C, scalar, fp64 accumulation) on this
+    host's cores, for every workload: one thread, then one per physical core
+    (OpenMP across tokens; the oracle takes a token's experts one after the
+    other, so a single token runs on one core).  Expert weights are eight
+    random experts' Q4_0 bytes tiled over the 256 (the time does not depend
+    on the values).  `value` is the all-core decode rate of the headline
+    workload, in the same algorithmic GB/s as the GPU figure.  The 40-layer
+    stack is timed on two layers and extrapolated x20 (labelled)."""
     import numpy as np
     import oracle
     g = synth.rng(7)
-    # eight random experts' bytes tiled over the 256 (timing does not depend
-    # on the values; keeps host generation short)
     gu8 = synth.q4_0_random_blocks(g, 8 * 2 * I, H).reshape(8, 2 * I, -1)
     d8 = synth.q4_0_random_blocks(g, 8 * H, I).reshape(8, H, -1)
     w_gu = np.ascontiguousarray(np.tile(gu8, (E // 8, 1, 1)))
     w_d = np.ascontiguousarray(np.tile(d8, (E // 8, 1, 1)))
     s_gu, s_d = gu8[0].copy(), d8[0].copy()
-    threads = oracle.threads()
-    batch = max(1, threads)
-    done_tokens, done_bytes, t_used = 0, 0, 0.0
-    while t_used < seconds:
-        x = synth.normal_f32(g, (batch, H))
-        ids, wts = synth.routing(g, batch, E, K_TOP)
-        t0 = time.perf_counter()
+    gamma = np.ones(H, np.float32)
+    n_all = oracle.threads()
+
+    def timed(fn, budget, min_reps=1):
+        reps, t = 0, 0.0
+        while reps < min_reps or t < budget:
+            t0 = time.perf_counter()
+            fn()
+            t += time.perf_counter() - t0
+            reps += 1
+        return t / reps, reps
+
+    def moe(x, ids, wts):
         oracle.moe(x, ids, wts, w_gu, w_d, s_gu, s_d, H, I, E, K_TOP, want_intermediates=False)
-        t_used += time.perf_counter() - t0
-        done_tokens += batch
-        done_bytes += sum(step_bytes(ids[t]) for t in range(batch))
-    return {"value": round(done_bytes / t_used / 1e9, 3), "unit": "GB/s", "cores": threads,
-            "kind": "oracle",
-            "sample": f"{done_tokens} independent M=1 decode steps of the same layer shape "
-                      f"(256+1 experts, top-8), {t_used:.1f} s, OpenMP across tokens, "
-                      f"{physical_threads_note()} physical cores on this host"}
+
+    res = {}
+    for label, nt in (("1_thread", 1), ("all_cores", n_all)):
+        oracle.set_threads(nt)
+        r = {}
+        # C1: the 1024 x 1024 GEMV
+        W = synth.q4_0_random_blocks(g, 1024, 1024)
+        xq = oracle.q8_0_quantize(synth.normal_f32(g, (1, 1024)))
+        t, n = timed(lambda: oracle.gemv(W, xq, 1024, 1024), 0.5, 3)
+        nb = 1024 * 32 * 18 + 32 * 34 + 1024 * 4
+        r["gemv_1024"] = {"us_per_call": round(t * 1e6, 1), "GBps": round(nb / t / 1e9, 3),
+                          "calls": n}
+        # C2: single-token decode layer, latency; all cores: throughput over
+        # independent tokens (the headline value)
+        x = synth.normal_f32(g, (1, H))
+        ids, wts = synth.routing(g, 1, E, K_TOP)
+        t, n = timed(lambda: moe(x, ids, wts), 1.0, 2)
+        r["decode_m1"] = {"ms_per_step": round(t * 1e3, 2),
+                          "GBps": round(step_bytes(ids[0]) / t / 1e9, 3), "steps": n}
+        if nt > 1:
+            batch = 2 * nt
+            done_t, done_b, used = 0, 0, 0.0
+            while used < seconds:
+                xb = synth.normal_f32(g, (batch, H))
+                ib, wb = synth.routing(g, batch, E, K_TOP)
+                t0 = time.perf_counter()
+                moe(xb, ib, wb)
+                used += time.perf_counter() - t0
+                done_t += batch
+                done_b += sum(step_bytes(ib[t_]) for t_ in range(batch))
+            r["decode_m1_throughput"] = {"GBps": round(done_b / used / 1e9, 3),
+                                         "tokens_per_s": round(done_t / used, 1),
+                                         "steps": done_t, "seconds": round(used, 1)}
+        # C3: the 32-token batched decode layer
+        x = synth.normal_f32(g, (32, H))
+        ids, wts = synth.routing(g, 32, E, K_TOP)
+        t, n = timed(lambda: moe(x, ids, wts), 1.0)
+        r["decode_m32"] = {"ms_per_layer": round(t * 1e3, 2),
+                           "tokens_per_s": round(32 / t, 1), "calls": n}
+        # C4: the 947-token prefill layer (biased routing); on one thread a
+        # sample of 24 of its tokens (the oracle's time is per token)
+        Tp = 947 if nt > 1 else 24
+        x = synth.normal_f32(g, (947, H))
+        ids, wts = synth.routing(g, 947, E, K_TOP, bias_std=1.0)
+        t, n = timed(lambda: moe(x[:Tp], ids[:Tp], wts[:Tp]), 0.5)
+        r["prefill_947"] = {"tokens_timed": Tp, "tokens_per_s": round(Tp / t, 1),
+                            "ms_per_layer": round(947 / (Tp / t) * 1e3, 1),
+                            "extrapolated_from_sample": Tp != 947}
+        # C5: two chained layers (residual add + RMSNorm + layer), x20
+        Tp5 = 947 if nt > 1 else 24
+        t0 = time.perf_counter()
+        xs, y = x[:Tp5], None
+        for _ in range(2):
+            xs, xn = oracle.rmsnorm_residual(xs, y, gamma)
+            y = oracle.moe(xn.astype(np.float32), ids[:Tp5], wts[:Tp5], w_gu, w_d, s_gu, s_d, H,
+                           I, E, K_TOP, want_intermediates=False).out.astype(np.float32)
+        t_pre = (time.perf_counter() - t0) * 20 * 947 / Tp5
+        ids1, wts1 = synth.routing(g, 4, E, K_TOP)
+        t0 = time.perf_counter()
+        for s_ in range(2):                      # two decode steps through two layers
+            xs, y = synth.normal_f32(g, (1, H)), None
+            for l in range(2):
+                xs, xn = oracle.rmsnorm_residual(xs, y, gamma)
+                y = oracle.moe(xn.astype(np.float32), ids1[2 * s_ + l:2 * s_ + l + 1],
+                               wts1[2 * s_ + l:2 * s_ + l + 1], w_gu, w_d, s_gu, s_d, H, I, E,
+                               K_TOP, want_intermediates=False).out.astype(np.float32)
+        t_dec = (time.perf_counter() - t0) / 2 * 20
+        r["stack_40_extrapolated"] = {"prefill_947_s": round(t_pre, 2),
+                                      "decode_ms_per_token": round(t_dec * 1e3, 1),
+                                      "decode_tokens_per_s": round(1.0 / t_dec, 2),
+                                      "note": "two layers timed, x20; prefill on one thread "
+                                              "from a 24-token sample" if nt == 1 else
+                                              "two layers timed, x20"}
+        res[label] = r
+    oracle.set_threads(n_all)
+    main = res["all_cores"]["decode_m1_throughput"]
+    return {"value": main["GBps"], "unit": "GB/s", "cores": n_all, "kind": "oracle",
+            "sample": f"{main['steps']} independent M=1 decode steps of the same layer shape "
+                      f"(256+1 experts, top-8), {main['seconds']} s, OpenMP across tokens on "
+                      f"{n_all} threads ({HOST['physical_cores']} physical cores on this host, "
+                      f"OMP_PROC_BIND=close, NUMA {HOST['numa_policy']} over "
+                      f"{HOST['numa_nodes']} node(s)); per-workload single-thread and all-core "
+                      f"times under 'configs'",
+            "configs": res, "host": HOST}
 
 
 def hbm_copy_rate(torch, dev, nbytes=2 << 30, reps=10):

@@ -72,6 +72,7 @@ def _load():
     lib.orc_q8_0_candidates.argtypes = [P, P, I64, P, P, P, P]
     lib.orc_q8_0_candidates.restype = ctypes.c_int
     lib.orc_threads.restype = ctypes.c_int
+    lib.orc_set_threads.argtypes = [ctypes.c_int]
     lib.orc_rmsnorm_residual.argtypes = [P, P, P, P, P, I64, I64, ctypes.c_double]
     lib.orc_router_topk.argtypes = [P, P, P, I64, I64, I64, P]
     _lib = lib
@@ -89,6 +90,12 @@ def _c(a, dtype):
 def threads() -> int:
     """OpenMP threads the oracle's parallel loops use (OMP_NUM_THREADS)."""
     return int(_load().orc_threads())
+
+
+def set_threads(n: int) -> None:
+    """Use n OpenMP threads from now on (timing only; results do not depend
+    on it)."""
+    _load().orc_set_threads(int(n))
 
 
 # ---------------------------------------------------------------- fp16

@@ -479,6 +479,13 @@ void orc_router_topk(const float *logits, int32_t *ids, double *weights, int64_t
     }
 }
 
+/* Threads for the parallel loops above from now on (timing of the oracle on
+ * one core and on all of them; the arithmetic does not depend on it). */
+void orc_set_threads(int n)
+{
+    if (n > 0) omp_set_num_threads(n);
+}
+
 /* Number of OpenMP threads the parallel loops above use. */
 int orc_threads(void)
 {
