@@ -431,6 +431,50 @@ __device__ void route_finish(DecodeArgs &a, float (&x)[RV], float g, int32_t *ri
   a.shared_w = rw + a.k;
 }
 
+// A down slab's eight weight blocks decoded while it waits for h: each
+// block's payload dwords as stored (the unsigned nibbles q) and with every
+// nibble xor 8 (the signed nibbles q - 8), and its fp32 scale.  After the
+// wait only the 4-bit dot products and one scaling per block remain.
+struct W8Dec {
+  uint32_t n[8][4], x[8][4];
+  float d[8];
+};
+__device__ __forceinline__ void decode_w8(const W8 &w, W8Dec &o) {
+#pragma unroll
+  for (int k = 0; k < 8; k++) {
+#pragma unroll
+    for (int c = 0; c < 4; c++) {
+      o.n[k][c] = w8_nib(w, k, c);
+      o.x[k][c] = o.n[k][c] ^ 0x88888888u;
+      // materialized here, ahead of the wait, not next to their use after it
+      asm volatile("" : "+v"(o.n[k][c]), "+v"(o.x[k][c]));
+    }
+    o.d[k] = w8_scale(w, k);
+    asm volatile("" : "+v"(o.d[k]));
+  }
+}
+// acc + sum over the eight blocks of d_w * d_h * s against activations
+// staged in LDS (see dot8_lds), on decoded weights.
+__device__ __forceinline__ float dot8_dec(const W8Dec &w, const uint4 *__restrict__ codes,
+                                          const float *__restrict__ d,
+                                          const int *__restrict__ corr, float acc) {
+#pragma unroll
+  for (int k = 0; k < 8; k++) {
+    const uint4 hi = codes[2 * k], lo = codes[2 * k + 1];
+    const uint32_t h4[4] = {hi.x, hi.y, hi.z, hi.w}, l4[4] = {lo.x, lo.y, lo.z, lo.w};
+    int sa = 0;
+    uint32_t sb = (uint32_t)corr[k];
+#pragma unroll
+    for (int c = 0; c < 4; c++) {
+      sa = __builtin_amdgcn_sdot8((int)w.x[k][c], (int)h4[c], sa, false);
+      sb = __builtin_amdgcn_udot8(w.n[k][c], l4[c], sb, false);
+    }
+    const int s = (int)(((uint32_t)sa << 4) + sb);
+    acc = fmaf((float)s, w.d[k] * d[k], acc);
+  }
+  return acc;
+}
+
 // LDS: Q8_0(x) staging, then Q8_0(h) staging of every pair, then the
 // weighted per-pair sums [rb][k+1 padded to 4] and, when I > 512, the down
 // partials (NT floats).
@@ -520,6 +564,8 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
   const ActBuf hb = act_buf(lds + lds_x_bytes(a.H), nbh);
   float *part = reinterpret_cast<float *>(lds + lds_x_bytes(a.H) + act_buf_bytes(nbh));
   if (threadIdx.x < 3) notdone[threadIdx.x] = 0;
+  W8Dec wd;
+  if (ulive) decode_w8(wpre, wd);
   __syncthreads();
   const bool ok = collect(a, hb, tag, XW * nbh, vmask, notdone);
   if (!ok) {
@@ -539,7 +585,7 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
   float acc = 0.0f;
   if (ulive) {
     const int blk0 = uq * nb_h + ug * 8;
-    acc = dot8_lds(wpre, group_codes(hb, blk0), hb.d + blk0, hb.corr + blk0, 0.0f);
+    acc = dot8_dec(wd, group_codes(hb, blk0), hb.d + blk0, hb.corr + blk0, 0.0f);
   }
   // weighted y_q[n] = w_q * (sum over g in order), stored transposed
   // yw[r][q] with the pair count padded to a multiple of 4 (pads and skipped
