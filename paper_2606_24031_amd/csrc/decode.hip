@@ -514,13 +514,15 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
     const int q = wg / nb_h, b = wg - q * nb_h;
     // x and the expert id land before the weights are issued: on every path
     // the later uses of x then wait for nothing in flight behind them
+    // (the call tag too: a load issued after the weights would be waited for
+    // together with them, since loads retire in order)
     int e;
     const bool valid = pair_valid(a, q, e);
-    asm volatile("" ::"v"(x0.x), "v"(x0.y), "v"(x0.z), "v"(x0.w), "v"(e));
+    const uint32_t tag = ld_agent(a.calls) + 1u;
+    asm volatile("" ::"v"(x0.x), "v"(x0.y), "v"(x0.z), "v"(x0.w), "v"(e), "v"(tag));
     W8 w0;
     const ARole r = a_role();
     if (valid && r.gg < a.H / 256) load_w8(a_row(a, e, b, r) + (int64_t)r.gg * (8 * Q4B), w0);
-    const uint32_t tag = ld_agent(a.calls) + 1u;
     if (valid || wg == 0) {
       quantize_x_to_lds(a, xb, wg == 0, x0);
       __syncthreads();
