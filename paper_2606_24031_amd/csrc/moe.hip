@@ -71,8 +71,20 @@ constexpr int LDS_INTS = 16000; // int32 cells of dynamic LDS for the route kern
 
 inline size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+constexpr int SLICE = ROUTE_T;   // pairs per slice of the split route
+constexpr int RCH = 16;          // pairs a route thread keeps in registers
+
+// The route splits into per-slice ranks beside the quantization and one
+// finishing workgroup when there are several slices' worth of pairs, the
+// slice's per-chunk counts fit in LDS (16 x E ints) and so do the finishing
+// workgroup's per-(expert, slice) counts.
+inline bool split_route(int64_t Pr, int64_t E) {
+  const int64_t nslice = (Pr + SLICE - 1) / SLICE;
+  return Pr > 64 && Pr <= (int64_t)RCH * SLICE && E <= 1024 && E * nslice <= LDS_INTS;
+}
+
 struct Layout {
-  size_t meta, sync, xfer, perm, count, rank, groups, tiles, chunks, xq, h, hq, y, xn, xs, hs,
+  size_t meta, sync, xfer, perm, count, rank, hist, groups, tiles, chunks, xq, h, hq, y, xn, xs, hs,
       xa, xd, ha, hd, sw, total;
   int64_t maxtiles, maxchunks;
 };
@@ -95,6 +107,7 @@ Layout make_layout(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k) {
   L.perm = off;   off += up256(sizeof(int32_t) * (P + SMALL_CHUNK));
   L.count = off;  off += up256(sizeof(int32_t) * E);
   L.rank = off;   off += up256(sizeof(int32_t) * (T * k + 1));
+  L.hist = off;   off += up256(sizeof(int32_t) * (size_t)E * ((T * k + SLICE - 1) / SLICE));
   L.groups = off; off += up256(sizeof(int4) * (E + 1));
   L.tiles = off;  off += up256(sizeof(int4) * L.maxtiles);
   L.maxchunks = small_max_chunks(T, E, k, 1);
@@ -191,7 +204,6 @@ __device__ void block_exscan(int *const (&a)[NA], int n, int (*wtot)[ROUTE_T / 6
   __syncthreads();
 }
 
-constexpr int RCH = 16;   // chunks of 64 pairs a wave keeps in registers
 
 struct RouteArgs {
   const int32_t *ids;
@@ -202,6 +214,7 @@ struct RouteArgs {
   int4 *chunks;     // groups of at most ms rows, cut into chunks of SMALL_CHUNK
                     // rows: {expert, first sorted position, rows, group}, in
                     // reverse group order
+  int *hist_g;      // split route: per-(expert, slice) counts, expert-major [E][nseg]
   int T, k, E, has_shared, seg, nseg, ebits, ms;
   int stage;        // REG path: the permutation goes through LDS (it fits)
 };
@@ -229,26 +242,90 @@ __device__ __forceinline__ int chunk_rank(int e, int s, int *hist, const RouteAr
   return r;
 }
 
+// Split route, first part, in the quantizing launch: slice s of ROUTE_T
+// pairs, one 64-pair chunk per wave.  Each pair's rank among the earlier
+// pairs of its slice with the same expert: its rank in its chunk (wave
+// ballots) plus that expert's count in the slice's earlier chunks (a scan
+// over the 16 chunks per expert, in LDS); the slice's count of each expert
+// goes to the expert-major histogram hist_g[e][s], the ranks to `rank`.
+__device__ void slice_ranks(const RouteArgs &a, int s) {
+  extern __shared__ int cnt[];   // [16 chunks][E]
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int Pr = a.T * a.k;
+  for (int i = tid; i < 16 * a.E; i += ROUTE_T) cnt[i] = 0;
+  const int p = s * SLICE + tid;
+  int e = -1;
+  if (p < Pr) {
+    e = a.ids[p];
+    if (e < 0 || e >= a.E) e = -1;
+  }
+  __syncthreads();
+  uint64_t peers = __ballot(e >= 0);
+  for (int bit = 0; bit < a.ebits; bit++) {
+    const int mine = (e >> bit) & 1;
+    const uint64_t b = __ballot(mine);
+    peers &= mine ? b : ~b;
+  }
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  const int r = __popcll(peers & lt);
+  if (e >= 0 && r == 0) cnt[wave * a.E + e] = __popcll(peers);   // the expert's first lane
+  __syncthreads();
+  for (int ee = tid; ee < a.E; ee += ROUTE_T) {
+    int run = 0;
+#pragma unroll
+    for (int w = 0; w < 16; w++) {
+      const int c = cnt[w * a.E + ee];
+      cnt[w * a.E + ee] = run;
+      run += c;
+    }
+    a.hist_g[ee * a.nseg + s] = run;
+  }
+  __syncthreads();
+  if (e >= 0) a.rank[p] = cnt[wave * a.E + e] + r;
+}
+
 // One workgroup.  Pairs are cut into segments of `seg` (a multiple of 64);
 // wave w owns segments w, w+16, ...  For every pair, its rank among the
 // earlier pairs of the same expert inside its segment comes from wave ballots;
 // the per-(expert, segment) counts, laid out expert-major, are then scanned
 // once, which yields at the same time each expert's offset and each segment's
-// base inside it.  The resulting order is stable in pair index.  REG: every
+// base inside it.  The resulting order is stable in pair index.  MODE 1: every
 // wave's chunks fit in RCH registers, so the ids are loaded in one batch and
-// the ranks stay in registers until the scatter (otherwise they go through
-// the workspace).
-template <bool REG>
+// the ranks stay in registers until the scatter; MODE 0: the ranks go through
+// the workspace; MODE 2: the segments are the slices of slice_ranks, whose
+// ranks and counts the previous launch left in the workspace.
+template <int MODE>
 __device__ __forceinline__ void route_body(const RouteArgs &a) {
+  constexpr bool REG = MODE == 1;
+  constexpr bool HELD = MODE != 0;   // the pairs' ids and ranks held in registers
   extern __shared__ int hist[];  // [E][nseg], later the group counters
   __shared__ int wtot[3][ROUTE_T / 64 + 1];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int Pr = a.T * a.k;
   const int L = a.E * a.nseg;
-  for (int i = tid; i < L; i += ROUTE_T) hist[i] = 0;
-
   const int cps = a.seg >> 6;    // chunks per segment
+  // register slot i: MODE 1, chunk i of this wave (segment wave + 16 (i / cps),
+  // its chunk i % cps); MODE 2, pair i * ROUTE_T + tid of slice i
+  auto pair_of = [&](int i) {
+    if (MODE == 2) return i * ROUTE_T + tid;
+    const int j = i / cps;
+    return (wave + 16 * j) * a.seg + 64 * (i - j * cps) + lane;
+  };
+  auto seg_of = [&](int i) { return MODE == 2 ? i : wave + 16 * (i / cps); };
   int er[RCH], rr[RCH];
+  if (MODE == 2) {
+    // every pair's id and slice rank in one batch, beside the counts
+#pragma unroll
+    for (int i = 0; i < RCH; i++) {
+      const int p = pair_of(i);
+      const bool live = p < Pr;
+      const int e = a.ids[live ? p : 0];
+      rr[i] = a.rank[live ? p : 0];
+      er[i] = (live && e >= 0 && e < a.E) ? e : -1;
+    }
+  }
+  for (int i = tid; i < L; i += ROUTE_T) hist[i] = MODE == 2 ? a.hist_g[i] : 0;
+
   if (REG) {
     // chunk i of this wave: segment wave + 16 (i / cps), its chunk i % cps
 #pragma unroll
@@ -268,7 +345,7 @@ __device__ __forceinline__ void route_body(const RouteArgs &a) {
       const int sg = wave + 16 * (i / cps);
       rr[i] = sg < a.nseg ? chunk_rank(er[i], sg, hist, a, lane) : 0;
     }
-  } else {
+  } else if (MODE == 0) {
     for (int sg = wave; sg < a.nseg; sg += ROUTE_T / 64) {
       const int end = (int)min((int64_t)(sg + 1) * a.seg, (int64_t)Pr);
       for (int base = sg * a.seg; base < end; base += 64) {
@@ -296,12 +373,11 @@ __device__ __forceinline__ void route_body(const RouteArgs &a) {
   // workspace, or (stage) through LDS so that the permutation leaves in
   // coalesced stores
   int dst[RCH];
-  if (REG) {
+  if (HELD) {
 #pragma unroll
     for (int i = 0; i < RCH; i++) {
-      const int j = i / cps, sg = wave + 16 * j;
-      const int p = sg * a.seg + 64 * (i - j * cps) + lane;
-      dst[i] = er[i] >= 0 ? hist[er[i] * a.nseg + sg] + rr[i] : -1;
+      const int p = pair_of(i);
+      dst[i] = er[i] >= 0 ? hist[er[i] * a.nseg + seg_of(i)] + rr[i] : -1;
       if (!a.stage && dst[i] >= 0) a.perm[dst[i]] = p;
     }
   } else {
@@ -340,12 +416,10 @@ __device__ __forceinline__ void route_body(const RouteArgs &a) {
     }
   }
   __syncthreads();
-  if (REG && a.stage) {
+  if (HELD && a.stage) {
 #pragma unroll
-    for (int i = 0; i < RCH; i++) {
-      const int j = i / cps, sg = wave + 16 * j;
-      if (dst[i] >= 0) hist[dst[i]] = sg * a.seg + 64 * (i - j * cps) + lane;
-    }
+    for (int i = 0; i < RCH; i++)
+      if (dst[i] >= 0) hist[dst[i]] = pair_of(i);
     if (a.has_shared)
       for (int t = tid; t < a.T; t += ROUTE_T) hist[nrouted + t] = Pr + t;
     __syncthreads();
@@ -410,16 +484,27 @@ struct Q8Args {
   int64_t nblocks, nbrow;   // blocks in all, per row
 };
 
-// Stages 1 and 2 in one launch (they are independent): workgroup 0 routes,
-// the others quantize the hidden rows, ROUTE_T / 8 blocks each.
-template <bool REG>
-__global__ __launch_bounds__(ROUTE_T) void prep_kernel(RouteArgs a, Q8Args q) {
-  if (blockIdx.x == 0) {
-    route_body<REG>(a);
+// Stages 1 and 2 in one launch (they are independent): the first `nroute`
+// workgroups route -- the whole route in workgroup 0 (MODE 0, 1), or the
+// ranks of one slice each (MODE 2, finished by route_finish) -- the others
+// quantize the hidden rows, ROUTE_T / 8 blocks each.
+template <int MODE>
+__global__ __launch_bounds__(ROUTE_T) void prep_kernel(RouteArgs a, Q8Args q, int nroute) {
+  if ((int)blockIdx.x < nroute) {
+    if (MODE == 2)
+      slice_ranks(a, blockIdx.x);
+    else
+      route_body<MODE>(a);
     return;
   }
   q8_0_lane(q.x, q.xq, q.xs, q.xa, q.xd, q.nblocks, q.nbrow,
-            (int64_t)(blockIdx.x - 1) * ROUTE_T + threadIdx.x);
+            (int64_t)(blockIdx.x - nroute) * ROUTE_T + threadIdx.x);
+}
+
+// The split route's second part: offsets, the permutation and the group,
+// tile and chunk lists, from the slices' counts and ranks.
+__global__ __launch_bounds__(ROUTE_T) void route_finish_kernel(RouteArgs a) {
+  route_body<2>(a);
 }
 
 // out[t] = sum_j y[t*k + j] (slots in order, skipped slots left out) + y[T*k + t].
@@ -513,26 +598,42 @@ int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
   ra.groups = reinterpret_cast<int4 *>(ws + L.groups);
   ra.tiles = reinterpret_cast<int4 *>(ws + L.tiles);
   ra.chunks = reinterpret_cast<int4 *>(ws + L.chunks);
+  ra.hist_g = reinterpret_cast<int32_t *>(ws + L.hist);
   ra.T = (int)T; ra.k = (int)k; ra.E = (int)E; ra.has_shared = has_shared; ra.ms = ms;
   const int64_t Pr = T * k;
-  // smallest segment (multiple of 64 pairs) whose histogram fits in LDS
-  const int64_t nseg_max = std::max<int64_t>(1, LDS_INTS / E);
-  const int64_t seg = std::max<int64_t>(64, ((Pr + nseg_max - 1) / nseg_max + 63) / 64 * 64);
-  const int64_t nseg = std::max<int64_t>(1, (Pr + seg - 1) / seg);
-  ra.seg = (int)seg;
-  ra.nseg = (int)nseg;
   ra.ebits = 0;
   while ((1 << ra.ebits) < E) ra.ebits++;
-  // every wave's chunks fit the register arrays: at most RCH per wave
-  const bool reg = (ra.nseg + 15) / 16 * (seg / 64) <= RCH;
-  ra.stage = reg && Pr + T + 3 * (E + 1) <= LDS_INTS;
-  const size_t lds = sizeof(int) * std::max<size_t>((size_t)E * ra.nseg,
-                                                    (ra.stage ? Pr + T : 0) + 3 * (E + 1));
-  const unsigned grid = (unsigned)(1 + (qa.nblocks * 8 + ROUTE_T - 1) / ROUTE_T);
-  if (reg)
-    prep_kernel<true><<<dim3(grid), dim3(ROUTE_T), lds, s>>>(ra, qa);
-  else
-    prep_kernel<false><<<dim3(grid), dim3(ROUTE_T), lds, s>>>(ra, qa);
+  const unsigned nq = (unsigned)((qa.nblocks * 8 + ROUTE_T - 1) / ROUTE_T);
+  const int64_t nslice = (Pr + SLICE - 1) / SLICE;
+  if (split_route(Pr, E)) {
+    // slices of ROUTE_T pairs ranked beside the quantization, then one
+    // workgroup for the offsets and lists
+    ra.seg = SLICE;
+    ra.nseg = (int)nslice;
+    ra.stage = Pr + T + 3 * (E + 1) <= LDS_INTS;
+    const size_t lds1 = sizeof(int) * 16 * (size_t)E;
+    prep_kernel<2><<<dim3((unsigned)nslice + nq), dim3(ROUTE_T), lds1, s>>>(ra, qa, (int)nslice);
+    if ((rc = check_launch()) != W4A8_OK) return rc;
+    const size_t lds2 = sizeof(int) * std::max<size_t>((size_t)E * ra.nseg,
+                                                       (ra.stage ? Pr + T : 0) + 3 * (E + 1));
+    route_finish_kernel<<<dim3(1), dim3(ROUTE_T), lds2, s>>>(ra);
+  } else {
+    // smallest segment (multiple of 64 pairs) whose histogram fits in LDS
+    const int64_t nseg_max = std::max<int64_t>(1, LDS_INTS / E);
+    const int64_t seg = std::max<int64_t>(64, ((Pr + nseg_max - 1) / nseg_max + 63) / 64 * 64);
+    const int64_t nseg = std::max<int64_t>(1, (Pr + seg - 1) / seg);
+    ra.seg = (int)seg;
+    ra.nseg = (int)nseg;
+    // every wave's chunks fit the register arrays: at most RCH per wave
+    const bool reg = (ra.nseg + 15) / 16 * (seg / 64) <= RCH;
+    ra.stage = reg && Pr + T + 3 * (E + 1) <= LDS_INTS;
+    const size_t lds = sizeof(int) * std::max<size_t>((size_t)E * ra.nseg,
+                                                      (ra.stage ? Pr + T : 0) + 3 * (E + 1));
+    if (reg)
+      prep_kernel<1><<<dim3(1 + nq), dim3(ROUTE_T), lds, s>>>(ra, qa, 1);
+    else
+      prep_kernel<0><<<dim3(1 + nq), dim3(ROUTE_T), lds, s>>>(ra, qa, 1);
+  }
   if ((rc = check_launch()) != W4A8_OK) return rc;
 
   uint8_t *hq = ws + L.hq;
