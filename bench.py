@@ -90,6 +90,7 @@ sys.path.insert(0, ROOT)
 H, I, E, K_TOP = 2048, 512, 256, 8
 EXPERT_BYTES = (2 * I * (H // 32) + H * (I // 32)) * 18   # 1,769,472
 HBM_PEAK_GBPS = 8000.0
+INT8_PEAK_TOPS = 5000.0    # dense int8 matrix-core peak, TOP/s
 METRIC = "MoE-layer W4A8 GEMV GB/s (% HBM peak) at M=1; prefill tokens/s per layer"
 
 
@@ -263,10 +264,12 @@ def bench_decode_invariants(torch, w4, synth, layers, args, dev, n=500):
     return res
 
 
-def bench_prefill(torch, w4, synth, layers, args, dev):
-    T = 947
-    rng = synth.rng(args.seed + 3)
-    n = args.prefill_steps
+def bench_prefill(torch, w4, synth, layers, args, dev, T=947, n=None):
+    """T tokens through one layer call (top-8 of 256 with a per-expert router
+    bias, so group sizes are uneven as in a real prompt), cycling the weight
+    sets; int8 operations counted over every valid pair's three products."""
+    rng = synth.rng(args.seed + 3 + T)
+    n = args.prefill_steps if n is None else n
     ids_l, wts_l, byts = [], [], []
     for _ in range(n + 2):
         ids, wts = synth.routing(rng, T, E, K_TOP, bias_std=1.0)
@@ -285,7 +288,7 @@ def bench_prefill(torch, w4, synth, layers, args, dev):
         w4.moe_forward(xs[i], ids_l[i], wts_l[i], L[0], L[1], L[2], L[3], H, I, E, K_TOP, ws,
                        out=out)
 
-    log(f"prefill 947 tokens: warmup 2, timed {n}")
+    log(f"prefill {T} tokens: warmup 2, timed {n}")
     step(n)
     step(n + 1)
     torch.cuda.synchronize()
@@ -297,10 +300,41 @@ def bench_prefill(torch, w4, synth, layers, args, dev):
     ev1.record()
     torch.cuda.synchronize()
     ms = ev0.elapsed_time(ev1) / n
+    ops = 2.0 * T * (K_TOP + 1) * 3 * H * I
     return {"tokens": T, "ms_per_layer": round(ms, 4),
             "tokens_per_s_per_layer": round(T / (ms / 1e3), 1),
             "GBps": round(sum(byts[:n]) / n / (ms / 1e3) / 1e9, 1),
-            "hbm_peak_frac": round(sum(byts[:n]) / n / (ms / 1e3) / 1e9 / HBM_PEAK_GBPS, 4)}
+            "hbm_peak_frac": round(sum(byts[:n]) / n / (ms / 1e3) / 1e9 / HBM_PEAK_GBPS, 4),
+            "int8_TOPs": round(ops / (ms / 1e3) / 1e12, 1),
+            "int8_peak_frac": round(ops / (ms / 1e3) / 1e12 / INT8_PEAK_TOPS, 4)}
+
+
+def bench_one_expert(torch, w4, synth, args, dev, T=947, n=20):
+    """One expert alone over T token rows (E = 1, k = 1, no shared expert:
+    one group of T rows through the grouped int8-MFMA kernels), the point of
+    the matrix-core sweep where the group is as large as the prompt."""
+    g = synth.rng(args.seed + 12)
+    w_gu = torch.from_numpy(synth.q4_0_random_blocks(g, 2 * I, H)).to(dev)
+    w_d = torch.from_numpy(synth.q4_0_random_blocks(g, H, I)).to(dev)
+    x = torch.from_numpy(synth.normal_f32(g, (T, H))).to(dev)
+    ids = torch.zeros((T, 1), dtype=torch.int32, device=dev)
+    wts = torch.ones((T, 1), dtype=torch.float32, device=dev)
+    ws = w4.moe_workspace(T, H, I, 1, 1, device=dev)
+    out = torch.empty((T, H), dtype=torch.float32, device=dev)
+    for _ in range(3):
+        w4.moe_forward(x, ids, wts, w_gu, w_d, None, None, H, I, 1, 1, ws, out=out)
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(n):
+        w4.moe_forward(x, ids, wts, w_gu, w_d, None, None, H, I, 1, 1, ws, out=out)
+    ev1.record()
+    torch.cuda.synchronize()
+    us = ev0.elapsed_time(ev1) / n * 1e3
+    ops = 2.0 * T * 3 * H * I
+    return {"tokens": T, "us_per_layer": round(us, 2), "int8_TOPs": round(ops / us / 1e6, 1),
+            "int8_peak_frac": round(ops / us / 1e6 / INT8_PEAK_TOPS, 4)}
 
 
 def bench_m32(torch, w4, synth, layers, args, dev):
@@ -506,6 +540,57 @@ def bench_lm_head(torch, w4, synth, args, dev):
             "GBps": round(nbytes / (us / 1e6) / 1e9, 1),
             "hbm_peak_frac": round(nbytes / (us / 1e6) / 1e9 / HBM_PEAK_GBPS, 4),
             "launch": "hipGraph"}
+
+
+def bench_gemm(torch, w4, synth, args, dev):
+    """Dense W4A8 products of M activation rows (q4q8_gemm, one Q8_0
+    alignment launch and one int8-MFMA launch): the output projection at
+    M = 32 (HBM-bound: 175 MB of Q4_0 weights) and an M-sweep at the
+    dense-layer shape N = K = 2048 (int8 operations against the matrix
+    cores' peak), each timed over a hipGraph of back-to-back calls."""
+    out = {}
+
+    def timed(w_list, M, N, K, n):
+        g = synth.rng(args.seed + 11 + M)
+        xq = w4.q8_0_quantize(torch.from_numpy(synth.normal_f32(g, (M, K))).to(dev))
+        y = torch.empty((M, N), dtype=torch.float32, device=dev)
+        ws = w4.gemm_workspace(M, K, device=dev)
+        for i in range(3):
+            w4.q4q8_gemm(w_list[i % len(w_list)], xq, M, N, K, y=y, workspace=ws)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for i in range(n):
+                w4.q4q8_gemm(w_list[i % len(w_list)], xq, M, N, K, y=y, workspace=ws)
+        graph.replay()
+        torch.cuda.synchronize()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        ev0.record()
+        graph.replay()
+        ev1.record()
+        torch.cuda.synchronize()
+        return ev0.elapsed_time(ev1) / n * 1e3
+
+    N, K, M = 151936, H, 32
+    g = synth.rng(args.seed + 10)
+    ws = [torch.from_numpy(synth.q4_0_random_blocks(g, N, K)).to(dev) for _ in range(2)]
+    us = timed(ws, M, N, K, 20)
+    nbytes = N * (K // 32) * 18 + M * (K // 32) * 34 + M * N * 4
+    out["lm_head_m32"] = {"M": M, "N": N, "K": K, "us_per_call": round(us, 2),
+                          "GBps": round(nbytes / us / 1e3, 1),
+                          "hbm_peak_frac": round(nbytes / us / 1e3 / HBM_PEAK_GBPS, 4)}
+    del ws
+    N = K = H
+    ws = [torch.from_numpy(synth.q4_0_random_blocks(g, N, K)).to(dev)]
+    sweep = []
+    for M in (32, 128, 947, 4096, 16384):
+        us = timed(ws, M, N, K, 20)
+        tops = 2.0 * M * N * K / us / 1e6
+        sweep.append({"M": M, "us_per_call": round(us, 2), "int8_TOPs": round(tops, 1),
+                      "int8_peak_frac": round(tops / INT8_PEAK_TOPS, 4)})
+    out["dense_2048x2048_sweep"] = sweep
+    return out
 
 
 def bench_stack(torch, w4, synth, args, dev):
@@ -809,12 +894,19 @@ def main():
         prefill = bench_prefill(torch, w4, synth, layers, args, dev)
         log(f"prefill: {prefill}")
 
+    prefill_5k = one_expert = None
+    if not args.no_prefill and not args.no_extras:
+        prefill_5k = bench_prefill(torch, w4, synth, layers, args, dev, T=5120, n=4)
+        log(f"prefill 5120: {prefill_5k}")
+        one_expert = bench_one_expert(torch, w4, synth, args, dev)
+        log(f"one expert, 947 rows: {one_expert}")
+
     m32 = None
     if not args.no_m32:
         m32 = bench_m32(torch, w4, synth, layers, args, dev)
         log(f"decode M=32: {m32}")
 
-    invariants = router = lm_head = gemv_1024 = gemv_sym = None
+    invariants = router = lm_head = gemv_1024 = gemv_sym = gemm = None
     if not args.no_extras:
         invariants = bench_decode_invariants(torch, w4, synth, layers, args, dev)
         log(f"decode invariants: {invariants}")
@@ -826,6 +918,8 @@ def main():
         log(f"gemv 1024x1024: {gemv_1024}")
         gemv_sym = bench_gemv_sym(torch, w4, synth, args, dev)
         log(f"gemv, paper's fp32-scale format: {gemv_sym}")
+        gemm = bench_gemm(torch, w4, synth, args, dev)
+        log(f"dense gemm: {gemm}")
 
     stack = None
     if not args.no_stack:
@@ -869,6 +963,8 @@ def main():
         "cpu_baseline": cpu,
         "hbm_copy_rate": dict(copy_rate, decode_frac_of_copy_rate=round(gbps / copy_rate["GBps"], 4)),
         "prefill_947": prefill,
+        "prefill_5120": prefill_5k,
+        "one_expert_947_rows": one_expert,
         "decode_m32": m32,
         "stack_40": stack,
         "decode_invariants": invariants,
@@ -876,6 +972,7 @@ def main():
         "gemv_lm_head": lm_head,
         "gemv_1024": gemv_1024,
         "gemv_lm_head_paper_format": gemv_sym,
+        "gemm": gemm,
     }
     print(json.dumps(rec), flush=True)
 

@@ -101,6 +101,25 @@ int q4_0_quantize(const float *w, void *wq, int64_t rows, int64_t K, void *strea
 int q4q8_gemv(const void *w, const void *xq, float *y, int64_t N, int64_t K, void *stream);
 
 /*
+ * W4A8 matrix product of M activation rows with one weight matrix (the dense
+ * per-layer projections and the output projection, about three quarters of
+ * the paper's decode time, Sec. 5.2; the prefill products, Sec. 3.2), with the
+ * block dot of Sec. 3.3:
+ *   y[m][n] = sum_b d_w[n,b] * d_x[m,b] * s[m,n,b],  s exact in int32,
+ *   the scaled sum in fp32.
+ *   w   [N][K/32] Q4_0 blocks;  xq [M][K/32] Q8_0 blocks;  y [M][N] fp32,
+ *   row-major (written).  M == 1 is q4q8_gemv (the workspace is not used);
+ *   M > 1 needs workspace >= q4q8_gemm_workspace_size(M, K) bytes (the
+ *   activations in the layout of the int8 matrix cores; no initialisation).
+ * K % 256 != 0, M < 0, N <= 0 or K <= 0 -> W4A8_ESHAPE; M, N >= 2^31,
+ * K > 2^20, M * N >= 2^40 or M * K >= 2^40 -> W4A8_ERANGE.  M == 0 is a no-op.
+ * q4q8_gemm_workspace_size returns 0 for invalid sizes.
+ */
+size_t q4q8_gemm_workspace_size(int64_t M, int64_t K);
+int q4q8_gemm(const void *w, const void *xq, float *y, int64_t M, int64_t N, int64_t K,
+              void *workspace, size_t ws_bytes, void *stream);
+
+/*
  * The paper's own block format (Sec. 2.3 "Weight quantization": each weight
  * an integer in {-7..7} with one FP32 scale per group, two per byte;
  * Sec. 3.3: activations quantized per group to 8 bits with an FP32 scale,

@@ -29,7 +29,8 @@ EXPORTS = ("w4a8_strerror", "q8_0_quantize", "q4_0_quantize", "q4q8_gemv",
            "moe_w4a8_workspace_layout", "moe_w4a8_forward", "moe_w4a8_layer",
            "rmsnorm_residual", "moe_router_topk", "moe_w4a8_layer_routed",
            "q4_sym_quantize", "q8_f32_quantize", "q4sym_q8f32_gemv",
-           "w4a8_decode_wait_bound", "moe_w4a8_forward_noalloc")
+           "w4a8_decode_wait_bound", "moe_w4a8_forward_noalloc", "q4q8_gemm_workspace_size",
+           "q4q8_gemm")
 
 _lib = None
 
@@ -81,6 +82,10 @@ def lib() -> ctypes.CDLL:
     L.w4a8_decode_wait_bound.restype = ctypes.c_int
     L.moe_w4a8_forward_noalloc.argtypes = [P, P, P, P, P, P, P, P, I64, I64, I64, I64, I64, P]
     L.moe_w4a8_forward_noalloc.restype = ctypes.c_int
+    L.q4q8_gemm_workspace_size.argtypes = [I64, I64]
+    L.q4q8_gemm_workspace_size.restype = SZ
+    L.q4q8_gemm.argtypes = [P, P, P, I64, I64, I64, P, SZ, P]
+    L.q4q8_gemm.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -139,6 +144,28 @@ def q4q8_gemv(w, xq, N, K, y=None, stream=None):
     if y is None:
         y = torch.empty(N, dtype=torch.float32, device=w.device)
     _check(lib().q4q8_gemv(_p(_u8(w)), _p(_u8(xq)), _p(y), N, K, _stream(stream)), "q4q8_gemv")
+    return y
+
+
+def gemm_workspace(M, K, device="cuda"):
+    """A workspace for q4q8_gemm with M activation rows of length K."""
+    import torch
+    n = int(lib().q4q8_gemm_workspace_size(M, K))
+    if n == 0:
+        raise W4A8Error(ESHAPE, "q4q8_gemm_workspace_size")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def q4q8_gemm(w, xq, M, N, K, y=None, workspace=None, stream=None):
+    """y[M, N] = W4A8(xq [M, K/32 Q8_0 blocks], w [N, K/32 Q4_0 blocks]) in fp32."""
+    import torch
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.float32, device=w.device)
+    if workspace is None and M > 1:
+        workspace = gemm_workspace(M, K, device=w.device)
+    nbytes = 0 if workspace is None else workspace.numel()
+    _check(lib().q4q8_gemm(_p(_u8(w)), _p(_u8(xq)), _p(y), M, N, K, _p(workspace), nbytes,
+                           _stream(stream)), "q4q8_gemm")
     return y
 
 

@@ -63,6 +63,8 @@ struct MArgs {
   float *hd;                       // gate/up: their scales [P][I/32]
   float *y;                        // down: w * y [P][H]
   int64_t T, k, E, N, K, I;
+  int64_t M;                       // dense product (M > 0): M activation rows in implicit
+                                   // 64-row tiles, one weight matrix (ws), no route
   int spw;                         // slices per workgroup
 };
 
@@ -222,7 +224,7 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
   if (tid < MT) {
     int p = -1, r = -1;
     if (tid < rows) {
-      p = a.perm[pos + tid];
+      p = a.M ? pos + tid : a.perm[pos + tid];
       r = GATEUP ? (p < a.T * a.k ? p / (int)a.k : p - (int)(a.T * a.k)) : p;
     }
     L.pair[tid] = p;
@@ -259,7 +261,8 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
       const int64_t col = (int64_t)s * 64 + 16 * wave + (r32 & 15);
       grow = r32 < 16 ? col : a.I + col;
     } else {
-      grow = (int64_t)s * WROWS + 32 * wave + r32;
+      // a last slice past N (dense products) reads row N - 1 and stores nothing
+      grow = min((int64_t)s * WROWS + 32 * wave + r32, a.N - 1);
     }
     return Wx + grow * rowbytes;
   };
@@ -353,14 +356,15 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
       }
     } else {
       const int64_t n = (int64_t)slice * WROWS + 32 * wave + r32;
+      const bool nlive = n < a.N;
 #pragma unroll
       for (int e = 0; e < 16; e++) {
         const int m = 8 * (e >> 2) + 4 * hh + (e & 3);
         const int p0 = L.pair[m];
-        if (p0 >= 0) a.y[(int64_t)p0 * a.N + n] = L.pw[m] * acc0[e];
+        if (p0 >= 0 && nlive) a.y[(int64_t)p0 * a.N + n] = L.pw[m] * acc0[e];
         if (TWO) {
           const int p1 = L.pair[32 + m];
-          if (p1 >= 0) a.y[(int64_t)p1 * a.N + n] = L.pw[32 + m] * acc1[e];
+          if (p1 >= 0 && nlive) a.y[(int64_t)p1 * a.N + n] = L.pw[32 + m] * acc1[e];
         }
         acc0[e] = 0.0f;
         acc1[e] = 0.0f;
@@ -378,19 +382,38 @@ __global__ __launch_bounds__(MNT) __attribute__((amdgpu_waves_per_eu(3))) void m
   // the short ones, each share a contiguous run of tiles (neighbouring tiles
   // of one expert share its weights in that XCD's L2), and all chunks of a
   // tile in a row (they share the tile's codes).
-  const int nsl = (int)(GATEUP ? a.I / 64 : a.N / WROWS);
+  const int nsl = (int)(GATEUP ? a.I / 64 : (a.N + WROWS - 1) / WROWS);
   const int nch = (nsl + a.spw - 1) / a.spw;
-  const int ntiles = ((CInt *)a.meta)[2], nlong = ((CInt *)a.meta)[4];   // META_NTILES, META_NLONG
   const int x = blockIdx.x & 7, q = blockIdx.x >> 3;
-  const int qt = q / nch, ch = q - qt * nch;
-  const int l0 = x * nlong / 8, nl = (x + 1) * nlong / 8 - l0;
-  const int nshort = ntiles - nlong;
-  const int s0t = nlong + x * nshort / 8, ns_ = nlong + (x + 1) * nshort / 8 - s0t;
-  if (qt >= nl + ns_) return;
-  const int tile = qt < nl ? l0 + qt : s0t + (qt - nl);
-  const int s0 = ch * a.spw, ns = min(a.spw, nsl - s0);
-  CInt *tp = (CInt *)a.tiles + 4 * tile;
-  const int expert = tp[0], pos = tp[1], rows = tp[2];
+  int expert, pos, rows, s0;
+  if (a.M) {
+    // Dense products: the items in chunk-major order (all 64-row tiles of
+    // the activations for one chunk of weight rows in a row), XCD x taking
+    // the x-th of 8 even contiguous runs: the tiles of one chunk share its
+    // weights in that XCD's L2, and every XCD streams its own part of the
+    // weights, so a handful of tiles still spreads over all 8.
+    const int ntl = (int)((a.M + MT - 1) / MT);
+    const int tot = nch * ntl;
+    const int i0 = x * tot / 8, nx = (x + 1) * tot / 8 - i0;
+    if (q >= nx) return;
+    const int c = (i0 + q) / ntl, tile = (i0 + q) - c * ntl;
+    s0 = c * a.spw;
+    expert = 0;                  // E = 0: the weights are ws
+    pos = tile * MT;
+    rows = (int)min((int64_t)MT, a.M - pos);
+  } else {
+    const int ch = q % nch, qt = q / nch;
+    const int ntiles = ((CInt *)a.meta)[2], nlong = ((CInt *)a.meta)[4];   // META_NTILES, META_NLONG
+    const int l0 = x * nlong / 8, nl = (x + 1) * nlong / 8 - l0;
+    const int nshort = ntiles - nlong;
+    const int s0t = nlong + x * nshort / 8, ns_ = nlong + (x + 1) * nshort / 8 - s0t;
+    if (qt >= nl + ns_) return;
+    const int tile = qt < nl ? l0 + qt : s0t + (qt - nl);
+    s0 = ch * a.spw;
+    CInt *tp = (CInt *)a.tiles + 4 * tile;
+    expert = tp[0]; pos = tp[1]; rows = tp[2];
+  }
+  const int ns = min(a.spw, nsl - s0);
   if (a.K <= 512) {
     if (rows > 32)
       mfma_tile<GATEUP, true, true>(a, L, expert, pos, rows, s0, ns);
@@ -436,6 +459,23 @@ int mfma_down(const uint8_t *w_d, const uint8_t *ws_d, const uint32_t *ha, const
   a.spw = I <= 512 ? (int)std::min<int64_t>(SPW_MAX, nsl) : 1;
   const int64_t nch = (nsl + a.spw - 1) / a.spw;
   mfma_kernel<false><<<dim3((unsigned)(8 * ((maxtiles + 7) / 8 + 1) * nch)), dim3(MNT), 0, s>>>(a);
+  return check_launch();
+}
+
+// Dense product y[m][n] = sum_b d_w[n,b] d_x[m,b] s[m,n,b] of M activation
+// rows (aligned codes and fp32 scales) with one weight matrix [N][K/32].
+int mfma_dense(const uint8_t *w, const uint32_t *act, const float *actd, float *y, int64_t M,
+               int64_t N, int64_t K, hipStream_t s) {
+  MArgs a{};
+  a.w = nullptr; a.ws = w; a.act = act; a.actd = actd; a.y = y;
+  a.T = 0; a.k = 0; a.E = 0; a.N = N; a.K = K; a.I = K; a.M = M;
+  const int64_t nsl = (N + WROWS - 1) / WROWS;
+  a.spw = K <= 512 ? (int)std::min<int64_t>(SPW_MAX, nsl) : 1;
+  const int64_t nch = (nsl + a.spw - 1) / a.spw;
+  const int64_t ntiles = (M + MT - 1) / MT;
+  const int64_t grid = 8 * ((nch * ntiles + 7) / 8);    // an XCD takes at most ceil(items/8)
+  if (grid >= ((int64_t)1 << 31)) return W4A8_ERANGE;
+  mfma_kernel<false><<<dim3((unsigned)grid), dim3(MNT), 0, s>>>(a);
   return check_launch();
 }
 

@@ -72,6 +72,29 @@ def test_gemv_argument_errors():
     assert G(_fake(A + 4), _fake(A), y, 8, 256, None) == w4.EALIGN
 
 
+def test_gemm_argument_errors():
+    L = w4.lib()
+    S = L.q4q8_gemm_workspace_size
+    assert S(33, 2048) >= 33 * 2048 + 33 * 64 * 4
+    assert S(4, 2000) == 0 and S(-1, 256) == 0 and S(1 << 31, 256) == 0   # K % 256, M range
+    ws, n = _fake(A + 0x100000), S(33, 2048)
+    G = L.q4q8_gemm
+    y = _fake(A + 0x200000)
+    assert G(None, _fake(A), y, 33, 64, 2048, ws, n, None) == w4.ENULL
+    assert G(_fake(A), _fake(A + 0x10), None, 33, 64, 2048, ws, n, None) == w4.ENULL
+    assert G(_fake(A), _fake(A + 0x10), y, 33, 64, 2048, None, n, None) == w4.ENULL
+    assert G(_fake(A), _fake(A + 0x10), y, 33, 64, 2000, ws, n, None) == w4.ESHAPE   # K % 256
+    assert G(_fake(A), _fake(A + 0x10), y, -1, 64, 2048, ws, n, None) == w4.ESHAPE
+    assert G(_fake(A), _fake(A + 0x10), y, 33, 0, 2048, ws, n, None) == w4.ESHAPE
+    assert G(_fake(A), _fake(A + 0x10), y, 1 << 31, 64, 256, ws, n, None) == w4.ERANGE
+    assert G(_fake(A), _fake(A + 0x10), y, 1 << 21, 1 << 20, 256, ws, n, None) == w4.ERANGE
+    assert G(_fake(A), _fake(A + 0x10), y, 33, 64, 2048, ws, n - 1, None) == w4.EWORKSPACE
+    assert G(_fake(A), _fake(A + 0x12), y, 33, 64, 2048, ws, n, None) == w4.EALIGN
+    assert G(_fake(A), _fake(A + 0x10), y, 33, 64, 2048, _fake(A + 0x100008), n,
+             None) == w4.EALIGN
+    assert G(_fake(A), _fake(A + 0x10), y, 0, 64, 2048, None, 0, None) == w4.OK   # empty
+
+
 def test_moe_workspace_size_and_layout():
     assert w4.moe_workspace_size(1, 2048, 512, 256, 8) > 0
     assert w4.moe_workspace_size(1, 2000, 512, 256, 8) == 0          # H % 256
