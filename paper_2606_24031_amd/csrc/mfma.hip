@@ -14,21 +14,29 @@
 //     (the nibble q ^ 8 in the high half of its byte), and one swap between
 //     the wave halves (v_permlane32_swap) leaves in lanes 0..31 the low and in
 //     lanes 32..63 the high codes of block j in one register and of block
-//     j + 4 in the other: the B operands of both blocks.
+//     j + 4 in the other: the A operands of both blocks.
 //   * Activations: the tile's aligned Q8_0 codes for 8 blocks go to LDS by
 //     direct loads (global_load_lds), the 16-byte chunks of a row XOR-swizzled
 //     by the row so the rows a half-wave reads sit in distinct banks.  With
 //     K <= 512 all of K stays resident and the workgroup runs several weight
 //     slices with no barrier; otherwise the next 8 blocks are staged while the
 //     current 8 are used, one barrier per 8 blocks.
+//   * Products: the weights are the A operand and the token rows the B
+//     operand, so element e of an MFMA in lane l is weight row
+//     8*(e/4) + 4*(l/32) + e%4 of the wave's 32 and token row l%32 of the
+//     half: a lane holds one token's sums for 16 weight rows.
 //   * Scaling: the accumulator input is 0x4B400000, so the int32 result read
-//     as a float is exactly 1.5*2^23 + 16 s (|16 s| < 2^22); t = fma(f, d_w,
-//     -1.5*2^23*d_w) = 16 s d_w rounded once, acc = fma(t, d_x/16, acc) (the
-//     activation scales are staged divided by 16, which is exact).
-// Output element e of an MFMA in lane l is token row 8*(e/4) + 4*(l/32) + e%4
-// of the half, weight row l%32.  Gate/up waves hold 16 gate rows and the 16
-// matching up rows, so SwiGLU is one lane exchange; Q8_0 of each 32-wide h
-// block goes through LDS.  Down tiles write w * y per pair.
+//     as a float is exactly 1.5*2^23 + 16 s (|16 s| < 2^22); with dx the
+//     token's activation scale divided by 16 (exact), t = fma(f, dx,
+//     -1.5*2^23*dx) = s dx rounded once and acc = fma(t, d_w, acc).  The
+//     per-lane factor is the activation scale; the per-element factor is
+//     the weight-row scale, which both token halves share: each wave puts
+//     its rows' scales of the current 8 blocks in a small LDS table and
+//     reads 16 of them per block (broadcast reads, one set for both halves).
+// Gate/up waves hold 16 gate rows and the 16 matching up rows, so element e
+// and e + 8 of a lane are the gate and up sums of one column and SwiGLU
+// needs no lane exchange; Q8_0 of each 32-wide h block goes through LDS.
+// Down tiles write w * y per pair, four consecutive columns per store.
 #include "w4a8_dev.h"
 #include "w4a8_host.h"
 
@@ -75,12 +83,15 @@ __device__ __forceinline__ float pair_weight(const MArgs &a, int p) {
   return p < pr ? a.topk_w[p] : (a.shared_w ? a.shared_w[p - pr] : 1.0f);
 }
 
+constexpr int DWS = 36;             // row stride of a wave's weight-scale table
+
 struct MLds {
   union {
     uint4 a[2][MT * 16];           // codes of 8 blocks, [buffer][row][chunk ^ row%16]
-    float hv[MT][65];              // gate/up epilogue: h of the tile, [row][64 columns]
+    float hv[MT][68];              // gate/up epilogue: h of the tile, [row][64 columns]
   };
   float dx[2][8][MT];              // activation scales of 8 blocks, [buffer][block][row]
+  float dw[4][8][DWS];             // weight-row scales of the current group, [wave][block][row]
   int arow[MT];                    // activation row of each tile row
   int pair[MT];                    // pair of each tile row (-1: padding)
   float pw[MT];                    // down: combine weight of the row's pair
@@ -112,7 +123,7 @@ __device__ __forceinline__ uint32_t hw_sdw(const HW &w, int j) {
   return (j & 1) == 0 ? w.D[9 * (j >> 1)] : w.D[9 * (j >> 1) + 4];
 }
 
-// B operands and scale dwords of blocks j and j + 4 of the group.
+// Weight operands and scale dwords of blocks j and j + 4 of the group.
 __device__ __forceinline__ void pair_ops(const HW &w, int j, v4i &b0, v4i &b1, uint32_t &s0,
                                          uint32_t &s1) {
 #pragma unroll
@@ -180,38 +191,46 @@ __device__ __forceinline__ v16f mm(v4i a, v4i b, v16i c) {
   return __builtin_bit_cast(v16f, __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, c, 0, 0, 0));
 }
 
-// acc[e] += s_e * dw * dx[row of e]; dx points at the scale of output row
-// 4*(l/32) of this 32-row half (rows 8q .. 8q + 3 past it for q = 0..3).
-__device__ __forceinline__ void scale16(float acc[16], v16f f, float dw, float dwb,
-                                        const float *dx) {
+// acc[e] += s_e * dx * dw[e] for elements 4q..4q+3: f holds the biased int32
+// results of one block for this lane's token (dx its activation scale
+// divided by 16, nbx = -1.5*2^23 * dx) and 16 weight rows; t = fma(f, dx,
+// nbx) = 16 s dx / 16 rounded once, then one fma with each row's weight
+// scale (dw4: rows 8q + 4hh .. +3).
+__device__ __forceinline__ void scale4(float acc[16], const v16f &f, int q, float dx, float nbx,
+                                       float4 dw4) {
+  acc[4 * q + 0] = fmaf(fmaf(f[4 * q + 0], dx, nbx), dw4.x, acc[4 * q + 0]);
+  acc[4 * q + 1] = fmaf(fmaf(f[4 * q + 1], dx, nbx), dw4.y, acc[4 * q + 1]);
+  acc[4 * q + 2] = fmaf(fmaf(f[4 * q + 2], dx, nbx), dw4.z, acc[4 * q + 2]);
+  acc[4 * q + 3] = fmaf(fmaf(f[4 * q + 3], dx, nbx), dw4.w, acc[4 * q + 3]);
+}
+
+// One block: the weight operand b (32 weight rows) against both token
+// halves; dw points at the block's 32 weight-row scales of this wave, dxb
+// at the block's 64 activation scales.  The scales of four weight rows are
+// read once for both halves.
+template <bool TWO>
+__device__ __forceinline__ void block(float acc0[16], float acc1[16], const uint4 *abuf,
+                                      const float *dw, const float *dxb, int kk, v4i b, int r32,
+                                      int hh, v16i c0) {
+  const v16f f0 = mm(b, aop(abuf, r32, kk, hh), c0);
+  v16f f1;
+  if (TWO) f1 = mm(b, aop(abuf, 32 + r32, kk, hh), c0);
+  const float dx0 = dxb[r32];
+  const float dx1 = TWO ? dxb[32 + r32] : 0.0f;
 #pragma unroll
   for (int q = 0; q < 4; q++) {
-    const float4 d = *reinterpret_cast<const float4 *>(dx + 8 * q);
-    acc[4 * q + 0] = fmaf(fmaf(f[4 * q + 0], dw, dwb), d.x, acc[4 * q + 0]);
-    acc[4 * q + 1] = fmaf(fmaf(f[4 * q + 1], dw, dwb), d.y, acc[4 * q + 1]);
-    acc[4 * q + 2] = fmaf(fmaf(f[4 * q + 2], dw, dwb), d.z, acc[4 * q + 2]);
-    acc[4 * q + 3] = fmaf(fmaf(f[4 * q + 3], dw, dwb), d.w, acc[4 * q + 3]);
+    const float4 dw4 = *reinterpret_cast<const float4 *>(dw + 8 * q + 4 * hh);
+    scale4(acc0, f0, q, dx0, -BIASF * dx0, dw4);
+    if (TWO) scale4(acc1, f1, q, dx1, -BIASF * dx1, dw4);
   }
 }
 
-// One block: both token halves against the weight operand b.
-template <bool TWO>
-__device__ __forceinline__ void block(float acc0[16], float acc1[16], const uint4 *abuf,
-                                      const float (*dxb)[MT], int kk, v4i b, float dw, int r32,
-                                      int hh, v16i c0) {
-  const float dwb = -BIASF * dw;
-  const v16f f0 = mm(aop(abuf, r32, kk, hh), b, c0);
-  v16f f1;
-  if (TWO) f1 = mm(aop(abuf, 32 + r32, kk, hh), b, c0);
-  scale16(acc0, f0, dw, dwb, &dxb[kk][4 * hh]);
-  if (TWO) scale16(acc1, f1, dw, dwb, &dxb[kk][32 + 4 * hh]);
-}
-
 // One tile: rows token rows (1..64) of expert's group from sorted position
-// pos, against weight slices s0 .. s0 + ns - 1 (ns > 1 only for resident
-// codes and the down projection).  TWO: the tile holds more than 32 rows (a
-// compile-time branch: a run-time one inside the block loop makes the
-// compiler keep every block's second product until the loop's end).
+// pos (or of the dense rows from pos), against weight slices s0 .. s0 + ns
+// - 1 (ns > 1 only for resident codes and the down projection).  TWO: the
+// tile holds more than 32 rows (a compile-time branch: a run-time one inside
+// the block loop makes the compiler keep every block's second product until
+// the loop's end).
 template <bool GATEUP, bool TWO, bool RES>
 __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, int pos, int rows,
                                           int s0, int ns) {
@@ -234,8 +253,8 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
   __syncthreads();
   if (tid < MT && L.arow[tid] < 0) L.arow[tid] = L.arow[0];   // padding rows read a valid row
   __syncthreads();
-  // scales: thread t moves row t%64, blocks t/64 and t/64 + 4 of each group,
-  // divided by 16 (zero for padding rows)
+  // activation scales: thread t moves row t%64, blocks t/64 and t/64 + 4 of
+  // each group, divided by 16 (zero for padding rows)
   const int dm = tid & (MT - 1), dj = tid >> 6;
   const float dlive = L.pair[dm] >= 0 ? 0.0625f : 0.0f;
   const float *dsrc = a.actd + (int64_t)L.arow[dm] * nblk + dj;
@@ -252,7 +271,8 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
     dx1 = dsrc[4];
   }
 
-  // this lane's half of its weight row in slice s
+  // this lane's half of its weight row in slice s, and the step to the
+  // next group of 8 blocks
   const int64_t rowbytes = (int64_t)nblk * Q4B;
   const uint8_t *Wx = (expert < a.E ? a.w + (int64_t)expert * a.N * rowbytes : a.ws) + 72 * hh;
   auto wrow = [&](int s) -> const uint8_t * {
@@ -266,6 +286,9 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
     }
     return Wx + grow * rowbytes;
   };
+  // this wave's weight-row scales of the current group: [block][row], rows
+  // padded to 36 so the two wave halves write distinct banks
+  float *const Lw = &L.dw[wave][0][0];
 
   float acc0[16], acc1[16];
 #pragma unroll
@@ -275,9 +298,9 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
   for (int e = 0; e < 16; e++) c0[e] = BIAS;
 
   const int J = ns * G;
-  HW w;
-  load_hw(wrow(s0), w);
-  for (int j = 0; j < J; j++) {
+  // group j with its weights in w; loads group j + 1 into wn (the last group
+  // reloads itself: no conditional loads into a register array)
+  auto step = [&](int j, const HW &w, HW &wn) {
     const int sj = j / G, g = j - sj * G;
     if (!resident) {
       // buffer g&1 was last read in group g - 2, before the previous barrier
@@ -288,8 +311,7 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
       __builtin_amdgcn_s_waitcnt(0);              // codes, scales and weights have landed
       __syncthreads();                            // ... for every wave
     }
-    // next group's codes, then its weights (the last group reloads itself:
-    // no conditional loads into a register array).  The codes go first: the
+    // next group's codes, then its weights.  The codes go first: the
     // compiler cannot tell the direct loads into the other buffer from the
     // reads of this one and waits for them before this group's products,
     // so only loads issued after them stay in flight across the group.
@@ -300,8 +322,16 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
     }
     const int jn = j + 1 < J ? j + 1 : j;
     const int sn = jn / G;
-    HW wn;
     load_hw(wrow(s0 + sn) + (int64_t)(jn - sn * G) * (8 * Q4B), wn);
+    // this group's weight-row scales to the wave's table: blocks 4hh..4hh+3
+    // of row r32 (the wave's earlier reads of the table were issued before
+    // these writes, and LDS runs one wave's accesses in order)
+#pragma unroll
+    for (int jj = 0; jj < 4; jj++) {
+      const uint32_t sd = hw_sdw(w, jj);
+      Lw[(4 * hh + jj) * DWS + r32] = f16_bits_to_f32((jj & 1) ? sd >> 16 : sd);
+    }
+    __builtin_amdgcn_wave_barrier();
     const int buf = resident ? g : (g & 1);
     const float(*dxb)[MT] = L.dx[buf];
     const uint4 *abuf = L.a[buf];
@@ -310,27 +340,27 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
       v4i b0, b1;
       uint32_t sd0, sd1;
       pair_ops(w, jj, b0, b1, sd0, sd1);
-      const float dw0 = f16_bits_to_f32((jj & 1) ? sd0 >> 16 : sd0);
-      const float dw1 = f16_bits_to_f32((jj & 1) ? sd1 >> 16 : sd1);
-      block<TWO>(acc0, acc1, abuf, dxb, jj, b0, dw0, r32, hh, c0);
-      block<TWO>(acc0, acc1, abuf, dxb, jj + 4, b1, dw1, r32, hh, c0);
+      block<TWO>(acc0, acc1, abuf, Lw + jj * DWS, dxb[jj], jj, b0, r32, hh, c0);
+      block<TWO>(acc0, acc1, abuf, Lw + (jj + 4) * DWS, dxb[jj + 4], jj + 4, b1, r32, hh, c0);
     }
-    w = wn;
-    if (g + 1 < G) continue;
+    if (g + 1 < G) return;
 
     const int slice = s0 + sj;
     if (GATEUP) {
       __syncthreads();                            // the code buffers become the h tile
-      // lane r32 < 16 holds the gate sums of column 16*wave + r32, lane
-      // r32 + 16 the matching up sums
+      // element e < 8 holds the gate sum and e + 8 the up sum of column
+      // 16*wave + 8*(e/4) + 4*hh + e%4 for this lane's token
 #pragma unroll
-      for (int e = 0; e < 16; e++) {
-        const float u0 = __shfl_xor(acc0[e], 16), u1 = __shfl_xor(acc1[e], 16);
-        if (r32 < 16) {
-          const int m = 8 * (e >> 2) + 4 * hh + (e & 3);
-          L.hv[m][16 * wave + r32] = silu_f32(acc0[e]) * u0;
-          if (TWO) L.hv[32 + m][16 * wave + r32] = silu_f32(acc1[e]) * u1;
-        }
+      for (int half = 0; half < (TWO ? 2 : 1); half++) {
+        const float *acc = half ? acc1 : acc0;
+        float *hrow = &L.hv[32 * half + r32][16 * wave + 4 * hh];
+#pragma unroll
+        for (int q = 0; q < 2; q++)
+          *reinterpret_cast<float4 *>(hrow + 8 * q) =
+              make_float4(silu_f32(acc[4 * q + 0]) * acc[4 * q + 8],
+                          silu_f32(acc[4 * q + 1]) * acc[4 * q + 9],
+                          silu_f32(acc[4 * q + 2]) * acc[4 * q + 10],
+                          silu_f32(acc[4 * q + 3]) * acc[4 * q + 11]);
       }
       __syncthreads();
       // Q8_0 of each row's two 32-wide blocks: 8 lanes per block
@@ -341,8 +371,8 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
         const int rb = idx >> 3, jq = idx & 7, m = rb >> 1, cb = rb & 1;
         const int p = L.pair[m];
         if (p >= 0) {                             // whole 8-lane groups agree
-          const float v[4] = {L.hv[m][32 * cb + 4 * jq], L.hv[m][32 * cb + 4 * jq + 1],
-                              L.hv[m][32 * cb + 4 * jq + 2], L.hv[m][32 * cb + 4 * jq + 3]};
+          const float4 hv4 = *reinterpret_cast<const float4 *>(&L.hv[m][32 * cb + 4 * jq]);
+          const float v[4] = {hv4.x, hv4.y, hv4.z, hv4.w};
           uint32_t d16;
           const uint32_t packed = q8_0_block8(v, d16);
           const int bi = 2 * slice + cb;
@@ -350,32 +380,50 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
           store_q8_0_block8(a.hq + blk * Q8B, jq, packed, d16);
           a.ha[blk * 8 + jq] = packed;
           if (jq == 0) a.hd[blk] = f16_bits_to_f32(d16);
-          *reinterpret_cast<float4 *>(a.h + (int64_t)p * a.I + 32 * bi + 4 * jq) =
-              make_float4(v[0], v[1], v[2], v[3]);
+          *reinterpret_cast<float4 *>(a.h + (int64_t)p * a.I + 32 * bi + 4 * jq) = hv4;
         }
       }
     } else {
-      const int64_t n = (int64_t)slice * WROWS + 32 * wave + r32;
-      const bool nlive = n < a.N;
+      // element 4q + i: output column slice*128 + 32*wave + 8q + 4hh + i
+      const int64_t n0 = (int64_t)slice * WROWS + 32 * wave + 4 * hh;
+      const bool vec = (a.N & 3) == 0;
 #pragma unroll
-      for (int e = 0; e < 16; e++) {
-        const int m = 8 * (e >> 2) + 4 * hh + (e & 3);
-        const int p0 = L.pair[m];
-        if (p0 >= 0 && nlive) a.y[(int64_t)p0 * a.N + n] = L.pw[m] * acc0[e];
-        if (TWO) {
-          const int p1 = L.pair[32 + m];
-          if (p1 >= 0 && nlive) a.y[(int64_t)p1 * a.N + n] = L.pw[32 + m] * acc1[e];
+      for (int half = 0; half < (TWO ? 2 : 1); half++) {
+        const float *acc = half ? acc1 : acc0;
+        const int m = 32 * half + r32;
+        const int p = L.pair[m];
+        const float pw = L.pw[m];
+        if (p < 0) continue;
+        float *yrow = a.y + (int64_t)p * a.N;
+#pragma unroll
+        for (int q = 0; q < 4; q++) {
+          const int64_t n = n0 + 8 * q;
+          if (vec && n + 3 < a.N) {
+            *reinterpret_cast<float4 *>(yrow + n) =
+                make_float4(pw * acc[4 * q], pw * acc[4 * q + 1], pw * acc[4 * q + 2],
+                            pw * acc[4 * q + 3]);
+          } else {
+#pragma unroll
+            for (int i = 0; i < 4; i++)
+              if (n + i < a.N) yrow[n + i] = pw * acc[4 * q + i];
+          }
         }
-        acc0[e] = 0.0f;
-        acc1[e] = 0.0f;
       }
     }
+#pragma unroll
+    for (int e = 0; e < 16; e++) { acc0[e] = 0.0f; acc1[e] = 0.0f; }
+  };
+
+  HW wa, wb;
+  load_hw(wrow(s0), wa);
+  for (int j = 0; j < J; j += 2) {
+    step(j, wa, wb);
+    if (j + 1 < J) step(j + 1, wb, wa);
   }
 }
 
-template <bool GATEUP>
-__global__ __launch_bounds__(MNT) __attribute__((amdgpu_waves_per_eu(3))) void mfma_kernel(MArgs a) {
-  __shared__ MLds L;
+template <bool GATEUP, bool SHORT>
+__device__ __forceinline__ void mfma_body(const MArgs &a, MLds &L) {
   // Work items are (tile, chunk), chunk = a run of spw slices.  Workgroup b
   // runs on XCD b % 8 and is the (b / 8)-th item there.  Each XCD takes an
   // even share of the long tiles (more than 32 rows), then an even share of
@@ -415,16 +463,32 @@ __global__ __launch_bounds__(MNT) __attribute__((amdgpu_waves_per_eu(3))) void m
   }
   const int ns = min(a.spw, nsl - s0);
   if (a.K <= 512) {
-    if (rows > 32)
+    if (!SHORT && rows > 32)
       mfma_tile<GATEUP, true, true>(a, L, expert, pos, rows, s0, ns);
     else
       mfma_tile<GATEUP, false, true>(a, L, expert, pos, rows, s0, ns);
   } else {
-    if (rows > 32)
+    if (!SHORT && rows > 32)
       mfma_tile<GATEUP, true, false>(a, L, expert, pos, rows, s0, ns);
     else
       mfma_tile<GATEUP, false, false>(a, L, expert, pos, rows, s0, ns);
   }
+}
+
+// Tiles of up to 64 rows: two waves per SIMD (the 64-row tile's two sets of
+// sums and products need about 200 registers a lane; at three waves the
+// compiler spills inside the block loop).
+template <bool GATEUP>
+__global__ __launch_bounds__(MNT) __attribute__((amdgpu_waves_per_eu(2))) void mfma_kernel(MArgs a) {
+  __shared__ MLds L;
+  mfma_body<GATEUP, false>(a, L);
+}
+
+// Dense products of at most 32 rows (every tile short): one set of sums,
+// three waves per SIMD to keep more weight bytes in flight.
+__global__ __launch_bounds__(MNT) __attribute__((amdgpu_waves_per_eu(3))) void mfma_short_kernel(MArgs a) {
+  __shared__ MLds L;
+  mfma_body<false, true>(a, L);
 }
 
 }  // namespace
@@ -475,7 +539,10 @@ int mfma_dense(const uint8_t *w, const uint32_t *act, const float *actd, float *
   const int64_t ntiles = (M + MT - 1) / MT;
   const int64_t grid = 8 * ((nch * ntiles + 7) / 8);    // an XCD takes at most ceil(items/8)
   if (grid >= ((int64_t)1 << 31)) return W4A8_ERANGE;
-  mfma_kernel<false><<<dim3((unsigned)grid), dim3(MNT), 0, s>>>(a);
+  if (M <= MT / 2)
+    mfma_short_kernel<<<dim3((unsigned)grid), dim3(MNT), 0, s>>>(a);
+  else
+    mfma_kernel<false><<<dim3((unsigned)grid), dim3(MNT), 0, s>>>(a);
   return check_launch();
 }
 
