@@ -639,7 +639,11 @@ int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
   uint8_t *hq = ws + L.hq;
   float *h = reinterpret_cast<float *>(ws + L.h);
   float *y = reinterpret_cast<float *>(ws + L.y);
-  const int64_t maxchunks = small_max_chunks(T, E, k, has_shared);
+  // launch bound on the small chunks: above SMALL_CHUNK-row groups (T > 32)
+  // every small group is one chunk and the shared group (T rows) is never
+  // small, so at most one chunk per routed expert that can be touched
+  const int64_t maxchunks =
+      ms < T ? std::min<int64_t>(E, T * k) : small_max_chunks(T, E, k, has_shared);
   if (ms > 0 && (rc = small_gateup(w_gu, ws_gu, xs, ra.meta, ra.perm, ra.chunks, h, hq, hs,
                                    maxchunks, T, H, I, E, k, s)) != W4A8_OK)
     return rc;

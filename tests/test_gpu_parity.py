@@ -420,6 +420,40 @@ def test_moe_prefill_947_all_tokens(qwen_layer):
     assert np.array_equal(out, out2)
 
 
+def _first_experts(L, E):
+    """A view of layer L restricted to its first E routed experts (the
+    expert-major weight arrays cut after expert E - 1), shared expert kept."""
+    V = Layer.__new__(Layer)
+    V.H, V.I, V.E = L.H, L.I, E
+    V.w_gu = L.w_gu.reshape(L.E, -1)[:E].reshape(-1)
+    V.w_d = L.w_d.reshape(L.E, -1)[:E].reshape(-1)
+    V.ws_gu, V.ws_d = L.ws_gu, L.ws_d
+    V.d_gu, V.d_d = dev(V.w_gu), dev(V.w_d)
+    V.d_sgu, V.d_sd = L.d_sgu, L.d_sd
+    V.g = L.g
+    return V
+
+
+@pytest.mark.parametrize("T,bias", [(1, 0.0), (32, 0.0), (947, 1.0)])
+@pytest.mark.parametrize("E,k", [(256, 4), (128, 8)])
+def test_moe_full_shape_top4_and_128_experts(qwen_layer, T, bias, E, k):
+    """The paper's two model variants at the full layer shape (H = 2048, I =
+    512): top-4 of 256 routed experts, and 128 routed experts (the pruned
+    model) at top-8, each at one token (the decode kernel), 32 tokens (the
+    small-group kernels) and 947 tokens with skewed routing (small groups,
+    MFMA tiles and the 947-row shared group); every token and pair through
+    the MoE check, the routing permutation exact."""
+    L = qwen_layer if E == qwen_layer.E else _first_experts(qwen_layer, E)
+    g = synth.rng(900 + T + E + k)
+    x = synth.normal_f32(g, (T, L.H))
+    ids, wts = synth.routing(g, T, E, k, bias_std=bias)
+    out, h, hq, perm, count, _ = L.run(x, ids, wts, k)
+    if T > 1:
+        _check_route(ids, E, True, perm, count)
+    st = L.check(x, ids, wts, k, out, h, hq)
+    assert st["pairs"] == T * (k + 1)
+
+
 # ------------------------------------------------------------ RMSNorm + residual
 @pytest.mark.parametrize("T,H,resid", [(1, 2048, True), (5, 256, False), (947, 2048, True), (3, 4100, True)])
 def test_rmsnorm_residual_matches_oracle(T, H, resid):
