@@ -151,6 +151,45 @@ int q4sym_q8f32_gemv(const void *w, const void *xq, float *y, int64_t N, int64_t
                      void *stream);
 
 /*
+ * The routed + shared MoE layer in the paper's own format (Sec. 2.2: top-k
+ * routed experts and one always-on shared expert; Sec. 2.3: Q4_SYM weights;
+ * Sec. 3.3: Q8_F32 activations, integer block dots scaled once per group):
+ *   for each token t, slot j with e = topk_ids[t][j] in [0, E):
+ *     xq = Q8_F32(hidden[t]);  g|u = W_gu[e] xq;  h = SiLU(g) * u (fp32);
+ *     hq = Q8_F32(h);  out[t] += topk_w[t][j] * (W_d[e] hq)
+ *   and the shared expert the same way with weight 1.  Products as in
+ *   q4sym_q8f32_gemv, SiLU and the sums in fp32.
+ *   hidden [T][H] fp32, topk_ids [T][k] int32 (an id outside [0, E) skips the
+ *   slot), topk_w [T][k] fp32; w_gate_up [E][2I][H/32] Q4_SYM blocks (the I
+ *   gate rows, then the I up rows), w_down [E][H][I/32]; ws_gate_up [2I][H/32]
+ *   and ws_down [H][I/32] the shared expert (both NULL: none); out [T][H]
+ *   fp32 (may be hidden itself: hidden is read only by the first launch).
+ * Four launches on the stream (quantize, gate/up, down, combine).  The
+ * workspace (>= moe_sym_workspace_size bytes, no initialisation) holds, at
+ * the offsets moe_sym_workspace_layout writes to offsets[0..2]:
+ *   W4A8_SYM_WS_XQ  Q8_F32(hidden), [T][H/32] blocks;
+ *   W4A8_SYM_WS_H   fp32 h, [P][I], P = T*k + T pairs (pair t*k + j, shared
+ *                   pair T*k + t; rows of skipped pairs are not written);
+ *   W4A8_SYM_WS_HQ  Q8_F32(h), [P][I/32] blocks.
+ * Errors: H or I not a multiple of 256, T < 0, E, k <= 0 -> W4A8_ESHAPE;
+ * H or I > 16384, k > 64, E or T >= 2^24, or more than 2^31 work items ->
+ * W4A8_ERANGE; a required pointer NULL, or only one of the shared pair ->
+ * W4A8_ENULL; base pointers not 16-byte aligned -> W4A8_EALIGN; workspace too
+ * small -> W4A8_EWORKSPACE.  T == 0 is a no-op.  moe_sym_workspace_size
+ * returns 0 for invalid sizes.
+ */
+#define W4A8_SYM_WS_XQ 0
+#define W4A8_SYM_WS_H  1
+#define W4A8_SYM_WS_HQ 2
+size_t moe_sym_workspace_size(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k);
+int moe_sym_workspace_layout(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
+                             size_t *offsets);
+int moe_sym_forward(const float *hidden, const int32_t *topk_ids, const float *topk_w,
+                    const void *w_gate_up, const void *w_down, const void *ws_gate_up,
+                    const void *ws_down, float *out, int64_t T, int64_t H, int64_t I,
+                    int64_t E, int64_t k, void *workspace, size_t ws_bytes, void *stream);
+
+/*
  * Bytes of device workspace moe_w4a8_forward needs for these sizes, or 0 if
  * the sizes are invalid.  The workspace must be zero-filled once before its
  * first use (moe_w4a8_workspace_init does that); the library leaves its

@@ -69,6 +69,8 @@ def _load():
     lib.orc_moe.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, I64, I64, P,
                             P, P, P, P, P, P, P]
     lib.orc_moe.restype = ctypes.c_int
+    lib.orc_moe_sym.argtypes = lib.orc_moe.argtypes
+    lib.orc_moe_sym.restype = ctypes.c_int
     lib.orc_q8_0_candidates.argtypes = [P, P, I64, P, P, P, P]
     lib.orc_q8_0_candidates.restype = ctypes.c_int
     lib.orc_threads.restype = ctypes.c_int
@@ -214,6 +216,44 @@ def moe(hidden, ids, wts, w_gu, w_d, ws_gu, ws_d, H, I, E, k, hq_in=None,
                          _ptr(shared_w))
     if rc != 0:
         raise ValueError(f"orc_moe failed ({rc})")
+    return MoeResult(out, R, gu, Rgu, h, hq)
+
+
+def moe_sym(hidden, ids, wts, w_gu, w_d, ws_gu, ws_d, H, I, E, k, hq_in=None,
+            want_intermediates=True, shared_w=None) -> MoeResult:
+    """The MoE layer of :func:`moe` in the paper's own format (Q4_SYM weights,
+    Q8_F32 activations and h; see orc_moe_sym): w_gu [E, 2I, H/32*20], w_d
+    [E, H, I/32*20]; hq and hq_in hold [P, I/32*36] Q8_F32 blocks."""
+    hidden = _c(hidden, np.float32).reshape(-1, H)
+    T = hidden.shape[0]
+    ids = _c(ids, np.int32).reshape(T, k)
+    wts = _c(wts, np.float32).reshape(T, k)
+    w_gu = _c(w_gu, np.uint8).ravel()
+    w_d = _c(w_d, np.uint8).ravel()
+    assert w_gu.size == E * 2 * I * (H // QK) * Q4S_BYTES
+    assert w_d.size == E * H * (I // QK) * Q4S_BYTES
+    if ws_gu is not None:
+        ws_gu = _c(ws_gu, np.uint8).ravel()
+        ws_d = _c(ws_d, np.uint8).ravel()
+    P = T * k + T
+    out = np.zeros((T, H), dtype=np.float64)
+    R = np.zeros((T, H), dtype=np.float64)
+    gu = Rgu = h = hq = None
+    if want_intermediates:
+        gu = np.zeros((P, 2 * I), dtype=np.float32)
+        Rgu = np.zeros((P, 2 * I), dtype=np.float64)
+        h = np.zeros((P, I), dtype=np.float32)
+        hq = np.zeros((P, I // QK * Q8F_BYTES), dtype=np.uint8)
+    if hq_in is not None:
+        hq_in = _c(hq_in, np.uint8).reshape(P, I // QK * Q8F_BYTES)
+    if shared_w is not None:
+        shared_w = _c(shared_w, np.float64).reshape(T)
+    rc = _load().orc_moe_sym(_ptr(hidden), _ptr(ids), _ptr(wts), _ptr(w_gu), _ptr(w_d),
+                             _ptr(ws_gu), _ptr(ws_d), T, H, I, E, k, _ptr(hq_in),
+                             _ptr(out), _ptr(R), _ptr(gu), _ptr(Rgu), _ptr(h), _ptr(hq),
+                             _ptr(shared_w))
+    if rc != 0:
+        raise ValueError(f"orc_moe_sym failed ({rc})")
     return MoeResult(out, R, gu, Rgu, h, hq)
 
 

@@ -616,3 +616,82 @@ void orc_gemv_sym(const uint8_t *w, const uint8_t *xq, int64_t N, int64_t K,
         if (R) R[n] = mag;
     }
 }
+
+/* ------------------------------------------------------------------ */
+/* The MoE layer in the paper's own format (Sec. 2.2 layer, Sec. 2.3  */
+/* weights, Sec. 3.3 activations and product): the steps of orc_moe   */
+/* with Q4_SYM weights, Q8_F32 quantization of x (once per token) and */
+/* of h (per token-expert pair), and the products of orc_gemv_sym.    */
+/* gu/Rgu/h/hq outputs and hq_in (codes of h to use in the down       */
+/* product) as in orc_moe; hq blocks are Q8_F32 (36 bytes).           */
+/* ------------------------------------------------------------------ */
+int orc_moe_sym(const float *hidden, const int32_t *ids, const float *wts,
+                const uint8_t *w_gu, const uint8_t *w_d,
+                const uint8_t *ws_gu, const uint8_t *ws_d,
+                int64_t T, int64_t H, int64_t I, int64_t E, int64_t k,
+                const uint8_t *hq_in,
+                double *out, double *R,
+                float *gu_out, double *Rgu_out, float *h_out, uint8_t *hq_out,
+                const double *shared_w)
+{
+    int64_t nbH = H / QK, nbI = I / QK;
+    size_t gu_bytes = (size_t)(2 * I) * nbH * Q4S_BYTES;   /* one expert's gate/up */
+    size_t d_bytes = (size_t)H * nbI * Q4S_BYTES;          /* one expert's down    */
+    for (int64_t i = 0; i < T * k; i++)
+        if (ids[i] >= E) return -1;
+
+    int bad = 0;
+    #pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t t = 0; t < T; t++) {
+        uint8_t *xq = malloc((size_t)nbH * Q8F_BYTES);
+        uint8_t *hq = malloc((size_t)nbI * Q8F_BYTES);
+        double *gu = malloc(sizeof(double) * 2 * I);
+        double *rgu = malloc(sizeof(double) * 2 * I);
+        float *h = malloc(sizeof(float) * I);
+        double *y = malloc(sizeof(double) * H);
+        double *ry = malloc(sizeof(double) * H);
+        if (!xq || !hq || !gu || !rgu || !h || !y || !ry) { bad = 1; goto done; }
+
+        orc_q8_f32_quantize(hidden + t * H, xq, 1, H);
+        for (int64_t n = 0; n < H; n++) { out[t * H + n] = 0.0; R[t * H + n] = 0.0; }
+
+        for (int64_t j = 0; j <= k; j++) {
+            const uint8_t *Wgu, *Wd;
+            double wj;
+            int64_t pair;
+            if (j < k) {
+                int32_t e = ids[t * k + j];
+                if (e < 0) continue;
+                Wgu = w_gu + (size_t)e * gu_bytes;
+                Wd = w_d + (size_t)e * d_bytes;
+                wj = (double)wts[t * k + j];
+                pair = t * k + j;
+            } else {
+                if (!ws_gu || !ws_d) continue;
+                Wgu = ws_gu;
+                Wd = ws_d;
+                wj = shared_w ? shared_w[t] : 1.0;
+                pair = T * k + t;
+            }
+            orc_gemv_sym(Wgu, xq, 2 * I, H, gu, rgu);
+            for (int64_t i = 0; i < I; i++) {
+                float g = (float)gu[i], u = (float)gu[I + i];
+                h[i] = (float)(silu_d((double)g) * (double)u);
+            }
+            if (gu_out) for (int64_t i = 0; i < 2 * I; i++) gu_out[pair * 2 * I + i] = (float)gu[i];
+            if (Rgu_out) for (int64_t i = 0; i < 2 * I; i++) Rgu_out[pair * 2 * I + i] = rgu[i];
+            if (h_out) memcpy(h_out + pair * I, h, sizeof(float) * I);
+            orc_q8_f32_quantize(h, hq, 1, I);
+            if (hq_out) memcpy(hq_out + pair * nbI * Q8F_BYTES, hq, (size_t)nbI * Q8F_BYTES);
+            const uint8_t *hq_use = hq_in ? hq_in + pair * nbI * Q8F_BYTES : hq;
+            orc_gemv_sym(Wd, hq_use, H, I, y, ry);
+            for (int64_t n = 0; n < H; n++) {
+                out[t * H + n] += wj * y[n];
+                R[t * H + n] += fabs(wj) * ry[n];
+            }
+        }
+    done:
+        free(xq); free(hq); free(gu); free(rgu); free(h); free(y); free(ry);
+    }
+    return bad ? -2 : 0;
+}

@@ -30,7 +30,7 @@ EXPORTS = ("w4a8_strerror", "q8_0_quantize", "q4_0_quantize", "q4q8_gemv",
            "rmsnorm_residual", "moe_router_topk", "moe_w4a8_layer_routed",
            "q4_sym_quantize", "q8_f32_quantize", "q4sym_q8f32_gemv",
            "w4a8_decode_wait_bound", "moe_w4a8_forward_noalloc", "q4q8_gemm_workspace_size",
-           "q4q8_gemm")
+           "q4q8_gemm", "moe_sym_workspace_size", "moe_sym_workspace_layout", "moe_sym_forward")
 
 _lib = None
 
@@ -86,6 +86,12 @@ def lib() -> ctypes.CDLL:
     L.q4q8_gemm_workspace_size.restype = SZ
     L.q4q8_gemm.argtypes = [P, P, P, I64, I64, I64, P, SZ, P]
     L.q4q8_gemm.restype = ctypes.c_int
+    L.moe_sym_workspace_size.argtypes = [I64, I64, I64, I64, I64]
+    L.moe_sym_workspace_size.restype = SZ
+    L.moe_sym_workspace_layout.argtypes = [I64, I64, I64, I64, I64, P]
+    L.moe_sym_workspace_layout.restype = ctypes.c_int
+    L.moe_sym_forward.argtypes = [P, P, P, P, P, P, P, P, I64, I64, I64, I64, I64, P, SZ, P]
+    L.moe_sym_forward.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -167,6 +173,39 @@ def q4q8_gemm(w, xq, M, N, K, y=None, workspace=None, stream=None):
     _check(lib().q4q8_gemm(_p(_u8(w)), _p(_u8(xq)), _p(y), M, N, K, _p(workspace), nbytes,
                            _stream(stream)), "q4q8_gemm")
     return y
+
+
+def moe_sym_workspace(T, H, I, E, k, device="cuda"):
+    """A workspace for moe_sym_forward."""
+    import torch
+    n = int(lib().moe_sym_workspace_size(T, H, I, E, k))
+    if n == 0:
+        raise W4A8Error(ESHAPE, "moe_sym_workspace_size")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def moe_sym_workspace_layout(T, H, I, E, k) -> dict:
+    offs = (ctypes.c_size_t * 3)()
+    _check(lib().moe_sym_workspace_layout(T, H, I, E, k, offs), "moe_sym_workspace_layout")
+    return {"xq": offs[0], "h": offs[1], "hq": offs[2]}
+
+
+def moe_sym_forward(hidden, topk_ids, topk_w, w_gate_up, w_down, ws_gate_up, ws_down,
+                    H, I, E, k, workspace, out=None, stream=None):
+    """The MoE layer in the paper's own format (Q4_SYM weights, Q8_F32
+    activations); returns out [T, H] fp32."""
+    import torch
+    T = hidden.shape[0]
+    assert hidden.dtype == torch.float32 and hidden.is_contiguous()
+    assert topk_ids.dtype == torch.int32 and topk_ids.is_contiguous()
+    assert topk_w.dtype == torch.float32 and topk_w.is_contiguous()
+    if out is None:
+        out = torch.empty((T, H), dtype=torch.float32, device=hidden.device)
+    rc = lib().moe_sym_forward(_p(hidden), _p(topk_ids), _p(topk_w), _p(_u8(w_gate_up)),
+                               _p(_u8(w_down)), _p(ws_gate_up), _p(ws_down), _p(out),
+                               T, H, I, E, k, _p(workspace), workspace.numel(), _stream(stream))
+    _check(rc, "moe_sym_forward")
+    return out
 
 
 def q4_sym_quantize(w, out=None, stream=None):

@@ -22,19 +22,6 @@ constexpr int Q4SB = W4A8_Q4_SYM_BLOCK_BYTES;   // 20
 constexpr int Q8FB = W4A8_Q8_F32_BLOCK_BYTES;   // 36
 constexpr int SYM_K_MAX = 32768;                // the LDS staging holds the whole vector
 
-// Reciprocal of a block scale, or 0 when the block's codes are all zero (a
-// zero scale, or one whose reciprocal overflows fp32).
-__device__ __forceinline__ float sym_inverse(float d) {
-  if (d == 0.0f) return 0.0f;
-  const float id = 1.0f / d;                    // correctly rounded division
-  return __builtin_isinf(id) ? 0.0f : id;
-}
-
-__device__ __forceinline__ int round_clamp(float v, int lim) {
-  const int q = (int)roundf(v);                 // half away from zero
-  return q > lim ? lim : (q < -lim ? -lim : q);
-}
-
 // Eight lanes per block, lane j holding elements 4j..4j+3: amax over the 8
 // lanes, one division, one reciprocal, one multiply per element.
 __device__ __forceinline__ void load4(const float *__restrict__ src, int64_t blk, int j, bool live,
@@ -94,33 +81,6 @@ __global__ __launch_bounds__(256) void q8_f32_kernel(const float *__restrict__ x
     *reinterpret_cast<uint32_t *>(b + 4 + 4 * j) = packed;
     if (j == 0) *reinterpret_cast<float *>(b) = d;
   }
-}
-
-// Eight Q4_SYM blocks of one row (160 bytes) in 40 raw dwords: block k's
-// scale in dword 5k, its payload in dwords 5k+1 .. 5k+4.
-struct W8S {
-  uint32_t D[40];
-};
-
-__device__ __forceinline__ void load_w8s(const uint8_t *__restrict__ p, W8S &w) {
-  const uint4 *v = reinterpret_cast<const uint4 *>(p);
-#pragma unroll
-  for (int i = 0; i < 10; i++) {
-    const uint4 t = v[i];
-    w.D[4 * i + 0] = t.x; w.D[4 * i + 1] = t.y; w.D[4 * i + 2] = t.z; w.D[4 * i + 3] = t.w;
-  }
-}
-
-__device__ __forceinline__ float dot8s_lds(const W8S &w, const uint4 *__restrict__ codes,
-                                           const float *__restrict__ d,
-                                           const int *__restrict__ corr, float acc) {
-#pragma unroll
-  for (int k = 0; k < 8; k++) {
-    const uint32_t n[4] = {w.D[5 * k + 1], w.D[5 * k + 2], w.D[5 * k + 3], w.D[5 * k + 4]};
-    const int s = blockdot_nib(n, codes[2 * k], codes[2 * k + 1], corr[k]);
-    acc = fmaf((float)s, __builtin_bit_cast(float, w.D[5 * k]) * d[k], acc);
-  }
-  return acc;
 }
 
 // LPR lanes share a row (one 160-byte group of eight blocks per lane at a

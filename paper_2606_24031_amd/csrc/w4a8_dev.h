@@ -378,4 +378,45 @@ __device__ __forceinline__ const uint4 *group_codes(ActBuf b, int blk0) {
   return b.codes + (blk0 >> 3) * GROUP_U4;
 }
 
+// Reciprocal of a block scale, or 0 when the block's codes are all zero (a
+// zero scale, or one whose reciprocal overflows fp32).
+__device__ __forceinline__ float sym_inverse(float d) {
+  if (d == 0.0f) return 0.0f;
+  const float id = 1.0f / d;                    // correctly rounded division
+  return __builtin_isinf(id) ? 0.0f : id;
+}
+
+__device__ __forceinline__ int round_clamp(float v, int lim) {
+  const int q = (int)roundf(v);                 // half away from zero
+  return q > lim ? lim : (q < -lim ? -lim : q);
+}
+
+// Eight Q4_SYM blocks of one row (160 bytes) in 40 raw dwords: block k's
+// scale in dword 5k, its payload in dwords 5k+1 .. 5k+4.
+struct W8S {
+  uint32_t D[40];
+};
+
+__device__ __forceinline__ void load_w8s(const uint8_t *__restrict__ p, W8S &w) {
+  const uint4 *v = reinterpret_cast<const uint4 *>(p);
+#pragma unroll
+  for (int i = 0; i < 10; i++) {
+    const uint4 t = v[i];
+    w.D[4 * i + 0] = t.x; w.D[4 * i + 1] = t.y; w.D[4 * i + 2] = t.z; w.D[4 * i + 3] = t.w;
+  }
+}
+
+__device__ __forceinline__ float dot8s_lds(const W8S &w, const uint4 *__restrict__ codes,
+                                           const float *__restrict__ d,
+                                           const int *__restrict__ corr, float acc) {
+#pragma unroll
+  for (int k = 0; k < 8; k++) {
+    const uint32_t n[4] = {w.D[5 * k + 1], w.D[5 * k + 2], w.D[5 * k + 3], w.D[5 * k + 4]};
+    const int s = blockdot_nib(n, codes[2 * k], codes[2 * k + 1], corr[k]);
+    acc = fmaf((float)s, __builtin_bit_cast(float, w.D[5 * k]) * d[k], acc);
+  }
+  return acc;
+}
+
+
 }  // namespace w4a8

@@ -69,3 +69,24 @@ def q4_0_random_blocks(g: np.random.Generator, rows: int, K: int,
     bits = table.view(np.uint16)[blocks[:, 0]] | ((blocks[:, 2].astype(np.uint16) & 1) << 15)
     blocks[:, 0:2] = bits.view(np.uint8).reshape(-1, 2)
     return blocks.reshape(rows, nb * 18)
+
+
+def q4_sym_random_blocks(g: np.random.Generator, rows: int, K: int,
+                         weight_std: float = 0.02) -> np.ndarray:
+    """Random bytes in the 20-byte symmetric 4-bit block layout (fp32 scale,
+    then 16 payload bytes of stored nibbles q + 8): nibbles uniform in 1..15
+    (codes -7..7) and a random-sign scale near that of N(0, weight_std^2)
+    weights (the largest |w| of 32 draws, about 2.0-2.8 std, divided by 7),
+    taken from the block's own random bytes 0 and 2."""
+    nb = K // 32
+    n = rows * nb
+    blocks = random_bytes(g, n * 20).reshape(n, 20)
+    u = blocks[:, 0].astype(np.float32) * np.float32(1.0 / 255.0)
+    d = np.float32(weight_std / 7.0) * (np.float32(2.0) + np.float32(0.8) * u)
+    d = np.where((blocks[:, 2] & 1) == 1, -d, d).astype(np.float32)
+    pay = blocks[:, 4:]
+    lo = (pay & 0x0F) % 15 + 1
+    hi = (pay >> 4) % 15 + 1
+    blocks[:, 4:] = (lo | (hi << 4)).astype(np.uint8)
+    blocks[:, 0:4] = d.view(np.uint8).reshape(-1, 4)
+    return blocks.reshape(rows, nb * 20)

@@ -40,12 +40,13 @@ def act_codes(g: np.random.Generator, K: int) -> np.ndarray:
     return x
 
 
-def design_rows(g: np.random.Generator, x: np.ndarray, targets: np.ndarray) -> np.ndarray:
-    """Codes Q [R, K] in 0..15 with (Q - 8) @ x == targets: random codes, then
+def design_rows(g: np.random.Generator, x: np.ndarray, targets: np.ndarray,
+                lo: int = 0) -> np.ndarray:
+    """Codes Q [R, K] in lo..15 with (Q - 8) @ x == targets: random codes, then
     repeatedly the single-code change that brings each row's residual
     closest to zero, over the positions of +-127, +-1 and 64 others."""
     R, K = len(targets), len(x)
-    Q = g.integers(0, 16, size=(R, K)).astype(np.int64)
+    Q = g.integers(lo, 16, size=(R, K)).astype(np.int64)
     big = np.nonzero(np.abs(x) == 127)[0]
     unit = np.nonzero(np.abs(x) == 1)[0]
     other = g.choice(np.nonzero(np.abs(x) > 1)[0], 64, replace=False)
@@ -58,7 +59,7 @@ def design_rows(g: np.random.Generator, x: np.ndarray, targets: np.ndarray) -> n
             return Q
         QC = Q[np.ix_(live, C)]
         D = np.rint(res[live, None] / xc[None, :])
-        D = np.clip(D, -QC, 15 - QC).astype(np.int64)
+        D = np.clip(D, lo - QC, 15 - QC).astype(np.int64)
         after = np.abs(res[live, None] - D * x[C][None, :])
         j = np.argmin(after, axis=1)
         d = D[np.arange(live.size), j]
@@ -90,13 +91,32 @@ def pack_q4_0(Q: np.ndarray) -> np.ndarray:
     return blk.reshape(R, K // QK * 18)
 
 
+def q4_0_to_sym(w: np.ndarray) -> np.ndarray:
+    """Q4_0 rows with every scale 1.0 and no nibble 0 -> the same weights as
+    symmetric 4-bit blocks (fp32 scale 1.0, the same 16 payload bytes); the
+    all-zero blocks of unused experts become zero blocks (scale 0, codes 0)."""
+    b = np.ascontiguousarray(w, dtype=np.uint8).reshape(-1, 18)
+    zero = ~b.any(axis=1)
+    used = b[~zero]
+    assert (used[:, 0:2].copy().view(np.uint16) == 0x3C00).all()
+    assert ((used[:, 2:] & 0x0F) != 0).all() and ((used[:, 2:] >> 4) != 0).all()
+    out = np.empty((b.shape[0], 20), np.uint8)
+    out[:, 0:4] = np.array([1.0], np.float32).view(np.uint8)
+    out[:, 4:] = b[:, 2:]
+    out[zero, 0:4] = 0
+    out[zero, 4:] = 0x88
+    return out.reshape(w.shape[:-1] + (w.shape[-1] // 18 * 20,))
+
+
 class ExactLayer:
     """clusters: list of (n_tokens, experts) with disjoint expert lists, each
     expert list of length k (skipped slots: -1).  shared: a shared expert
-    (only with one cluster)."""
+    (only with one cluster).  lo: smallest stored code (1 keeps every weight
+    in -7..7, so q4_0_to_sym gives the same layer in the symmetric format)."""
 
-    def __init__(self, seed, H, I, E, k, clusters, shared):
+    def __init__(self, seed, H, I, E, k, clusters, shared, lo=0):
         g = np.random.default_rng(seed)
+        self.lo = lo
         assert not shared or len(clusters) == 1
         self.H, self.I, self.E, self.k = H, I, E, k
         self.w_gu = np.zeros((E, 2 * I, H // QK * 18), np.uint8)
@@ -110,7 +130,7 @@ class ExactLayer:
                 if e >= 0 and e not in xvec:
                     xvec[e] = x
                     self.w_gu[e] = self._gateup(g, x)
-                    self.w_d[e] = pack_q4_0(g.integers(0, 16, size=(H, I)))
+                    self.w_d[e] = pack_q4_0(g.integers(lo, 16, size=(H, I)))
             xs.append(np.repeat(x[None, :], n, axis=0))
             ids.append(np.repeat(np.asarray(experts, np.int32)[None, :], n, axis=0))
         for e, x in xvec.items():
@@ -122,9 +142,14 @@ class ExactLayer:
         self.ws_gu = self.ws_d = None
         if shared:
             self.ws_gu = self._gateup(g, xs[0][0])
-            self.ws_d = pack_q4_0(g.integers(0, 16, size=(H, I)))
+            self.ws_d = pack_q4_0(g.integers(self.lo, 16, size=(H, I)))
 
     def _gateup(self, g, x):
         gt, ut = gateup_targets(g, self.I)
-        return np.concatenate([pack_q4_0(design_rows(g, x, gt)),
-                               pack_q4_0(design_rows(g, x, ut))])
+        return np.concatenate([pack_q4_0(design_rows(g, x, gt, self.lo)),
+                               pack_q4_0(design_rows(g, x, ut, self.lo))])
+
+    def sym(self):
+        """(w_gu, w_d, ws_gu, ws_d) in the symmetric format (needs lo >= 1)."""
+        c = (lambda w: None if w is None else q4_0_to_sym(w))
+        return c(self.w_gu), c(self.w_d), c(self.ws_gu), c(self.ws_d)

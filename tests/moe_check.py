@@ -129,3 +129,50 @@ def gather_tokens(tokens, T, k, out_gpu, h_gpu, hq_gpu):
     Ts = len(tokens)
     rows = [t * k + j for t in tokens for j in range(k)] + [T * k + t for t in tokens]
     return out_gpu[tokens], h_gpu[rows], hq_gpu[rows], Ts
+
+
+def check_sym_layer(out_gpu, h_gpu, hq_gpu, x, ids, wts, w_gu, w_d, ws_gu, ws_d, H, I, E, k,
+                    max_flips=None):
+    """The same check for the layer in the paper's own format (Q8_F32 h,
+    hq_gpu [P, I/32*36]): Q8_F32(h) of the GPU's own h byte for byte, h
+    within dh of the oracle's h (so the codes are those of an h the float
+    tolerance allows), flips against the oracle's own codes counted, and the
+    output teacher-forced on the GPU's codes within 1e-5 * sum |terms|."""
+    shared = ws_gu is not None
+    r = oracle.moe_sym(x, ids, wts, w_gu, w_d, ws_gu, ws_d, H, I, E, k)
+    pairs = np.asarray(valid_pairs(ids, E, shared), dtype=np.int64)
+    nb = I // 32
+    np_ = len(pairs)
+    hg = np.ascontiguousarray(h_gpu[pairs], dtype=np.float32)
+    qg = np.ascontiguousarray(hq_gpu[pairs], dtype=np.uint8)
+    q_own = oracle.q8_f32_quantize(hg) if np_ else qg
+    if not np.array_equal(qg, q_own):
+        bad = np.nonzero((qg != q_own).reshape(np_, nb, 36).any(axis=2))
+        raise AssertionError(f"Q8_F32(h) differs from Q8_F32 of the GPU's own h at "
+                             f"{len(bad[0])} blocks, first (pair {pairs[bad[0][0]]}, "
+                             f"block {bad[1][0]})")
+    dh = delta_h(r.gu[pairs], r.Rgu[pairs], I)
+    err = np.abs(hg.astype(np.float64) - r.h[pairs].astype(np.float64))
+    ratio = err / dh
+    if np_ and not np.all(err <= dh):
+        i, j = np.unravel_index(np.argmax(ratio), ratio.shape)
+        raise AssertionError(f"h of pair {pairs[i]} column {j}: err/bound {ratio[i, j]:.3g}")
+    # a flip: a block whose codes differ from the oracle's (the fp32 scale
+    # follows h's last bits and is bounded through h)
+    flips = int((qg.reshape(np_, nb, 36)[..., 4:] !=
+                 r.hq[pairs].reshape(np_, nb, 36)[..., 4:]).any(axis=2).sum())
+    if max_flips is not None:
+        assert flips <= max_flips, f"{flips} Q8_F32(h) blocks differ from the oracle's choice"
+    sel = r.hq.copy()
+    sel[pairs] = qg
+    r2 = oracle.moe_sym(x, ids, wts, w_gu, w_d, ws_gu, ws_d, H, I, E, k, hq_in=sel,
+                        want_intermediates=False)
+    err = np.abs(out_gpu.astype(np.float64) - r2.out)
+    bad = err > EPS * r2.R
+    assert not bad.any(), (f"{bad.sum()} outputs beyond 1e-5 * sum|terms|; worst ratio "
+                           f"{np.max(err / np.maximum(EPS * r2.R, 1e-300)):.3g}")
+    rel = float(np.max(err / np.maximum(r2.R, 1e-300)))
+    st = {"pairs": np_, "flips": flips, "blocks": np_ * nb, "max_rel_err": rel,
+          "h_err_over_bound": float(ratio.max()) if np_ else 0.0}
+    STATS.append((os.environ.get("PYTEST_CURRENT_TEST", "").split(" ")[0], st))
+    return st

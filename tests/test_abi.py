@@ -95,6 +95,33 @@ def test_gemm_argument_errors():
     assert G(_fake(A), _fake(A + 0x10), y, 0, 64, 2048, None, 0, None) == w4.OK   # empty
 
 
+def test_moe_sym_argument_errors():
+    L = w4.lib()
+    S = L.moe_sym_workspace_size
+    assert S(1, 2048, 512, 256, 8) > 0
+    assert S(1, 2000, 512, 256, 8) == 0 and S(1, 2048, 500, 256, 8) == 0      # H, I % 256
+    assert S(1, 2048, 512, 256, 0) == 0 and S(-1, 2048, 512, 256, 8) == 0
+    assert S(1, 32768, 512, 256, 8) == 0                                        # H > 16384
+    n = S(2, 2048, 512, 256, 8)
+    offs = (ctypes.c_size_t * 3)()
+    assert L.moe_sym_workspace_layout(2, 2048, 512, 256, 8, offs) == w4.OK
+    assert offs[0] < offs[1] < offs[2] < n
+    assert L.moe_sym_workspace_layout(2, 2048, 512, 256, 8, None) == w4.ENULL
+    F = L.moe_sym_forward
+    p = [_fake(A + 0x1000 * i) for i in range(10)]
+    args = lambda **kw: [kw.get(k, v) for k, v in zip(
+        ("x", "ids", "w", "gu", "d", "sgu", "sd", "out"), p[:8])]
+    ok = args()
+    assert F(*args(x=None), 2, 2048, 512, 256, 8, p[8], n, None) == w4.ENULL
+    assert F(*args(sgu=None), 2, 2048, 512, 256, 8, p[8], n, None) == w4.ENULL   # one of the pair
+    assert F(*ok, 2, 2048, 512, 256, 8, None, n, None) == w4.ENULL
+    assert F(*ok, 2, 2000, 512, 256, 8, p[8], n, None) == w4.ESHAPE
+    assert F(*ok, 2, 2048, 512, 256, 65, p[8], n, None) == w4.ERANGE
+    assert F(*ok, 2, 2048, 512, 256, 8, p[8], n - 1, None) == w4.EWORKSPACE
+    assert F(*args(out=_fake(A + 0x7004)), 2, 2048, 512, 256, 8, p[8], n, None) == w4.EALIGN
+    assert F(*ok, 0, 2048, 512, 256, 8, p[8], n, None) == w4.OK                  # empty
+
+
 def test_moe_workspace_size_and_layout():
     assert w4.moe_workspace_size(1, 2048, 512, 256, 8) > 0
     assert w4.moe_workspace_size(1, 2000, 512, 256, 8) == 0          # H % 256

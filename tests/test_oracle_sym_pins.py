@@ -201,3 +201,74 @@ def test_gemv_sym_closed_forms():
     assert y[1] == want and y[0] == 0 and y[2] == 0
     s = oracle.blockdot_sym(w[1, 1], xq.reshape(2, -1)[1])
     assert s == 7 * int(pa[1].view(np.int8)[5])
+
+
+# ------------------------------------------------------------ the MoE layer
+def test_moe_sym_equals_q4_0_layer_on_exact_layers():
+    """On a layer whose weights are codes in -7..7 with every scale 1.0 and
+    whose activations and h are integers with a largest magnitude of 127 per
+    block, both formats describe the same numbers (a Q4_0 block of scale 1.0
+    and a symmetric block of scale 1.0 with the same nibbles; Q8_0 and Q8_F32
+    both give scale 1.0 and the values as codes), so the layer in the paper's
+    format must reproduce the pinned Q4_0 layer exactly: gate/up sums, h, the
+    codes of h and the output (routed slots with weights 0.5/1/2, a skipped
+    slot, the shared expert)."""
+    from tests.exact_layers import ExactLayer
+    H, I, E, k = 512, 256, 6, 3
+    L = ExactLayer(31, H, I, E, k, [(3, [0, 4, -1])], shared=True, lo=1)
+    r0 = oracle.moe(L.x, L.ids, L.wts, L.w_gu, L.w_d, L.ws_gu, L.ws_d, H, I, E, k)
+    w_gu, w_d, ws_gu, ws_d = L.sym()
+    r1 = oracle.moe_sym(L.x, L.ids, L.wts, w_gu, w_d, ws_gu, ws_d, H, I, E, k)
+    assert np.array_equal(r0.out, r1.out) and np.array_equal(r0.R, r1.R)
+    assert np.array_equal(r0.gu, r1.gu) and np.array_equal(r0.h, r1.h)
+    P = L.x.shape[0] * (k + 1)
+    q0 = r0.hq.reshape(P, I // 32, 34)
+    q1 = r1.hq.reshape(P, I // 32, 36)
+    live = [p for p in range(P) if p >= 3 * k or L.ids.ravel()[p] >= 0]
+    assert np.array_equal(q0[live, :, 2:], q1[live, :, 4:])           # the codes
+    assert (q0[live, :, 0:2].copy().view(np.uint16) == 0x3C00).all()  # Q8_0 scale 1.0
+    assert (q1[live, :, 0:4].copy().view(np.float32) == 1.0).all()    # Q8_F32 scale 1.0
+    assert np.abs(r1.out).max() > 1000                                 # not a trivial layer
+
+
+def _sym_layer(seed, H, I, E, T, k, shared=True):
+    from paper_2606_24031_amd import synth
+    g = synth.rng(seed)
+    w = dict(w_gu=synth.q4_sym_random_blocks(g, E * 2 * I, H),
+             w_d=synth.q4_sym_random_blocks(g, E * H, I),
+             ws_gu=synth.q4_sym_random_blocks(g, 2 * I, H) if shared else None,
+             ws_d=synth.q4_sym_random_blocks(g, H, I) if shared else None)
+    x = synth.normal_f32(g, (T, H))
+    ids, wts = synth.routing(g, T, E, k)
+    return w, x, ids, wts
+
+
+def test_moe_sym_slot_order_and_linearity():
+    """Routing invariants of the layer: permuting a token's slots (ids and
+    weights together) leaves its output unchanged up to the order of the fp64
+    sums; an expert named in two slots with weights a and b equals one slot
+    of weight a + b (exact in fp32) and a skipped slot; a skipped slot is
+    the same as weight 0."""
+    H, I, E, T, k = 256, 256, 5, 3, 3
+    w, x, ids, wts = _sym_layer(51, H, I, E, T, k)
+    args = (w["w_gu"], w["w_d"], w["ws_gu"], w["ws_d"], H, I, E, k)
+    r = oracle.moe_sym(x, ids, wts, *args)
+    perm = np.array([2, 0, 1])
+    rp = oracle.moe_sym(x, ids[:, perm], wts[:, perm], *args)
+    assert np.all(np.abs(rp.out - r.out) <= 1e-12 * r.R)
+    ids2 = ids.copy()
+    wts2 = wts.copy()
+    ids2[:, 1] = ids2[:, 0]
+    wts2[:, 0], wts2[:, 1] = 0.25, 0.5
+    ra = oracle.moe_sym(x, ids2, wts2, *args)
+    ids3, wts3 = ids2.copy(), wts2.copy()
+    ids3[:, 1] = -1
+    wts3[:, 0] = 0.75
+    rb = oracle.moe_sym(x, ids3, wts3, *args)
+    assert np.all(np.abs(ra.out - rb.out) <= 1e-12 * ra.R)
+    wts4 = wts3.copy()
+    wts4[:, 1] = 0.0
+    ids4 = ids3.copy()
+    ids4[:, 1] = ids2[:, 1]
+    rc = oracle.moe_sym(x, ids4, wts4, *args)
+    assert np.all(np.abs(rc.out - rb.out) <= 1e-12 * rb.R)
