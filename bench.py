@@ -117,6 +117,9 @@ def parse():
     ap.add_argument("--no-stack", action="store_true")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the E/k invariants, router, LM-head and 1024x1024 GEMV lines")
+    ap.add_argument("--section", choices=["gemm", "sym_layer"],
+                    help="run only this extra section and print its result as JSON "
+                         "(for profiling one kernel family)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 256 MiB device copy 5 times (for scaling the "
                          "rocprofv3 FETCH_SIZE / WRITE_SIZE counters)")
@@ -593,6 +596,52 @@ def bench_gemm(torch, w4, synth, args, dev):
     return out
 
 
+def bench_sym_layer(torch, w4, synth, args, dev, n=200):
+    """The MoE layer in the paper's own format (Q4_SYM weights, Q8_F32
+    activations; four launches) at one token, top-8 of 256 plus the shared
+    expert, two weight sets alternated, replayed from a hipGraph."""
+    g = synth.rng(args.seed + 13)
+    sets = []
+    for _ in range(2):
+        sets.append([torch.from_numpy(synth.q4_sym_random_blocks(g, E * 2 * I, H)).to(dev),
+                     torch.from_numpy(synth.q4_sym_random_blocks(g, E * H, I)).to(dev),
+                     torch.from_numpy(synth.q4_sym_random_blocks(g, 2 * I, H)).to(dev),
+                     torch.from_numpy(synth.q4_sym_random_blocks(g, H, I)).to(dev)])
+    ids_all, wts_all = synth.routing(g, n, E, K_TOP)
+    ids_d = torch.from_numpy(ids_all).to(dev).view(n, 1, K_TOP)
+    wts_d = torch.from_numpy(wts_all).to(dev).view(n, 1, K_TOP)
+    x = torch.from_numpy(synth.normal_f32(g, (n, 1, H))).to(dev)
+    ws = w4.moe_sym_workspace(1, H, I, E, K_TOP, device=dev)
+    out = torch.empty((1, H), dtype=torch.float32, device=dev)
+
+    def step(i):
+        L = sets[i % 2]
+        w4.moe_sym_forward(x[i], ids_d[i], wts_d[i], L[0], L[1], L[2], L[3], H, I, E, K_TOP, ws,
+                           out=out)
+
+    for i in range(4):
+        step(i)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for i in range(n):
+            step(i)
+    graph.replay()
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    graph.replay()
+    ev1.record()
+    torch.cuda.synchronize()
+    us = ev0.elapsed_time(ev1) / n * 1e3
+    expert = (2 * I * (H // 32) + H * (I // 32)) * 20
+    nbytes = sum((len(set(r.tolist())) + 1) * expert for r in ids_all) / n
+    del sets
+    return {"T": 1, "us_per_layer": round(us, 2), "GBps": round(nbytes / us / 1e3, 1),
+            "hbm_peak_frac": round(nbytes / us / 1e3 / HBM_PEAK_GBPS, 4), "launch": "hipGraph"}
+
+
 def bench_stack(torch, w4, synth, args, dev):
     """40 chained pre-norm residual layers (x <- x + MoE_l(RMSNorm_l(x)), one
     moe_w4a8_layer call each, the residual add and norm fused into the layer
@@ -869,6 +918,11 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
 
+    if args.section:
+        fn = {"gemm": bench_gemm, "sym_layer": bench_sym_layer}[args.section]
+        print(json.dumps({args.section: fn(torch, w4, synth, args, dev)}), flush=True)
+        return
+
     log(f"generating {args.layers} layers of Q4_0 weights on the GPU")
     gen = torch.Generator(device=dev)
     gen.manual_seed(args.seed)
@@ -906,7 +960,7 @@ def main():
         m32 = bench_m32(torch, w4, synth, layers, args, dev)
         log(f"decode M=32: {m32}")
 
-    invariants = router = lm_head = gemv_1024 = gemv_sym = gemm = None
+    invariants = router = lm_head = gemv_1024 = gemv_sym = gemm = sym_layer = None
     if not args.no_extras:
         invariants = bench_decode_invariants(torch, w4, synth, layers, args, dev)
         log(f"decode invariants: {invariants}")
@@ -920,6 +974,8 @@ def main():
         log(f"gemv, paper's fp32-scale format: {gemv_sym}")
         gemm = bench_gemm(torch, w4, synth, args, dev)
         log(f"dense gemm: {gemm}")
+        sym_layer = bench_sym_layer(torch, w4, synth, args, dev)
+        log(f"layer in the paper's format: {sym_layer}")
 
     stack = None
     if not args.no_stack:
@@ -973,6 +1029,7 @@ def main():
         "gemv_1024": gemv_1024,
         "gemv_lm_head_paper_format": gemv_sym,
         "gemm": gemm,
+        "moe_layer_paper_format_m1": sym_layer,
     }
     print(json.dumps(rec), flush=True)
 
