@@ -482,7 +482,60 @@ struct Q8Args {
   uint32_t *xa;     // aligned codes and fp32 scales (MFMA kernels), or null
   float *xd;
   int64_t nblocks, nbrow;   // blocks in all, per row
+  // pre-norm residual step folded in (norm_rows > 0): x_out = x + resid,
+  // xn = RMSNorm(x_out) * gamma, and the Q8_0 forms are those of xn
+  const float *resid;       // or null (no residual add)
+  const float *gamma;
+  float *x_out, *xn;
+  float eps;
+  int norm_rows;            // whole rows per quantizing workgroup, or 0
 };
+
+// The quantizing workgroup wg with the residual step folded in: rows
+// wg * norm_rows .. + norm_rows - 1, H/4 threads per row (a multiple of 64),
+// each thread the four elements 4c..4c+3 of its row: x_out = x + resid (one
+// fp32 add per element), the sum of squares in a fixed order (the lane's four
+// in index order, a butterfly over the wave, the row's waves in order), then
+// xn = x_out * (1 / sqrt(sum / H + eps)) * gamma, written out and quantized
+// in registers.  Every thread of the workgroup must call it.
+__device__ void norm_q8_rows(const Q8Args &q, int64_t wg) {
+  __shared__ float wsum[ROUTE_T / 64];
+  const int h4 = (int)(q.nbrow * 8);
+  const int t = (int)threadIdx.x;
+  const int rl = t / h4, c = t - rl * h4;
+  const int64_t T = q.nblocks / q.nbrow;
+  const int64_t row = wg * q.norm_rows + rl;
+  const bool live = rl < q.norm_rows && row < T;
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (live) {
+    v = reinterpret_cast<const float4 *>(q.x)[row * h4 + c];
+    if (q.resid) {
+      const float4 d = reinterpret_cast<const float4 *>(q.resid)[row * h4 + c];
+      v.x += d.x; v.y += d.y; v.z += d.z; v.w += d.w;
+    }
+    reinterpret_cast<float4 *>(q.x_out)[row * h4 + c] = v;
+  }
+  float ss = 0.0f;
+  ss = fmaf(v.x, v.x, ss);
+  ss = fmaf(v.y, v.y, ss);
+  ss = fmaf(v.z, v.z, ss);
+  ss = fmaf(v.w, v.w, ss);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
+  if ((t & 63) == 0) wsum[t >> 6] = ss;
+  __syncthreads();
+  const int w0 = (rl * h4) >> 6, nw = h4 >> 6;
+  float tot = 0.0f;
+  for (int w = 0; w < nw && live; w++) tot += wsum[w0 + w];
+  const float r = 1.0f / sqrtf(tot / (float)(h4 * 4) + q.eps);
+  float xn[4] = {0.f, 0.f, 0.f, 0.f};
+  if (live) {
+    const float4 g = reinterpret_cast<const float4 *>(q.gamma)[c];
+    xn[0] = v.x * r * g.x; xn[1] = v.y * r * g.y; xn[2] = v.z * r * g.z; xn[3] = v.w * r * g.w;
+    reinterpret_cast<float4 *>(q.xn)[row * h4 + c] = make_float4(xn[0], xn[1], xn[2], xn[3]);
+  }
+  q8_0_lane_vals(xn, q.xq, q.xs, q.xa, q.xd, q.nbrow, row * q.nbrow + (c >> 3), c & 7, live);
+}
 
 // Stages 1 and 2 in one launch (they are independent): the first `nroute`
 // workgroups route -- the whole route in workgroup 0 (MODE 0, 1), or the
@@ -497,8 +550,11 @@ __global__ __launch_bounds__(ROUTE_T) void prep_kernel(RouteArgs a, Q8Args q, in
       route_body<MODE>(a);
     return;
   }
-  q8_0_lane(q.x, q.xq, q.xs, q.xa, q.xd, q.nblocks, q.nbrow,
-            (int64_t)(blockIdx.x - nroute) * ROUTE_T + threadIdx.x);
+  if (q.norm_rows)
+    norm_q8_rows(q, (int64_t)(blockIdx.x - nroute));
+  else
+    q8_0_lane(q.x, q.xq, q.xs, q.xa, q.xd, q.nblocks, q.nbrow,
+              (int64_t)(blockIdx.x - nroute) * ROUTE_T + threadIdx.x);
 }
 
 // The split route's second part: offsets, the permutation and the group,
@@ -565,7 +621,10 @@ int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
                           reinterpret_cast<uint32_t *>(ws + L.xfer), ws + L.xq,
                           reinterpret_cast<float *>(ws + L.h), ws + L.hq, s);
 
-  if (norm.gamma) {
+  // the pre-norm residual step: inside the quantizing workgroups of the
+  // prep launch when a row fits one of them, else a launch of its own
+  const bool fold_norm = norm.gamma && H / 4 <= ROUTE_T;
+  if (norm.gamma && !fold_norm) {
     if ((rc = launch_rmsnorm(hidden, norm.resid, norm.gamma, norm.x_out, norm.xn, T, H, norm.eps,
                              s)) != W4A8_OK)
       return rc;
@@ -588,6 +647,12 @@ int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
   qa.xd = xd;
   qa.nblocks = T * (H / QK);
   qa.nbrow = H / QK;
+  qa.resid = norm.resid;
+  qa.gamma = norm.gamma;
+  qa.x_out = norm.x_out;
+  qa.xn = norm.xn;
+  qa.eps = norm.eps;
+  qa.norm_rows = fold_norm ? (int)(ROUTE_T / (H / 4)) : 0;
 
   RouteArgs ra;
   ra.ids = ids;
@@ -603,7 +668,8 @@ int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
   const int64_t Pr = T * k;
   ra.ebits = 0;
   while ((1 << ra.ebits) < E) ra.ebits++;
-  const unsigned nq = (unsigned)((qa.nblocks * 8 + ROUTE_T - 1) / ROUTE_T);
+  const unsigned nq = qa.norm_rows ? (unsigned)((T + qa.norm_rows - 1) / qa.norm_rows)
+                                   : (unsigned)((qa.nblocks * 8 + ROUTE_T - 1) / ROUTE_T);
   const int64_t nslice = (Pr + SLICE - 1) / SLICE;
   if (split_route(Pr, E)) {
     // slices of ROUTE_T pairs ranked beside the quantization, then one

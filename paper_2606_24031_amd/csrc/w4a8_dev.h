@@ -308,19 +308,13 @@ __device__ __forceinline__ void store_q8_0_block8(uint8_t *blk, int j, uint32_t 
 // elements 4 (tid % 8) .. + 3): the 34-byte block, and when the pointers are
 // set its nibble-split form (xs, rows of nbrow blocks, see split_blk) and its
 // 32 codes on a 32-byte boundary with the fp32 scale (xa, xd).  Lanes past
-// nblocks take part in the exchanges and store nothing.
-__device__ __forceinline__ void q8_0_lane(const float *__restrict__ x, uint8_t *__restrict__ xq,
-                                          uint8_t *__restrict__ xs, uint32_t *__restrict__ xa,
-                                          float *__restrict__ xd, int64_t nblocks, int64_t nbrow,
-                                          int64_t tid) {
-  const int64_t blk = tid >> 3;
-  const int j = (int)(tid & 7);
-  float v[4] = {0.f, 0.f, 0.f, 0.f};
-  const bool live = blk < nblocks;
-  if (live) {
-    const float4 t = reinterpret_cast<const float4 *>(x + blk * QK)[j];
-    v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
-  }
+// nblocks take part in the exchanges and store nothing.  q8_0_lane_vals
+// takes the lane's four values already in registers (elements 4j..4j+3 of
+// block blk; live: the block exists); q8_0_lane loads them from x.
+__device__ __forceinline__ void q8_0_lane_vals(const float v[4], uint8_t *__restrict__ xq,
+                                               uint8_t *__restrict__ xs, uint32_t *__restrict__ xa,
+                                               float *__restrict__ xd, int64_t nbrow, int64_t blk,
+                                               int j, bool live) {
   uint32_t d16;
   const uint32_t packed = q8_0_block8(v, d16);
   if (live) store_q8_0_block8(xq + blk * Q8B, j, packed, d16);
@@ -341,6 +335,21 @@ __device__ __forceinline__ void q8_0_lane(const float *__restrict__ x, uint8_t *
     xa[blk * 8 + j] = packed;
     if (j == 0) xd[blk] = f16_bits_to_f32(d16);
   }
+}
+
+__device__ __forceinline__ void q8_0_lane(const float *__restrict__ x, uint8_t *__restrict__ xq,
+                                          uint8_t *__restrict__ xs, uint32_t *__restrict__ xa,
+                                          float *__restrict__ xd, int64_t nblocks, int64_t nbrow,
+                                          int64_t tid) {
+  const int64_t blk = tid >> 3;
+  const int j = (int)(tid & 7);
+  float v[4] = {0.f, 0.f, 0.f, 0.f};
+  const bool live = blk < nblocks;
+  if (live) {
+    const float4 t = reinterpret_cast<const float4 *>(x + blk * QK)[j];
+    v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+  }
+  q8_0_lane_vals(v, xq, xs, xa, xd, nbrow, blk, j, live);
 }
 
 // LDS staging of activation blocks (see dot8_lds): each block's nibble-split

@@ -489,7 +489,8 @@ def test_moe_layer_residual_norm(qwen_layer, T, with_prev):
     """x_out = x + y_prev is one fp32 add, xn = RMSNorm(x_out) * gamma is within
     fp32 rounding of the oracle, Q8_0(xn) is bit-exact for the GPU's own xn,
     and the layer output is the MoE layer of that xn (T = 1: the norm inside
-    the single decode launch; T > 1: rmsnorm kernel, then the grouped path)."""
+    the single decode launch; T > 1: the norm inside the quantizing
+    workgroups of the prep launch, then the grouped path)."""
     L = qwen_layer
     g = synth.rng(60 + T)
     x = synth.normal_f32(g, (T, L.H))
@@ -513,6 +514,36 @@ def test_moe_layer_residual_norm(qwen_layer, T, with_prev):
     h = wsn[lay["h"]:lay["h"] + P * L.I * 4].view(np.float32).reshape(P, L.I)
     hq = wsn[lay["hq"]:lay["hq"] + P * (L.I // 32) * 34].reshape(P, -1)
     L.check(xn, ids, wts, 8, host(out), h, hq)
+
+
+@pytest.mark.parametrize("H,T", [(4352, 5), (768, 21)])
+def test_moe_layer_residual_norm_other_widths(H, T):
+    """Rows wider than one quantizing workgroup (H = 4352: the norm in a
+    launch of its own) and a width that leaves threads of the workgroup idle
+    (H = 768: five rows per workgroup, 64 threads without a row)."""
+    I, E, k = 256, 4, 2
+    L = Layer(80 + H, H, I, E)
+    g = synth.rng(81 + H)
+    x = synth.normal_f32(g, (T, H))
+    y_prev = synth.normal_f32(g, (T, H), 0.3)
+    gamma = (np.float32(1.0) + synth.normal_f32(g, (H,), 0.1)).astype(np.float32)
+    ids, wts = synth.routing(g, T, E, k)
+    ws = w4.moe_workspace(T, H, I, E, k)
+    x_out, out = w4.moe_layer(dev(x), dev(y_prev), dev(gamma), dev(ids), dev(wts), L.d_gu, L.d_d,
+                              L.d_sgu, L.d_sd, H, I, E, k, ws)
+    xo_ref, xn_ref = oracle.rmsnorm_residual(x, y_prev, gamma, eps=1e-6)
+    assert np.array_equal(host(x_out), xo_ref)
+    lay = w4.moe_workspace_layout(T, H, I, E, k)
+    wsn = host(ws)
+    xn = wsn[lay["xn"]:lay["xn"] + T * H * 4].view(np.float32).reshape(T, H)
+    err = np.abs(xn.astype(np.float64) - xn_ref)
+    assert np.all(err <= 2e-6 * np.abs(xn_ref) + 1e-7 * np.abs(gamma).max())
+    xq = wsn[lay["xq"]:lay["xq"] + T * (H // 32) * 34].reshape(T, -1)
+    assert np.array_equal(xq, oracle.q8_0_quantize(xn)), "Q8_0 of the normalized row"
+    P = T * k + T
+    h = wsn[lay["h"]:lay["h"] + P * I * 4].view(np.float32).reshape(P, I)
+    hq = wsn[lay["hq"]:lay["hq"] + P * (I // 32) * 34].reshape(P, -1)
+    L.check(xn, ids, wts, k, host(out), h, hq)
 
 
 @pytest.mark.parametrize("T,gated", [(1, True), (1, False), (6, True), (40, True), (40, False)])
