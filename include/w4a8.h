@@ -304,8 +304,10 @@ int moe_w4a8_forward(const float *hidden, const int32_t *topk_ids, const float *
  *   out   = moe_w4a8_forward's layer applied to xn
  * Arguments as for moe_w4a8_forward, plus x [T][H], y_prev [T][H] or NULL,
  * gamma [H], eps >= 0, x_out [T][H]; x_out and out must not alias x,
- * y_prev or each other (equal base addresses -> W4A8_EALIAS).  At T = 1 the norm runs inside the single decode
- * launch (every workgroup normalizes the row it quantizes).  gamma or x_out
+ * y_prev or each other (equal base addresses -> W4A8_EALIAS).  At T = 1 the
+ * norm runs inside the single decode launch (every workgroup normalizes the
+ * row it quantizes); at T > 1 inside the quantizing workgroups of the first
+ * launch when H <= 4096 (a launch of its own for wider rows).  gamma or x_out
  * NULL -> W4A8_ENULL; eps < 0 -> W4A8_ESHAPE; other errors as for
  * moe_w4a8_forward.
  */
