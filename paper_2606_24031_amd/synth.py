@@ -90,3 +90,22 @@ def q4_sym_random_blocks(g: np.random.Generator, rows: int, K: int,
     blocks[:, 4:] = (lo | (hi << 4)).astype(np.uint8)
     blocks[:, 0:4] = d.view(np.uint8).reshape(-1, 4)
     return blocks.reshape(rows, nb * 20)
+
+
+def gdn_inputs(g: np.random.Generator, T: int, NH: int, DK: int, DV: int,
+               with_state: bool = True):
+    """Inputs of the gated-delta-net recurrence as its layer hands them over:
+    q and k drawn N(0, 1) and scaled to unit length per token and head (the
+    layer L2-normalizes them), v ~ N(0, 1), the log decay gate g = -0.5 *
+    softplus(N(-2.5, 1)) (decays mostly between 0.9 and 1), the step
+    beta = sigmoid(N(0, 1)), and an initial state N(0, 0.1^2) (or None)."""
+    q = normal_f32(g, (T, NH, DK))
+    k = normal_f32(g, (T, NH, DK))
+    q /= np.sqrt((q.astype(np.float64) ** 2).sum(axis=2, keepdims=True)).astype(np.float32)
+    k /= np.sqrt((k.astype(np.float64) ** 2).sum(axis=2, keepdims=True)).astype(np.float32)
+    v = normal_f32(g, (T, NH, DV))
+    z = normal_f32(g, (T, NH)).astype(np.float64) - 2.5
+    gate = (-0.5 * np.log1p(np.exp(z))).astype(np.float32)
+    beta = (1.0 / (1.0 + np.exp(-normal_f32(g, (T, NH)).astype(np.float64)))).astype(np.float32)
+    s0 = normal_f32(g, (NH, DK, DV), 0.1) if with_state else None
+    return q.astype(np.float32), k.astype(np.float32), v, gate, beta, s0
