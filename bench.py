@@ -117,7 +117,7 @@ def parse():
     ap.add_argument("--no-stack", action="store_true")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the E/k invariants, router, LM-head and 1024x1024 GEMV lines")
-    ap.add_argument("--section", choices=["gemm", "sym_layer"],
+    ap.add_argument("--section", choices=["gemm", "sym_layer", "gdn"],
                     help="run only this extra section and print its result as JSON "
                          "(for profiling one kernel family)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -642,6 +642,41 @@ def bench_sym_layer(torch, w4, synth, args, dev, n=200):
             "hbm_peak_frac": round(nbytes / us / 1e3 / HBM_PEAK_GBPS, 4), "launch": "hipGraph"}
 
 
+def bench_gdn(torch, w4, synth, args, dev):
+    """The gated-delta-net recurrence of one linear-attention layer at the
+    paper's head shape (32 value heads, dk = dv = 128) as a chunked scan:
+    the 947-token prompt and a single decode token, each continuing a given
+    state, replayed from a hipGraph."""
+    out = {}
+    for T, n in ((947, 20), (1, 200)):
+        g = synth.rng(args.seed + 14 + T)
+        q, k, v, gate, beta, s0 = synth.gdn_inputs(g, T, 32, 128, 128)
+        d = [torch.from_numpy(a).to(dev) for a in (q, k, v, gate, beta, s0)]
+        o = torch.empty((T, 32, 128), dtype=torch.float32, device=dev)
+        s_out = torch.empty_like(d[5])
+        ws = torch.empty(int(w4.lib().gdn_workspace_size(T, 32, 128, 128)), dtype=torch.uint8,
+                         device=dev)
+        for _ in range(3):
+            w4.gdn_scan(*d, out=o, s_out=s_out, workspace=ws)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for _ in range(n):
+                w4.gdn_scan(*d, out=o, s_out=s_out, workspace=ws)
+        graph.replay()
+        torch.cuda.synchronize()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        ev0.record()
+        graph.replay()
+        ev1.record()
+        torch.cuda.synchronize()
+        us = ev0.elapsed_time(ev1) / n * 1e3
+        out[f"T{T}"] = {"us_per_layer": round(us, 2), "tokens_per_s": round(T / us * 1e6, 1),
+                        "heads": 32, "dk": 128, "dv": 128, "chunk": 32, "launch": "hipGraph"}
+    return out
+
+
 def bench_stack(torch, w4, synth, args, dev):
     """40 chained pre-norm residual layers (x <- x + MoE_l(RMSNorm_l(x)), one
     moe_w4a8_layer call each, the residual add and norm fused into the layer
@@ -919,7 +954,7 @@ def main():
     torch.cuda.set_device(dev)
 
     if args.section:
-        fn = {"gemm": bench_gemm, "sym_layer": bench_sym_layer}[args.section]
+        fn = {"gemm": bench_gemm, "sym_layer": bench_sym_layer, "gdn": bench_gdn}[args.section]
         print(json.dumps({args.section: fn(torch, w4, synth, args, dev)}), flush=True)
         return
 
@@ -960,7 +995,7 @@ def main():
         m32 = bench_m32(torch, w4, synth, layers, args, dev)
         log(f"decode M=32: {m32}")
 
-    invariants = router = lm_head = gemv_1024 = gemv_sym = gemm = sym_layer = None
+    invariants = router = lm_head = gemv_1024 = gemv_sym = gemm = sym_layer = gdn = None
     if not args.no_extras:
         invariants = bench_decode_invariants(torch, w4, synth, layers, args, dev)
         log(f"decode invariants: {invariants}")
@@ -976,6 +1011,8 @@ def main():
         log(f"dense gemm: {gemm}")
         sym_layer = bench_sym_layer(torch, w4, synth, args, dev)
         log(f"layer in the paper's format: {sym_layer}")
+        gdn = bench_gdn(torch, w4, synth, args, dev)
+        log(f"GDN recurrence, chunked scan: {gdn}")
 
     stack = None
     if not args.no_stack:
@@ -1030,6 +1067,7 @@ def main():
         "gemv_lm_head_paper_format": gemv_sym,
         "gemm": gemm,
         "moe_layer_paper_format_m1": sym_layer,
+        "gdn_recurrence": gdn,
     }
     print(json.dumps(rec), flush=True)
 

@@ -190,6 +190,37 @@ int moe_sym_forward(const float *hidden, const int32_t *topk_ids, const float *t
                     int64_t E, int64_t k, void *workspace, size_t ws_bytes, void *stream);
 
 /*
+ * The gated-delta-net recurrence of the model's linear-attention layers
+ * (Sec. 2.2: a state S in R^{dk x dv} per value head, updated token by token;
+ * Sec. 5.5: a chunked / parallel scan as the lever for prefill), with the
+ * update the gated delta rule of the work the paper cites, per head h and
+ * token t (fp32):
+ *   S_t = exp(g_t) (I - beta_t k_t k_t^T) S_{t-1} + beta_t k_t v_t^T
+ *   o_t = S_t^T q_t
+ * computed as a chunked scan (chunks of 32 tokens: per-chunk triangular
+ * solve and products in parallel, the chunks in order per head and group of
+ * 8 value columns).  The layer's projections, short convolutions, q/k
+ * normalization and output gate are the caller's.
+ *   q, k [T][NH][DK], v and out [T][NH][DV], g (log decay, <= 0 in the
+ *   model) and beta [T][NH], all fp32; s0 [NH][DK][DV] the state before the
+ *   first token (NULL: zero); s_out [NH][DK][DV] the state after the last
+ *   (NULL: not written; may equal s0).  workspace >= gdn_workspace_size
+ *   bytes, no initialisation.
+ * Errors: DK not 64 or 128, DV not a positive multiple of 8, NH <= 0 or
+ * T < 0 -> W4A8_ESHAPE; T >= 2^31, NH >= 2^16, DV > 4096 or too many
+ * chunks -> W4A8_ERANGE; q, k, v, g, beta, out or workspace NULL ->
+ * W4A8_ENULL (T == 0 without s_out is a no-op); q, k, v, out, s0, s_out or
+ * the workspace not 16-byte aligned, g or beta not 4-byte aligned ->
+ * W4A8_EALIGN; workspace too small -> W4A8_EWORKSPACE.
+ * gdn_workspace_size returns 0 for invalid sizes.
+ */
+size_t gdn_workspace_size(int64_t T, int64_t NH, int64_t DK, int64_t DV);
+int gdn_chunked_scan(const float *q, const float *k, const float *v, const float *g,
+                     const float *beta, const float *s0, float *out, float *s_out, int64_t T,
+                     int64_t NH, int64_t DK, int64_t DV, void *workspace, size_t ws_bytes,
+                     void *stream);
+
+/*
  * Bytes of device workspace moe_w4a8_forward needs for these sizes, or 0 if
  * the sizes are invalid.  The workspace must be zero-filled once before its
  * first use (moe_w4a8_workspace_init does that); the library leaves its

@@ -30,7 +30,8 @@ EXPORTS = ("w4a8_strerror", "q8_0_quantize", "q4_0_quantize", "q4q8_gemv",
            "rmsnorm_residual", "moe_router_topk", "moe_w4a8_layer_routed",
            "q4_sym_quantize", "q8_f32_quantize", "q4sym_q8f32_gemv",
            "w4a8_decode_wait_bound", "moe_w4a8_forward_noalloc", "q4q8_gemm_workspace_size",
-           "q4q8_gemm", "moe_sym_workspace_size", "moe_sym_workspace_layout", "moe_sym_forward")
+           "q4q8_gemm", "moe_sym_workspace_size", "moe_sym_workspace_layout", "moe_sym_forward",
+           "gdn_workspace_size", "gdn_chunked_scan")
 
 _lib = None
 
@@ -92,6 +93,10 @@ def lib() -> ctypes.CDLL:
     L.moe_sym_workspace_layout.restype = ctypes.c_int
     L.moe_sym_forward.argtypes = [P, P, P, P, P, P, P, P, I64, I64, I64, I64, I64, P, SZ, P]
     L.moe_sym_forward.restype = ctypes.c_int
+    L.gdn_workspace_size.argtypes = [I64, I64, I64, I64]
+    L.gdn_workspace_size.restype = SZ
+    L.gdn_chunked_scan.argtypes = [P, P, P, P, P, P, P, P, I64, I64, I64, I64, P, SZ, P]
+    L.gdn_chunked_scan.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -206,6 +211,30 @@ def moe_sym_forward(hidden, topk_ids, topk_w, w_gate_up, w_down, ws_gate_up, ws_
                                T, H, I, E, k, _p(workspace), workspace.numel(), _stream(stream))
     _check(rc, "moe_sym_forward")
     return out
+
+
+def gdn_scan(q, k, v, g, beta, s0=None, out=None, s_out=None, workspace=None, stream=None):
+    """The gated-delta-net recurrence as a chunked scan (gdn_chunked_scan):
+    q, k [T, NH, DK], v [T, NH, DV], g and beta [T, NH], s0 [NH, DK, DV] or
+    None; returns (out [T, NH, DV], s_out [NH, DK, DV]), fp32."""
+    import torch
+    T, NH, DK = k.shape
+    DV = v.shape[2]
+    for t in (q, k, v, g, beta, s0):
+        assert t is None or (t.dtype == torch.float32 and t.is_contiguous())
+    if out is None:
+        out = torch.empty((T, NH, DV), dtype=torch.float32, device=k.device)
+    if s_out is None:
+        s_out = torch.empty((NH, DK, DV), dtype=torch.float32, device=k.device)
+    if workspace is None:
+        n = int(lib().gdn_workspace_size(T, NH, DK, DV))
+        if n == 0:
+            raise W4A8Error(ESHAPE, "gdn_workspace_size")
+        workspace = torch.empty(n, dtype=torch.uint8, device=k.device)
+    _check(lib().gdn_chunked_scan(_p(q), _p(k), _p(v), _p(g), _p(beta), _p(s0), _p(out),
+                                  _p(s_out), T, NH, DK, DV, _p(workspace), workspace.numel(),
+                                  _stream(stream)), "gdn_chunked_scan")
+    return out, s_out
 
 
 def q4_sym_quantize(w, out=None, stream=None):

@@ -1,0 +1,372 @@
+// The gated-delta-net (GDN) recurrence of the model's linear-attention layers
+// (Sec. 2.2: a state S in R^{dk x dv} per value head, updated token by token;
+// the update is the gated delta rule of the work the paper cites)
+//   S_t = a_t (I - b_t k_t k_t^T) S_{t-1} + b_t k_t v_t^T,   o_t = S_t^T q_t,
+// a_t = exp(g_t), as a chunked scan: the paper names a chunked / parallel scan
+// as the lever its token-by-token kernel lacked (Sec. 5.5).
+//
+// Within a chunk of C = 32 tokens, with L_i the sum of g over the chunk up to
+// token i, the delta-rule corrections u_i = b_i (v_i - a_i S_{i-1}^T k_i)
+// solve a unit lower-triangular system, and everything else is products:
+//   (I + A) U = diag(b) (V - diag(e^L) K S),  A_ij = b_i e^{L_i - L_j} k_i.k_j (j < i)
+//   O = diag(e^L) Q S + P U,                  P_ij = e^{L_i - L_j} q_i.k_j  (j <= i)
+//   S <- e^{L_C} S + K^T diag(e^{L_C - L}) U.
+// Two launches:
+//   gdn_prep: per (head, chunk), in parallel: L, the dot products k.k and q.k,
+//     A and P, and T' = (I + A)^{-1} diag(b) by forward substitution (each
+//     column of the inverse depends only on itself: one lane per column);
+//   gdn_scan: per (head, 8 columns of the value dimension) -- the columns of
+//     S evolve independently -- the chunks in order, the workgroup's slice of
+//     S in registers (thread: one column, DK/32 consecutive rows): X = K S and
+//     Y = Q S from per-thread partials reduced over the rows (8 neighbouring
+//     lanes by DPP, then the four waves through LDS), W = V - e^L X,
+//     U = T' W, O = e^L Y + P U, and the state update.
+// All arithmetic in fp32.
+#include "w4a8_dev.h"
+#include "w4a8_host.h"
+
+namespace w4a8 {
+
+namespace {
+
+constexpr int GC = 32;      // tokens per chunk
+constexpr int GNT = 256;    // threads per workgroup
+constexpr int DVS = 8;      // value columns per scan workgroup
+constexpr int MAT = GC * GC;
+
+inline size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct GdnArgs {
+  const float *q, *k, *v, *g, *beta, *s0;
+  float *out, *s_out;
+  float *tw, *pw, *lw;      // workspace: T' and P [NH][nch][C][C], L [NH][nch][C]
+  int64_t T, NH, DV;
+  int nch;
+};
+
+// Rows t0 .. t0 + 31 of head h of a [T][NH][D] tensor into LDS rows of
+// stride D + 4 (zero past T).
+template <int D>
+__device__ __forceinline__ void load_rows(float (*dst)[D + 4], const float *src, int64_t t0,
+                                          int64_t T, int64_t NH, int64_t h) {
+  constexpr int D4 = D / 4;
+  for (int idx = threadIdx.x; idx < GC * D4; idx += GNT) {
+    const int i = idx / D4, c4 = idx - i * D4;
+    const int64_t t = t0 + i;
+    float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (t < T) x = reinterpret_cast<const float4 *>(src)[(t * NH + h) * D4 + c4];
+    *reinterpret_cast<float4 *>(&dst[i][4 * c4]) = x;
+  }
+}
+
+// One chunk's inputs of a scan workgroup, loaded into registers while the
+// previous chunk is computed: rows of K and Q (KF float4 per thread), the
+// 32 x 16 slice of V, T' and P (4 values each) and L.
+template <int DK>
+struct ChunkRegs {
+  static constexpr int KF = GC * DK / 4 / GNT;
+  float4 k[KF], q[KF];
+  float v[GC * DVS / GNT], tp[MAT / GNT], p[MAT / GNT], l;
+};
+
+template <int DK>
+__device__ __forceinline__ void chunk_load(const GdnArgs &a, int64_t h, int cb, int ch,
+                                           ChunkRegs<DK> &r) {
+  constexpr int D4 = DK / 4;
+  const int tid = threadIdx.x;
+  const int64_t t0 = (int64_t)ch * GC;
+#pragma unroll
+  for (int u = 0; u < ChunkRegs<DK>::KF; u++) {
+    const int idx = tid + u * GNT, i = idx / D4, c4 = idx - i * D4;
+    const int64_t t = t0 + i;
+    r.k[u] = r.q[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (t < a.T) {
+      r.k[u] = reinterpret_cast<const float4 *>(a.k)[(t * a.NH + h) * D4 + c4];
+      r.q[u] = reinterpret_cast<const float4 *>(a.q)[(t * a.NH + h) * D4 + c4];
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < GC * DVS / GNT; u++) {
+    const int idx = tid + u * GNT, i = idx / DVS, cc = idx - i * DVS;
+    const int64_t t = t0 + i;
+    r.v[u] = t < a.T ? a.v[(t * a.NH + h) * a.DV + cb + cc] : 0.0f;
+  }
+  const int64_t mat = (h * a.nch + ch) * MAT;
+#pragma unroll
+  for (int u = 0; u < MAT / GNT; u++) {
+    r.tp[u] = a.tw[mat + tid + u * GNT];
+    r.p[u] = a.pw[mat + tid + u * GNT];
+  }
+  r.l = tid < GC ? a.lw[(h * a.nch + ch) * GC + tid] : 0.0f;
+}
+
+template <int DK>
+__global__ __launch_bounds__(GNT) void gdn_prep_kernel(GdnArgs a) {
+  __shared__ __align__(16) float Ks[GC][DK + 4];
+  __shared__ __align__(16) float Qs[GC][DK + 4];
+  __shared__ float Am[GC][GC + 1];
+  __shared__ float Lc[GC], Bc[GC];
+  const int tid = threadIdx.x;
+  const int64_t h = blockIdx.x % a.NH;
+  const int ch = (int)(blockIdx.x / a.NH);
+  const int64_t t0 = (int64_t)ch * GC;
+  load_rows<DK>(Ks, a.k, t0, a.T, a.NH, h);
+  load_rows<DK>(Qs, a.q, t0, a.T, a.NH, h);
+  if (tid < GC) {
+    const int64_t t = t0 + tid;
+    Lc[tid] = t < a.T ? a.g[t * a.NH + h] : 0.0f;      // g, summed below
+    Bc[tid] = t < a.T ? a.beta[t * a.NH + h] : 0.0f;
+  }
+  __syncthreads();
+  if (tid == 0) {                                      // inclusive sums, in token order
+    float acc = 0.0f;
+    for (int i = 0; i < GC; i++) {
+      acc += Lc[i];
+      Lc[i] = acc;
+    }
+  }
+  __syncthreads();
+  // k_i.k_j and q_i.k_j for i = tid / 8, j = 4 (tid % 8) .. + 3
+  const int i = tid >> 3, j4 = (tid & 7) * 4;
+  float kk[4] = {0.f, 0.f, 0.f, 0.f}, qk[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int c = 0; c < DK; c += 4) {
+    const float4 ki = *reinterpret_cast<const float4 *>(&Ks[i][c]);
+    const float4 qi = *reinterpret_cast<const float4 *>(&Qs[i][c]);
+#pragma unroll
+    for (int jj = 0; jj < 4; jj++) {
+      const float4 kj = *reinterpret_cast<const float4 *>(&Ks[j4 + jj][c]);
+      kk[jj] = fmaf(ki.x, kj.x, fmaf(ki.y, kj.y, fmaf(ki.z, kj.z, fmaf(ki.w, kj.w, kk[jj]))));
+      qk[jj] = fmaf(qi.x, kj.x, fmaf(qi.y, kj.y, fmaf(qi.z, kj.z, fmaf(qi.w, kj.w, qk[jj]))));
+    }
+  }
+  const int64_t mat = ((int64_t)h * a.nch + ch) * MAT;
+#pragma unroll
+  for (int jj = 0; jj < 4; jj++) {
+    const int j = j4 + jj;
+    const float d = j <= i ? expf(Lc[i] - Lc[j]) : 0.0f;
+    Am[i][j] = j < i ? Bc[i] * d * kk[jj] : 0.0f;
+    a.pw[mat + i * GC + j] = d * qk[jj];
+  }
+  if (tid < GC) a.lw[((int64_t)h * a.nch + ch) * GC + tid] = Lc[tid];
+  __syncthreads();
+  // column j of (I + A)^{-1}: m_ij = -sum_{l=j}^{i-1} A_il m_lj (i > j), m_jj = 1
+  // (rows above j are zero, so the sum may start at l = 0; both loops are
+  // unrolled so the column stays in registers)
+  if (tid < GC) {
+    const int j = tid;
+    float m[GC];
+#pragma unroll
+    for (int r = 0; r < GC; r++) {
+      float acc = r == j ? 1.0f : 0.0f;
+#pragma unroll
+      for (int l = 0; l < r; l++) acc = fmaf(-Am[r][l], m[l], acc);
+      m[r] = r >= j ? acc : 0.0f;
+    }
+    const float bj = Bc[j];
+#pragma unroll
+    for (int r = 0; r < GC; r++) a.tw[mat + r * GC + j] = m[r] * bj;
+  }
+}
+
+template <int DK>
+__global__ __launch_bounds__(GNT) void gdn_scan_kernel(GdnArgs a) {
+  constexpr int LPC = 64 / DVS;          // lanes of a wave per column (row groups in a wave)
+  constexpr int RG = GNT / DVS;          // row groups
+  constexpr int RPT = DK / RG;           // state rows per thread
+  static_assert(RPT % 2 == 0 && LPC == 8, "row groups of the scan");
+  __shared__ __align__(16) float Ks[GC][DK + 4];
+  // Q's rows until Y is formed, then the waves' partial sums
+  __shared__ __align__(16) union {
+    float Qs[GC][DK + 4];
+    float red[GNT / 64][2][GC][DVS];
+  } QR;
+  __shared__ float Tp[GC][GC + 1], Ps[GC][GC + 1];
+  __shared__ float Vs[GC][DVS + 1], Us[GC][DVS + 1], Ug[GC][DVS + 1], Ws[GC][DVS + 1];
+  __shared__ float Lc[GC];
+  auto &Qs = QR.Qs;
+  auto &red = QR.red;
+  const int tid = threadIdx.x;
+  const int nsl = (int)(a.DV / DVS);
+  const int64_t h = blockIdx.x / nsl;
+  const int cb = (int)(blockIdx.x % nsl) * DVS;
+  // lane l of wave w: column l / 8, row group 8 w + l % 8, so the row groups
+  // of a column in a wave are 8 neighbouring lanes (DPP reductions)
+  const int wave = tid >> 6, part = tid & (LPC - 1);
+  const int c = (tid >> 3) & (DVS - 1), rg = LPC * wave + part;
+  const int r0 = rg * RPT;
+  float S[RPT];
+#pragma unroll
+  for (int m = 0; m < RPT; m++)
+    S[m] = a.s0 ? a.s0[(h * DK + r0 + m) * a.DV + cb + c] : 0.0f;
+  // the (i, column) output of the small products
+  const int oi = tid / DVS, oc = tid % DVS;
+
+  ChunkRegs<DK> nx;
+  if (a.nch > 0) chunk_load<DK>(a, h, cb, 0, nx);
+  for (int ch = 0; ch < a.nch; ch++) {
+    const int64_t t0 = (int64_t)ch * GC;
+    {
+      constexpr int D4 = DK / 4;
+#pragma unroll
+      for (int u = 0; u < ChunkRegs<DK>::KF; u++) {
+        const int idx = tid + u * GNT, i = idx / D4, c4 = idx - i * D4;
+        *reinterpret_cast<float4 *>(&Ks[i][4 * c4]) = nx.k[u];
+        *reinterpret_cast<float4 *>(&Qs[i][4 * c4]) = nx.q[u];
+      }
+#pragma unroll
+      for (int u = 0; u < GC * DVS / GNT; u++) {
+        const int idx = tid + u * GNT;
+        Vs[idx / DVS][idx % DVS] = nx.v[u];
+      }
+#pragma unroll
+      for (int u = 0; u < MAT / GNT; u++) {
+        const int idx = tid + u * GNT;
+        Tp[idx >> 5][idx & 31] = nx.tp[u];
+        Ps[idx >> 5][idx & 31] = nx.p[u];
+      }
+      if (tid < GC) Lc[tid] = nx.l;
+    }
+    __syncthreads();
+    // the next chunk's inputs stream in while this one is computed
+    if (ch + 1 < a.nch) chunk_load<DK>(a, h, cb, ch + 1, nx);
+
+    // X = K S and Y = Q S: this thread's rows, then the wave's 8 row groups
+    // of each column (DPP), then the four waves (LDS)
+    float xp[GC], yp[GC];
+#pragma unroll
+    for (int i = 0; i < GC; i++) {
+      float xs = 0.0f, ys = 0.0f;
+#pragma unroll
+      for (int m = 0; m < RPT; m += 2) {
+        const float2 kv = *reinterpret_cast<const float2 *>(&Ks[i][r0 + m]);
+        const float2 qv = *reinterpret_cast<const float2 *>(&Qs[i][r0 + m]);
+        xs = fmaf(kv.x, S[m], fmaf(kv.y, S[m + 1], xs));
+        ys = fmaf(qv.x, S[m], fmaf(qv.y, S[m + 1], ys));
+      }
+      xp[i] = sum8(xs);
+      yp[i] = sum8(ys);
+    }
+    __syncthreads();                       // Q's rows are read by every wave
+#pragma unroll
+    for (int i = 0; i < GC; i++) {
+      if ((i >> 2) == part) {              // lane part of the 8 writes i = 4 part .. + 3
+        red[wave][0][i][c] = xp[i];
+        red[wave][1][i][c] = yp[i];
+      }
+    }
+    __syncthreads();
+    // W = V - e^L X; the output's first term e^L Y stays in a register
+    float yt;
+    {
+      const float eL = expf(Lc[oi]);
+      float x = 0.0f, y = 0.0f;
+#pragma unroll
+      for (int w = 0; w < GNT / 64; w++) {
+        x += red[w][0][oi][oc];
+        y += red[w][1][oi][oc];
+      }
+      Ws[oi][oc] = Vs[oi][oc] - eL * x;
+      yt = eL * y;
+    }
+    __syncthreads();
+    // U = T' W (T' lower triangular), and e^{L_C - L_i} U for the state
+    {
+      float u = 0.0f;
+#pragma unroll
+      for (int j = 0; j < GC; j++) u = fmaf(Tp[oi][j], Ws[j][oc], u);   // zero above the diagonal
+      Us[oi][oc] = u;
+      Ug[oi][oc] = expf(Lc[GC - 1] - Lc[oi]) * u;
+    }
+    __syncthreads();
+    // O = e^L Y + P U
+    {
+      float o = yt;
+#pragma unroll
+      for (int j = 0; j < GC; j++) o = fmaf(Ps[oi][j], Us[j][oc], o);     // zero above the diagonal
+      const int64_t t = t0 + oi;
+      if (t < a.T) a.out[(t * a.NH + h) * a.DV + cb + oc] = o;
+    }
+    // S <- e^{L_C} S + K^T Ug
+    {
+      const float eC = expf(Lc[GC - 1]);
+#pragma unroll
+      for (int m = 0; m < RPT; m++) S[m] *= eC;
+#pragma unroll 4
+      for (int i = 0; i < GC; i++) {
+        const float ug = Ug[i][c];
+#pragma unroll
+        for (int m = 0; m < RPT; m += 2) {
+          const float2 kv = *reinterpret_cast<const float2 *>(&Ks[i][r0 + m]);
+          S[m] = fmaf(kv.x, ug, S[m]);
+          S[m + 1] = fmaf(kv.y, ug, S[m + 1]);
+        }
+      }
+    }
+    __syncthreads();                       // the chunk's LDS is reloaded next
+  }
+  if (a.s_out) {
+#pragma unroll
+    for (int m = 0; m < RPT; m++) a.s_out[(h * DK + r0 + m) * a.DV + cb + c] = S[m];
+  }
+}
+
+int gdn_validate(int64_t T, int64_t NH, int64_t DK, int64_t DV) {
+  if (T < 0 || NH <= 0 || DV <= 0 || DV % DVS != 0 || (DK != 64 && DK != 128)) return W4A8_ESHAPE;
+  if (T >= ((int64_t)1 << 31) || NH >= (1 << 16) || DV > 4096) return W4A8_ERANGE;
+  const int64_t nch = (T + GC - 1) / GC;
+  if (nch * NH >= ((int64_t)1 << 31) || T * NH * (DK > DV ? DK : DV) >= ((int64_t)1 << 40))
+    return W4A8_ERANGE;
+  return W4A8_OK;
+}
+
+}  // namespace
+
+}  // namespace w4a8
+
+using namespace w4a8;
+
+extern "C" size_t gdn_workspace_size(int64_t T, int64_t NH, int64_t DK, int64_t DV) {
+  if (gdn_validate(T, NH, DK, DV) != W4A8_OK) return 0;
+  const int64_t nch = (T + GC - 1) / GC;
+  return 2 * up256(sizeof(float) * (size_t)(NH * nch) * MAT) +
+         up256(sizeof(float) * (size_t)(NH * nch) * GC) + 256;
+}
+
+extern "C" int gdn_chunked_scan(const float *q, const float *k, const float *v, const float *g,
+                                const float *beta, const float *s0, float *out, float *s_out,
+                                int64_t T, int64_t NH, int64_t DK, int64_t DV, void *workspace,
+                                size_t ws_bytes, void *stream) {
+  int rc = gdn_validate(T, NH, DK, DV);
+  if (rc != W4A8_OK) return rc;
+  if (T == 0 && !s_out) return W4A8_OK;
+  if (!q || !k || !v || !g || !beta || !out || !workspace) return W4A8_ENULL;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) || !aligned16(s0) ||
+      !aligned16(s_out) || !aligned16(workspace) || (reinterpret_cast<uintptr_t>(g) & 3) ||
+      (reinterpret_cast<uintptr_t>(beta) & 3))
+    return W4A8_EALIGN;
+  if (ws_bytes < gdn_workspace_size(T, NH, DK, DV)) return W4A8_EWORKSPACE;
+  if ((rc = check_device()) != W4A8_OK) return rc;
+  hipStream_t s = as_stream(stream);
+  const int64_t nch = (T + GC - 1) / GC;
+  uint8_t *ws = reinterpret_cast<uint8_t *>(workspace);
+  GdnArgs a{};
+  a.q = q; a.k = k; a.v = v; a.g = g; a.beta = beta; a.s0 = s0;
+  a.out = out; a.s_out = s_out;
+  a.tw = reinterpret_cast<float *>(ws);
+  a.pw = reinterpret_cast<float *>(ws + up256(sizeof(float) * (size_t)(NH * nch) * MAT));
+  a.lw = reinterpret_cast<float *>(ws + 2 * up256(sizeof(float) * (size_t)(NH * nch) * MAT));
+  a.T = T; a.NH = NH; a.DV = DV; a.nch = (int)nch;
+  if (nch > 0) {
+    if (DK == 128)
+      gdn_prep_kernel<128><<<dim3((unsigned)(NH * nch)), dim3(GNT), 0, s>>>(a);
+    else
+      gdn_prep_kernel<64><<<dim3((unsigned)(NH * nch)), dim3(GNT), 0, s>>>(a);
+    if ((rc = check_launch()) != W4A8_OK) return rc;
+  }
+  const unsigned nwg = (unsigned)(NH * (DV / DVS));
+  if (DK == 128)
+    gdn_scan_kernel<128><<<dim3(nwg), dim3(GNT), 0, s>>>(a);
+  else
+    gdn_scan_kernel<64><<<dim3(nwg), dim3(GNT), 0, s>>>(a);
+  return check_launch();
+}

@@ -122,6 +122,28 @@ def test_moe_sym_argument_errors():
     assert F(*ok, 0, 2048, 512, 256, 8, p[8], n, None) == w4.OK                  # empty
 
 
+def test_gdn_argument_errors():
+    L = w4.lib()
+    S = L.gdn_workspace_size
+    assert S(947, 32, 128, 128) > 0 and S(0, 32, 128, 128) > 0
+    assert S(8, 2, 96, 128) == 0 and S(8, 2, 128, 36) == 0 and S(8, 0, 128, 128) == 0
+    assert S(8, 2, 128, 8192) == 0 and S(-1, 2, 128, 128) == 0
+    n = S(40, 2, 128, 64)
+    p = [_fake(A + 0x10000 * i) for i in range(9)]
+    F = L.gdn_chunked_scan
+    ok = lambda **kw: [kw.get(name, p[i]) for i, name in enumerate(
+        ("q", "k", "v", "g", "beta", "s0", "out", "s_out"))]
+    assert F(*ok(q=None), 40, 2, 128, 64, p[8], n, None) == w4.ENULL
+    assert F(*ok(beta=None), 40, 2, 128, 64, p[8], n, None) == w4.ENULL
+    assert F(*ok(), 40, 2, 128, 64, None, n, None) == w4.ENULL
+    assert F(*ok(), 40, 2, 96, 64, p[8], n, None) == w4.ESHAPE
+    assert F(*ok(), 40, 2, 128, 64, p[8], n - 1, None) == w4.EWORKSPACE
+    assert F(*ok(v=_fake(A + 0x20008)), 40, 2, 128, 64, p[8], n, None) == w4.EALIGN
+    assert F(*ok(g=_fake(A + 0x30002)), 40, 2, 128, 64, p[8], n, None) == w4.EALIGN
+    assert F(None, None, None, None, None, None, None, None, 0, 2, 128, 64, None, 0,
+             None) == w4.OK                                               # empty, no state out
+
+
 def test_moe_workspace_size_and_layout():
     assert w4.moe_workspace_size(1, 2048, 512, 256, 8) > 0
     assert w4.moe_workspace_size(1, 2000, 512, 256, 8) == 0          # H % 256
