@@ -905,6 +905,14 @@ def cpu_baseline(synth, seconds):
                                               "two layers timed, x20"}
         res[label] = r
     oracle.set_threads(n_all)
+    # the GDN recurrence's oracle (numpy fp64, one token at a time, all 32
+    # heads at once): a 64-token sample of the 947-token prompt, scaled
+    from oracle.gdn import gdn_recurrent
+    q, k, v, gate, beta, s0 = synth.gdn_inputs(g, 64, 32, 128, 128)
+    t, n = timed(lambda: gdn_recurrent(q, k, v, gate, beta, s0), 0.5)
+    res["gdn_recurrence_numpy"] = {"tokens_timed": 64, "tokens_per_s": round(64 / t, 1),
+                                   "ms_per_layer_947": round(947 / (64 / t) * 1e3, 1),
+                                   "extrapolated_from_sample": True}
     main = res["all_cores"]["decode_m1_throughput"]
     return {"value": main["GBps"], "unit": "GB/s", "cores": n_all, "kind": "oracle",
             "sample": f"{main['steps']} independent M=1 decode steps of the same layer shape "
