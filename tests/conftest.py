@@ -37,12 +37,17 @@ def pytest_terminal_summary(terminalreporter):
         return
     if not moe_check.STATS:
         return
+    # (the GDN and stack lines below are printed with the MoE checks)
     tr = terminalreporter
     tr.write_sep("-", "MoE-layer checks: Q8_0(h) flips / blocks, max |out - ref| / sum|terms|")
     for name, st in moe_check.STATS:
         tr.write_line(f"{st['flips']:4d} / {st['blocks']:6d}  {st['max_rel_err']:.2e}  {name}")
     import sys
-    stack = sys.modules.get("tests.test_gpu_stack")
-    for T, nl, rel in getattr(stack, "DRIFT", []):
-        tr.write_line(f"stack drift, {nl} layers, T = {T}: max over tokens of "
-                      f"|x_gpu - x_oracle|_2 / |x_oracle|_2 = {rel:.3g}")
+    for name, mod in list(sys.modules.items()):
+        if name.endswith("test_gpu_stack"):
+            for T, nl, rel in getattr(mod, "DRIFT", []):
+                tr.write_line(f"stack drift, {nl} layers, T = {T}: max over tokens of "
+                              f"|x_gpu - x_oracle|_2 / |x_oracle|_2 = {rel:.3g}")
+        if name.endswith("test_gpu_gdn"):
+            for case, eo, es in getattr(mod, "REL", []):
+                tr.write_line(f"gdn {case}: max error / bound: output {eo:.3g}, state {es:.3g}")
