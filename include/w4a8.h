@@ -199,7 +199,7 @@ int moe_sym_forward(const float *hidden, const int32_t *topk_ids, const float *t
  *   o_t = S_t^T q_t
  * computed as a chunked scan (chunks of 32 tokens: per-chunk triangular
  * solve and products in parallel, the chunks in order per head and group of
- * 8 value columns).  The layer's projections, short convolutions, q/k
+ * 8 value columns); up to 8 tokens (decode) step by step in one launch.  The layer's projections, short convolutions, q/k
  * normalization and output gate are the caller's.
  *   q, k [T][NH][DK], v and out [T][NH][DV], g (log decay, <= 0 in the
  *   model) and beta [T][NH], all fp32; s0 [NH][DK][DV] the state before the

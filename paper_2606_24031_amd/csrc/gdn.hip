@@ -11,7 +11,8 @@
 //   (I + A) U = diag(b) (V - diag(e^L) K S),  A_ij = b_i e^{L_i - L_j} k_i.k_j (j < i)
 //   O = diag(e^L) Q S + P U,                  P_ij = e^{L_i - L_j} q_i.k_j  (j <= i)
 //   S <- e^{L_C} S + K^T diag(e^{L_C - L}) U.
-// Two launches:
+// Up to 8 tokens (decode) one launch steps through the recurrence as
+// written (gdn_step).  Longer sequences take two launches:
 //   gdn_prep: per (head, chunk), in parallel: L, the dot products k.k and q.k,
 //     A and P, and T' = (I + A)^{-1} diag(b) by forward substitution (each
 //     column of the inverse depends only on itself: one lane per column);
@@ -33,6 +34,7 @@ constexpr int GC = 32;      // tokens per chunk
 constexpr int GNT = 256;    // threads per workgroup
 constexpr int DVS = 8;      // value columns per scan workgroup
 constexpr int MAT = GC * GC;
+constexpr int GDN_STEP_T = 8;   // up to this many tokens: the step kernel, no chunks
 
 inline size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
 
@@ -310,6 +312,69 @@ __global__ __launch_bounds__(GNT) void gdn_scan_kernel(GdnArgs a) {
   }
 }
 
+// A few tokens (decode) step by step, the recurrence as written: per token,
+// d = k^T S and o = S^T q reduced over the rows (8 neighbouring lanes by DPP,
+// the four waves through LDS), S <- a (S - b k d^T) + b k v^T in between.
+// Same thread layout as the scan (8 value columns per workgroup, DK/32 rows
+// per thread).
+template <int DK>
+__global__ __launch_bounds__(GNT) void gdn_step_kernel(GdnArgs a) {
+  constexpr int RPT = DK / (GNT / DVS);
+  __shared__ float red[2][GNT / 64][DVS];
+  const int tid = threadIdx.x;
+  const int nsl = (int)(a.DV / DVS);
+  const int64_t h = blockIdx.x / nsl;
+  const int cb = (int)(blockIdx.x % nsl) * DVS;
+  const int wave = tid >> 6, part = tid & 7;
+  const int c = (tid >> 3) & (DVS - 1), r0 = (8 * wave + part) * RPT;
+  float S[RPT];
+#pragma unroll
+  for (int m = 0; m < RPT; m++)
+    S[m] = a.s0 ? a.s0[(h * DK + r0 + m) * a.DV + cb + c] : 0.0f;
+  for (int64_t t = 0; t < a.T; t++) {
+    const int64_t tk = (t * a.NH + h) * DK + r0;
+    float kr[RPT], qr[RPT];
+#pragma unroll
+    for (int m = 0; m < RPT; m += 2) {
+      const float2 k2 = *reinterpret_cast<const float2 *>(a.k + tk + m);
+      const float2 q2 = *reinterpret_cast<const float2 *>(a.q + tk + m);
+      kr[m] = k2.x; kr[m + 1] = k2.y;
+      qr[m] = q2.x; qr[m + 1] = q2.y;
+    }
+    const float vc = a.v[(t * a.NH + h) * a.DV + cb + c];
+    const float al = expf(a.g[t * a.NH + h]), be = a.beta[t * a.NH + h];
+    float dp = 0.0f;
+#pragma unroll
+    for (int m = 0; m < RPT; m++) dp = fmaf(kr[m], S[m], dp);
+    dp = sum8(dp);
+    if (part == 0) red[0][wave][c] = dp;
+    __syncthreads();
+    float d = 0.0f;
+#pragma unroll
+    for (int w = 0; w < GNT / 64; w++) d += red[0][w][c];
+    float op = 0.0f;
+#pragma unroll
+    for (int m = 0; m < RPT; m++) {
+      S[m] = al * (S[m] - be * kr[m] * d) + be * kr[m] * vc;
+      op = fmaf(qr[m], S[m], op);
+    }
+    op = sum8(op);
+    if (part == 0) red[1][wave][c] = op;
+    __syncthreads();
+    if (tid < DVS) {
+      float o = 0.0f;
+#pragma unroll
+      for (int w = 0; w < GNT / 64; w++) o += red[1][w][tid];
+      a.out[(t * a.NH + h) * a.DV + cb + tid] = o;
+    }
+    __syncthreads();                       // red is rewritten for the next token
+  }
+  if (a.s_out) {
+#pragma unroll
+    for (int m = 0; m < RPT; m++) a.s_out[(h * DK + r0 + m) * a.DV + cb + c] = S[m];
+  }
+}
+
 int gdn_validate(int64_t T, int64_t NH, int64_t DK, int64_t DV) {
   if (T < 0 || NH <= 0 || DV <= 0 || DV % DVS != 0 || (DK != 64 && DK != 128)) return W4A8_ESHAPE;
   if (T >= ((int64_t)1 << 31) || NH >= (1 << 16) || DV > 4096) return W4A8_ERANGE;
@@ -356,6 +421,14 @@ extern "C" int gdn_chunked_scan(const float *q, const float *k, const float *v, 
   a.pw = reinterpret_cast<float *>(ws + up256(sizeof(float) * (size_t)(NH * nch) * MAT));
   a.lw = reinterpret_cast<float *>(ws + 2 * up256(sizeof(float) * (size_t)(NH * nch) * MAT));
   a.T = T; a.NH = NH; a.DV = DV; a.nch = (int)nch;
+  const unsigned nwg = (unsigned)(NH * (DV / DVS));
+  if (T <= GDN_STEP_T) {                      // a few tokens: the recurrence step by step
+    if (DK == 128)
+      gdn_step_kernel<128><<<dim3(nwg), dim3(GNT), 0, s>>>(a);
+    else
+      gdn_step_kernel<64><<<dim3(nwg), dim3(GNT), 0, s>>>(a);
+    return check_launch();
+  }
   if (nch > 0) {
     if (DK == 128)
       gdn_prep_kernel<128><<<dim3((unsigned)(NH * nch)), dim3(GNT), 0, s>>>(a);
@@ -363,7 +436,6 @@ extern "C" int gdn_chunked_scan(const float *q, const float *k, const float *v, 
       gdn_prep_kernel<64><<<dim3((unsigned)(NH * nch)), dim3(GNT), 0, s>>>(a);
     if ((rc = check_launch()) != W4A8_OK) return rc;
   }
-  const unsigned nwg = (unsigned)(NH * (DV / DVS));
   if (DK == 128)
     gdn_scan_kernel<128><<<dim3(nwg), dim3(GNT), 0, s>>>(a);
   else

@@ -42,10 +42,12 @@ def check(q, k, v, g, beta, s0, o, s, case):
     assert es.max() <= 1.0, f"state error {es.max():.3g} of the bound"
 
 
-# T: one token, a ragged first chunk, exactly one chunk, one past it, several
-# chunks, the paper's 947-token prompt at its head shape (32 heads, 128 x 128)
+# T: one token and up to 8 (the step kernel), 9 (the smallest chunked case, a
+# ragged chunk), exactly one chunk, one past it, several chunks, the paper's
+# 947-token prompt at its head shape (32 heads, 128 x 128)
 @pytest.mark.parametrize("T,NH,DK,DV,state", [
-    (1, 1, 128, 128, True), (5, 3, 128, 32, False), (32, 2, 128, 128, True),
+    (1, 1, 128, 128, True), (5, 3, 128, 32, False), (8, 2, 128, 64, True),
+    (9, 2, 64, 32, True), (32, 2, 128, 128, True),
     (33, 2, 64, 48, True), (100, 4, 128, 128, True), (947, 32, 128, 128, True)])
 def test_gdn_matches_oracle(T, NH, DK, DV, state):
     g_ = synth.rng(1000 + T + NH)
