@@ -392,7 +392,9 @@ int rmsnorm_residual(const float *x, const float *y, const float *gamma, float *
  * progress never depends on the order in which workgroups start.  Process
  * wide: rounds >= 0 sets it, rounds < 0 leaves it; returns the previous
  * value.  Default 2000, or W4A8_DECODE_SPIN_ROUNDS when set in the
- * environment at the library's first use.
+ * environment at the library's first use.  (W4A8_DECODE_PREFETCH=0 there
+ * turns off the kernel's L2 prefetch of gate/up rows by the down workgroups:
+ * a timing aid, the results are the same.)
  */
 int w4a8_decode_wait_bound(int64_t rounds);
 

@@ -16,8 +16,10 @@
 //   The block dots run on the 4-bit dot products: activations are staged
 //   in a nibble-split form (see split_word) so that the Q4_0 payload dwords
 //   feed the dots as loaded, with no unpacking of the weight nibbles.
-//   down slabs (rb down rows, all pairs): issue the down weight loads of every
-//     pair first, collect every pair's Q8_0(h), take the dots and write
+//   down slabs (rb down rows, all pairs): first load into their XCD's L2 a
+//     share of the gate/up rows that the items on that XCD read last (see
+//     prefetch_gateup), then issue the down weight loads of every pair,
+//     collect every pair's Q8_0(h), take the dots and write
 //     out[n] = sum_q w_q y_q[n] (slots in order, then the shared expert) --
 //     the combine never leaves the workgroup.  The slabs fill the compute
 //     units the gate/up items leave free.
@@ -101,6 +103,7 @@ struct DecodeArgs {
   int H, I, E, k;
   int rb;                  // down rows per slab
   int spin_rounds;         // poll rounds before a slab computes h itself
+  int prefetch;            // down slabs first load the late gate/up rows (L2)
 };
 
 __device__ __forceinline__ bool pair_valid(const DecodeArgs &a, int q, int &expert) {
@@ -146,14 +149,68 @@ __device__ __forceinline__ float4 input4(const DecodeArgs &a, int t) {
   return v;
 }
 
+// The lane's first float4 of x, of resid and of gamma (norm mode), loaded
+// ahead of the weight loads: the first chunk of the input then needs no load
+// issued after them (loads retire in order, so waiting for one issued after
+// the weights would wait for the weights too).
+struct XFirst {
+  float4 x, r, g;
+};
+__device__ __forceinline__ XFirst issue_x_first(const DecodeArgs &a) {
+  const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+  XFirst f{z, z, z};
+  if ((int)threadIdx.x < a.H / 4) {
+    f.x = reinterpret_cast<const float4 *>(a.x)[threadIdx.x];
+    if (a.resid) f.r = reinterpret_cast<const float4 *>(a.resid)[threadIdx.x];
+    if (a.gamma) f.g = reinterpret_cast<const float4 *>(a.gamma)[threadIdx.x];
+  }
+  return f;
+}
+__device__ __forceinline__ float4 x_first(const DecodeArgs &a, const XFirst &f) {
+  float4 v = f.x;
+  if (a.resid) {
+    v.x += f.r.x; v.y += f.r.y; v.z += f.r.z; v.w += f.r.w;
+  }
+  return v;
+}
+
 // Q8_0 of the layer's input (x, or RMSNorm(x + resid) * gamma) into the LDS
 // staging; with `first_wg` also the 34-byte blocks to xq and, in norm mode,
 // x + resid to x_out and the normalized row to xn.  8 lanes per block, 4
-// values per lane.  `first` is the lane's first float4 of the input, loaded
-// by the caller ahead of the weight loads.  Every thread must call it.
-__device__ void quantize_x_to_lds(const DecodeArgs &a, ActBuf xb, bool first_wg, float4 first) {
+// values per lane.  `xf` holds the lane's first float4 of the inputs, loaded
+// by the caller ahead of the weight loads; for H <= 4 * NT nothing else is
+// loaded.  Every thread must call it.
+__device__ __forceinline__ void quantize_chunk(const DecodeArgs &a, ActBuf xb, bool first_wg,
+                                               int t, float4 f, float4 g, float r) {
+  const bool live = t < a.H / 4;  // H / 4 % 8 == 0: whole 8-lane groups agree
+  float v[4] = {0.f, 0.f, 0.f, 0.f};
+  if (live) {
+    if (a.gamma) {
+      if (first_wg) reinterpret_cast<float4 *>(a.x_out)[t] = f;
+      f = make_float4(f.x * r * g.x, f.y * r * g.y, f.z * r * g.z, f.w * r * g.w);
+      if (first_wg) reinterpret_cast<float4 *>(a.xn)[t] = f;
+    }
+    v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
+  }
+  uint32_t d16;
+  const uint32_t packed = q8_0_block8(v, d16);
+  const uint32_t word = split_word(packed, t & 7);
+  const int lsum = sum8(low_nibble_sum(packed));
+  if (live) {
+    const int blk = t >> 3, j = t & 7;
+    *code_word(xb, blk, j) = word;
+    if (j == 0) {
+      xb.d[blk] = f16_bits_to_f32(d16);
+      xb.corr[blk] = -8 * lsum;
+    }
+    if (first_wg) store_q8_0_block8(a.xq + blk * Q8B, j, packed, d16);
+  }
+}
+__device__ void quantize_x_to_lds(const DecodeArgs &a, ActBuf xb, bool first_wg,
+                                  const XFirst &xf) {
   __shared__ float wss[NT / 64];
   const int tasks = a.H / 4;
+  const float4 first = x_first(a, xf);
   float r = 1.0f;
   if (a.gamma) {
     // sum of squares in a fixed order: per thread in index order, a
@@ -181,33 +238,17 @@ __device__ void quantize_x_to_lds(const DecodeArgs &a, ActBuf xb, bool first_wg,
     for (int w = 0; w < NT / 64; w++) tot += wss[w];
     r = 1.0f / sqrtf(tot / (float)a.H + a.eps);
   }
-  for (int t0 = 0; t0 < tasks; t0 += NT) {
+  // the first chunk from registers, outside the loop: at the loop's head the
+  // compiler waits for every load in flight, the weights included
+  quantize_chunk(a, xb, first_wg, threadIdx.x, first, xf.g, r);
+  for (int t0 = NT; t0 < tasks; t0 += NT) {
     const int t = t0 + threadIdx.x;
-    const bool live = t < tasks;  // tasks % 8 == 0: whole 8-lane groups agree
-    float v[4] = {0.f, 0.f, 0.f, 0.f};
-    if (live) {
-      float4 f = t0 == 0 ? first : input4(a, t);
-      if (a.gamma) {
-        if (first_wg) reinterpret_cast<float4 *>(a.x_out)[t] = f;
-        const float4 g = reinterpret_cast<const float4 *>(a.gamma)[t];
-        f = make_float4(f.x * r * g.x, f.y * r * g.y, f.z * r * g.z, f.w * r * g.w);
-        if (first_wg) reinterpret_cast<float4 *>(a.xn)[t] = f;
-      }
-      v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
+    float4 f = make_float4(0.f, 0.f, 0.f, 0.f), g = f;
+    if (t < tasks) {
+      f = input4(a, t);
+      if (a.gamma) g = reinterpret_cast<const float4 *>(a.gamma)[t];
     }
-    uint32_t d16;
-    const uint32_t packed = q8_0_block8(v, d16);
-    const uint32_t word = split_word(packed, t & 7);
-    const int lsum = sum8(low_nibble_sum(packed));
-    if (live) {
-      const int blk = t >> 3, j = t & 7;
-      *code_word(xb, blk, j) = word;
-      if (j == 0) {
-        xb.d[blk] = f16_bits_to_f32(d16);
-        xb.corr[blk] = -8 * lsum;
-      }
-      if (first_wg) store_q8_0_block8(a.xq + blk * Q8B, j, packed, d16);
-    }
+    quantize_chunk(a, xb, first_wg, t, f, g, r);
   }
 }
 
@@ -287,29 +328,6 @@ __device__ void gateup_block(const DecodeArgs &a, int q, int e, int b, ActBuf xb
   }
 }
 
-__device__ __forceinline__ float4 load_x_first(const DecodeArgs &a) {
-  return (int)threadIdx.x < a.H / 4 ? input4(a, threadIdx.x) : make_float4(0.f, 0.f, 0.f, 0.f);
-}
-// The same in two halves: the loads of x and resid issued, the sum taken later.
-struct XFirst {
-  float4 x, r;
-};
-__device__ __forceinline__ XFirst issue_x_first(const DecodeArgs &a) {
-  XFirst f{make_float4(0.f, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f)};
-  if ((int)threadIdx.x < a.H / 4) {
-    f.x = reinterpret_cast<const float4 *>(a.x)[threadIdx.x];
-    if (a.resid) f.r = reinterpret_cast<const float4 *>(a.resid)[threadIdx.x];
-  }
-  return f;
-}
-__device__ __forceinline__ float4 x_first(const DecodeArgs &a, const XFirst &f) {
-  float4 v = f.x;
-  if (a.resid) {
-    v.x += f.r.x; v.y += f.r.y; v.z += f.r.z; v.w += f.r.w;
-  }
-  return v;
-}
-
 // Every workgroup arrives once; the last arrival of the launch advances the
 // call counter to `tag` and clears the arrival counters.  Each workgroup has
 // read the call counter before it arrives.
@@ -339,9 +357,9 @@ __device__ __forceinline__ void stage_word(ActBuf hb, int blk, int w, uint32_t v
 
 // Collect hand-off words [0, cnt) of the valid pairs into the staging (word
 // i is word i % XW of block i / XW); lane takes the words
-// threadIdx.x + j * NT, j < NWMAX.  Every wave polls its own words with two
-// rounds of loads in flight (a word seen twice is staged twice, with the same
-// value) and no barrier between rounds; a wave that passes the round bound
+// threadIdx.x + j * NT, j < NWMAX.  Every wave polls its own words, one
+// round of loads in flight (two in flight were slower: the doubled poll
+// traffic), with no barrier between rounds; a wave that passes the round bound
 // sets notdone[0].  One barrier at the end; returns false (uniformly) when
 // some wave passed the bound.  notdone[0] must be zero on entry.
 constexpr int NWMAX = 8;
@@ -475,6 +493,53 @@ __device__ __forceinline__ float dot8_dec(const W8Dec &w, const uint4 *__restric
   return acc;
 }
 
+// L2 prefetch by the down slabs.  A compute unit keeps only about 36 KB of
+// loads in flight, so a gate/up item (72 KB of weights for H = 2048) streams
+// in two rounds: waves 4..7 (h columns 16..31 of the block) can issue their
+// loads only once those of waves 0..3 have returned.  The down slabs need
+// their own weights only after every h block is in, so each first loads a
+// share of those late rows of the gate/up items on its own XCD (workgroup w
+// runs on XCD w % 8, and the compute units of one XCD share its L2): the
+// items' second round then hits in L2.  The late rows of an item form two
+// chunks of 16 consecutive rows (gate rows, then up rows); the C chunks on
+// XCD x go to its S slabs in even runs of whole chunks, at most PF_CH chunks
+// and PF_U 16-byte loads per lane and chunk.  Returns the values loaded (to
+// be waited for and dropped by the caller) in pf; false (uniformly) when the
+// slab has no chunk.
+constexpr int PF_CH = 3, PF_U = 3;
+__device__ __forceinline__ bool prefetch_gateup(const DecodeArgs &a, int wg, int nbh, int nb_h,
+                                                uint64_t vmask, int ev,
+                                                uint4 (&pf)[PF_CH][PF_U]) {
+  const int x = wg & 7;
+  const int nitems = nbh > x ? (nbh - x + 7) / 8 : 0;
+  const int first = nbh + ((x - nbh % 8) + 8) % 8;           // first slab on XCD x
+  const int nslabs = (int)gridDim.x > first ? ((int)gridDim.x - first + 7) / 8 : 0;
+  if (nitems == 0 || nslabs == 0) return false;
+  const int slab = (wg - first) / 8;
+  const int c0 = 2 * nitems * slab / nslabs, c1 = 2 * nitems * (slab + 1) / nslabs;
+  if (c1 <= c0) return false;
+  const int64_t rowbytes = (int64_t)(a.H / 32) * Q4B;
+  const int cu = (int)rowbytes;                               // 16-byte units per chunk
+#pragma unroll
+  for (int j = 0; j < PF_CH; j++) {
+    // chunk c0 + j (the last chunk again past c1), wave-uniform
+    const int c = min(c0 + j, c1 - 1);
+    const int item = x + 8 * (c >> 1);
+    const int q = item / nb_h, b = item - q * nb_h;
+    const int e = __builtin_amdgcn_readlane(ev, q);
+    const bool live = (vmask >> q) & 1;
+    const uint8_t *base = live ? expert_gu(a, e) + (((c & 1) ? a.I : 0) + b * 32 + 16) * rowbytes
+                               : reinterpret_cast<const uint8_t *>(a.x);
+    const int span = live ? cu : 1;
+#pragma unroll
+    for (int i = 0; i < PF_U; i++) {
+      const int u = min((int)threadIdx.x + i * NT, span - 1);
+      pf[j][i] = reinterpret_cast<const uint4 *>(base)[u];
+    }
+  }
+  return true;
+}
+
 // LDS: Q8_0(x) staging, then Q8_0(h) staging of every pair, then the
 // weighted per-pair sums [rb][k+1 padded to 4] and, when I > 512, the down
 // partials (NT floats).
@@ -504,10 +569,14 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
   float lx[RVX];
   float lg = 0.0f;
   if (RV > 0 && threadIdx.x < 64) route_issue<RVX>(a, lx, lg);
-  XFirst xf{make_float4(0.f, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f)};
-  if (wg < nbh) xf = issue_x_first(a);
+  const float4 z4 = make_float4(0.f, 0.f, 0.f, 0.f);
+  XFirst xf{z4, z4, z4};
+  uint32_t calls = 0;
+  if (wg < nbh) {
+    xf = issue_x_first(a);
+    calls = ld_agent(a.calls);   // in flight with x and the expert id
+  }
   if (RV > 0) route_finish<RVX>(a, lx, lg, rid, rw);
-  const float4 x0 = x_first(a, xf);
 
   if (wg < nbh) {
     // --------------------------------------------------- gate/up item
@@ -518,13 +587,15 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
     // together with them, since loads retire in order)
     int e;
     const bool valid = pair_valid(a, q, e);
-    const uint32_t tag = ld_agent(a.calls) + 1u;
-    asm volatile("" ::"v"(x0.x), "v"(x0.y), "v"(x0.z), "v"(x0.w), "v"(e), "v"(tag));
+    const uint32_t tag = calls + 1u;
+    asm volatile("" ::"v"(xf.x.x), "v"(xf.x.y), "v"(xf.x.z), "v"(xf.x.w), "v"(xf.r.x),
+                 "v"(xf.r.y), "v"(xf.r.z), "v"(xf.r.w), "v"(xf.g.x), "v"(xf.g.y), "v"(xf.g.z),
+                 "v"(xf.g.w), "v"(e), "v"(tag));
     W8 w0;
     const ARole r = a_role();
     if (valid && r.gg < a.H / 256) load_w8(a_row(a, e, b, r) + (int64_t)r.gg * (8 * Q4B), w0);
     if (valid || wg == 0) {
-      quantize_x_to_lds(a, xb, wg == 0, x0);
+      quantize_x_to_lds(a, xb, wg == 0, xf);
       __syncthreads();
     }
     if (valid) gateup_block<true>(a, q, e, b, xb, w0, hv, tag, nullptr);
@@ -546,16 +617,30 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
   // slot q) and the routing weights land before the weight loads are issued
   int ue = 0;
   const bool ulive = (int)threadIdx.x < units && un < a.H && pair_valid(a, uq, ue);
-  int ev;
+  int ev = 0;
   const int lq = threadIdx.x & 63;
   const bool lane_valid = lq < npairs && pair_valid(a, lq, ev);
   const float wl = (int)threadIdx.x < a.k ? a.topk_w[threadIdx.x]
                                            : (a.shared_w ? a.shared_w[0] : 1.0f);
   asm volatile("" ::"v"(ue), "v"((int)ulive), "v"((int)lane_valid), "v"(wl));
+  const uint64_t vmask = __ballot(lane_valid);    // wave-uniform
+  if (a.prefetch) {
+    uint4 pf[PF_CH][PF_U];
+    if (prefetch_gateup(a, wg, nbh, nb_h, vmask, ev, pf)) {
+      // the values are dropped (an empty asm that takes them keeps the
+      // loads); waiting for them here also holds the slab's own weight
+      // loads back until the gate/up rows are in
+      uint32_t sink = 0;
+#pragma unroll
+      for (int j = 0; j < PF_CH; j++)
+#pragma unroll
+        for (int i = 0; i < PF_U; i++) sink ^= pf[j][i].x ^ pf[j][i].y ^ pf[j][i].z ^ pf[j][i].w;
+      asm volatile("" ::"v"(sink));
+    }
+  }
   W8 wpre;
   if (ulive)
     load_w8(expert_d(a, ue) + un * ((int64_t)GI * 8 * Q4B) + (int64_t)ug * (8 * Q4B), wpre);
-  const uint64_t vmask = __ballot(lane_valid);    // wave-uniform
   if ((int)threadIdx.x < npairs) wq[threadIdx.x] = wl;
   const uint32_t tag = ld_agent(a.calls) + 1u;
   // a workgroup may arrive as soon as it has read the tag; here the atomic's
@@ -572,7 +657,7 @@ __global__ __launch_bounds__(NT) void decode_kernel(DecodeArgs a) {
   const bool ok = collect(a, hb, tag, XW * nbh, vmask, notdone);
   if (!ok) {
     // fallback: compute every pair's Q8_0(h) here (same code, same bytes)
-    quantize_x_to_lds(a, xb, false, load_x_first(a));
+    quantize_x_to_lds(a, xb, false, issue_x_first(a));
     __syncthreads();
     for (int q = 0; q < npairs; q++) {
       if (!((vmask >> q) & 1)) continue;
@@ -680,6 +765,15 @@ int spin_rounds() {
   return g_spin_rounds.load(std::memory_order_relaxed);
 }
 
+// L2 prefetch by the down slabs: off when W4A8_DECODE_PREFETCH is 0.
+int prefetch_on() {
+  static const int on = [] {
+    const char *env = std::getenv("W4A8_DECODE_PREFETCH");
+    return env == nullptr || std::atoi(env) != 0 ? 1 : 0;
+  }();
+  return on;
+}
+
 // Router in front of the launch: the logits of E experts fit wave 0's
 // registers.
 bool decode_routes(int64_t E, int64_t k) { return E <= 512 && k <= 32 && k <= E; }
@@ -726,6 +820,7 @@ int decode_forward(const float *x, const DecodeNorm &norm, const DecodeRoute *ro
   int grid = 0;
   decode_grid(H, I, k, ncu, grid, a.rb);
   a.spin_rounds = spin_rounds();
+  a.prefetch = prefetch_on();
   const size_t lds = lds_bytes((int)H, (int)I, (int)k, a.rb);
   if (route == nullptr)
     decode_kernel<0><<<dim3((unsigned)grid), dim3(NT), lds, s>>>(a);
