@@ -90,7 +90,8 @@ struct MLds {
     uint4 a[2][MT * 16];           // codes of 8 blocks, [buffer][row][chunk ^ row%16]
     float hv[MT][68];              // gate/up epilogue: h of the tile, [row][64 columns]
   };
-  float dx[2][8][MT];              // activation scales of 8 blocks, [buffer][block][row]
+  float2 dx[2][8][MT];             // activation scales of 8 blocks divided by 16, and
+                                   // their products with -1.5*2^23: [buffer][block][row]
   float dw[4][8][DWS];             // weight-row scales of the current group, [wave][block][row]
   int arow[MT];                    // activation row of each tile row
   int pair[MT];                    // pair of each tile row (-1: padding)
@@ -129,10 +130,15 @@ __device__ __forceinline__ void pair_ops(const HW &w, int j, v4i &b0, v4i &b1, u
 #pragma unroll
   for (int c = 0; c < 4; c++) {
     // q ^ 8 read as a signed 4-bit number is q - 8; placed in the high half
-    // of a byte it is the int8 16 * (q - 8)
-    const uint32_t x8 = hw_nib(w, j, c) ^ 0x88888888u;
-    const v2u r = __builtin_amdgcn_permlane32_swap((x8 << 4) & 0xF0F0F0F0u, x8 & 0xF0F0F0F0u,
-                                                   false, false);
+    // of a byte it is the int8 16 * (q - 8).  nib << 4 for the low nibbles
+    // comes from one funnel shift of the two dwords the payload straddles
+    // (the bits shifted in land in the masked low half of each byte)
+    const int i = j >> 1;
+    const uint32_t nib = hw_nib(w, j, c);
+    const uint32_t sh = (j & 1) == 0 ? __builtin_amdgcn_alignbit(w.D[9 * i + c + 1], w.D[9 * i + c], 12)
+                                     : nib << 4;
+    const v2u r = __builtin_amdgcn_permlane32_swap((sh ^ 0x80808080u) & 0xF0F0F0F0u,
+                                                   (nib ^ 0x88888888u) & 0xF0F0F0F0u, false, false);
     b0[c] = (int)r.x;
     b1[c] = (int)r.y;
   }
@@ -204,24 +210,28 @@ __device__ __forceinline__ void scale4(float acc[16], const v16f &f, int q, floa
   acc[4 * q + 3] = fmaf(fmaf(f[4 * q + 3], dx, nbx), dw4.w, acc[4 * q + 3]);
 }
 
+// A token's activation scale of one block (divided by 16) with its product
+// with -1.5*2^23, staged once per tile and group instead of formed per block.
+__device__ __forceinline__ float2 scale_pair(float dx) { return make_float2(dx, -BIASF * dx); }
+
 // One block: the weight operand b (32 weight rows) against both token
 // halves; dw points at the block's 32 weight-row scales of this wave, dxb
 // at the block's 64 activation scales.  The scales of four weight rows are
 // read once for both halves.
 template <bool TWO>
 __device__ __forceinline__ void block(float acc0[16], float acc1[16], const uint4 *abuf,
-                                      const float *dw, const float *dxb, int kk, v4i b, int r32,
+                                      const float *dw, const float2 *dxb, int kk, v4i b, int r32,
                                       int hh, v16i c0) {
   const v16f f0 = mm(b, aop(abuf, r32, kk, hh), c0);
   v16f f1;
   if (TWO) f1 = mm(b, aop(abuf, 32 + r32, kk, hh), c0);
-  const float dx0 = dxb[r32];
-  const float dx1 = TWO ? dxb[32 + r32] : 0.0f;
+  const float2 dx0 = dxb[r32];
+  const float2 dx1 = TWO ? dxb[32 + r32] : make_float2(0.0f, 0.0f);
 #pragma unroll
   for (int q = 0; q < 4; q++) {
     const float4 dw4 = *reinterpret_cast<const float4 *>(dw + 8 * q + 4 * hh);
-    scale4(acc0, f0, q, dx0, -BIASF * dx0, dw4);
-    if (TWO) scale4(acc1, f1, q, dx1, -BIASF * dx1, dw4);
+    scale4(acc0, f0, q, dx0.x, dx0.y, dw4);
+    if (TWO) scale4(acc1, f1, q, dx1.x, dx1.y, dw4);
   }
 }
 
@@ -262,8 +272,8 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
   if (resident) {
     for (int g = 0; g < G; g++) {
       stage_codes(a, L, g, g, TWO, wave, lane, nblk);
-      L.dx[g][dj][dm] = dlive * dsrc[8 * g];
-      L.dx[g][dj + 4][dm] = dlive * dsrc[8 * g + 4];
+      L.dx[g][dj][dm] = scale_pair(dlive * dsrc[8 * g]);
+      L.dx[g][dj + 4][dm] = scale_pair(dlive * dsrc[8 * g + 4]);
     }
   } else {
     stage_codes(a, L, 0, 0, TWO, wave, lane, nblk);
@@ -304,8 +314,8 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
     const int sj = j / G, g = j - sj * G;
     if (!resident) {
       // buffer g&1 was last read in group g - 2, before the previous barrier
-      L.dx[g & 1][dj][dm] = dlive * dx0;
-      L.dx[g & 1][dj + 4][dm] = dlive * dx1;
+      L.dx[g & 1][dj][dm] = scale_pair(dlive * dx0);
+      L.dx[g & 1][dj + 4][dm] = scale_pair(dlive * dx1);
     }
     if (!resident || j == 0) {
       __builtin_amdgcn_s_waitcnt(0);              // codes, scales and weights have landed
@@ -333,7 +343,7 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
     }
     __builtin_amdgcn_wave_barrier();
     const int buf = resident ? g : (g & 1);
-    const float(*dxb)[MT] = L.dx[buf];
+    const float2(*dxb)[MT] = L.dx[buf];
     const uint4 *abuf = L.a[buf];
 #pragma unroll
     for (int jj = 0; jj < 4; jj++) {
