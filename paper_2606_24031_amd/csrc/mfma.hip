@@ -218,18 +218,44 @@ __device__ __forceinline__ float2 scale_pair(float dx) { return make_float2(dx, 
 // halves; dw points at the block's 32 weight-row scales of this wave, dxb
 // at the block's 64 activation scales.  The scales of four weight rows are
 // read once for both halves.
-template <bool TWO>
-__device__ __forceinline__ void block(float acc0[16], float acc1[16], const uint4 *abuf,
-                                      const float *dw, const float2 *dxb, int kk, v4i b, int r32,
-                                      int hh, v16i c0) {
-  const v16f f0 = mm(b, aop(abuf, r32, kk, hh), c0);
+// The operands of one block read from LDS: the token codes of both halves,
+// the weight-row scales (four rows per float4) and the activation scales.
+// AHEAD: the scales too are read with the codes (else at their use, for the
+// short kernel's register budget).
+struct BlockIn {
+  v4i a0, a1;
+  float4 dw[4];
+  float2 dx0, dx1;
+  const float *dwp;
+  const float2 *dxp;
+};
+template <bool TWO, bool AHEAD>
+__device__ __forceinline__ BlockIn block_in(const uint4 *abuf, const float *dw, const float2 *dxb,
+                                            int kk, int r32, int hh) {
+  BlockIn o;
+  o.a0 = aop(abuf, r32, kk, hh);
+  o.a1 = TWO ? aop(abuf, 32 + r32, kk, hh) : v4i{0, 0, 0, 0};
+  o.dwp = dw + 4 * hh;
+  o.dxp = dxb;
+  if (AHEAD) {
+#pragma unroll
+    for (int q = 0; q < 4; q++) o.dw[q] = *reinterpret_cast<const float4 *>(dw + 8 * q + 4 * hh);
+    o.dx0 = dxb[r32];
+    o.dx1 = TWO ? dxb[32 + r32] : make_float2(0.0f, 0.0f);
+  }
+  return o;
+}
+template <bool TWO, bool AHEAD>
+__device__ __forceinline__ void block(float acc0[16], float acc1[16], const BlockIn &in, v4i b,
+                                      v16i c0, int r32) {
+  const v16f f0 = mm(b, in.a0, c0);
   v16f f1;
-  if (TWO) f1 = mm(b, aop(abuf, 32 + r32, kk, hh), c0);
-  const float2 dx0 = dxb[r32];
-  const float2 dx1 = TWO ? dxb[32 + r32] : make_float2(0.0f, 0.0f);
+  if (TWO) f1 = mm(b, in.a1, c0);
+  const float2 dx0 = AHEAD ? in.dx0 : in.dxp[r32];
+  const float2 dx1 = AHEAD ? in.dx1 : (TWO ? in.dxp[32 + r32] : make_float2(0.0f, 0.0f));
 #pragma unroll
   for (int q = 0; q < 4; q++) {
-    const float4 dw4 = *reinterpret_cast<const float4 *>(dw + 8 * q + 4 * hh);
+    const float4 dw4 = AHEAD ? in.dw[q] : *reinterpret_cast<const float4 *>(in.dwp + 8 * q);
     scale4(acc0, f0, q, dx0.x, dx0.y, dw4);
     if (TWO) scale4(acc1, f1, q, dx1.x, dx1.y, dw4);
   }
@@ -241,7 +267,7 @@ __device__ __forceinline__ void block(float acc0[16], float acc1[16], const uint
 // tile holds more than 32 rows (a compile-time branch: a run-time one inside
 // the block loop makes the compiler keep every block's second product until
 // the loop's end).
-template <bool GATEUP, bool TWO, bool RES>
+template <bool GATEUP, bool TWO, bool RES, bool SK>
 __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, int pos, int rows,
                                           int s0, int ns) {
   const int tid = threadIdx.x;
@@ -345,13 +371,21 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
     const int buf = resident ? g : (g & 1);
     const float2(*dxb)[MT] = L.dx[buf];
     const uint4 *abuf = L.a[buf];
+    // each block's LDS operands are read one block ahead of its products
+    // (order 0, 4, 1, 5, 2, 6, 3, 7)
+    BlockIn nx = block_in<TWO, !SK>(abuf, Lw, dxb[0], 0, r32, hh);
 #pragma unroll
     for (int jj = 0; jj < 4; jj++) {
       v4i b0, b1;
       uint32_t sd0, sd1;
       pair_ops(w, jj, b0, b1, sd0, sd1);
-      block<TWO>(acc0, acc1, abuf, Lw + jj * DWS, dxb[jj], jj, b0, r32, hh, c0);
-      block<TWO>(acc0, acc1, abuf, Lw + (jj + 4) * DWS, dxb[jj + 4], jj + 4, b1, r32, hh, c0);
+      BlockIn cur = nx;
+      nx = block_in<TWO, !SK>(abuf, Lw + (jj + 4) * DWS, dxb[jj + 4], jj + 4, r32, hh);
+      block<TWO, !SK>(acc0, acc1, cur, b0, c0, r32);
+      cur = nx;
+      if (jj + 1 < 4)
+        nx = block_in<TWO, !SK>(abuf, Lw + (jj + 1) * DWS, dxb[jj + 1], jj + 1, r32, hh);
+      block<TWO, !SK>(acc0, acc1, cur, b1, c0, r32);
     }
     if (g + 1 < G) return;
 
@@ -474,14 +508,14 @@ __device__ __forceinline__ void mfma_body(const MArgs &a, MLds &L) {
   const int ns = min(a.spw, nsl - s0);
   if (a.K <= 512) {
     if (!SHORT && rows > 32)
-      mfma_tile<GATEUP, true, true>(a, L, expert, pos, rows, s0, ns);
+      mfma_tile<GATEUP, true, true, SHORT>(a, L, expert, pos, rows, s0, ns);
     else
-      mfma_tile<GATEUP, false, true>(a, L, expert, pos, rows, s0, ns);
+      mfma_tile<GATEUP, false, true, SHORT>(a, L, expert, pos, rows, s0, ns);
   } else {
     if (!SHORT && rows > 32)
-      mfma_tile<GATEUP, true, false>(a, L, expert, pos, rows, s0, ns);
+      mfma_tile<GATEUP, true, false, SHORT>(a, L, expert, pos, rows, s0, ns);
     else
-      mfma_tile<GATEUP, false, false>(a, L, expert, pos, rows, s0, ns);
+      mfma_tile<GATEUP, false, false, SHORT>(a, L, expert, pos, rows, s0, ns);
   }
 }
 
