@@ -18,10 +18,10 @@
 //     column of the inverse depends only on itself: one lane per column);
 //   gdn_scan: per (head, 8 columns of the value dimension) -- the columns of
 //     S evolve independently -- the chunks in order, the workgroup's slice of
-//     S in registers (thread: one column, DK/32 consecutive rows): X = K S and
-//     Y = Q S from per-thread partials reduced over the rows (8 neighbouring
-//     lanes by DPP, then the four waves through LDS), W = V - e^L X,
-//     U = T' W, O = e^L Y + P U, and the state update.
+//     S in registers (thread: one column, DK/32 consecutive rows) and copied
+//     column-major to LDS at each chunk; one (token, column) per thread for
+//     X = K S and Y = Q S over all DK rows (no cross-lane reductions),
+//     W = V - e^L X, U = T' W and O = e^L Y + P U, then the state update.
 // All arithmetic in fp32.
 #include "w4a8_dev.h"
 #include "w4a8_host.h"
@@ -172,35 +172,39 @@ __global__ __launch_bounds__(GNT) void gdn_prep_kernel(GdnArgs a) {
 
 template <int DK>
 __global__ __launch_bounds__(GNT) void gdn_scan_kernel(GdnArgs a) {
-  constexpr int LPC = 64 / DVS;          // lanes of a wave per column (row groups in a wave)
-  constexpr int RG = GNT / DVS;          // row groups
+  constexpr int RG = GNT / DVS;          // row groups of the state
   constexpr int RPT = DK / RG;           // state rows per thread
-  static_assert(RPT % 2 == 0 && LPC == 8, "row groups of the scan");
-  __shared__ __align__(16) float Ks[GC][DK + 4];
-  // Q's rows until Y is formed, then the waves' partial sums
-  __shared__ __align__(16) union {
-    float Qs[GC][DK + 4];
-    float red[GNT / 64][2][GC][DVS];
-  } QR;
+  constexpr int DKP = DK + 4;            // LDS row stride (rows of 8 threads hit distinct banks)
+  static_assert(RPT % 2 == 0 && GC * DVS == GNT, "thread roles of the scan");
+  __shared__ __align__(16) float Ks[GC][DKP], Qs[GC][DKP];
+  __shared__ __align__(16) float St[DVS][DKP];       // the slice of S, column-major
   __shared__ float Tp[GC][GC + 1], Ps[GC][GC + 1];
-  __shared__ float Vs[GC][DVS + 1], Us[GC][DVS + 1], Ug[GC][DVS + 1], Ws[GC][DVS + 1];
+  __shared__ float Ws[GC][DVS + 1], Us[GC][DVS + 1], Ug[GC][DVS + 1];
   __shared__ float Lc[GC];
-  auto &Qs = QR.Qs;
-  auto &red = QR.red;
   const int tid = threadIdx.x;
   const int nsl = (int)(a.DV / DVS);
-  const int64_t h = blockIdx.x / nsl;
-  const int cb = (int)(blockIdx.x % nsl) * DVS;
-  // lane l of wave w: column l / 8, row group 8 w + l % 8, so the row groups
-  // of a column in a wave are 8 neighbouring lanes (DPP reductions)
-  const int wave = tid >> 6, part = tid & (LPC - 1);
-  const int c = (tid >> 3) & (DVS - 1), rg = LPC * wave + part;
-  const int r0 = rg * RPT;
+  // workgroup b runs on XCD b % 8: with NH a multiple of 8, all column
+  // slices of head h run on XCD h % 8, so each head's K, Q, T' and P come
+  // from HBM once and are shared in that XCD's L2
+  int64_t h;
+  int sl;
+  if (a.NH % 8 == 0) {
+    const int x = blockIdx.x % 8, slot = blockIdx.x / 8;
+    h = x + 8 * (slot / nsl);
+    sl = slot % nsl;
+  } else {
+    h = blockIdx.x / nsl;
+    sl = blockIdx.x % nsl;
+  }
+  const int cb = sl * DVS;
+  // state role: column sc, rows r0 .. r0 + RPT - 1 in registers
+  const int sc = (tid >> 3) & (DVS - 1), r0 = ((tid >> 6) * 8 + (tid & 7)) * RPT;
   float S[RPT];
 #pragma unroll
   for (int m = 0; m < RPT; m++)
-    S[m] = a.s0 ? a.s0[(h * DK + r0 + m) * a.DV + cb + c] : 0.0f;
-  // the (i, column) output of the small products
+    S[m] = a.s0 ? a.s0[(h * DK + r0 + m) * a.DV + cb + sc] : 0.0f;
+  // token role: token oi of the chunk, column oc (its value v_{oi,oc} is
+  // element tid of the chunk's V slice)
   const int oi = tid / DVS, oc = tid % DVS;
 
   ChunkRegs<DK> nx;
@@ -216,58 +220,36 @@ __global__ __launch_bounds__(GNT) void gdn_scan_kernel(GdnArgs a) {
         *reinterpret_cast<float4 *>(&Qs[i][4 * c4]) = nx.q[u];
       }
 #pragma unroll
-      for (int u = 0; u < GC * DVS / GNT; u++) {
-        const int idx = tid + u * GNT;
-        Vs[idx / DVS][idx % DVS] = nx.v[u];
-      }
-#pragma unroll
       for (int u = 0; u < MAT / GNT; u++) {
         const int idx = tid + u * GNT;
         Tp[idx >> 5][idx & 31] = nx.tp[u];
         Ps[idx >> 5][idx & 31] = nx.p[u];
       }
       if (tid < GC) Lc[tid] = nx.l;
+#pragma unroll
+      for (int m = 0; m < RPT; m += 2)
+        *reinterpret_cast<float2 *>(&St[sc][r0 + m]) = make_float2(S[m], S[m + 1]);
     }
+    const float vv = nx.v[0];
     __syncthreads();
     // the next chunk's inputs stream in while this one is computed
     if (ch + 1 < a.nch) chunk_load<DK>(a, h, cb, ch + 1, nx);
 
-    // X = K S and Y = Q S: this thread's rows, then the wave's 8 row groups
-    // of each column (DPP), then the four waves (LDS)
-    float xp[GC], yp[GC];
-#pragma unroll
-    for (int i = 0; i < GC; i++) {
-      float xs = 0.0f, ys = 0.0f;
-#pragma unroll
-      for (int m = 0; m < RPT; m += 2) {
-        const float2 kv = *reinterpret_cast<const float2 *>(&Ks[i][r0 + m]);
-        const float2 qv = *reinterpret_cast<const float2 *>(&Qs[i][r0 + m]);
-        xs = fmaf(kv.x, S[m], fmaf(kv.y, S[m + 1], xs));
-        ys = fmaf(qv.x, S[m], fmaf(qv.y, S[m + 1], ys));
-      }
-      xp[i] = sum8(xs);
-      yp[i] = sum8(ys);
-    }
-    __syncthreads();                       // Q's rows are read by every wave
-#pragma unroll
-    for (int i = 0; i < GC; i++) {
-      if ((i >> 2) == part) {              // lane part of the 8 writes i = 4 part .. + 3
-        red[wave][0][i][c] = xp[i];
-        red[wave][1][i][c] = yp[i];
-      }
-    }
-    __syncthreads();
-    // W = V - e^L X; the output's first term e^L Y stays in a register
+    // X = K S and Y = Q S, one (token, column) per thread over all DK rows;
+    // W = V - e^L X, and the output's first term e^L Y stays in a register
     float yt;
     {
-      const float eL = expf(Lc[oi]);
       float x = 0.0f, y = 0.0f;
-#pragma unroll
-      for (int w = 0; w < GNT / 64; w++) {
-        x += red[w][0][oi][oc];
-        y += red[w][1][oi][oc];
+#pragma unroll 8
+      for (int r = 0; r < DK; r += 4) {
+        const float4 kv = *reinterpret_cast<const float4 *>(&Ks[oi][r]);
+        const float4 qv = *reinterpret_cast<const float4 *>(&Qs[oi][r]);
+        const float4 sv = *reinterpret_cast<const float4 *>(&St[oc][r]);
+        x = fmaf(kv.x, sv.x, fmaf(kv.y, sv.y, fmaf(kv.z, sv.z, fmaf(kv.w, sv.w, x))));
+        y = fmaf(qv.x, sv.x, fmaf(qv.y, sv.y, fmaf(qv.z, sv.z, fmaf(qv.w, sv.w, y))));
       }
-      Ws[oi][oc] = Vs[oi][oc] - eL * x;
+      const float eL = expf(Lc[oi]);
+      Ws[oi][oc] = vv - eL * x;
       yt = eL * y;
     }
     __syncthreads();
@@ -295,7 +277,7 @@ __global__ __launch_bounds__(GNT) void gdn_scan_kernel(GdnArgs a) {
       for (int m = 0; m < RPT; m++) S[m] *= eC;
 #pragma unroll 4
       for (int i = 0; i < GC; i++) {
-        const float ug = Ug[i][c];
+        const float ug = Ug[i][sc];
 #pragma unroll
         for (int m = 0; m < RPT; m += 2) {
           const float2 kv = *reinterpret_cast<const float2 *>(&Ks[i][r0 + m]);
@@ -304,11 +286,11 @@ __global__ __launch_bounds__(GNT) void gdn_scan_kernel(GdnArgs a) {
         }
       }
     }
-    __syncthreads();                       // the chunk's LDS is reloaded next
+    __syncthreads();                       // the chunk's LDS is rewritten next
   }
   if (a.s_out) {
 #pragma unroll
-    for (int m = 0; m < RPT; m++) a.s_out[(h * DK + r0 + m) * a.DV + cb + c] = S[m];
+    for (int m = 0; m < RPT; m++) a.s_out[(h * DK + r0 + m) * a.DV + cb + sc] = S[m];
   }
 }
 
