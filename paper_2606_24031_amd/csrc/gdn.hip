@@ -106,7 +106,7 @@ template <int DK>
 __global__ __launch_bounds__(GNT) void gdn_prep_kernel(GdnArgs a) {
   __shared__ __align__(16) float Ks[GC][DK + 4];
   __shared__ __align__(16) float Qs[GC][DK + 4];
-  __shared__ float Am[GC][GC + 1];
+  __shared__ float Am[GC][GC + 1], Pm[GC][GC + 1];
   __shared__ float Lc[GC], Bc[GC];
   const int tid = threadIdx.x;
   const int64_t h = blockIdx.x % a.NH;
@@ -147,7 +147,7 @@ __global__ __launch_bounds__(GNT) void gdn_prep_kernel(GdnArgs a) {
     const int j = j4 + jj;
     const float d = j <= i ? expf(Lc[i] - Lc[j]) : 0.0f;
     Am[i][j] = j < i ? Bc[i] * d * kk[jj] : 0.0f;
-    a.pw[mat + i * GC + j] = d * qk[jj];
+    Pm[i][j] = d * qk[jj];
   }
   if (tid < GC) a.lw[((int64_t)h * a.nch + ch) * GC + tid] = Lc[tid];
   __syncthreads();
@@ -166,7 +166,19 @@ __global__ __launch_bounds__(GNT) void gdn_prep_kernel(GdnArgs a) {
     }
     const float bj = Bc[j];
 #pragma unroll
-    for (int r = 0; r < GC; r++) a.tw[mat + r * GC + j] = m[r] * bj;
+    for (int r = 0; r < GC; r++) {
+      m[r] *= bj;
+      a.tw[mat + r * GC + j] = m[r];
+    }
+    // column j of P T' (both lower triangular): the scan forms the output's
+    // second term P U = (P T') W from W directly
+#pragma unroll
+    for (int r = 0; r < GC; r++) {
+      float acc = 0.0f;
+#pragma unroll
+      for (int l = 0; l <= r; l++) acc = fmaf(Pm[r][l], m[l], acc);
+      a.pw[mat + r * GC + j] = acc;
+    }
   }
 }
 
@@ -176,10 +188,12 @@ __global__ __launch_bounds__(GNT) void gdn_scan_kernel(GdnArgs a) {
   constexpr int RPT = DK / RG;           // state rows per thread
   constexpr int DKP = DK + 4;            // LDS row stride (rows of 8 threads hit distinct banks)
   static_assert(RPT % 2 == 0 && GC * DVS == GNT, "thread roles of the scan");
-  __shared__ __align__(16) float Ks[GC][DKP], Qs[GC][DKP];
+  // K in two buffers: the next chunk's rows are written while the state
+  // update still reads this chunk's
+  __shared__ __align__(16) float Ks[2][GC][DKP], Qs[GC][DKP];
   __shared__ __align__(16) float St[DVS][DKP];       // the slice of S, column-major
-  __shared__ float Tp[GC][GC + 1], Ps[GC][GC + 1];
-  __shared__ float Ws[GC][DVS + 1], Us[GC][DVS + 1], Ug[GC][DVS + 1];
+  __shared__ float Tp[GC][GC + 1], PT[GC][GC + 1];   // T' and P T'
+  __shared__ float Ws[GC][DVS + 1], Ug[GC][DVS + 1];
   __shared__ float Lc[GC];
   const int tid = threadIdx.x;
   const int nsl = (int)(a.DV / DVS);
@@ -211,19 +225,20 @@ __global__ __launch_bounds__(GNT) void gdn_scan_kernel(GdnArgs a) {
   if (a.nch > 0) chunk_load<DK>(a, h, cb, 0, nx);
   for (int ch = 0; ch < a.nch; ch++) {
     const int64_t t0 = (int64_t)ch * GC;
+    float(*const Kb)[DKP] = Ks[ch & 1];
     {
       constexpr int D4 = DK / 4;
 #pragma unroll
       for (int u = 0; u < ChunkRegs<DK>::KF; u++) {
         const int idx = tid + u * GNT, i = idx / D4, c4 = idx - i * D4;
-        *reinterpret_cast<float4 *>(&Ks[i][4 * c4]) = nx.k[u];
+        *reinterpret_cast<float4 *>(&Kb[i][4 * c4]) = nx.k[u];
         *reinterpret_cast<float4 *>(&Qs[i][4 * c4]) = nx.q[u];
       }
 #pragma unroll
       for (int u = 0; u < MAT / GNT; u++) {
         const int idx = tid + u * GNT;
         Tp[idx >> 5][idx & 31] = nx.tp[u];
-        Ps[idx >> 5][idx & 31] = nx.p[u];
+        PT[idx >> 5][idx & 31] = nx.p[u];
       }
       if (tid < GC) Lc[tid] = nx.l;
 #pragma unroll
@@ -242,7 +257,7 @@ __global__ __launch_bounds__(GNT) void gdn_scan_kernel(GdnArgs a) {
       float x = 0.0f, y = 0.0f;
 #pragma unroll 8
       for (int r = 0; r < DK; r += 4) {
-        const float4 kv = *reinterpret_cast<const float4 *>(&Ks[oi][r]);
+        const float4 kv = *reinterpret_cast<const float4 *>(&Kb[oi][r]);
         const float4 qv = *reinterpret_cast<const float4 *>(&Qs[oi][r]);
         const float4 sv = *reinterpret_cast<const float4 *>(&St[oc][r]);
         x = fmaf(kv.x, sv.x, fmaf(kv.y, sv.y, fmaf(kv.z, sv.z, fmaf(kv.w, sv.w, x))));
@@ -253,26 +268,25 @@ __global__ __launch_bounds__(GNT) void gdn_scan_kernel(GdnArgs a) {
       yt = eL * y;
     }
     __syncthreads();
-    // U = T' W (T' lower triangular), and e^{L_C - L_i} U for the state
+    // U = T' W (T' lower triangular) and e^{L_C - L_i} U for the state;
+    // O = e^L Y + P U = e^L Y + (P T') W
+    const float eC = expf(Lc[GC - 1]);
     {
-      float u = 0.0f;
+      float u = 0.0f, o = yt;
 #pragma unroll
-      for (int j = 0; j < GC; j++) u = fmaf(Tp[oi][j], Ws[j][oc], u);   // zero above the diagonal
-      Us[oi][oc] = u;
+      for (int j = 0; j < GC; j++) {
+        const float w = Ws[j][oc];
+        u = fmaf(Tp[oi][j], w, u);           // zero above the diagonal
+        o = fmaf(PT[oi][j], w, o);
+      }
       Ug[oi][oc] = expf(Lc[GC - 1] - Lc[oi]) * u;
-    }
-    __syncthreads();
-    // O = e^L Y + P U
-    {
-      float o = yt;
-#pragma unroll
-      for (int j = 0; j < GC; j++) o = fmaf(Ps[oi][j], Us[j][oc], o);     // zero above the diagonal
       const int64_t t = t0 + oi;
       if (t < a.T) a.out[(t * a.NH + h) * a.DV + cb + oc] = o;
     }
-    // S <- e^{L_C} S + K^T Ug
+    __syncthreads();
+    // S <- e^{L_C} S + K^T Ug (this chunk's K stays in its buffer while the
+    // next chunk's inputs go to the other one)
     {
-      const float eC = expf(Lc[GC - 1]);
 #pragma unroll
       for (int m = 0; m < RPT; m++) S[m] *= eC;
 #pragma unroll 4
@@ -280,13 +294,12 @@ __global__ __launch_bounds__(GNT) void gdn_scan_kernel(GdnArgs a) {
         const float ug = Ug[i][sc];
 #pragma unroll
         for (int m = 0; m < RPT; m += 2) {
-          const float2 kv = *reinterpret_cast<const float2 *>(&Ks[i][r0 + m]);
+          const float2 kv = *reinterpret_cast<const float2 *>(&Kb[i][r0 + m]);
           S[m] = fmaf(kv.x, ug, S[m]);
           S[m + 1] = fmaf(kv.y, ug, S[m + 1]);
         }
       }
     }
-    __syncthreads();                       // the chunk's LDS is rewritten next
   }
   if (a.s_out) {
 #pragma unroll
