@@ -38,6 +38,8 @@ constexpr int GDN_STEP_T = 8;   // up to this many tokens: the step kernel, no c
 
 inline size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+typedef float v4f __attribute__((ext_vector_type(4)));
+
 struct GdnArgs {
   const float *q, *k, *v, *g, *beta, *s0;
   float *out, *s_out;
@@ -192,9 +194,14 @@ __global__ __launch_bounds__(GNT) void gdn_scan_kernel(GdnArgs a) {
   // update still reads this chunk's
   __shared__ __align__(16) float Ks[2][GC][DKP], Qs[GC][DKP];
   __shared__ __align__(16) float St[DVS][DKP];       // the slice of S, column-major
-  __shared__ float Tp[GC][GC + 1], PT[GC][GC + 1];   // T' and P T'
-  __shared__ float Ws[GC][DVS + 1], Ug[GC][DVS + 1];
-  __shared__ float Lc[GC];
+  // rows of T' and P T', and the columns of W and of e^{L_C - L} U, padded
+  // to 36 floats: 16-byte reads, and the 8 rows a wave reads at once fall
+  // in distinct banks
+  constexpr int MP = GC + 4;
+  __shared__ __align__(16) float Tp[GC][MP], PT[GC][MP];
+  __shared__ __align__(16) float Wt[DVS][MP], Ugt[DVS][MP], Yt[DVS][MP];
+  __shared__ float Vs[GC][DVS + 1];
+  __shared__ float Lc[GC], eLs[GC];
   const int tid = threadIdx.x;
   const int nsl = (int)(a.DV / DVS);
   // workgroup b runs on XCD b % 8: with NH a multiple of 8, all column
@@ -240,46 +247,65 @@ __global__ __launch_bounds__(GNT) void gdn_scan_kernel(GdnArgs a) {
         Tp[idx >> 5][idx & 31] = nx.tp[u];
         PT[idx >> 5][idx & 31] = nx.p[u];
       }
-      if (tid < GC) Lc[tid] = nx.l;
+      if (tid < GC) {
+        Lc[tid] = nx.l;
+        eLs[tid] = expf(nx.l);
+      }
+      Vs[oi][oc] = nx.v[0];
 #pragma unroll
       for (int m = 0; m < RPT; m += 2)
         *reinterpret_cast<float2 *>(&St[sc][r0 + m]) = make_float2(S[m], S[m + 1]);
     }
-    const float vv = nx.v[0];
     __syncthreads();
     // the next chunk's inputs stream in while this one is computed
     if (ch + 1 < a.nch) chunk_load<DK>(a, h, cb, ch + 1, nx);
 
-    // X = K S and Y = Q S, one (token, column) per thread over all DK rows;
-    // W = V - e^L X, and the output's first term e^L Y stays in a register
-    float yt;
+    // X = K S (waves 0, 1: tokens 0..15, 16..31) and Y = Q S (waves 2, 3)
+    // on fp32 matrix products of 16 x 16 x 4 (value columns 8..15 of the
+    // product are zero padding); lane group g = lane / 16 feeds the four k
+    // of each step, taken as 4 consecutive rows per 4 steps so each operand
+    // is one 16-byte LDS read per 4 products.  Then W = V - e^L X and e^L Y
+    // into LDS by column.
     {
-      float x = 0.0f, y = 0.0f;
-#pragma unroll 8
-      for (int r = 0; r < DK; r += 4) {
-        const float4 kv = *reinterpret_cast<const float4 *>(&Kb[oi][r]);
-        const float4 qv = *reinterpret_cast<const float4 *>(&Qs[oi][r]);
-        const float4 sv = *reinterpret_cast<const float4 *>(&St[oc][r]);
-        x = fmaf(kv.x, sv.x, fmaf(kv.y, sv.y, fmaf(kv.z, sv.z, fmaf(kv.w, sv.w, x))));
-        y = fmaf(qv.x, sv.x, fmaf(qv.y, sv.y, fmaf(qv.z, sv.z, fmaf(qv.w, sv.w, y))));
+      const int wave = tid >> 6, lane = tid & 63, n = lane & 15, gq = lane >> 4;
+      const float(*A)[DKP] = wave < 2 ? Kb : Qs;
+      const int arow = 16 * (wave & 1) + n;
+      v4f acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+      for (int kb = 0; kb < DK; kb += 16) {
+        const float4 av = *reinterpret_cast<const float4 *>(&A[arow][kb + 4 * gq]);
+        const float4 bv = n < DVS ? *reinterpret_cast<const float4 *>(&St[n][kb + 4 * gq])
+                                  : make_float4(0.f, 0.f, 0.f, 0.f);
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, bv.x, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, bv.y, acc1, 0, 0, 0);
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, bv.z, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, bv.w, acc1, 0, 0, 0);
       }
-      const float eL = expf(Lc[oi]);
-      Ws[oi][oc] = vv - eL * x;
-      yt = eL * y;
+      if (n < DVS) {
+#pragma unroll
+        for (int e = 0; e < 4; e++) {
+          const int tk = 16 * (wave & 1) + 4 * gq + e;
+          const float d = acc0[e] + acc1[e];
+          if (wave < 2) Wt[n][tk] = Vs[tk][n] - eLs[tk] * d;
+          else Yt[n][tk] = eLs[tk] * d;
+        }
+      }
     }
     __syncthreads();
     // U = T' W (T' lower triangular) and e^{L_C - L_i} U for the state;
     // O = e^L Y + P U = e^L Y + (P T') W
     const float eC = expf(Lc[GC - 1]);
     {
-      float u = 0.0f, o = yt;
+      float u = 0.0f, o = Yt[oc][oi];
 #pragma unroll
-      for (int j = 0; j < GC; j++) {
-        const float w = Ws[j][oc];
-        u = fmaf(Tp[oi][j], w, u);           // zero above the diagonal
-        o = fmaf(PT[oi][j], w, o);
+      for (int j = 0; j < GC; j += 4) {      // zero above the diagonal
+        const float4 w = *reinterpret_cast<const float4 *>(&Wt[oc][j]);
+        const float4 t = *reinterpret_cast<const float4 *>(&Tp[oi][j]);
+        const float4 pt = *reinterpret_cast<const float4 *>(&PT[oi][j]);
+        u = fmaf(t.w, w.w, fmaf(t.z, w.z, fmaf(t.y, w.y, fmaf(t.x, w.x, u))));
+        o = fmaf(pt.w, w.w, fmaf(pt.z, w.z, fmaf(pt.y, w.y, fmaf(pt.x, w.x, o))));
       }
-      Ug[oi][oc] = expf(Lc[GC - 1] - Lc[oi]) * u;
+      Ugt[oc][oi] = expf(Lc[GC - 1] - Lc[oi]) * u;
       const int64_t t = t0 + oi;
       if (t < a.T) a.out[(t * a.NH + h) * a.DV + cb + oc] = o;
     }
@@ -289,14 +315,18 @@ __global__ __launch_bounds__(GNT) void gdn_scan_kernel(GdnArgs a) {
     {
 #pragma unroll
       for (int m = 0; m < RPT; m++) S[m] *= eC;
-#pragma unroll 4
-      for (int i = 0; i < GC; i++) {
-        const float ug = Ug[i][sc];
+#pragma unroll 2
+      for (int i = 0; i < GC; i += 4) {
+        const float4 ug = *reinterpret_cast<const float4 *>(&Ugt[sc][i]);
+        const float u4[4] = {ug.x, ug.y, ug.z, ug.w};
 #pragma unroll
-        for (int m = 0; m < RPT; m += 2) {
-          const float2 kv = *reinterpret_cast<const float2 *>(&Kb[i][r0 + m]);
-          S[m] = fmaf(kv.x, ug, S[m]);
-          S[m + 1] = fmaf(kv.y, ug, S[m + 1]);
+        for (int ii = 0; ii < 4; ii++) {
+#pragma unroll
+          for (int m = 0; m < RPT; m += 2) {
+            const float2 kv = *reinterpret_cast<const float2 *>(&Kb[i + ii][r0 + m]);
+            S[m] = fmaf(kv.x, u4[ii], S[m]);
+            S[m + 1] = fmaf(kv.y, u4[ii], S[m + 1]);
+          }
         }
       }
     }
