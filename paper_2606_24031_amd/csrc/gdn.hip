@@ -186,10 +186,8 @@ __global__ __launch_bounds__(GNT) void gdn_prep_kernel(GdnArgs a) {
 
 template <int DK>
 __global__ __launch_bounds__(GNT) void gdn_scan_kernel(GdnArgs a) {
-  constexpr int RG = GNT / DVS;          // row groups of the state
-  constexpr int RPT = DK / RG;           // state rows per thread
   constexpr int DKP = DK + 4;            // LDS row stride (rows of 8 threads hit distinct banks)
-  static_assert(RPT % 2 == 0 && GC * DVS == GNT, "thread roles of the scan");
+  static_assert(DK % 64 == 0 && GC * DVS == GNT && GC == 32 && DVS <= 16, "roles of the scan");
   // K in two buffers: the next chunk's rows are written while the state
   // update still reads this chunk's
   __shared__ __align__(16) float Ks[2][GC][DKP], Qs[GC][DKP];
@@ -218,12 +216,20 @@ __global__ __launch_bounds__(GNT) void gdn_scan_kernel(GdnArgs a) {
     sl = blockIdx.x % nsl;
   }
   const int cb = sl * DVS;
-  // state role: column sc, rows r0 .. r0 + RPT - 1 in registers
-  const int sc = (tid >> 3) & (DVS - 1), r0 = ((tid >> 6) * 8 + (tid & 7)) * RPT;
-  float S[RPT];
+  // state: the slice S (DK x 8) as TPW 16 x 16 product tiles per wave
+  // (columns 8..15 zero padding): lane l of wave w holds rows
+  // 16 (TPW w + t) + 4 (l / 16) + e, e = 0..3, of column l % 16
+  constexpr int TPW = DK / 64;
+  const int wave = tid >> 6, lane = tid & 63, n = lane & 15, gq = lane >> 4;
+  v4f S[TPW];
 #pragma unroll
-  for (int m = 0; m < RPT; m++)
-    S[m] = a.s0 ? a.s0[(h * DK + r0 + m) * a.DV + cb + sc] : 0.0f;
+  for (int t = 0; t < TPW; t++) {
+#pragma unroll
+    for (int e = 0; e < 4; e++) {
+      const int row = 16 * (TPW * wave + t) + 4 * gq + e;
+      S[t][e] = a.s0 && n < DVS ? a.s0[(h * DK + row) * a.DV + cb + n] : 0.0f;
+    }
+  }
   // token role: token oi of the chunk, column oc (its value v_{oi,oc} is
   // element tid of the chunk's V slice)
   const int oi = tid / DVS, oc = tid % DVS;
@@ -252,9 +258,12 @@ __global__ __launch_bounds__(GNT) void gdn_scan_kernel(GdnArgs a) {
         eLs[tid] = expf(nx.l);
       }
       Vs[oi][oc] = nx.v[0];
+      if (n < DVS) {
 #pragma unroll
-      for (int m = 0; m < RPT; m += 2)
-        *reinterpret_cast<float2 *>(&St[sc][r0 + m]) = make_float2(S[m], S[m + 1]);
+        for (int t = 0; t < TPW; t++)
+          *reinterpret_cast<float4 *>(&St[n][16 * (TPW * wave + t) + 4 * gq]) =
+              make_float4(S[t][0], S[t][1], S[t][2], S[t][3]);
+      }
     }
     __syncthreads();
     // the next chunk's inputs stream in while this one is computed
@@ -267,7 +276,6 @@ __global__ __launch_bounds__(GNT) void gdn_scan_kernel(GdnArgs a) {
     // is one 16-byte LDS read per 4 products.  Then W = V - e^L X and e^L Y
     // into LDS by column.
     {
-      const int wave = tid >> 6, lane = tid & 63, n = lane & 15, gq = lane >> 4;
       const float(*A)[DKP] = wave < 2 ? Kb : Qs;
       const int arow = 16 * (wave & 1) + n;
       v4f acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
@@ -310,30 +318,34 @@ __global__ __launch_bounds__(GNT) void gdn_scan_kernel(GdnArgs a) {
       if (t < a.T) a.out[(t * a.NH + h) * a.DV + cb + oc] = o;
     }
     __syncthreads();
-    // S <- e^{L_C} S + K^T Ug (this chunk's K stays in its buffer while the
-    // next chunk's inputs go to the other one)
+    // S <- e^{L_C} S + K^T Ug on the same products: A = K^T (this lane's
+    // row of the tile, four tokens per four products), B = Ug by column
+    // (this chunk's K stays in its buffer while the next chunk's inputs go to
+    // the other one)
     {
 #pragma unroll
-      for (int m = 0; m < RPT; m++) S[m] *= eC;
-#pragma unroll 2
-      for (int i = 0; i < GC; i += 4) {
-        const float4 ug = *reinterpret_cast<const float4 *>(&Ugt[sc][i]);
-        const float u4[4] = {ug.x, ug.y, ug.z, ug.w};
+      for (int t = 0; t < TPW; t++) S[t] *= eC;
 #pragma unroll
-        for (int ii = 0; ii < 4; ii++) {
+      for (int kb = 0; kb < GC; kb += 16) {
+        const float4 bv = n < DVS ? *reinterpret_cast<const float4 *>(&Ugt[n][kb + 4 * gq])
+                                  : make_float4(0.f, 0.f, 0.f, 0.f);
+        const float b4[4] = {bv.x, bv.y, bv.z, bv.w};
 #pragma unroll
-          for (int m = 0; m < RPT; m += 2) {
-            const float2 kv = *reinterpret_cast<const float2 *>(&Kb[i + ii][r0 + m]);
-            S[m] = fmaf(kv.x, u4[ii], S[m]);
-            S[m + 1] = fmaf(kv.y, u4[ii], S[m + 1]);
-          }
+        for (int t = 0; t < TPW; t++) {
+          const int row = 16 * (TPW * wave + t) + n;
+#pragma unroll
+          for (int u = 0; u < 4; u++)
+            S[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(Kb[kb + 4 * gq + u][row], b4[u], S[t], 0, 0, 0);
         }
       }
     }
   }
-  if (a.s_out) {
+  if (a.s_out && n < DVS) {
 #pragma unroll
-    for (int m = 0; m < RPT; m++) a.s_out[(h * DK + r0 + m) * a.DV + cb + sc] = S[m];
+    for (int t = 0; t < TPW; t++)
+#pragma unroll
+      for (int e = 0; e < 4; e++)
+        a.s_out[(h * DK + 16 * (TPW * wave + t) + 4 * gq + e) * a.DV + cb + n] = S[t][e];
   }
 }
 
