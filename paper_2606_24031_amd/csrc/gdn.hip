@@ -234,9 +234,9 @@ __global__ __launch_bounds__(GNT) void gdn_scan_kernel(GdnArgs a) {
   // element tid of the chunk's V slice)
   const int oi = tid / DVS, oc = tid % DVS;
 
-  ChunkRegs<DK> nx;
-  if (a.nch > 0) chunk_load<DK>(a, h, cb, 0, nx);
-  for (int ch = 0; ch < a.nch; ch++) {
+  // chunk ch's inputs in nx, loaded two chunks ahead: once its values are
+  // in LDS, nx takes chunk ch + 2
+  auto chunk_step = [&](int ch, ChunkRegs<DK> &nx) {
     const int64_t t0 = (int64_t)ch * GC;
     float(*const Kb)[DKP] = Ks[ch & 1];
     {
@@ -267,7 +267,7 @@ __global__ __launch_bounds__(GNT) void gdn_scan_kernel(GdnArgs a) {
     }
     __syncthreads();
     // the next chunk's inputs stream in while this one is computed
-    if (ch + 1 < a.nch) chunk_load<DK>(a, h, cb, ch + 1, nx);
+    if (ch + 2 < a.nch) chunk_load<DK>(a, h, cb, ch + 2, nx);
 
     // X = K S (waves 0, 1: tokens 0..15, 16..31) and Y = Q S (waves 2, 3)
     // on fp32 matrix products of 16 x 16 x 4 (value columns 8..15 of the
@@ -339,6 +339,13 @@ __global__ __launch_bounds__(GNT) void gdn_scan_kernel(GdnArgs a) {
         }
       }
     }
+  };
+  ChunkRegs<DK> na, nb;
+  if (a.nch > 0) chunk_load<DK>(a, h, cb, 0, na);
+  if (a.nch > 1) chunk_load<DK>(a, h, cb, 1, nb);
+  for (int ch = 0; ch < a.nch; ch += 2) {
+    chunk_step(ch, na);
+    if (ch + 1 < a.nch) chunk_step(ch + 1, nb);
   }
   if (a.s_out && n < DVS) {
 #pragma unroll
