@@ -14,14 +14,19 @@
 // Up to 8 tokens (decode) one launch steps through the recurrence as
 // written (gdn_step).  Longer sequences take two launches:
 //   gdn_prep: per (head, chunk), in parallel: L, the dot products k.k and q.k,
-//     A and P, and T' = (I + A)^{-1} diag(b) by forward substitution (each
-//     column of the inverse depends only on itself: one lane per column);
+//     A and P, T' = (I + A)^{-1} diag(b) by forward substitution (each
+//     column of the inverse depends only on itself: one lane per column) and
+//     P T';
 //   gdn_scan: per (head, 8 columns of the value dimension) -- the columns of
-//     S evolve independently -- the chunks in order, the workgroup's slice of
-//     S in registers (thread: one column, DK/32 consecutive rows) and copied
-//     column-major to LDS at each chunk; one (token, column) per thread for
-//     X = K S and Y = Q S over all DK rows (no cross-lane reductions),
-//     W = V - e^L X, U = T' W and O = e^L Y + P U, then the state update.
+//     S evolve independently -- the chunks in order.  The workgroup's slice
+//     of S (DK x 8) stays in the accumulators of 16 x 16 x 4 fp32 matrix
+//     products and is copied column-major to LDS at each chunk; per chunk:
+//     X = K S and Y = Q S on those products (one wave per 16-token tile of K
+//     or of Q), W = V - e^L X, then per (token, column) thread U = T' W and
+//     O = e^L Y + (P T') W (P T' from gdn_prep), and the state update
+//     S <- e^{L_C} S + K^T (e^{L_C - L} U) on the products again.  All
+//     column slices of a head run on one XCD, so the head's inputs are
+//     fetched into that XCD's L2 once.
 // All arithmetic in fp32.
 #include "w4a8_dev.h"
 #include "w4a8_host.h"
@@ -43,7 +48,7 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 struct GdnArgs {
   const float *q, *k, *v, *g, *beta, *s0;
   float *out, *s_out;
-  float *tw, *pw, *lw;      // workspace: T' and P [NH][nch][C][C], L [NH][nch][C]
+  float *tw, *pw, *lw;      // workspace: T' and P T' [NH][nch][C][C], L [NH][nch][C]
   int64_t T, NH, DV;
   int nch;
 };
@@ -65,7 +70,7 @@ __device__ __forceinline__ void load_rows(float (*dst)[D + 4], const float *src,
 
 // One chunk's inputs of a scan workgroup, loaded into registers while the
 // previous chunk is computed: rows of K and Q (KF float4 per thread), the
-// 32 x 16 slice of V, T' and P (4 values each) and L.
+// 32 x 8 slice of V, T' and P T' (4 values each) and L.
 template <int DK>
 struct ChunkRegs {
   static constexpr int KF = GC * DK / 4 / GNT;
