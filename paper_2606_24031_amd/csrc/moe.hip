@@ -74,14 +74,11 @@ inline size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
 constexpr int SLICE = ROUTE_T;   // pairs per slice of the split route
 constexpr int RCH = 16;          // pairs a route thread keeps in registers
 
-// The route splits into per-slice ranks beside the quantization and one
-// finishing workgroup when there are several slices' worth of pairs, the
-// slice's per-chunk counts fit in LDS (16 x E ints) and so do the finishing
-// workgroup's per-(expert, slice) counts.
-inline bool split_route(int64_t Pr, int64_t E) {
-  const int64_t nslice = (Pr + SLICE - 1) / SLICE;
-  return Pr > 64 && Pr <= (int64_t)RCH * SLICE && E <= 1024 && E * nslice <= LDS_INTS;
-}
+// The route splits into slices of ROUTE_T pairs ranked beside the
+// quantization when a slice's per-chunk counts fit in LDS (16 x E ints); a
+// single slice finishes the route in its own workgroup, several in a
+// finishing launch of one workgroup per slice plus one for the lists.
+inline bool split_route(int64_t E) { return E <= 1024; }
 
 struct Layout {
   size_t meta, sync, xfer, perm, count, rank, hist, groups, tiles, chunks, xq, h, hq, y, xn, xs, hs,
@@ -214,8 +211,9 @@ struct RouteArgs {
   int4 *chunks;     // groups of at most ms rows, cut into chunks of SMALL_CHUNK
                     // rows: {expert, first sorted position, rows, group}, in
                     // reverse group order
-  int *hist_g;      // split route: per-(expert, slice) counts, expert-major [E][nseg]
+  int *hist_g;      // split route: per-(slice, expert) counts, slice-major [nseg][E]
   int T, k, E, has_shared, seg, nseg, ebits, ms;
+  int tpe;          // split route: threads per expert summing the slices' counts
   int stage;        // REG path: the permutation goes through LDS (it fits)
 };
 
@@ -242,14 +240,21 @@ __device__ __forceinline__ int chunk_rank(int e, int s, int *hist, const RouteAr
   return r;
 }
 
+__device__ void build_lists(const RouteArgs &a, const int *rows_l, int *start_l, int *gi_l,
+                            int *t0_l);
+
 // Split route, first part, in the quantizing launch: slice s of ROUTE_T
 // pairs, one 64-pair chunk per wave.  Each pair's rank among the earlier
 // pairs of its slice with the same expert: its rank in its chunk (wave
 // ballots) plus that expert's count in the slice's earlier chunks (a scan
 // over the 16 chunks per expert, in LDS); the slice's count of each expert
-// goes to the expert-major histogram hist_g[e][s], the ranks to `rank`.
+// goes to the slice-major histogram hist_g[s][e], the ranks to `rank`.
+// WHOLE: the slice is every pair (at most ROUTE_T), so the same workgroup
+// finishes the route: the counts are the groups' rows, the lists come from
+// them, and each pair's sorted position is its group's start plus its rank.
+template <bool WHOLE>
 __device__ void slice_ranks(const RouteArgs &a, int s) {
-  extern __shared__ int cnt[];   // [16 chunks][E]
+  extern __shared__ int cnt[];   // [16 chunks][E], later (WHOLE) the lists' 4 x (E + 1)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int Pr = a.T * a.k;
   for (int i = tid; i < 16 * a.E; i += ROUTE_T) cnt[i] = 0;
@@ -270,6 +275,7 @@ __device__ void slice_ranks(const RouteArgs &a, int s) {
   const int r = __popcll(peers & lt);
   if (e >= 0 && r == 0) cnt[wave * a.E + e] = __popcll(peers);   // the expert's first lane
   __syncthreads();
+  int own = 0;    // WHOLE: the count of expert tid (E <= ROUTE_T)
   for (int ee = tid; ee < a.E; ee += ROUTE_T) {
     int run = 0;
 #pragma unroll
@@ -278,13 +284,94 @@ __device__ void slice_ranks(const RouteArgs &a, int s) {
       cnt[w * a.E + ee] = run;
       run += c;
     }
-    a.hist_g[ee * a.nseg + s] = run;
+    if (WHOLE)
+      own = run;
+    else
+      a.hist_g[s * a.E + ee] = run;
   }
   __syncthreads();
-  if (e >= 0) a.rank[p] = cnt[wave * a.E + e] + r;
+  const int rk = e >= 0 ? cnt[wave * a.E + e] + r : 0;
+  if (!WHOLE) {
+    if (e >= 0) a.rank[p] = rk;
+    return;
+  }
+  __syncthreads();
+  const int n = a.E + 1;
+  int *rows_l = cnt, *start_l = cnt + n, *gi_l = cnt + 2 * n, *t0_l = cnt + 3 * n;
+  if (tid < a.E) rows_l[tid] = own;
+  if (tid == 0) rows_l[a.E] = a.has_shared ? a.T : 0;
+  __syncthreads();
+  build_lists(a, rows_l, start_l, gi_l, t0_l);
+  if (e >= 0) a.perm[start_l[e] + rk] = p;
+  if (a.has_shared && tid < a.T) a.perm[start_l[a.E] + tid] = Pr + tid;
 }
 
-// One workgroup.  Pairs are cut into segments of `seg` (a multiple of 64);
+// Experts per route thread: e = tid + j * ROUTE_T, j < EPT, covers E + 1 <=
+// EPT * ROUTE_T groups (the shared expert is group E) for E <= 4096.
+constexpr int EPT = 5;
+
+// The group lists.  gst[j], grw[j]: first sorted position and rows of group
+// e = tid + j * ROUTE_T (e <= E; the shared expert is group E, the last).
+// Writes the compacted list of non-empty groups (expert order); a group of at
+// most ms rows goes to the small-group list, a larger one gets its MFMA row
+// tiles: those of more than MC/2 rows (full cost) first, in expert order, then
+// the tiles of at most MC/2 rows (half cost), so each XCD can take an even
+// share of both kinds, the longer work first.  The small-chunk and short-tile
+// counts share one scanned word (low and high 16 bits: each total is at most
+// E + 1).  cnt3: 3 x (E + 1) ints of LDS.  Every thread of the workgroup
+// calls it.
+__device__ void group_lists(const RouteArgs &a, const int (&gst)[EPT], const int (&grw)[EPT],
+                            int *cnt3, int (*wtot)[ROUTE_T / 64 + 1], int nrouted) {
+  const int tid = threadIdx.x;
+  int *gflag = cnt3, *gtile = cnt3 + a.E + 1, *gsmall = gtile + a.E + 1;
+#pragma unroll
+  for (int j = 0; j < EPT; j++) {
+    const int e = tid + j * ROUTE_T, rows = grw[j];
+    if (e > a.E) break;
+    gflag[e] = rows > 0 ? 1 : 0;
+    const int rem = rows % MC;
+    const bool tiled = rows > a.ms;
+    gsmall[e] = ((rows > 0 && !tiled) ? (rows + SMALL_CHUNK - 1) / SMALL_CHUNK : 0) |
+                ((tiled && rem > 0 && rem <= MC / 2) ? 1 << 16 : 0);
+    gtile[e] = tiled ? rows / MC + (rem > MC / 2 ? 1 : 0) : 0;
+  }
+  __syncthreads();
+  int tot[3];
+  {
+    int *const arr[3] = {gflag, gtile, gsmall};
+    block_exscan<3>(arr, a.E + 1, wtot, tot);
+  }
+  const int ngroups = tot[0], nlong = tot[1], nsmall = tot[2] & 0xFFFF;
+  const int ntiles = nlong + (tot[2] >> 16);
+#pragma unroll
+  for (int j = 0; j < EPT; j++) {
+    const int e = tid + j * ROUTE_T, start_e = gst[j], rows = grw[j];
+    if (e > a.E) break;
+    if (rows == 0) continue;
+    const int gi = gflag[e], t0 = gtile[e];
+    a.groups[gi] = make_int4(e, start_e, rows, t0);
+    if (rows <= a.ms) {
+      // back to front: the shared expert (the largest group) comes first
+      for (int m0 = 0, c = gsmall[e] & 0xFFFF; m0 < rows; m0 += SMALL_CHUNK, c++)
+        a.chunks[nsmall - 1 - c] = make_int4(e, start_e + m0, min(SMALL_CHUNK, rows - m0), gi);
+    } else {
+      for (int m0 = 0, t = t0; m0 < rows; m0 += MC) {
+        const int r = min(MC, rows - m0);
+        a.tiles[r > MC / 2 ? t++ : nlong + (gsmall[e] >> 16)] = make_int4(e, start_e + m0, r, gi);
+      }
+    }
+  }
+  if (tid == 0) {
+    a.meta[META_NROUTED] = nrouted;
+    a.meta[META_NGROUPS] = ngroups;
+    a.meta[META_NTILES] = ntiles;
+    a.meta[META_NSMALL] = nsmall;
+    a.meta[META_NLONG] = nlong;
+  }
+}
+
+// The route in one workgroup, for expert counts above the split route's
+// (E > 1024).  Pairs are cut into segments of `seg` (a multiple of 64);
 // wave w owns segments w, w+16, ...  For every pair, its rank among the
 // earlier pairs of the same expert inside its segment comes from wave ballots;
 // the per-(expert, segment) counts, laid out expert-major, are then scanned
@@ -292,42 +379,27 @@ __device__ void slice_ranks(const RouteArgs &a, int s) {
 // base inside it.  The resulting order is stable in pair index.  MODE 1: every
 // wave's chunks fit in RCH registers, so the ids are loaded in one batch and
 // the ranks stay in registers until the scatter; MODE 0: the ranks go through
-// the workspace; MODE 2: the segments are the slices of slice_ranks, whose
-// ranks and counts the previous launch left in the workspace.
+// the workspace.
 template <int MODE>
 __device__ __forceinline__ void route_body(const RouteArgs &a) {
   constexpr bool REG = MODE == 1;
-  constexpr bool HELD = MODE != 0;   // the pairs' ids and ranks held in registers
   extern __shared__ int hist[];  // [E][nseg], later the group counters
   __shared__ int wtot[3][ROUTE_T / 64 + 1];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int Pr = a.T * a.k;
   const int L = a.E * a.nseg;
   const int cps = a.seg >> 6;    // chunks per segment
-  // register slot i: MODE 1, chunk i of this wave (segment wave + 16 (i / cps),
-  // its chunk i % cps); MODE 2, pair i * ROUTE_T + tid of slice i
+  // register slot i (MODE 1): chunk i of this wave, segment wave + 16 (i /
+  // cps), its chunk i % cps
   auto pair_of = [&](int i) {
-    if (MODE == 2) return i * ROUTE_T + tid;
     const int j = i / cps;
     return (wave + 16 * j) * a.seg + 64 * (i - j * cps) + lane;
   };
-  auto seg_of = [&](int i) { return MODE == 2 ? i : wave + 16 * (i / cps); };
+  auto seg_of = [&](int i) { return wave + 16 * (i / cps); };
   int er[RCH], rr[RCH];
-  if (MODE == 2) {
-    // every pair's id and slice rank in one batch, beside the counts
-#pragma unroll
-    for (int i = 0; i < RCH; i++) {
-      const int p = pair_of(i);
-      const bool live = p < Pr;
-      const int e = a.ids[live ? p : 0];
-      rr[i] = a.rank[live ? p : 0];
-      er[i] = (live && e >= 0 && e < a.E) ? e : -1;
-    }
-  }
-  for (int i = tid; i < L; i += ROUTE_T) hist[i] = MODE == 2 ? a.hist_g[i] : 0;
+  for (int i = tid; i < L; i += ROUTE_T) hist[i] = 0;
 
   if (REG) {
-    // chunk i of this wave: segment wave + 16 (i / cps), its chunk i % cps
 #pragma unroll
     for (int i = 0; i < RCH; i++) {
       const int j = i / cps, sg = wave + 16 * j;
@@ -345,7 +417,7 @@ __device__ __forceinline__ void route_body(const RouteArgs &a) {
       const int sg = wave + 16 * (i / cps);
       rr[i] = sg < a.nseg ? chunk_rank(er[i], sg, hist, a, lane) : 0;
     }
-  } else if (MODE == 0) {
+  } else {
     for (int sg = wave; sg < a.nseg; sg += ROUTE_T / 64) {
       const int end = (int)min((int64_t)(sg + 1) * a.seg, (int64_t)Pr);
       for (int base = sg * a.seg; base < end; base += 64) {
@@ -373,7 +445,7 @@ __device__ __forceinline__ void route_body(const RouteArgs &a) {
   // workspace, or (stage) through LDS so that the permutation leaves in
   // coalesced stores
   int dst[RCH];
-  if (HELD) {
+  if (REG) {
 #pragma unroll
     for (int i = 0; i < RCH; i++) {
       const int p = pair_of(i);
@@ -390,17 +462,8 @@ __device__ __forceinline__ void route_body(const RouteArgs &a) {
   if (a.has_shared && !a.stage)
     for (int t = tid; t < a.T; t += ROUTE_T) a.perm[nrouted + t] = Pr + t;
 
-  // counts, then the compacted list of non-empty groups (expert order); a
-  // group of at most ms rows goes to the small-group list, a larger one gets
-  // its MFMA row tiles: those of more than MC/2 rows (full cost) first, in
-  // expert order, then the tiles of at most MC/2 rows (half cost), so each
-  // XCD can take an even share of both kinds, the longer work first.  The
-  // small-chunk and short-tile counts share one scanned word (low and high
-  // 16 bits: each total is at most E + 1).  The shared expert is the last
-  // group.  Each
-  // thread keeps the start and size of its experts (e = tid + j*ROUTE_T) in
-  // registers, and the histogram's space then holds the three group counters.
-  constexpr int EPT = 5;         // (E + 1) <= EPT * ROUTE_T for E <= 4096
+  // Each thread keeps the start and size of its groups in registers, and
+  // the histogram's space then holds the three group counters.
   int gst[EPT], grw[EPT];
 #pragma unroll
   for (int j = 0; j < EPT; j++) {
@@ -416,7 +479,7 @@ __device__ __forceinline__ void route_body(const RouteArgs &a) {
     }
   }
   __syncthreads();
-  if (HELD && a.stage) {
+  if (REG && a.stage) {
 #pragma unroll
     for (int i = 0; i < RCH; i++)
       if (dst[i] >= 0) hist[dst[i]] = pair_of(i);
@@ -426,53 +489,191 @@ __device__ __forceinline__ void route_body(const RouteArgs &a) {
     const int ptot = nrouted + (a.has_shared ? a.T : 0);
     for (int i = tid; i < ptot; i += ROUTE_T) a.perm[i] = hist[i];
   }
-  int *gflag = hist + (a.stage ? Pr + a.T : 0);   // 3 x (E + 1) entries
-  int *gtile = gflag + a.E + 1;
-  int *gsmall = gtile + a.E + 1;
+  group_lists(a, gst, grw, hist + (a.stage ? Pr + a.T : 0), wtot, nrouted);
+}
+
+// Split route, second part: expert e's count over all slices (tot[e]) and
+// over the slices before s (pre[e], if pre is not null), from the slice-major
+// histogram; tpe consecutive threads per expert (a power of two dividing 64)
+// each sum every tpe-th slice, eight loads in flight at a time, and combine
+// with butterfly exchanges.  tot[E] = the shared expert's rows.  `between`
+// runs once the first eight loads are issued (a loop head would wait for
+// every load in flight, the caller's own included).  Every thread of the
+// workgroup calls it.
+template <typename F>
+__device__ void expert_sums(const RouteArgs &a, int s, int *tot, int *pre, F between) {
+  const int tid = threadIdx.x;
+  const int e = tid / a.tpe, sub = tid & (a.tpe - 1);
+  const int ec = e < a.E ? e : 0;     // threads past the experts read expert 0 and drop it
+  int t = 0, b = 0;
+  auto round = [&](int sg0, int (&v)[8]) {
 #pragma unroll
-  for (int j = 0; j < EPT; j++) {
-    const int e = tid + j * ROUTE_T, rows = grw[j];
-    if (e > a.E) break;
-    gflag[e] = rows > 0 ? 1 : 0;
-    const int rem = rows % MC;
-    const bool tiled = rows > a.ms;
-    gsmall[e] = ((rows > 0 && !tiled) ? (rows + SMALL_CHUNK - 1) / SMALL_CHUNK : 0) |
-                ((tiled && rem > 0 && rem <= MC / 2) ? 1 << 16 : 0);
-    gtile[e] = tiled ? rows / MC + (rem > MC / 2 ? 1 : 0) : 0;
-  }
-  __syncthreads();
-  int tot[3];
-  {
-    int *const arr[3] = {gflag, gtile, gsmall};
-    block_exscan<3>(arr, a.E + 1, wtot, tot);
-  }
-  const int ngroups = tot[0], nlong = tot[1], nsmall = tot[2] & 0xFFFF;
-  const int ntiles = nlong + (tot[2] >> 16);
+    for (int i = 0; i < 8; i++) v[i] = a.hist_g[min(sg0 + i * a.tpe, a.nseg - 1) * a.E + ec];
+  };
+  auto add = [&](int sg0, const int (&v)[8]) {
 #pragma unroll
-  for (int j = 0; j < EPT; j++) {
-    const int e = tid + j * ROUTE_T, start = gst[j], rows = grw[j];
-    if (e > a.E) break;
-    if (rows == 0) continue;
-    const int gi = gflag[e], t0 = gtile[e];
-    a.groups[gi] = make_int4(e, start, rows, t0);
-    if (rows <= a.ms) {
-      // back to front: the shared expert (the largest group) comes first
-      for (int m0 = 0, c = gsmall[e] & 0xFFFF; m0 < rows; m0 += SMALL_CHUNK, c++)
-        a.chunks[nsmall - 1 - c] = make_int4(e, start + m0, min(SMALL_CHUNK, rows - m0), gi);
-    } else {
-      for (int m0 = 0, t = t0; m0 < rows; m0 += MC) {
-        const int r = min(MC, rows - m0);
-        a.tiles[r > MC / 2 ? t++ : nlong + (gsmall[e] >> 16)] = make_int4(e, start + m0, r, gi);
+    for (int i = 0; i < 8; i++) {
+      const int sg = sg0 + i * a.tpe;
+      const int x = sg < a.nseg ? v[i] : 0;
+      t += x;
+      b += sg < s ? x : 0;
+    }
+  };
+  int v[8];
+  round(sub, v);
+  between();
+  add(sub, v);
+  for (int sg0 = sub + 8 * a.tpe; sg0 < a.nseg; sg0 += 8 * a.tpe) {
+    round(sg0, v);
+    add(sg0, v);
+  }
+  if (e >= a.E) t = b = 0;
+  for (int o = 1; o < a.tpe; o <<= 1) {
+    t += __shfl_xor(t, o);
+    b += __shfl_xor(b, o);
+  }
+  if (e < a.E && sub == 0) {
+    tot[e] = t;
+    if (pre) pre[e] = b;
+  }
+  if (tid == 0) tot[a.E] = a.has_shared ? a.T : 0;
+}
+
+// Exclusive scan of n ints of LDS in place by one whole wave: lane l sums its
+// contiguous run of ceil(n / 64) entries, the runs' sums are scanned across
+// the wave, and each lane rewrites its run.  Returns the total (every lane).
+__device__ int wave_exscan(int *v, int n) {
+  const int lane = threadIdx.x & 63;
+  const int per = (n + 63) / 64;
+  const int lo = min(lane * per, n), hi = min(lo + per, n);
+  int sum = 0;
+  for (int i = lo; i < hi; i++) sum += v[i];
+  const int incl = scan_incl<false>(sum);
+  int base = incl - sum;
+  for (int i = lo; i < hi; i++) { const int x = v[i]; v[i] = base; base += x; }
+  return __shfl(incl, 63);
+}
+
+// The group lists from the groups' rows rows_l[0..E] (LDS; the shared expert
+// is group E, the last), in the layout group_lists describes: wave 0 sums, per
+// lane, a contiguous run of groups' rows, list entries, full tiles, small
+// chunks and short tiles, scans the runs across the wave, and writes each
+// group's first sorted position (start_l), list index (gi_l) and first full
+// tile (t0_l) to LDS and its count, group, chunk and short-tile records; then
+// every thread writes full tiles, each finding its group by binary search over
+// t0_l.  Every thread of the workgroup calls it; start_l is valid on return.
+__device__ void build_lists(const RouteArgs &a, const int *rows_l, int *start_l, int *gi_l,
+                            int *t0_l) {
+  __shared__ int nlong_s;
+  const int tid = threadIdx.x;
+  const int n = a.E + 1;
+  if (tid < 64) {
+    // lane l: groups [l * per, (l + 1) * per), the per-group quantities of
+    // group_lists summed over the run, scanned across the wave, then each
+    // group's records written from its bases
+    const int lane = tid, per = (n + 63) / 64;
+    const int lo = min(lane * per, n), hi = min(lo + per, n);
+    int c[5] = {0, 0, 0, 0, 0};   // rows, groups, full tiles, small chunks, short tiles
+    for (int g = lo; g < hi; g++) {
+      const int rows = rows_l[g], rem = rows % MC;
+      const bool tiled = rows > a.ms;
+      c[0] += rows;
+      c[1] += rows > 0 ? 1 : 0;
+      c[2] += tiled ? rows / MC + (rem > MC / 2 ? 1 : 0) : 0;
+      c[3] += (rows > 0 && !tiled) ? (rows + SMALL_CHUNK - 1) / SMALL_CHUNK : 0;
+      c[4] += (tiled && rem > 0 && rem <= MC / 2) ? 1 : 0;
+    }
+    int base[5], tot5[5];
+#pragma unroll
+    for (int j = 0; j < 5; j++) {
+      const int incl = scan_incl<false>(c[j]);
+      base[j] = incl - c[j];
+      tot5[j] = __shfl(incl, 63);
+    }
+    const int nlong = tot5[2], nsmall = tot5[3];
+    for (int g = lo; g < hi; g++) {
+      const int rows = rows_l[g], rem = rows % MC;
+      const bool tiled = rows > a.ms;
+      const int start = base[0], gi = base[1], t0 = base[2];
+      start_l[g] = start;
+      gi_l[g] = gi;
+      t0_l[g] = t0;
+      if (g < a.E) a.count[g] = rows;
+      if (rows > 0) {
+        a.groups[gi] = make_int4(g, start, rows, t0);
+        if (!tiled) {
+          // back to front: the shared group (the largest) comes first
+          for (int m0 = 0, ch = base[3]; m0 < rows; m0 += SMALL_CHUNK, ch++)
+            a.chunks[nsmall - 1 - ch] = make_int4(g, start + m0, min(SMALL_CHUNK, rows - m0), gi);
+        } else if (rem > 0 && rem <= MC / 2) {
+          a.tiles[nlong + base[4]] = make_int4(g, start + rows - rem, rem, gi);
+        }
       }
+      base[0] += rows;
+      base[1] += rows > 0 ? 1 : 0;
+      base[2] += tiled ? rows / MC + (rem > MC / 2 ? 1 : 0) : 0;
+      base[3] += (rows > 0 && !tiled) ? (rows + SMALL_CHUNK - 1) / SMALL_CHUNK : 0;
+      base[4] += (tiled && rem > 0 && rem <= MC / 2) ? 1 : 0;
+    }
+    if (lane == 0) {
+      nlong_s = nlong;
+      a.meta[META_NROUTED] = tot5[0] - (a.has_shared ? a.T : 0);
+      a.meta[META_NGROUPS] = tot5[1];
+      a.meta[META_NTILES] = nlong + tot5[4];
+      a.meta[META_NSMALL] = nsmall;
+      a.meta[META_NLONG] = nlong;
     }
   }
-  if (tid == 0) {
-    a.meta[META_NROUTED] = nrouted;
-    a.meta[META_NGROUPS] = ngroups;
-    a.meta[META_NTILES] = ntiles;
-    a.meta[META_NSMALL] = nsmall;
-    a.meta[META_NLONG] = nlong;
+  __syncthreads();
+  // full tiles, one per thread: tile ti belongs to the last group whose
+  // first full tile is at most ti (binary search over the scanned counts)
+  const int nlong = nlong_s;
+  for (int ti = tid; ti < nlong; ti += ROUTE_T) {
+    int lo = 0, hi = a.E;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (t0_l[mid] <= ti) lo = mid; else hi = mid - 1;
+    }
+    const int m0 = (ti - t0_l[lo]) * MC;
+    a.tiles[ti] = make_int4(lo, start_l[lo] + m0, min(MC, rows_l[lo] - m0), gi_l[lo]);
   }
+}
+
+// Split route, second part, one workgroup per slice plus one: workgroup s <
+// nseg writes the sorted positions of slice s's pairs (the expert's offset,
+// plus its count in the earlier slices, plus the pair's rank in its slice;
+// stable in pair index) and of the shared expert's rows s * SLICE ..; the
+// last workgroup writes the counts, the group, tile and chunk lists and the
+// meta words (the list layout of group_lists).
+__global__ __launch_bounds__(ROUTE_T) void route_finish_kernel(RouteArgs a) {
+  extern __shared__ int sm[];     // 4 x (E + 1) ints
+  const int tid = threadIdx.x;
+  const int s = blockIdx.x;
+  const int n = a.E + 1;
+  if (s < a.nseg) {
+    const int Pr = a.T * a.k;
+    const int p = s * SLICE + tid;
+    // loaded from a clamped index beside the counts (a pair past the end
+    // or with a skipped slot is dropped below)
+    const int pc = min(p, Pr - 1);
+    int e0, r;
+    int *tot = sm, *pre = sm + n;
+    expert_sums(a, s, tot, pre, [&] {
+      e0 = a.ids[pc];
+      r = a.rank[pc];
+    });
+    const int e = (p < Pr && e0 >= 0 && e0 < a.E) ? e0 : -1;
+    __syncthreads();
+    if (tid < 64) wave_exscan(tot, n);
+    __syncthreads();
+    if (e >= 0) a.perm[tot[e] + pre[e] + r] = p;
+    if (a.has_shared && p < a.T) a.perm[tot[a.E] + p] = Pr + p;
+    return;
+  }
+  int *rows_l = sm, *start_l = sm + n, *gi_l = sm + 2 * n, *t0_l = sm + 3 * n;
+  expert_sums(a, -1, rows_l, nullptr, [] {});
+  __syncthreads();
+  build_lists(a, rows_l, start_l, gi_l, t0_l);
 }
 
 struct Q8Args {
@@ -538,14 +739,15 @@ __device__ void norm_q8_rows(const Q8Args &q, int64_t wg) {
 }
 
 // Stages 1 and 2 in one launch (they are independent): the first `nroute`
-// workgroups route -- the whole route in workgroup 0 (MODE 0, 1), or the
-// ranks of one slice each (MODE 2, finished by route_finish) -- the others
-// quantize the hidden rows, ROUTE_T / 8 blocks each.
+// workgroups route -- the whole route in workgroup 0 (MODE 0, 1; MODE 3, one
+// slice of at most ROUTE_T pairs), or the ranks of one slice each (MODE 2,
+// finished by route_finish) -- the others quantize the hidden rows, ROUTE_T /
+// 8 blocks each.
 template <int MODE>
 __global__ __launch_bounds__(ROUTE_T) void prep_kernel(RouteArgs a, Q8Args q, int nroute) {
   if ((int)blockIdx.x < nroute) {
-    if (MODE == 2)
-      slice_ranks(a, blockIdx.x);
+    if (MODE >= 2)
+      slice_ranks<MODE == 3>(a, blockIdx.x);
     else
       route_body<MODE>(a);
     return;
@@ -555,12 +757,6 @@ __global__ __launch_bounds__(ROUTE_T) void prep_kernel(RouteArgs a, Q8Args q, in
   else
     q8_0_lane(q.x, q.xq, q.xs, q.xa, q.xd, q.nblocks, q.nbrow,
               (int64_t)(blockIdx.x - nroute) * ROUTE_T + threadIdx.x);
-}
-
-// The split route's second part: offsets, the permutation and the group,
-// tile and chunk lists, from the slices' counts and ranks.
-__global__ __launch_bounds__(ROUTE_T) void route_finish_kernel(RouteArgs a) {
-  route_body<2>(a);
 }
 
 // out[t] = sum_j y[t*k + j] (slots in order, skipped slots left out) + y[T*k + t].
@@ -666,23 +862,31 @@ int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
   ra.hist_g = reinterpret_cast<int32_t *>(ws + L.hist);
   ra.T = (int)T; ra.k = (int)k; ra.E = (int)E; ra.has_shared = has_shared; ra.ms = ms;
   const int64_t Pr = T * k;
+  ra.tpe = 1;
   ra.ebits = 0;
   while ((1 << ra.ebits) < E) ra.ebits++;
   const unsigned nq = qa.norm_rows ? (unsigned)((T + qa.norm_rows - 1) / qa.norm_rows)
                                    : (unsigned)((qa.nblocks * 8 + ROUTE_T - 1) / ROUTE_T);
   const int64_t nslice = (Pr + SLICE - 1) / SLICE;
-  if (split_route(Pr, E)) {
-    // slices of ROUTE_T pairs ranked beside the quantization, then one
-    // workgroup for the offsets and lists
+  if (split_route(E)) {
+    // slices of ROUTE_T pairs ranked beside the quantization; a single slice
+    // finishes the route in the same workgroup, several in one more launch
+    // (one workgroup per slice for the permutation, one for the lists)
     ra.seg = SLICE;
     ra.nseg = (int)nslice;
-    ra.stage = Pr + T + 3 * (E + 1) <= LDS_INTS;
+    ra.stage = 0;
+    int e2 = 1;
+    while (e2 < E) e2 *= 2;
+    ra.tpe = (int)std::max<int64_t>(1, std::min<int64_t>(64, ROUTE_T / e2));
     const size_t lds1 = sizeof(int) * 16 * (size_t)E;
-    prep_kernel<2><<<dim3((unsigned)nslice + nq), dim3(ROUTE_T), lds1, s>>>(ra, qa, (int)nslice);
-    if ((rc = check_launch()) != W4A8_OK) return rc;
-    const size_t lds2 = sizeof(int) * std::max<size_t>((size_t)E * ra.nseg,
-                                                       (ra.stage ? Pr + T : 0) + 3 * (E + 1));
-    route_finish_kernel<<<dim3(1), dim3(ROUTE_T), lds2, s>>>(ra);
+    if (nslice == 1) {
+      prep_kernel<3><<<dim3(1 + nq), dim3(ROUTE_T), lds1, s>>>(ra, qa, 1);
+    } else {
+      prep_kernel<2><<<dim3((unsigned)nslice + nq), dim3(ROUTE_T), lds1, s>>>(ra, qa, (int)nslice);
+      if ((rc = check_launch()) != W4A8_OK) return rc;
+      route_finish_kernel<<<dim3((unsigned)nslice + 1), dim3(ROUTE_T),
+                            sizeof(int) * 4 * (size_t)(E + 1), s>>>(ra);
+    }
   } else {
     // smallest segment (multiple of 64 pairs) whose histogram fits in LDS
     const int64_t nseg_max = std::max<int64_t>(1, LDS_INTS / E);

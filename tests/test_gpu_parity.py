@@ -401,6 +401,35 @@ def test_moe_route_4096_experts():
     L.check(x, ids, wts, k, out, h, hq)
 
 
+@pytest.mark.parametrize("seed,E,T,k", [
+    (45, 8, 100, 2),        # 200 pairs, one slice; 64 threads per expert sum the counts
+    (46, 300, 129, 8),      # two threads per expert, two slices
+    (47, 1000, 300, 8),     # one thread per expert (E not a power of two), three slices
+    (48, 1024, 64, 8),      # the largest expert count of the split route
+    (50, 256, 128, 8),      # exactly one full slice (1024 pairs): routed in the prep launch
+    (49, 64, 2600, 8),      # 20800 pairs in 21 slices
+])
+def test_moe_split_route_shapes(seed, E, T, k):
+    """The split route (per-slice ranks beside the quantization; a single
+    slice finished in its own workgroup, several by one workgroup per slice
+    placing its pairs and one writing the group lists) across expert counts
+    and slice counts, with skipped and duplicate slots: the permutation and
+    counts exact, every pair through the MoE check."""
+    L = Layer(seed, 256, 256, E)
+    g = synth.rng(seed + 200)
+    x = synth.normal_f32(g, (T, L.H))
+    ids, wts = synth.routing(g, T, L.E, k, bias_std=1.0)
+    ids[1, 0] = -1                       # skipped slot
+    ids[2, k - 1] = E                    # id >= E: skipped
+    if k > 1:
+        ids[3, 1] = ids[3, 0]            # duplicate expert in one token
+    ids[min(T - 1, 70):, 0] = E - 1      # one long group on the MFMA tiles
+    out, h, hq, perm, count, _ = L.run(x, ids, wts, k)
+    _check_route(ids, L.E, True, perm, count)
+    ids_o = ids.copy(); ids_o[ids_o >= L.E] = -1
+    L.check(x, ids_o, wts, k, out, h, hq)
+
+
 def test_moe_prefill_947_all_tokens(qwen_layer):
     """The 947-token prefill with biased routing (skewed expert load: empty
     experts, groups of a few rows on the VALU kernels, groups of hundreds of
