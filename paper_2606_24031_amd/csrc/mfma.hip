@@ -167,13 +167,13 @@ __device__ __forceinline__ void lds_dma16(const uint32_t *src, const void *dst) 
 }
 #pragma clang diagnostic pop
 
-// Copy the tile's codes of blocks 8g..8g+7 into buffer buf: wave w moves rows
-// 16w..16w+15 (only the first 32 rows when `two` is false), four rows per
+// Copy the tile's codes of blocks 8g..8g+7 into buffer buf: wave w < nwv
+// moves rows 16w..16w+15 (the tile's rows rounded up to 16, 32 or 64), four rows per
 // instruction; lane l writes chunk position l%16 of row r0 + l/16, which holds
 // chunk (l%16) ^ (row % 16) of the row's 256 bytes.
-__device__ __forceinline__ void stage_codes(const MArgs &a, MLds &L, int g, int buf, bool two,
+__device__ __forceinline__ void stage_codes(const MArgs &a, MLds &L, int g, int buf, int nwv,
                                             int wave, int lane, int nblk) {
-  if (!two && wave >= 2) return;
+  if (wave >= nwv) return;
 #pragma unroll
   for (int i = 0; i < 4; i++) {
     const int r0 = wave * 16 + i * 4;
@@ -261,15 +261,81 @@ __device__ __forceinline__ void block(float acc0[16], float acc1[16], const Bloc
   }
 }
 
+// Tiles of at most 16 rows run v_mfma_i32_16x16x32_i8 instead (half the
+// padding of a 32-row half): per block and wave two products, weight rows
+// 0..15 and 16..31 of the wave as the A operand, the tile's 16 token rows as
+// the B operand.  Lane l of a product holds token l%16 and weight rows
+// 4*(l/16)..+3 of the product's 16, so a lane takes eight sums of one token:
+// e < 4 of rows 4*(l/16) + e, e >= 4 of rows 16 + 4*(l/16) + e - 4.
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ v4f mm16(long a, long b, v4i c) {
+  return __builtin_bit_cast(v4f, __builtin_amdgcn_mfma_i32_16x16x32_i8(a, b, c, 0, 0, 0));
+}
+
+// The A operands of both products of one block from its 32x32x32 A operand
+// b (lane l < 32: codes 0..15 of wave row l; lane l + 32: codes 16..31 of
+// the same row).  A 16x16x32 product wants in lane l codes 8*(l/16)..+7 of
+// row l%16 (of its 16 rows): each 16-lane row of the wave keeps the half it
+// needs for one product and trades the other half with its neighbouring
+// row, one v_permlane16_swap per dword (odd rows of the first operand
+// against even rows of the second).
+__device__ __forceinline__ void split16(v4i b, long &m0, long &m1) {
+  const v2u s0 = __builtin_amdgcn_permlane16_swap((uint32_t)b[0], (uint32_t)b[2], false, false);
+  const v2u s1 = __builtin_amdgcn_permlane16_swap((uint32_t)b[1], (uint32_t)b[3], false, false);
+  m0 = __builtin_bit_cast(long, v2u{s0.x, s1.x});
+  m1 = __builtin_bit_cast(long, v2u{s0.y, s1.y});
+}
+
+// B operand of block kk for token row t: codes 8c..8c+7 of the block, c =
+// lane / 16, from the swizzled staging buffer.
+__device__ __forceinline__ long aop16(const uint4 *abuf, int t, int kk, int c) {
+  const v2u *p = reinterpret_cast<const v2u *>(abuf + t * 16 + ((2 * kk + (c >> 1)) ^ (t & 15)));
+  return __builtin_bit_cast(long, p[c & 1]);
+}
+
+struct BlockIn16 {
+  long a;
+  float4 dw0, dw1;
+  float2 dx;
+};
+__device__ __forceinline__ BlockIn16 block_in16(const uint4 *abuf, const float *dw,
+                                                const float2 *dxb, int kk, int t, int c) {
+  BlockIn16 o;
+  o.a = aop16(abuf, t, kk, c);
+  o.dw0 = *reinterpret_cast<const float4 *>(dw + 4 * c);
+  o.dw1 = *reinterpret_cast<const float4 *>(dw + 16 + 4 * c);
+  o.dx = dxb[t];
+  return o;
+}
+// One block of a 16-row tile: acc[e] += s_e * dx * dw[e] as in scale4.
+__device__ __forceinline__ void block16(float acc[16], const BlockIn16 &in, v4i b, v4i c4) {
+  long m0, m1;
+  split16(b, m0, m1);
+  const v4f f0 = mm16(m0, in.a, c4);
+  const v4f f1 = mm16(m1, in.a, c4);
+  const float dx = in.dx.x, nbx = in.dx.y;
+  acc[0] = fmaf(fmaf(f0[0], dx, nbx), in.dw0.x, acc[0]);
+  acc[1] = fmaf(fmaf(f0[1], dx, nbx), in.dw0.y, acc[1]);
+  acc[2] = fmaf(fmaf(f0[2], dx, nbx), in.dw0.z, acc[2]);
+  acc[3] = fmaf(fmaf(f0[3], dx, nbx), in.dw0.w, acc[3]);
+  acc[4] = fmaf(fmaf(f1[0], dx, nbx), in.dw1.x, acc[4]);
+  acc[5] = fmaf(fmaf(f1[1], dx, nbx), in.dw1.y, acc[5]);
+  acc[6] = fmaf(fmaf(f1[2], dx, nbx), in.dw1.z, acc[6]);
+  acc[7] = fmaf(fmaf(f1[3], dx, nbx), in.dw1.w, acc[7]);
+}
+
 // One tile: rows token rows (1..64) of expert's group from sorted position
 // pos (or of the dense rows from pos), against weight slices s0 .. s0 + ns
 // - 1 (ns > 1 only for resident codes and the down projection).  TWO: the
 // tile holds more than 32 rows (a compile-time branch: a run-time one inside
 // the block loop makes the compiler keep every block's second product until
 // the loop's end).
-template <bool GATEUP, bool TWO, bool RES, bool SK>
+template <bool GATEUP, bool TWO, bool RES, bool SK, bool H16 = false>
 __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, int pos, int rows,
                                           int s0, int ns) {
+  static_assert(!(TWO && H16), "a 16-row tile has one half");
+  constexpr int NWV = TWO ? 4 : (H16 ? 1 : 2);   // waves that stage the codes
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int r32 = lane & 31, hh = lane >> 5;
@@ -297,12 +363,12 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
   float dx0 = 0.0f, dx1 = 0.0f;
   if (resident) {
     for (int g = 0; g < G; g++) {
-      stage_codes(a, L, g, g, TWO, wave, lane, nblk);
+      stage_codes(a, L, g, g, NWV, wave, lane, nblk);
       L.dx[g][dj][dm] = scale_pair(dlive * dsrc[8 * g]);
       L.dx[g][dj + 4][dm] = scale_pair(dlive * dsrc[8 * g + 4]);
     }
   } else {
-    stage_codes(a, L, 0, 0, TWO, wave, lane, nblk);
+    stage_codes(a, L, 0, 0, NWV, wave, lane, nblk);
     dx0 = dsrc[0];
     dx1 = dsrc[4];
   }
@@ -352,7 +418,7 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
     // reads of this one and waits for them before this group's products,
     // so only loads issued after them stay in flight across the group.
     if (!resident && g + 1 < G) {
-      stage_codes(a, L, g + 1, (g + 1) & 1, TWO, wave, lane, nblk);
+      stage_codes(a, L, g + 1, (g + 1) & 1, NWV, wave, lane, nblk);
       dx0 = dsrc[8 * (g + 1)];
       dx1 = dsrc[8 * (g + 1) + 4];
     }
@@ -373,19 +439,37 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
     const uint4 *abuf = L.a[buf];
     // each block's LDS operands are read one block ahead of its products
     // (order 0, 4, 1, 5, 2, 6, 3, 7)
-    BlockIn nx = block_in<TWO, !SK>(abuf, Lw, dxb[0], 0, r32, hh);
+    if constexpr (H16) {
+      const int t16 = lane & 15, c16 = lane >> 4;
+      const v4i c4 = v4i{BIAS, BIAS, BIAS, BIAS};
+      BlockIn16 nx = block_in16(abuf, Lw, dxb[0], 0, t16, c16);
 #pragma unroll
-    for (int jj = 0; jj < 4; jj++) {
-      v4i b0, b1;
-      uint32_t sd0, sd1;
-      pair_ops(w, jj, b0, b1, sd0, sd1);
-      BlockIn cur = nx;
-      nx = block_in<TWO, !SK>(abuf, Lw + (jj + 4) * DWS, dxb[jj + 4], jj + 4, r32, hh);
-      block<TWO, !SK>(acc0, acc1, cur, b0, c0, r32);
-      cur = nx;
-      if (jj + 1 < 4)
-        nx = block_in<TWO, !SK>(abuf, Lw + (jj + 1) * DWS, dxb[jj + 1], jj + 1, r32, hh);
-      block<TWO, !SK>(acc0, acc1, cur, b1, c0, r32);
+      for (int jj = 0; jj < 4; jj++) {
+        v4i b0, b1;
+        uint32_t sd0, sd1;
+        pair_ops(w, jj, b0, b1, sd0, sd1);
+        BlockIn16 cur = nx;
+        nx = block_in16(abuf, Lw + (jj + 4) * DWS, dxb[jj + 4], jj + 4, t16, c16);
+        block16(acc0, cur, b0, c4);
+        cur = nx;
+        if (jj + 1 < 4) nx = block_in16(abuf, Lw + (jj + 1) * DWS, dxb[jj + 1], jj + 1, t16, c16);
+        block16(acc0, cur, b1, c4);
+      }
+    } else {
+      BlockIn nx = block_in<TWO, !SK>(abuf, Lw, dxb[0], 0, r32, hh);
+#pragma unroll
+      for (int jj = 0; jj < 4; jj++) {
+        v4i b0, b1;
+        uint32_t sd0, sd1;
+        pair_ops(w, jj, b0, b1, sd0, sd1);
+        BlockIn cur = nx;
+        nx = block_in<TWO, !SK>(abuf, Lw + (jj + 4) * DWS, dxb[jj + 4], jj + 4, r32, hh);
+        block<TWO, !SK>(acc0, acc1, cur, b0, c0, r32);
+        cur = nx;
+        if (jj + 1 < 4)
+          nx = block_in<TWO, !SK>(abuf, Lw + (jj + 1) * DWS, dxb[jj + 1], jj + 1, r32, hh);
+        block<TWO, !SK>(acc0, acc1, cur, b1, c0, r32);
+      }
     }
     if (g + 1 < G) return;
 
@@ -393,7 +477,15 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
     if (GATEUP) {
       __syncthreads();                            // the code buffers become the h tile
       // element e < 8 holds the gate sum and e + 8 the up sum of column
-      // 16*wave + 8*(e/4) + 4*hh + e%4 for this lane's token
+      // 16*wave + 8*(e/4) + 4*hh + e%4 for this lane's token (16-row tiles:
+      // e < 4 gate and e + 4 up of column 16*wave + 4*(lane/16) + e of
+      // token lane%16)
+      if constexpr (H16) {
+        const float *acc = acc0;
+        *reinterpret_cast<float4 *>(&L.hv[lane & 15][16 * wave + 4 * (lane >> 4)]) =
+            make_float4(silu_f32(acc[0]) * acc[4], silu_f32(acc[1]) * acc[5],
+                        silu_f32(acc[2]) * acc[6], silu_f32(acc[3]) * acc[7]);
+      } else {
 #pragma unroll
       for (int half = 0; half < (TWO ? 2 : 1); half++) {
         const float *acc = half ? acc1 : acc0;
@@ -405,6 +497,7 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
                           silu_f32(acc[4 * q + 1]) * acc[4 * q + 9],
                           silu_f32(acc[4 * q + 2]) * acc[4 * q + 10],
                           silu_f32(acc[4 * q + 3]) * acc[4 * q + 11]);
+      }
       }
       __syncthreads();
       // Q8_0 of each row's two 32-wide blocks: 8 lanes per block
@@ -429,10 +522,34 @@ __device__ __forceinline__ void mfma_tile(const MArgs &a, MLds &L, int expert, i
       }
     } else {
       // element 4q + i: output column slice*128 + 32*wave + 8q + 4hh + i
-      const int64_t n0 = (int64_t)slice * WROWS + 32 * wave + 4 * hh;
+      // (16-row tiles: element 4q + i of token lane%16, column slice*128 +
+      // 32*wave + 16q + 4*(lane/16) + i)
       const bool vec = (a.N & 3) == 0;
+      if constexpr (H16) {
+        const int m = lane & 15;
+        const int p = L.pair[m];
+        const float pw = L.pw[m];
+        if (p >= 0) {
+          float *yrow = a.y + (int64_t)p * a.N;
+          const int64_t nb = (int64_t)slice * WROWS + 32 * wave + 4 * (lane >> 4);
 #pragma unroll
-      for (int half = 0; half < (TWO ? 2 : 1); half++) {
+          for (int q = 0; q < 2; q++) {
+            const int64_t n = nb + 16 * q;
+            if (vec && n + 3 < a.N) {
+              *reinterpret_cast<float4 *>(yrow + n) =
+                  make_float4(pw * acc0[4 * q], pw * acc0[4 * q + 1], pw * acc0[4 * q + 2],
+                              pw * acc0[4 * q + 3]);
+            } else {
+#pragma unroll
+              for (int i = 0; i < 4; i++)
+                if (n + i < a.N) yrow[n + i] = pw * acc0[4 * q + i];
+            }
+          }
+        }
+      }
+      const int64_t n0 = (int64_t)slice * WROWS + 32 * wave + 4 * hh;
+#pragma unroll
+      for (int half = 0; half < (H16 ? 0 : (TWO ? 2 : 1)); half++) {
         const float *acc = half ? acc1 : acc0;
         const int m = 32 * half + r32;
         const int p = L.pair[m];
@@ -509,13 +626,17 @@ __device__ __forceinline__ void mfma_body(const MArgs &a, MLds &L) {
   if (a.K <= 512) {
     if (!SHORT && rows > 32)
       mfma_tile<GATEUP, true, true, SHORT>(a, L, expert, pos, rows, s0, ns);
-    else
+    else if (rows > 16)
       mfma_tile<GATEUP, false, true, SHORT>(a, L, expert, pos, rows, s0, ns);
+    else
+      mfma_tile<GATEUP, false, true, SHORT, true>(a, L, expert, pos, rows, s0, ns);
   } else {
     if (!SHORT && rows > 32)
       mfma_tile<GATEUP, true, false, SHORT>(a, L, expert, pos, rows, s0, ns);
-    else
+    else if (rows > 16)
       mfma_tile<GATEUP, false, false, SHORT>(a, L, expert, pos, rows, s0, ns);
+    else
+      mfma_tile<GATEUP, false, false, SHORT, true>(a, L, expert, pos, rows, s0, ns);
   }
 }
 

@@ -13,8 +13,8 @@
 //   3. gate/up: per (row tile, 64 h columns) the gate and up rows of the
 //      expert against the tile's token rows, SwiGLU, Q8_0 of the 32-wide h
 //      blocks (mfma.hip)                               -> workspace h, hq
-//      (groups of few rows: the VALU kernels of smallm.hip instead, which
-//      take the activations in nibble-split form)
+//      (a batch of at most 32 tokens: the VALU kernels of smallm.hip
+//      instead, which take the activations in nibble-split form)
 //   4. down: per (row tile, 128 output rows) the down rows against Q8_0(h),
 //      scaled by the routing weight                    -> workspace y
 //   5. combine: out[t] = sum over slots in slot order, then the shared pair
@@ -87,10 +87,12 @@ struct Layout {
 };
 
 // Largest group that takes the VALU path (small_gateup / small_down, in
-// chunks of SMALL_CHUNK rows): every group of a batch of up to 32 tokens,
-// else groups of up to 8 rows, which would fill a quarter of a 32-row MFMA
-// tile at most.
-inline int small_rows(int64_t T) { return T <= 32 ? 32 : 8; }
+// chunks of SMALL_CHUNK rows): every group of a batch of up to 32 tokens;
+// above that every group goes to the MFMA tiles, whose 16-row tiles pad a
+// few-row group less than the VALU path's separate launches cost (measured
+// at 947 tokens: 207 us per layer against 214-218 with groups of up to 8
+// rows on the VALU kernels, those on a second stream beside the tiles).
+inline int small_rows(int64_t T) { return T <= 32 ? 32 : 0; }
 
 // Region sizes depend only on (T, H, I, E, k).
 Layout make_layout(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k) {

@@ -2,10 +2,11 @@
 // (paper Sec. 3.2: the token-expert pairs grouped by expert; Sec. 3.3: 4-bit
 // weight codes times 8-bit activation codes, one scaling per 32 elements).
 //
-// The grouped MFMA kernels pad each group to 32-row halves of their tiles, so
-// a group of a few rows -- the routed experts of a batch of a few dozen
-// tokens, or the sparsely routed experts of a prefill -- would spend most of
-// that work on padding.  Here the small groups are cut into chunks of at most
+// The grouped MFMA kernels pad each group to tiles of 16, 32 or 64 rows, so
+// the groups of a batch of up to 32 tokens (a few rows each: every routed
+// expert of the batch) would spend most of that work on padding, and in a
+// call of that size the launches of the tile path cost more than they save.
+// Here those groups are cut into chunks of at most
 // SMALL_CHUNK token rows, and a workgroup takes one chunk and a slab of
 // weight rows.  Each weight row is read by LPR consecutive lanes, one
 // 144-byte group of eight blocks each (LPR = K/256 rounded up to a power of

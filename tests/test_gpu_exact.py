@@ -4,7 +4,8 @@ On the layers of tests/exact_layers.py every block dot is an integer, every
 scale 1.0 and every scaled sum exact in fp32, so the GPU's fp32 h, its Q8_0(h)
 bytes and the layer output must equal the oracle's bit for bit: a block dot
 off by one in any kernel -- the single-token decode kernel, the small-group
-VALU kernels or the int8 MFMA tiles, gate/up or down -- changes them.
+VALU kernels or the int8 MFMA tiles (64-, 32- and 16-row), gate/up or down --
+changes them.
 """
 import numpy as np
 import pytest
@@ -84,12 +85,14 @@ def test_exact_small_group_path():
 
 
 def test_exact_mfma_path():
-    """T > 32: groups of 40 rows (one tile, both 32-row halves), 70 rows (a
-    full 64-row tile and a 6-row tile) on the int8 MFMA kernels, beside groups
-    of 5 rows on the VALU kernels in the same call; then one cluster of 70
-    tokens with the shared expert (70-row shared group)."""
-    L = ExactLayer(5, H, I, 24, 8, [(40, list(range(0, 8))), (70, list(range(8, 16))),
-                                    (5, list(range(16, 24)))], shared=False)
+    """T > 32, every group on the int8 MFMA tiles: groups of 40 rows (one
+    tile, both 32-row halves), 70 rows (a full 64-row tile and a 6-row tile
+    on the 16x16x32 products), 5 and 16 rows (16-row tiles) and 17 rows (a
+    32-row half); then one cluster of 70 tokens with the shared expert
+    (70-row shared group)."""
+    L = ExactLayer(5, H, I, 40, 8, [(40, list(range(0, 8))), (70, list(range(8, 16))),
+                                    (5, list(range(16, 24))), (16, list(range(24, 32))),
+                                    (17, list(range(32, 40)))], shared=False)
     run_exact(L)
     L2 = ExactLayer(6, H, I, 8, 8, [(70, list(range(8)))], shared=True)
     run_exact(L2)

@@ -323,24 +323,24 @@ def test_moe_decode_m32(qwen_layer):
     L.check(x, ids, wts, 8, out, h, hq)
 
 
-def test_moe_group_size_boundary_between_paths(small_layer):
-    """Above 32 tokens, expert groups of up to 8 rows take the VALU path and
-    larger ones the MFMA tiles: two groups of 8 rows (VALU), groups of 9 and
-    33 rows and the shared expert's 40 (MFMA), checked token by token."""
+def test_moe_tile_kinds_above_32_tokens(small_layer):
+    """Above 32 tokens every expert group takes the MFMA tiles, its last tile
+    by its rows: groups of 8 and 16 rows (16-row tiles, 16x16x32 products),
+    17 rows (one 32-row half), 33 rows and the shared expert's 40 (64-row
+    tiles, both halves), checked token by token; six skipped slots."""
     L = small_layer
     g = synth.rng(31)
     T, k = 40, 2
     x = synth.normal_f32(g, (T, L.H))
     ids = np.full((T, k), -1, dtype=np.int32)
     ids[:8, 0] = 0                       # expert 0: 8 rows
-    ids[8:17, 0] = 1                     # expert 1: 9 rows
-    ids[17:40, 0] = 2                    # expert 2: 23 + 10 = 33 rows
-    ids[:10, 1] = 2
-    ids[10:17, 1] = 3                    # expert 3: 7 rows + 1
-    ids[39, 1] = 3
+    ids[8:24, 0] = 1                     # expert 1: 16 rows
+    ids[24:40, 0] = 2                    # expert 2: 16 + 1 = 17 rows
+    ids[:1, 1] = 2
+    ids[1:34, 1] = 3                     # expert 3: 33 rows
     wts = g.random((T, k), dtype=np.float32)
     out, h, hq, perm, count, _ = L.run(x, ids, wts, k)
-    assert count.tolist() == [8, 9, 33, 8]
+    assert count.tolist() == [8, 16, 17, 33]
     _check_route(ids, L.E, True, perm, count)
     L.check(x, ids, wts, k, out, h, hq)
 
@@ -372,8 +372,8 @@ def test_moe_tiles_across_64_row_boundaries(small_layer):
     (43, 2560, 256, 2, True, 40, 1),     # K = 2560: ten staged groups for gate/up
 ])
 def test_moe_mfma_path_shapes(seed, H, I, E, shared, T, k):
-    """Shapes other than the paper's layer with groups large enough for the
-    MFMA tiles (more than 8 rows at T > 32)."""
+    """Shapes other than the paper's layer on the MFMA tiles (every group at
+    T > 32)."""
     L = Layer(seed, H, I, E, shared=shared)
     g = synth.rng(seed + 100)
     x = synth.normal_f32(g, (T, L.H))
@@ -432,8 +432,8 @@ def test_moe_split_route_shapes(seed, E, T, k):
 
 def test_moe_prefill_947_all_tokens(qwen_layer):
     """The 947-token prefill with biased routing (skewed expert load: empty
-    experts, groups of a few rows on the VALU kernels, groups of hundreds of
-    rows on the MFMA tiles, the 947-row shared group): every token and every
+    experts, groups of a few rows on 16-row tiles, groups of hundreds of
+    rows on 64-row tiles, the 947-row shared group): every token and every
     pair through the MoE check, and a second call bit-identical."""
     L = qwen_layer
     g = synth.rng(22)
