@@ -208,6 +208,35 @@ def test_moe_no_shared_expert():
     L.check(x, ids, wts, k, out, h, hq)
 
 
+def test_moe_token_without_pairs_gets_zeros():
+    """No shared expert and a token whose every slot is skipped (-1, or an id
+    >= E): its output row is exactly zero, also where the combine runs in
+    the small-group down kernel (T <= 32) and the output buffer held NaN;
+    every other row as the oracle."""
+    L = Layer(13, 512, 256, 3, shared=False)
+    g = synth.rng(14)
+    for T in (9, 40):
+        k = 2
+        x = synth.normal_f32(g, (T, L.H))
+        ids, wts = synth.routing(g, T, L.E, k)
+        ids[4, :] = -1
+        ids[6, 0] = -1
+        ids[6, 1] = 77
+        ws = w4.moe_workspace(T, L.H, L.I, L.E, k)
+        out = torch.full((T, L.H), float("nan"), device="cuda")
+        w4.moe_forward(dev(x), dev(ids), dev(wts), L.d_gu, L.d_d, None, None, L.H, L.I, L.E, k,
+                       ws, out=out)
+        o = host(out)
+        assert np.all(o[4] == 0.0) and np.all(o[6] == 0.0)
+        lay = w4.moe_workspace_layout(T, L.H, L.I, L.E, k)
+        P = T * k + T
+        wsn = host(ws)
+        h = wsn[lay["h"]:lay["h"] + P * L.I * 4].view(np.float32).reshape(P, L.I)
+        hq = wsn[lay["hq"]:lay["hq"] + P * (L.I // 32) * 34].reshape(P, -1)
+        ids_o = ids.copy(); ids_o[ids_o >= L.E] = -1
+        L.check(x, ids_o, wts, k, o, h, hq)
+
+
 def test_moe_ragged_group_count_and_odd_K():
     """H = I = 768 (three 8-block groups per row, not a power of two)."""
     L = Layer(11, 768, 768, 5)
