@@ -13,7 +13,7 @@
 //   3. gate/up: per (row tile, 64 h columns) the gate and up rows of the
 //      expert against the tile's token rows, SwiGLU, Q8_0 of the 32-wide h
 //      blocks (mfma.hip)                               -> workspace h, hq
-//      (a batch of at most 32 tokens: the VALU kernels of smallm.hip
+//      (a batch of at most 128 tokens: the VALU kernels of smallm.hip
 //      instead, which take the activations in nibble-split form)
 //   4. down: per (row tile, 128 output rows) the down rows against Q8_0(h),
 //      scaled by the routing weight                    -> workspace y
@@ -87,12 +87,16 @@ struct Layout {
 };
 
 // Largest group that takes the VALU path (small_gateup / small_down, in
-// chunks of SMALL_CHUNK rows): every group of a batch of up to 32 tokens;
-// above that every group goes to the MFMA tiles, whose 16-row tiles pad a
-// few-row group less than the VALU path's separate launches cost (measured
-// at 947 tokens: 207 us per layer against 214-218 with groups of up to 8
-// rows on the VALU kernels, those on a second stream beside the tiles).
-inline int small_rows(int64_t T) { return T <= 32 ? 32 : 0; }
+// chunks of SMALL_CHUNK rows): every group of a batch of up to 128 tokens,
+// whose few-row groups are bound by weight streaming, where the VALU
+// kernels keep every weight load of a workgroup in flight at once (64
+// tokens: 104 us per layer against 127 on the tiles; 128 tokens: 137
+// against 148; 256 tokens: 213 against 157).  Above that every group goes
+// to the MFMA tiles, whose 16-row tiles pad a few-row group less than
+// separate VALU launches for those groups cost (947 tokens: 207 us per
+// layer against 214-218 with groups of up to 8 rows on the VALU kernels).
+constexpr int64_t SMALL_T_MAX = 128;
+inline int small_rows(int64_t T) { return T <= SMALL_T_MAX ? (int)SMALL_T_MAX : 0; }
 
 // Region sizes depend only on (T, H, I, E, k).
 Layout make_layout(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k) {
@@ -911,11 +915,8 @@ int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
   uint8_t *hq = ws + L.hq;
   float *h = reinterpret_cast<float *>(ws + L.h);
   float *y = reinterpret_cast<float *>(ws + L.y);
-  // launch bound on the small chunks: above SMALL_CHUNK-row groups (T > 32)
-  // every small group is one chunk and the shared group (T rows) is never
-  // small, so at most one chunk per routed expert that can be touched
-  const int64_t maxchunks =
-      ms < T ? std::min<int64_t>(E, T * k) : small_max_chunks(T, E, k, has_shared);
+  // launch bound on the small chunks (every group small when there are any)
+  const int64_t maxchunks = small_max_chunks(T, E, k, has_shared);
   if (ms > 0 && (rc = small_gateup(w_gu, ws_gu, xs, ra.meta, ra.perm, ra.chunks, h, hq, hs,
                                    maxchunks, T, H, I, E, k, s)) != W4A8_OK)
     return rc;

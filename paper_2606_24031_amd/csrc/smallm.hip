@@ -2,11 +2,11 @@
 // (paper Sec. 3.2: the token-expert pairs grouped by expert; Sec. 3.3: 4-bit
 // weight codes times 8-bit activation codes, one scaling per 32 elements).
 //
-// The grouped MFMA kernels pad each group to tiles of 16, 32 or 64 rows, so
-// the groups of a batch of up to 32 tokens (a few rows each: every routed
-// expert of the batch) would spend most of that work on padding, and in a
-// call of that size the launches of the tile path cost more than they save.
-// Here those groups are cut into chunks of at most
+// The grouped MFMA kernels pad each group to tiles of 16, 32 or 64 rows and
+// stream a tile's weights one group of eight blocks at a time, so the
+// groups of a batch of up to 128 tokens (a few rows each: the routed experts
+// of the batch) would spend most of that work on padding and wait on each
+// group's load.  Here those groups are cut into chunks of at most
 // SMALL_CHUNK token rows, and a workgroup takes one chunk and a slab of
 // weight rows.  Each weight row is read by LPR consecutive lanes, one
 // 144-byte group of eight blocks each (LPR = K/256 rounded up to a power of

@@ -74,7 +74,7 @@ def test_exact_decode_single_token():
 
 
 def test_exact_small_group_path():
-    """T <= 32: every group on the VALU kernels in chunks of 8 rows -- three
+    """T <= 128: every group on the VALU kernels in chunks of 8 rows -- three
     clusters of 8 tokens on disjoint experts, and one cluster of 20 tokens
     (chunks 8, 8, 4) with the shared expert."""
     L = ExactLayer(3, H, I, 24, 8, [(8, list(range(0, 8))), (8, list(range(8, 16))),
@@ -85,14 +85,14 @@ def test_exact_small_group_path():
 
 
 def test_exact_mfma_path():
-    """T > 32, every group on the int8 MFMA tiles: groups of 40 rows (one
+    """T > 128, every group on the int8 MFMA tiles: groups of 40 rows (one
     tile, both 32-row halves), 70 rows (a full 64-row tile and a 6-row tile
     on the 16x16x32 products), 5 and 16 rows (16-row tiles) and 17 rows (a
-    32-row half); then one cluster of 70 tokens with the shared expert
-    (70-row shared group)."""
+    32-row half); then one cluster of 150 tokens with the shared expert
+    (150-row shared group: two full tiles and a 22-row half)."""
     L = ExactLayer(5, H, I, 40, 8, [(40, list(range(0, 8))), (70, list(range(8, 16))),
                                     (5, list(range(16, 24))), (16, list(range(24, 32))),
                                     (17, list(range(32, 40)))], shared=False)
     run_exact(L)
-    L2 = ExactLayer(6, H, I, 8, 8, [(70, list(range(8)))], shared=True)
+    L2 = ExactLayer(6, H, I, 8, 8, [(150, list(range(8)))], shared=True)
     run_exact(L2)

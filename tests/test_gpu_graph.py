@@ -27,7 +27,7 @@ def test_grouped_layer_parity_determinism_and_graph_replays():
     w_gu, w_d = synth.q4_0_random_blocks(g, E * 2 * I, H), synth.q4_0_random_blocks(g, E * H, I)
     ws_gu, ws_d = synth.q4_0_random_blocks(g, 2 * I, H), synth.q4_0_random_blocks(g, H, I)
     d_gu, d_d, d_sgu, d_sd = dev(w_gu), dev(w_d), dev(ws_gu), dev(ws_d)
-    T = 120
+    T = 136
     x = synth.normal_f32(g, (T, H))
     ids, wts = synth.routing(g, T, E, K, bias_std=1.5)
     c = np.bincount(ids.ravel(), minlength=E)

@@ -352,14 +352,15 @@ def test_moe_decode_m32(qwen_layer):
     L.check(x, ids, wts, 8, out, h, hq)
 
 
-def test_moe_tile_kinds_above_32_tokens(small_layer):
-    """Above 32 tokens every expert group takes the MFMA tiles, its last tile
-    by its rows: groups of 8 and 16 rows (16-row tiles, 16x16x32 products),
-    17 rows (one 32-row half), 33 rows and the shared expert's 40 (64-row
-    tiles, both halves), checked token by token; six skipped slots."""
+def test_moe_tile_kinds_above_128_tokens(small_layer):
+    """Above 128 tokens every expert group takes the MFMA tiles, its last
+    tile by its rows: groups of 8 and 16 rows (16-row tiles, 16x16x32
+    products), 17 rows (one 32-row half), 33 rows (a 64-row tile, both
+    halves) and the shared expert's 136 (two full tiles and an 8-row tile),
+    checked token by token; the other slots skipped."""
     L = small_layer
     g = synth.rng(31)
-    T, k = 40, 2
+    T, k = 136, 2
     x = synth.normal_f32(g, (T, L.H))
     ids = np.full((T, k), -1, dtype=np.int32)
     ids[:8, 0] = 0                       # expert 0: 8 rows
@@ -377,17 +378,19 @@ def test_moe_tile_kinds_above_32_tokens(small_layer):
 def test_moe_tiles_across_64_row_boundaries(small_layer):
     """MFMA row tiles of 64: groups of 64 (one full tile), 65 (a full tile
     and a 1-row tile), 97 (a full tile and a 33-row tile, second half of the
-    tile in use) and 30 rows, plus the shared expert's 128 (two full tiles)."""
+    tile in use) and 30 rows, plus the shared expert's 136 (two full tiles
+    and an 8-row tile); eight tokens with a skipped second slot."""
     L = small_layer
     g = synth.rng(33)
-    T, k = 128, 2
+    T, k = 136, 2
     x = synth.normal_f32(g, (T, L.H))
-    ids = np.empty((T, k), dtype=np.int32)
+    ids = np.full((T, k), -1, dtype=np.int32)
     ids[:64, 0] = 0
     ids[64:128, 0] = 1
+    ids[128:, 0] = 3
     ids[:1, 1] = 1                       # expert 1: 65 rows
     ids[1:98, 1] = 2                     # expert 2: 97 rows
-    ids[98:128, 1] = 3                   # expert 3: 30 rows
+    ids[98:120, 1] = 3                   # expert 3: 8 + 22 = 30 rows
     wts = g.random((T, k), dtype=np.float32)
     out, h, hq, perm, count, _ = L.run(x, ids, wts, k)
     assert count.tolist() == [64, 65, 97, 30]
@@ -396,13 +399,13 @@ def test_moe_tiles_across_64_row_boundaries(small_layer):
 
 
 @pytest.mark.parametrize("seed,H,I,E,shared,T,k", [
-    (41, 768, 768, 5, True, 48, 2),      # three 8-block groups per row on both sides
-    (42, 512, 256, 3, False, 40, 2),     # no shared expert; down K = 256 (one group)
-    (43, 2560, 256, 2, True, 40, 1),     # K = 2560: ten staged groups for gate/up
+    (41, 768, 768, 5, True, 136, 2),     # three 8-block groups per row on both sides
+    (42, 512, 256, 3, False, 136, 2),    # no shared expert; down K = 256 (one group)
+    (43, 2560, 256, 2, True, 136, 1),    # K = 2560: ten staged groups for gate/up
 ])
 def test_moe_mfma_path_shapes(seed, H, I, E, shared, T, k):
-    """Shapes other than the paper's layer on the MFMA tiles (every group at
-    T > 32)."""
+    """Shapes other than the paper's layer on the MFMA tiles (every group
+    above 128 tokens)."""
     L = Layer(seed, H, I, E, shared=shared)
     g = synth.rng(seed + 100)
     x = synth.normal_f32(g, (T, L.H))
@@ -416,15 +419,15 @@ def test_moe_mfma_path_shapes(seed, H, I, E, shared, T, k):
 def test_moe_route_4096_experts():
     """The largest expert count the library accepts: the route kernel's
     histogram then holds one segment per expert and the group counters reuse
-    its space.  Tokens spread over few experts so some groups reach the MFMA
-    tiles."""
+    its space.  136 tokens: every group on the MFMA tiles, groups of one or
+    two rows on 16-row tiles."""
     L = Layer(44, 256, 256, 4096)
     g = synth.rng(144)
-    T, k = 96, 3
+    T, k = 136, 3
     x = synth.normal_f32(g, (T, L.H))
     ids, wts = synth.routing(g, T, L.E, k)
-    ids[:40, 0] = 4095                   # one group of 40 rows (MFMA)
-    ids[40:52, 1] = 17                   # one of 12 (MFMA) beside single rows
+    ids[:40, 0] = 4095                   # one group of 40 rows
+    ids[40:52, 1] = 17                   # one of 12 beside single rows
     out, h, hq, perm, count, _ = L.run(x, ids, wts, k)
     _check_route(ids, L.E, True, perm, count)
     L.check(x, ids, wts, k, out, h, hq)
@@ -452,11 +455,29 @@ def test_moe_split_route_shapes(seed, E, T, k):
     ids[2, k - 1] = E                    # id >= E: skipped
     if k > 1:
         ids[3, 1] = ids[3, 0]            # duplicate expert in one token
-    ids[min(T - 1, 70):, 0] = E - 1      # one long group on the MFMA tiles
+    ids[min(T - 1, 70):, 0] = E - 1      # one long group (MFMA tiles above 128 tokens)
     out, h, hq, perm, count, _ = L.run(x, ids, wts, k)
     _check_route(ids, L.E, True, perm, count)
     ids_o = ids.copy(); ids_o[ids_o >= L.E] = -1
     L.check(x, ids_o, wts, k, out, h, hq)
+
+
+@pytest.mark.parametrize("T", [100, 128])
+def test_moe_mid_batch_on_the_valu_path(qwen_layer, T):
+    """Up to 128 tokens every group takes the small-group VALU kernels in
+    chunks of 8 rows, also groups of dozens of rows and the shared group of
+    T rows (13 and 16 chunks), with biased routing: every token and pair
+    through the MoE check."""
+    L = qwen_layer
+    g = synth.rng(23 + T)
+    k = 8
+    x = synth.normal_f32(g, (T, L.H))
+    ids, wts = synth.routing(g, T, L.E, k, bias_std=1.0)
+    out, h, hq, perm, count, _ = L.run(x, ids, wts, k)
+    _check_route(ids, L.E, True, perm, count)
+    assert count.max() > 16
+    st = L.check(x, ids, wts, k, out, h, hq)
+    assert st["pairs"] == T * (k + 1)
 
 
 def test_moe_prefill_947_all_tokens(qwen_layer):
@@ -604,15 +625,15 @@ def test_moe_layer_residual_norm_other_widths(H, T):
     L.check(xn, ids, wts, k, host(out), h, hq)
 
 
-@pytest.mark.parametrize("T,gated", [(1, True), (1, False), (6, True), (40, True), (40, False)])
+@pytest.mark.parametrize("T,gated", [(1, True), (1, False), (6, True), (40, True), (136, False)])
 def test_moe_layer_routed(qwen_layer, T, gated):
     """Router in front of the residual layer: ids bit-exact with the oracle's
     top-k of the logits and weights within 4e-6; x_out, the normalized row
     and its Q8_0 as for moe_layer; the output through the MoE check, with the
     GPU's own routing weights for the routed slots (they are the layer's
     input) and the oracle's fp64 sigmoid of the gate for the shared expert
-    (T = 1: the routing inside the single decode launch; T = 6: VALU path;
-    T = 40: MFMA tiles as well)."""
+    (T = 1: the routing inside the single decode launch; T = 6 and 40: the
+    VALU path; T = 136: the MFMA tiles)."""
     L = qwen_layer
     g = synth.rng(80 + T)
     x = synth.normal_f32(g, (T, L.H))
