@@ -164,7 +164,9 @@ int q4sym_q8f32_gemv(const void *w, const void *xq, float *y, int64_t N, int64_t
  *   gate rows, then the I up rows), w_down [E][H][I/32]; ws_gate_up [2I][H/32]
  *   and ws_down [H][I/32] the shared expert (both NULL: none); out [T][H]
  *   fp32 (may be hidden itself: hidden is read only by the first launch).
- * Four launches on the stream (quantize, gate/up, down, combine).  The
+ * Two launches on the stream (gate/up with the quantization of hidden; down
+ * with the combine), or three when a token's Q8_F32(h) of all k + 1 pairs
+ * exceeds 48 KiB (down, then the combine on its own).  The
  * workspace (>= moe_sym_workspace_size bytes, no initialisation) holds, at
  * the offsets moe_sym_workspace_layout writes to offsets[0..2]:
  *   W4A8_SYM_WS_XQ  Q8_F32(hidden), [T][H/32] blocks;
