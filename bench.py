@@ -340,12 +340,12 @@ def bench_one_expert(torch, w4, synth, args, dev, T=947, n=20):
             "int8_peak_frac": round(ops / us / 1e6 / INT8_PEAK_TOPS, 4)}
 
 
-def bench_m32(torch, w4, synth, layers, args, dev):
-    """Batched decode, 32 tokens per layer call, each routed independently
+def bench_m32(torch, w4, synth, layers, args, dev, T=32, n=None):
+    """Batched decode, T tokens (32) per layer call, each routed independently
     (top-8 of 256, no router bias); the calls cycle the weight sets and are
     replayed from one HIP graph."""
-    T, n = 32, args.m32_steps
-    rng = synth.rng(args.seed + 5)
+    n = args.m32_steps if n is None else n
+    rng = synth.rng(args.seed + 5 + T)
     ids_l, wts_l, byts = [], [], []
     for _ in range(n):
         ids, wts = synth.routing(rng, T, E, K_TOP)
@@ -998,10 +998,16 @@ def main():
         one_expert = bench_one_expert(torch, w4, synth, args, dev)
         log(f"one expert, 947 rows: {one_expert}")
 
-    m32 = None
+    m32 = batch_sweep = None
     if not args.no_m32:
         m32 = bench_m32(torch, w4, synth, layers, args, dev)
         log(f"decode M=32: {m32}")
+        if not args.no_extras:
+            # batches on either side of the switch from the small-group VALU
+            # kernels (up to 128 tokens) to the MFMA tiles
+            batch_sweep = [bench_m32(torch, w4, synth, layers, args, dev, T=t, n=16)
+                           for t in (64, 128, 129, 256)]
+            log(f"batch sweep: {batch_sweep}")
 
     invariants = router = lm_head = gemv_1024 = gemv_sym = gemm = sym_layer = gdn = None
     if not args.no_extras:
@@ -1067,6 +1073,7 @@ def main():
         "prefill_5120": prefill_5k,
         "one_expert_947_rows": one_expert,
         "decode_m32": m32,
+        "batch_sweep": batch_sweep,
         "stack_40": stack,
         "decode_invariants": invariants,
         "router_topk": router,
