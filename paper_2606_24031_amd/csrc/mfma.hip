@@ -72,7 +72,8 @@ struct MArgs {
   float *y;                        // down: w * y [P][H]
   int64_t T, k, E, N, K, I;
   int64_t M;                       // dense product (M > 0): M activation rows in implicit
-                                   // 64-row tiles, one weight matrix (ws), no route
+                                   // tiles of tr rows, one weight matrix (ws), no route
+  int tr;                          // dense product: rows per tile
   int spw;                         // slices per workgroup
 };
 
@@ -601,15 +602,15 @@ __device__ __forceinline__ void mfma_body(const MArgs &a, MLds &L) {
     // the x-th of 8 even contiguous runs: the tiles of one chunk share its
     // weights in that XCD's L2, and every XCD streams its own part of the
     // weights, so a handful of tiles still spreads over all 8.
-    const int ntl = (int)((a.M + MT - 1) / MT);
+    const int ntl = (int)((a.M + a.tr - 1) / a.tr);
     const int tot = nch * ntl;
     const int i0 = x * tot / 8, nx = (x + 1) * tot / 8 - i0;
     if (q >= nx) return;
     const int c = (i0 + q) / ntl, tile = (i0 + q) - c * ntl;
     s0 = c * a.spw;
     expert = 0;                  // E = 0: the weights are ws
-    pos = tile * MT;
-    rows = (int)min((int64_t)MT, a.M - pos);
+    pos = tile * a.tr;
+    rows = (int)min((int64_t)a.tr, a.M - pos);
   } else {
     const int ch = q % nch, qt = q / nch;
     const int ntiles = ((CInt *)a.meta)[2], nlong = ((CInt *)a.meta)[4];   // META_NTILES, META_NLONG
@@ -678,14 +679,16 @@ int mfma_gateup(const uint8_t *w_gu, const uint8_t *ws_gu, const uint32_t *xa, c
 int mfma_down(const uint8_t *w_d, const uint8_t *ws_d, const uint32_t *ha, const float *hd,
               const int32_t *meta, const int32_t *perm, const int4 *tiles, const float *topk_w,
               const float *shared_w, float *y, int64_t maxtiles, int64_t T, int64_t H, int64_t I,
-              int64_t E, int64_t k, hipStream_t s) {
+              int64_t E, int64_t k, bool few, hipStream_t s) {
   MArgs a{};
   a.w = w_d; a.ws = ws_d; a.act = ha; a.actd = hd;
   a.meta = meta; a.perm = perm; a.tiles = tiles;
   a.topk_w = topk_w; a.shared_w = shared_w; a.y = y;
   a.T = T; a.k = k; a.E = E; a.N = H; a.K = I; a.I = I;
   const int64_t nsl = H / WROWS;
-  a.spw = I <= 512 ? (int)std::min<int64_t>(SPW_MAX, nsl) : 1;
+  // few tiles: one slice per workgroup, so the slices spread over more
+  // compute units
+  a.spw = I <= 512 && !few ? (int)std::min<int64_t>(SPW_MAX, nsl) : 1;
   const int64_t nch = (nsl + a.spw - 1) / a.spw;
   mfma_kernel<false><<<dim3((unsigned)(8 * ((maxtiles + 7) / 8 + 1) * nch)), dim3(MNT), 0, s>>>(a);
   return check_launch();
@@ -699,9 +702,10 @@ int mfma_dense(const uint8_t *w, const uint32_t *act, const float *actd, float *
   a.w = nullptr; a.ws = w; a.act = act; a.actd = actd; a.y = y;
   a.T = 0; a.k = 0; a.E = 0; a.N = N; a.K = K; a.I = K; a.M = M;
   const int64_t nsl = (N + WROWS - 1) / WROWS;
+  a.tr = MT;
   a.spw = K <= 512 ? (int)std::min<int64_t>(SPW_MAX, nsl) : 1;
   const int64_t nch = (nsl + a.spw - 1) / a.spw;
-  const int64_t ntiles = (M + MT - 1) / MT;
+  const int64_t ntiles = (M + a.tr - 1) / a.tr;
   const int64_t grid = 8 * ((nch * ntiles + 7) / 8);    // an XCD takes at most ceil(items/8)
   if (grid >= ((int64_t)1 << 31)) return W4A8_ERANGE;
   if (M <= MT / 2)

@@ -46,7 +46,7 @@ int mfma_gateup(const uint8_t *w_gu, const uint8_t *ws_gu, const uint32_t *xa, c
 int mfma_down(const uint8_t *w_d, const uint8_t *ws_d, const uint32_t *ha, const float *hd,
               const int32_t *meta, const int32_t *perm, const int4 *tiles, const float *topk_w,
               const float *shared_w, float *y, int64_t maxtiles, int64_t T, int64_t H, int64_t I,
-              int64_t E, int64_t k, hipStream_t s);
+              int64_t E, int64_t k, bool few, hipStream_t s);
 size_t decode_sync_words(int64_t H);
 size_t decode_xfer_words();
 bool decode_supported(int64_t H, int64_t I, int64_t k);
@@ -66,6 +66,7 @@ int router_launch(const float *logits, int32_t *ids, float *weights, const float
 namespace {
 
 constexpr int MC = 64;          // token rows per tile of the grouped MFMA kernels
+constexpr int MC_FEW = 32;      // ... when 64-row tiles would leave compute units idle
 constexpr int ROUTE_T = 1024;   // threads of the route kernel
 constexpr int LDS_INTS = 16000; // int32 cells of dynamic LDS for the route kernel (< 64 KB)
 
@@ -102,7 +103,7 @@ inline int small_rows(int64_t T) { return T <= SMALL_T_MAX ? (int)SMALL_T_MAX : 
 Layout make_layout(int64_t T, int64_t H, int64_t I, int64_t E, int64_t k) {
   Layout L;
   const int64_t P = T * k + T;
-  L.maxtiles = (T * k + MC - 1) / MC + std::min<int64_t>(E, T * k) + (T + MC - 1) / MC + 1;
+  L.maxtiles = (T * k + MC_FEW - 1) / MC_FEW + std::min<int64_t>(E, T * k) + (T + MC_FEW - 1) / MC_FEW + 1;
   size_t off = 0;
   L.meta = off;   off += 256;
   L.sync = off;   off += up256(sizeof(uint32_t) * decode_sync_words(H));
@@ -212,13 +213,14 @@ struct RouteArgs {
   const int32_t *ids;
   int32_t *meta, *perm, *count, *rank;
   int4 *groups;     // {expert (E = shared), first sorted position, rows, first tile}
-  int4 *tiles;      // groups of more than ms rows, cut into tiles of MC rows:
+  int4 *tiles;      // groups of more than ms rows, cut into tiles of mc rows:
                     // {expert, first sorted position, rows, group}
   int4 *chunks;     // groups of at most ms rows, cut into chunks of SMALL_CHUNK
                     // rows: {expert, first sorted position, rows, group}, in
                     // reverse group order
   int *hist_g;      // split route: per-(slice, expert) counts, slice-major [nseg][E]
   int T, k, E, has_shared, seg, nseg, ebits, ms;
+  int mc;           // token rows per MFMA tile (MC, or MC_FEW for few tiles)
   int tpe;          // split route: threads per expert summing the slices' counts
   int stage;        // REG path: the permutation goes through LDS (it fits)
 };
@@ -320,8 +322,8 @@ constexpr int EPT = 5;
 // e = tid + j * ROUTE_T (e <= E; the shared expert is group E, the last).
 // Writes the compacted list of non-empty groups (expert order); a group of at
 // most ms rows goes to the small-group list, a larger one gets its MFMA row
-// tiles: those of more than MC/2 rows (full cost) first, in expert order, then
-// the tiles of at most MC/2 rows (half cost), so each XCD can take an even
+// tiles: those of more than mc/2 rows (full cost) first, in expert order, then
+// the tiles of at most mc/2 rows (half cost), so each XCD can take an even
 // share of both kinds, the longer work first.  The small-chunk and short-tile
 // counts share one scanned word (low and high 16 bits: each total is at most
 // E + 1).  cnt3: 3 x (E + 1) ints of LDS.  Every thread of the workgroup
@@ -335,11 +337,11 @@ __device__ void group_lists(const RouteArgs &a, const int (&gst)[EPT], const int
     const int e = tid + j * ROUTE_T, rows = grw[j];
     if (e > a.E) break;
     gflag[e] = rows > 0 ? 1 : 0;
-    const int rem = rows % MC;
+    const int rem = rows % a.mc;
     const bool tiled = rows > a.ms;
     gsmall[e] = ((rows > 0 && !tiled) ? (rows + SMALL_CHUNK - 1) / SMALL_CHUNK : 0) |
-                ((tiled && rem > 0 && rem <= MC / 2) ? 1 << 16 : 0);
-    gtile[e] = tiled ? rows / MC + (rem > MC / 2 ? 1 : 0) : 0;
+                ((tiled && rem > 0 && rem <= a.mc / 2) ? 1 << 16 : 0);
+    gtile[e] = tiled ? rows / a.mc + (rem > a.mc / 2 ? 1 : 0) : 0;
   }
   __syncthreads();
   int tot[3];
@@ -361,9 +363,9 @@ __device__ void group_lists(const RouteArgs &a, const int (&gst)[EPT], const int
       for (int m0 = 0, c = gsmall[e] & 0xFFFF; m0 < rows; m0 += SMALL_CHUNK, c++)
         a.chunks[nsmall - 1 - c] = make_int4(e, start_e + m0, min(SMALL_CHUNK, rows - m0), gi);
     } else {
-      for (int m0 = 0, t = t0; m0 < rows; m0 += MC) {
-        const int r = min(MC, rows - m0);
-        a.tiles[r > MC / 2 ? t++ : nlong + (gsmall[e] >> 16)] = make_int4(e, start_e + m0, r, gi);
+      for (int m0 = 0, t = t0; m0 < rows; m0 += a.mc) {
+        const int r = min(a.mc, rows - m0);
+        a.tiles[r > a.mc / 2 ? t++ : nlong + (gsmall[e] >> 16)] = make_int4(e, start_e + m0, r, gi);
       }
     }
   }
@@ -581,13 +583,13 @@ __device__ void build_lists(const RouteArgs &a, const int *rows_l, int *start_l,
     const int lo = min(lane * per, n), hi = min(lo + per, n);
     int c[5] = {0, 0, 0, 0, 0};   // rows, groups, full tiles, small chunks, short tiles
     for (int g = lo; g < hi; g++) {
-      const int rows = rows_l[g], rem = rows % MC;
+      const int rows = rows_l[g], rem = rows % a.mc;
       const bool tiled = rows > a.ms;
       c[0] += rows;
       c[1] += rows > 0 ? 1 : 0;
-      c[2] += tiled ? rows / MC + (rem > MC / 2 ? 1 : 0) : 0;
+      c[2] += tiled ? rows / a.mc + (rem > a.mc / 2 ? 1 : 0) : 0;
       c[3] += (rows > 0 && !tiled) ? (rows + SMALL_CHUNK - 1) / SMALL_CHUNK : 0;
-      c[4] += (tiled && rem > 0 && rem <= MC / 2) ? 1 : 0;
+      c[4] += (tiled && rem > 0 && rem <= a.mc / 2) ? 1 : 0;
     }
     int base[5], tot5[5];
 #pragma unroll
@@ -598,7 +600,7 @@ __device__ void build_lists(const RouteArgs &a, const int *rows_l, int *start_l,
     }
     const int nlong = tot5[2], nsmall = tot5[3];
     for (int g = lo; g < hi; g++) {
-      const int rows = rows_l[g], rem = rows % MC;
+      const int rows = rows_l[g], rem = rows % a.mc;
       const bool tiled = rows > a.ms;
       const int start = base[0], gi = base[1], t0 = base[2];
       start_l[g] = start;
@@ -611,15 +613,15 @@ __device__ void build_lists(const RouteArgs &a, const int *rows_l, int *start_l,
           // back to front: the shared group (the largest) comes first
           for (int m0 = 0, ch = base[3]; m0 < rows; m0 += SMALL_CHUNK, ch++)
             a.chunks[nsmall - 1 - ch] = make_int4(g, start + m0, min(SMALL_CHUNK, rows - m0), gi);
-        } else if (rem > 0 && rem <= MC / 2) {
+        } else if (rem > 0 && rem <= a.mc / 2) {
           a.tiles[nlong + base[4]] = make_int4(g, start + rows - rem, rem, gi);
         }
       }
       base[0] += rows;
       base[1] += rows > 0 ? 1 : 0;
-      base[2] += tiled ? rows / MC + (rem > MC / 2 ? 1 : 0) : 0;
+      base[2] += tiled ? rows / a.mc + (rem > a.mc / 2 ? 1 : 0) : 0;
       base[3] += (rows > 0 && !tiled) ? (rows + SMALL_CHUNK - 1) / SMALL_CHUNK : 0;
-      base[4] += (tiled && rem > 0 && rem <= MC / 2) ? 1 : 0;
+      base[4] += (tiled && rem > 0 && rem <= a.mc / 2) ? 1 : 0;
     }
     if (lane == 0) {
       nlong_s = nlong;
@@ -640,8 +642,8 @@ __device__ void build_lists(const RouteArgs &a, const int *rows_l, int *start_l,
       const int mid = (lo + hi + 1) >> 1;
       if (t0_l[mid] <= ti) lo = mid; else hi = mid - 1;
     }
-    const int m0 = (ti - t0_l[lo]) * MC;
-    a.tiles[ti] = make_int4(lo, start_l[lo] + m0, min(MC, rows_l[lo] - m0), gi_l[lo]);
+    const int m0 = (ti - t0_l[lo]) * a.mc;
+    a.tiles[ti] = make_int4(lo, start_l[lo] + m0, min(a.mc, rows_l[lo] - m0), gi_l[lo]);
   }
 }
 
@@ -867,6 +869,17 @@ int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
   ra.chunks = reinterpret_cast<int4 *>(ws + L.chunks);
   ra.hist_g = reinterpret_cast<int32_t *>(ws + L.hist);
   ra.T = (int)T; ra.k = (int)k; ra.E = (int)E; ra.has_shared = has_shared; ra.ms = ms;
+  // 64-row tiles, unless the pairs fill so few of them that most compute
+  // units would get no gate/up workgroup (one expert over a prompt, a short
+  // prompt's shared group): then 32-row tiles, and one down slice per
+  // workgroup
+  const int64_t est64 = (std::max<int64_t>((T * k + MC - 1) / MC, std::min<int64_t>(E, T * k)) +
+                         (has_shared ? (T + MC - 1) / MC : 0)) * (I / 64);
+  ra.mc = est64 < 2 * std::max(1, device_cus()) ? MC_FEW : MC;
+  // launch bound on the tiles at this tile size (the workspace's tile list
+  // is sized for MC_FEW)
+  const int64_t gtiles =
+      (T * k + ra.mc - 1) / ra.mc + std::min<int64_t>(E, T * k) + (T + ra.mc - 1) / ra.mc + 1;
   const int64_t Pr = T * k;
   ra.tpe = 1;
   ra.ebits = 0;
@@ -921,13 +934,13 @@ int moe_forward_impl(const float *hidden, DecodeNorm norm, const int32_t *ids,
                                    maxchunks, T, H, I, E, k, s)) != W4A8_OK)
     return rc;
   if (tiles && (rc = mfma_gateup(w_gu, ws_gu, xa, xd, ra.meta, ra.perm, ra.tiles, h, hq, ha, hd,
-                                 L.maxtiles, T, H, I, E, k, s)) != W4A8_OK)
+                                 gtiles, T, H, I, E, k, s)) != W4A8_OK)
     return rc;
   if (ms > 0 && (rc = small_down(w_d, ws_d, hs, ra.meta, ra.perm, ra.chunks, topk_w, shared_w, y,
                                  maxchunks, T, H, I, E, k, s)) != W4A8_OK)
     return rc;
   if (tiles && (rc = mfma_down(w_d, ws_d, ha, hd, ra.meta, ra.perm, ra.tiles, topk_w, shared_w,
-                               y, L.maxtiles, T, H, I, E, k, s)) != W4A8_OK)
+                               y, gtiles, T, H, I, E, k, ra.mc == MC_FEW, s)) != W4A8_OK)
     return rc;
 
   const int64_t n4 = T * (H / 4);

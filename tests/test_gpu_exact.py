@@ -85,12 +85,14 @@ def test_exact_small_group_path():
 
 
 def test_exact_mfma_path():
-    """T > 128, every group on the int8 MFMA tiles: groups of 40 rows (one
-    tile, both 32-row halves), 70 rows (a full 64-row tile and a 6-row tile
-    on the 16x16x32 products), 5 and 16 rows (16-row tiles) and 17 rows (a
-    32-row half); then one cluster of 150 tokens with the shared expert
-    (150-row shared group: two full tiles and a 22-row half)."""
-    L = ExactLayer(5, H, I, 40, 8, [(40, list(range(0, 8))), (70, list(range(8, 16))),
+    """T > 128, every group on the int8 MFMA tiles: with 128 experts (88 of
+    them unused) the route cuts 64-row tiles -- groups of 40 rows (one tile,
+    both 32-row halves), 70 rows (a full 64-row tile and a 6-row tile on the
+    16x16x32 products), 5 and 16 rows (16-row tiles) and 17 rows (a 32-row
+    half); then one cluster of 150 tokens over 8 experts with the shared
+    expert, so few tiles that the route cuts 32-row ones (four full tiles and
+    a 22-row tile per group)."""
+    L = ExactLayer(5, H, I, 128, 8, [(40, list(range(0, 8))), (70, list(range(8, 16))),
                                     (5, list(range(16, 24))), (16, list(range(24, 32))),
                                     (17, list(range(32, 40)))], shared=False)
     run_exact(L)
