@@ -272,4 +272,25 @@ int small_down(const uint8_t *w_d, const uint8_t *ws_d, const uint8_t *hs, const
   return check_launch();
 }
 
+// Dense product of a few activation rows (q4q8_gemm, M <= 32) on the down
+// kernel: the rows are the "pairs" 0..M-1 of chunks of SMALL_CHUNK rows
+// against one weight matrix (ws), each scaled by 1; act holds the rows in
+// nibble-split form, perm the identity (padded by a chunk), chunks their
+// records and meta[3] their count (written by the caller's conversion launch).
+int small_dense(const uint8_t *w, const uint8_t *act, const int32_t *meta, const int32_t *perm,
+                const int4 *chunks, float *y, int64_t M, int64_t N, int64_t K, hipStream_t s) {
+  SmallArgs a{};
+  a.w = nullptr; a.ws = w; a.act = act;
+  a.meta = meta; a.perm = perm; a.chunks = chunks;
+  a.y = y;
+  a.T = 0; a.k = 0; a.E = 0; a.N = N; a.K = K; a.I = K;
+  a.lpr = small_lpr(K);
+  const int64_t wgr = SW * (64 / a.lpr);         // output rows per workgroup
+  a.nslab = (int)((N + wgr - 1) / wgr);
+  const int64_t nchunks = (M + SC - 1) / SC;
+  if (nchunks * a.nslab >= ((int64_t)1 << 31)) return W4A8_ERANGE;
+  small_kernel<false><<<dim3((unsigned)(nchunks * a.nslab)), dim3(SNT), 0, s>>>(a);
+  return check_launch();
+}
+
 }  // namespace w4a8

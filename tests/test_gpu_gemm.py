@@ -31,11 +31,12 @@ def _rows_check(y, w, xq, N, K, rows, cols=None):
         assert np.all(np.abs(got.astype(np.float64) - ref) <= 1e-5 * R), f"row {m}"
 
 
-# M: two rows; 33 (one tile, both 32-row halves); 64 and 65 (a full tile,
-# then a 1-row tile); 96 (a full and a 32-row tile); N: ragged past a
-# 128-row slice; K: 512 (codes resident, several slices per workgroup), 768
-# (three staged groups), 2048.
-@pytest.mark.parametrize("M", [2, 33, 64, 65, 96])
+# M: 2, 8, 17 and 32 rows (the VALU kernel of the small groups, chunks of 8:
+# one partial, one full, three with a 1-row chunk, four full); 33 (one tile,
+# both 32-row halves); 64 and 65 (a full tile, then a 1-row tile); 96 (a full
+# and a 32-row tile); N: ragged past a 128-row slice; K: 512 (codes resident,
+# several slices per workgroup), 768 (three staged groups), 2048.
+@pytest.mark.parametrize("M", [2, 8, 17, 32, 33, 64, 65, 96])
 @pytest.mark.parametrize("N,K", [(1000, 2048), (4096, 512), (333, 768), (40, 256)])
 def test_gemm_matches_oracle(M, N, K):
     print(f"gemm M={M} N={N} K={K}", flush=True)
@@ -71,7 +72,7 @@ def test_gemm_lm_head_shape_sampled():
     _rows_check(y, w, xq, N, K, rows, cols)
 
 
-@pytest.mark.parametrize("M,N,K", [(70, 300, 2048), (40, 256, 512)])
+@pytest.mark.parametrize("M,N,K", [(70, 300, 2048), (40, 256, 512), (19, 300, 2048), (32, 200, 768)])
 def test_gemm_unit_scales_exact(M, N, K):
     """Every scale 1.0: each block term and every partial sum is an integer
     below 2^24, so the fp32 result is the exact integer sum."""
@@ -103,7 +104,7 @@ def test_gemm_workspace_reused_and_output_rows_untouched_past_m():
     g = synth.rng(88)
     w = synth.q4_0_random_blocks(g, N, K).reshape(N, -1)
     ws = w4.gemm_workspace(80, K)
-    for M in (80, 35):
+    for M in (80, 35, 20, 3):
         xq = oracle.q8_0_quantize(synth.normal_f32(g, (M, K))).reshape(M, -1)
         y = torch.full((M + 3, N), 7.0, device="cuda")
         w4.q4q8_gemm(dev(w), dev(xq), M, N, K, y=y, workspace=ws)
