@@ -20,15 +20,16 @@ bool small_supported(int64_t H, int64_t I);
 int small_dense(const uint8_t *w, const uint8_t *act, const int32_t *meta, const int32_t *perm,
                 const int4 *chunks, float *y, int64_t M, int64_t N, int64_t K, hipStream_t s);
 
-// A few rows (K <= 2048) run on the small-group VALU kernel: its workgroups
-// keep every weight load in flight at once, where the matrix-core tiles of a
-// handful of rows stream the weights one group of eight blocks at a time
-// over few workgroups.  Each chunk of 8 rows reads the whole weight matrix,
-// so only while the weights times the chunks stay small (the re-reads then
-// come from the caches): 32 x 2048 x 2048 14.3 us against 19.4 on the tiles,
-// but the output projection of 151936 x 2048 (175 MB) 224 us against 60 at
-// 32 rows and 66 against 43 at 8 rows.
-constexpr int64_t DENSE_SMALL_M = 32;
+// Up to 128 rows (K <= 2048) run on the small-group VALU kernel: its
+// workgroups keep every weight load in flight at once, where the matrix-core
+// tiles of a handful of rows stream the weights one group of eight blocks at
+// a time over few workgroups (32 and 64 rows over 2048 x 2048: 14.7 and 14.7
+// us against 14.6-15.3 and 22.7 on the tiles; 128 rows 20.7 against 23.1).
+// Each chunk of 8 rows reads the whole weight matrix, so only while the
+// weights times the chunks stay small (the re-reads then come from the
+// caches): the output projection of 151936 x 2048 (175 MB) took 224 us
+// against 60 at 32 rows and 66 against 43 at 8 rows.
+constexpr int64_t DENSE_SMALL_M = 128;
 constexpr int64_t DENSE_SMALL_REREAD = (int64_t)64 << 20;   // bytes of weights x chunks
 inline bool dense_small_ws(int64_t M, int64_t K) {           // the workspace may need it
   return M <= DENSE_SMALL_M && small_supported(K, 256);

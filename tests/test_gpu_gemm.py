@@ -31,13 +31,15 @@ def _rows_check(y, w, xq, N, K, rows, cols=None):
         assert np.all(np.abs(got.astype(np.float64) - ref) <= 1e-5 * R), f"row {m}"
 
 
-# M: 2, 8, 17 and 32 rows (the VALU kernel of the small groups, chunks of 8:
-# one partial, one full, three with a 1-row chunk, four full); 33 (one tile,
-# both 32-row halves); 64 and 65 (a full tile, then a 1-row tile); 96 (a full
-# and a 32-row tile); N: ragged past a 128-row slice; K: 512 (codes resident,
-# several slices per workgroup), 768 (three staged groups), 2048.
-@pytest.mark.parametrize("M", [2, 8, 17, 32, 33, 64, 65, 96])
-@pytest.mark.parametrize("N,K", [(1000, 2048), (4096, 512), (333, 768), (40, 256)])
+# K <= 2048 and M <= 128: the VALU kernel of the small groups, the rows in
+# chunks of 8 (2 one partial chunk, 8 one full, 17 a 1-row chunk last, 128
+# sixteen full); M = 129 and K = 4096: the MFMA tiles (33 one tile, both
+# 32-row halves; 64 and 65 a full tile, then a 1-row tile; 96 a full and a
+# 32-row tile; 2-32 the 32-row tiles of a few rows).  N: ragged past a
+# 128-row slice; K: 512 (codes resident, several slices per workgroup), 768
+# (three staged groups), 2048, 4096.
+@pytest.mark.parametrize("M", [2, 8, 17, 32, 33, 64, 65, 96, 128, 129])
+@pytest.mark.parametrize("N,K", [(1000, 2048), (4096, 512), (333, 768), (40, 256), (300, 4096)])
 def test_gemm_matches_oracle(M, N, K):
     print(f"gemm M={M} N={N} K={K}", flush=True)
     g = synth.rng(10 * M + N + K)
@@ -72,7 +74,8 @@ def test_gemm_lm_head_shape_sampled():
     _rows_check(y, w, xq, N, K, rows, cols)
 
 
-@pytest.mark.parametrize("M,N,K", [(70, 300, 2048), (40, 256, 512), (19, 300, 2048), (32, 200, 768)])
+@pytest.mark.parametrize("M,N,K", [(70, 300, 2048), (40, 256, 512), (19, 300, 2048), (32, 200, 768),
+                                   (70, 200, 4096), (19, 100, 4096)])
 def test_gemm_unit_scales_exact(M, N, K):
     """Every scale 1.0: each block term and every partial sum is an integer
     below 2^24, so the fp32 result is the exact integer sum."""
