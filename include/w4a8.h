@@ -110,7 +110,9 @@ int q4q8_gemv(const void *w, const void *xq, float *y, int64_t N, int64_t K, voi
  *   w   [N][K/32] Q4_0 blocks;  xq [M][K/32] Q8_0 blocks;  y [M][N] fp32,
  *   row-major (written).  M == 1 is q4q8_gemv (the workspace is not used);
  *   M > 1 needs workspace >= q4q8_gemm_workspace_size(M, K) bytes (the
- *   activations in the layout of the int8 matrix cores; no initialisation).
+ *   activations re-laid for the int8 matrix cores, or, for up to 128 rows
+ *   over a small weight matrix, in nibble-split form with their chunk list
+ *   for the VALU kernel; no initialisation).  Two launches per call.
  * K % 256 != 0, M < 0, N <= 0 or K <= 0 -> W4A8_ESHAPE; M, N >= 2^31,
  * K > 2^20, M * N >= 2^40 or M * K >= 2^40 -> W4A8_ERANGE.  M == 0 is a no-op.
  * q4q8_gemm_workspace_size returns 0 for invalid sizes.

@@ -272,7 +272,7 @@ int small_down(const uint8_t *w_d, const uint8_t *ws_d, const uint8_t *hs, const
   return check_launch();
 }
 
-// Dense product of a few activation rows (q4q8_gemm, M <= 32) on the down
+// Dense product of a few activation rows (q4q8_gemm, M <= 128) on the down
 // kernel: the rows are the "pairs" 0..M-1 of chunks of SMALL_CHUNK rows
 // against one weight matrix (ws), each scaled by 1; act holds the rows in
 // nibble-split form, perm the identity (padded by a chunk), chunks their
